@@ -1,0 +1,262 @@
+"""CPU oracle for one SeKV decode step.  TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
+import this module; the product path (the HIP library and its Python binding)
+never does.  It shares no code with that path and imports nothing from it.
+
+It is a plain, slow, float64 NumPy rendering of the paper's decode step
+(Sec. 3.3, "Trained Zoom-In Mechanism", with the routing gate and the
+reconstruction of Sec. 3.2):
+
+1. routing score of every span for every query head (eq. routing_gate),
+2. per-KV-head selection of the top-k spans (the budget rule of Sec. 3.3:
+   keep spans in decreasing routing-score order until the budget is filled),
+3. reconstruction of the selected spans from their factors
+   (eq. key_reconstruction; the same decomposition for the value matrix),
+4. one softmax over the mixed-resolution memory: anchors at full resolution,
+   one coarse entry per unexpanded span with ln|S| added to its score, and
+   the reconstructed tokens of the expanded spans (Sec. 3.3).
+
+Readings taken where the paper leaves the decode step open (each is listed
+with its reason in the design notes):
+
+* Routing uses the coarse mean key k_bar_S itself as the summary, with an
+  identity projection (d' = d_h), no normalisation and scale 1/sqrt(d_h).  The
+  routing score then equals the coarse entry's attention score, ln|S| included.
+* The zoom rule is top-k on that score (the sigmoid is monotone, so ranking the
+  pre-sigmoid score ranks the gate).  A KV head's key for span S is the maximum
+  of its query heads' scores: the union of per-head decisions under one shared
+  threshold.  Ties go to the lower span index.
+* The rank gates are folded into sigma (m_i = 1 for the stored components).
+* ln is the natural logarithm; an expanded span's coarse entry is replaced by
+  its tokens, never kept beside them.
+
+Floating point.  The routing score is defined bit for bit so that selection is
+exact: s = sum_j q[j] * k_bar[j] accumulated left to right in float64 (every
+product of two bfloat16 or two float32 values is exact in float64), then
+score = (s * scale) + ln|S| as two separately rounded float64 operations.
+Everything else is float64 with no particular order.
+
+Stored inputs are bfloat16 bit patterns (uint16) or float32; they are widened
+exactly to float64 before use.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+SOFTMAX_SUM_TOL = 1e-12
+
+
+# ---------------------------------------------------------------------------
+# stored values -> float64
+# ---------------------------------------------------------------------------
+
+def widen(a, dtype: str) -> np.ndarray:
+    """Exact float64 value of a stored array ('bf16' bit patterns or 'f32')."""
+    if dtype == "bf16":
+        bits = np.asarray(a, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+        return bits.view(np.float32).astype(np.float64)
+    if dtype == "f32":
+        return np.asarray(a, dtype=np.float32).astype(np.float64)
+    raise ValueError(f"unknown storage dtype {dtype!r}")
+
+
+def _elem(dtype: str):
+    return {"bf16": (np.uint16, 2), "f32": (np.float32, 4)}[dtype]
+
+
+def read_span_block(factors: np.ndarray, offset: int, length: int, rank: int,
+                    head_dim: int, dtype: str) -> dict:
+    """Factors of one span: U_K[|S|][r], sigma_K[r], Vt_K[r][d], then the same for V.
+
+    This is the per-span storage of Sec. 3.2 (U of |S| x r_S, Sigma of r_S
+    values, V of d_h x r_S, for keys and for values), one contiguous block.
+    """
+    np_t, e = _elem(dtype)
+    if offset % e:
+        raise ValueError("misaligned block offset")
+    L, r, d = int(length), int(rank), int(head_dim)
+    n = 2 * (L * r + r + r * d)
+    raw = np.frombuffer(np.asarray(factors, dtype=np.uint8).data, dtype=np_t,
+                        count=n, offset=int(offset))
+    x = widen(raw, dtype)
+    out = {}
+    pos = 0
+    for side in ("K", "V"):
+        out["U" + side] = x[pos:pos + L * r].reshape(L, r)
+        pos += L * r
+        out["s" + side] = x[pos:pos + r].copy()
+        pos += r
+        out["Vt" + side] = x[pos:pos + r * d].reshape(r, d)
+        pos += r * d
+    return out
+
+
+# ---------------------------------------------------------------------------
+# the steps
+# ---------------------------------------------------------------------------
+
+def reconstruct(U: np.ndarray, sigma: np.ndarray, Vt: np.ndarray) -> np.ndarray:
+    """Token-level matrix of a span, sum_i sigma_i u_i v_i^T (eq. key_reconstruction).
+
+    The rank gates m_i are folded into sigma, so the stored components are
+    used as they are.
+    """
+    return U @ np.diag(sigma) @ Vt
+
+
+def routing_logits(q, sum_k, span_logsize, n_spans, scale: float) -> np.ndarray:
+    """Pre-sigmoid routing score of every span for every query head.
+
+    eq. routing_gate with the summary read as the coarse mean key and an
+    identity projection: score[b,h,S] = (q_h . k_bar_S) * scale + ln|S|.
+    The dot product is summed left to right in float64; padding spans get -inf.
+    Returns float64 [B][Hq][M_max].
+    """
+    q = np.asarray(q, dtype=np.float64)
+    sum_k = np.asarray(sum_k, dtype=np.float64)
+    B, Hq, d = q.shape
+    Hkv, M = sum_k.shape[1], sum_k.shape[2]
+    G = Hq // Hkv
+    out = np.full((B, Hq, M), -np.inf)
+    for b in range(B):
+        m = int(n_spans[b])
+        for h in range(Hq):
+            kb = sum_k[b, h // G, :m, :]
+            s = np.zeros(m)
+            for j in range(d):
+                s = s + q[b, h, j] * kb[:, j]
+            out[b, h, :m] = s * scale + span_logsize[b, :m]
+    return out
+
+
+def group_keys(logits: np.ndarray, n_kv_heads: int) -> np.ndarray:
+    """Selection key of each span for a KV head: the largest score over its query heads."""
+    B, Hq, M = logits.shape
+    G = Hq // n_kv_heads
+    return logits.reshape(B, n_kv_heads, G, M).max(axis=2)
+
+
+def select_topk(keys: np.ndarray, n_spans, k: int) -> np.ndarray:
+    """Spans to expand per (b, KV head): the k highest keys, ties to the lower index.
+
+    This is the budget rule of Sec. 3.3 (keep spans in decreasing routing
+    score until the budget is filled) with a budget of k spans.  Listed in
+    that order; slots past the number of spans hold -1.
+    """
+    B, Hkv, M = keys.shape
+    sel = np.full((B, Hkv, k), -1, dtype=np.int32)
+    for b in range(B):
+        m = int(n_spans[b])
+        for g in range(Hkv):
+            order = sorted(range(m), key=lambda S: (-keys[b, g, S], S))
+            chosen = order[:min(k, m)]
+            sel[b, g, :len(chosen)] = chosen
+    return sel
+
+
+def softmax_weights(logits: np.ndarray) -> np.ndarray:
+    z = np.exp(logits - logits.max())
+    return z / z.sum()
+
+
+def mixed_attention_head(qh, scale, anchor_k, anchor_v, coarse_logits, coarse_v, zoom):
+    """One softmax over anchors, coarse span entries and zoomed tokens (Sec. 3.3).
+
+    qh: [d]; anchor_k/v: [A][d]; coarse_logits: [n_c] (ln|S| already in);
+    coarse_v: [n_c][d]; zoom: list of (K_hat [L][d], V_hat [L][d]).
+    Returns (out [d], weights [n]) with the weights ordered anchors, coarse, zoom.
+    """
+    logit_parts = [scale * (anchor_k @ qh), np.asarray(coarse_logits, dtype=np.float64)]
+    value_parts = [anchor_v, coarse_v]
+    for K_hat, V_hat in zoom:
+        logit_parts.append(scale * (K_hat @ qh))
+        value_parts.append(V_hat)
+    logits = np.concatenate(logit_parts)
+    values = np.concatenate(value_parts, axis=0)
+    if logits.size == 0:
+        raise ValueError("empty attention set: no anchors and no spans")
+    p = softmax_weights(logits)
+    if abs(p.sum() - 1.0) > SOFTMAX_SUM_TOL:
+        raise AssertionError("softmax weights do not sum to one")
+    return p @ values, p
+
+
+def zoom_attend(q, anchor_k, anchor_v, n_anchors, sum_v, n_spans, span_len, factors,
+                block_off, sel, logits, *, rank: int, softmax_scale: float,
+                dtype: str) -> np.ndarray:
+    """Mixed-resolution decode attention given the selection and routing scores.
+
+    q and the cache arrays are stored values (widened here); logits are the
+    float64 routing scores from routing_logits.  Returns float64 [B][Hq][d].
+    """
+    qf = widen(q, dtype)
+    ak, av, sv = widen(anchor_k, dtype), widen(anchor_v, dtype), widen(sum_v, dtype)
+    B, Hq, d = qf.shape
+    Hkv = ak.shape[1]
+    G = Hq // Hkv
+    out = np.zeros((B, Hq, d))
+    for b in range(B):
+        A, m = int(n_anchors[b]), int(n_spans[b])
+        for g in range(Hkv):
+            chosen = [int(S) for S in sel[b, g] if S >= 0]
+            zoom = []
+            for S in chosen:
+                f = read_span_block(factors, int(block_off[b, g, S]), int(span_len[b, S]),
+                                    rank, d, dtype)
+                zoom.append((reconstruct(f["UK"], f["sK"], f["VtK"]),
+                             reconstruct(f["UV"], f["sV"], f["VtV"])))
+            coarse = [S for S in range(m) if S not in set(chosen)]
+            for h in range(g * G, (g + 1) * G):
+                out[b, h], _ = mixed_attention_head(
+                    qf[b, h], softmax_scale, ak[b, g, :A], av[b, g, :A],
+                    logits[b, h, coarse], sv[b, g, coarse], zoom)
+    return out
+
+
+def decode_step(q, anchor_k, anchor_v, n_anchors, sum_k, sum_v, n_spans, span_len,
+                span_logsize, factors, block_off, *, rank: int, top_k: int,
+                softmax_scale: float, dtype: str) -> dict:
+    """Route, select, reconstruct and attend: one SeKV decode step for one layer."""
+    qf = widen(q, dtype)
+    logits = routing_logits(qf, widen(sum_k, dtype), np.asarray(span_logsize, np.float64),
+                            n_spans, softmax_scale)
+    keys = group_keys(logits, np.asarray(sum_k).shape[1])
+    sel = select_topk(keys, n_spans, top_k)
+    out = zoom_attend(q, anchor_k, anchor_v, n_anchors, sum_v, n_spans, span_len, factors,
+                      block_off, sel, logits, rank=rank, softmax_scale=softmax_scale,
+                      dtype=dtype)
+    return {"sel": sel, "out": out, "logits": logits, "keys": keys}
+
+
+# ---------------------------------------------------------------------------
+# split softmax algebra and the factored identity (test aids)
+# ---------------------------------------------------------------------------
+
+def softmax_partial(logits: np.ndarray, values: np.ndarray):
+    """(max, sum of exp(logit - max), sum of exp(logit - max) * value) over one chunk."""
+    logits = np.asarray(logits, dtype=np.float64)
+    if logits.size == 0:
+        return -np.inf, 0.0, np.zeros(values.shape[1])
+    mx = logits.max()
+    w = np.exp(logits - mx)
+    return mx, w.sum(), w @ values
+
+
+def merge_partials(parts) -> np.ndarray:
+    """Combine chunk partials into the output of the one softmax over their union."""
+    M = max(p[0] for p in parts)
+    l = sum(p[1] * np.exp(p[0] - M) for p in parts if p[1] > 0)
+    o = sum(p[2] * np.exp(p[0] - M) for p in parts if p[1] > 0)
+    return o / l
+
+
+def zoom_scores_factored(qh, scale, U, sigma, Vt):
+    """scale * q . K_hat_t for every token without forming K_hat: U (sigma * (Vt q))."""
+    return scale * (U @ (sigma * (Vt @ qh)))
+
+
+def zoom_values_factored(p, U, sigma, Vt):
+    """sum_t p_t V_hat_t without forming V_hat: ((p^T U) * sigma) Vt."""
+    return ((p @ U) * sigma) @ Vt

@@ -1,0 +1,609 @@
+"""Seeded synthetic SeKV caches (stored inputs of one decode step).
+
+Everything here is input synthesis.  The values come from a counter-based
+generator so that any slice of any cache can be regenerated exactly, on any
+machine, in any order and from any number of threads:
+
+* key    = chain of splitmix64 finalisers over (seed, variant, layer, stream, b, g)
+* z[i]   = splitmix64 finaliser of (key + i * 0x9E3779B97F4A7C15)   (mod 2**64)
+* normal = NTAB[z >> 48], NTAB[j] = Phi^-1((j + 0.5) / 65536)  (tails cut at 4.32 sigma)
+* uniform= (z >> 11) * 2**-53
+
+The splitmix64 finaliser is the published mixing function of Steele, Lea and
+Flood ("Fast splittable pseudorandom number generators", OOPSLA 2014) with
+Vigna's constants.
+
+Storage rounding: every stored value is computed in float64 and rounded once
+to the storage type (float32, or bfloat16 with round-to-nearest-even, done as
+float64 -> float32 with round-to-odd -> bfloat16 with round-to-nearest-even,
+which is a correct single rounding since float32 carries more than 8 + 2 bits).
+
+Span partition (one per sequence, shared by every layer and head): the first
+``n_prefix_anchors`` tokens and the last ``window`` tokens are kept at full
+resolution; the tokens between are cut left to right into spans whose lengths
+are drawn i.i.d. (uniform integers, or ``min(hi, floor(exp(u)))`` with
+``u ~ U(ln lo, ln(hi + 1))`` for the log-uniform law); a final remainder
+shorter than ``span_min`` joins the full-resolution set, as spans shorter than
+the minimum length stay at full resolution in the paper (Sec. 3.2, low-rank
+basis paragraph).
+
+Span summaries are the means of the span's reconstructed keys and values (the
+workload definition), formed in float64 from the already-rounded stored factors
+as (1/|S|) (1^T U) diag(sigma) V^T and then rounded to storage.
+
+Factor arena: one block per (b, kv head, span), in (b, g, S) order, each block
+starting on a 256-byte boundary and laid out as
+``U_K[|S|][r] | sigma_K[r] | Vt_K[r][d] | U_V[|S|][r] | sigma_V[r] | Vt_V[r][d]``
+in the storage type.  ``block_off[b][g][S]`` is the block's byte offset.
+"""
+
+from __future__ import annotations
+
+import math
+import os
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass, field, replace
+
+import numpy as np
+
+try:  # inverse normal CDF for the quantile table
+    from scipy.special import ndtri as _ndtri
+except Exception:  # pragma: no cover - scipy is present in this image
+    from statistics import NormalDist
+
+    def _ndtri(p):
+        nd = NormalDist()
+        return np.array([nd.inv_cdf(float(x)) for x in np.ravel(p)])
+
+
+_MASK64 = (1 << 64) - 1
+_GOLDEN_I = 0x9E3779B97F4A7C15
+_GOLDEN = np.uint64(_GOLDEN_I)
+_M1 = np.uint64(0xBF58476D1CE4E5B9)
+_M2 = np.uint64(0x94D049BB133111EB)
+_S30, _S27, _S31 = np.uint64(30), np.uint64(27), np.uint64(31)
+_S48, _S11 = np.uint64(48), np.uint64(11)
+
+NTAB = _ndtri((np.arange(65536, dtype=np.float64) + 0.5) / 65536.0)
+
+_CHUNK = 1 << 20
+
+# stream ids
+ST_PART, ST_Q, ST_AK, ST_AV = 1, 2, 3, 4
+ST_UK, ST_SK, ST_VK, ST_UV, ST_SV, ST_VV = 5, 6, 7, 8, 9, 10
+ST_NEEDLE = 11
+
+VARIANTS = {"L": 0, "N": 1}
+PLANT_DELTA = 6.0
+
+
+def _mix_int(x: int) -> int:
+    x &= _MASK64
+    x ^= x >> 30
+    x = (x * 0xBF58476D1CE4E5B9) & _MASK64
+    x ^= x >> 27
+    x = (x * 0x94D049BB133111EB) & _MASK64
+    x ^= x >> 31
+    return x
+
+
+def stream_key(*parts: int) -> int:
+    k = 0
+    for p in parts:
+        k = _mix_int(k + _GOLDEN_I * (int(p) + 1))
+    return k
+
+
+def _hash_block(key: int, start: int, n: int) -> np.ndarray:
+    z = np.arange(start, start + n, dtype=np.uint64)
+    z *= _GOLDEN
+    z += np.uint64(key)
+    z ^= z >> _S30
+    z *= _M1
+    z ^= z >> _S27
+    z *= _M2
+    z ^= z >> _S31
+    return z
+
+
+def normals(key: int, n: int) -> np.ndarray:
+    out = np.empty(n, dtype=np.float64)
+    for s in range(0, n, _CHUNK):
+        m = min(_CHUNK, n - s)
+        out[s:s + m] = NTAB[(_hash_block(key, s, m) >> _S48).astype(np.intp)]
+    return out
+
+
+def uniforms(key: int, n: int) -> np.ndarray:
+    out = np.empty(n, dtype=np.float64)
+    for s in range(0, n, _CHUNK):
+        m = min(_CHUNK, n - s)
+        out[s:s + m] = (_hash_block(key, s, m) >> _S11).astype(np.float64) * (2.0 ** -53)
+    return out
+
+
+# ---------------------------------------------------------------------------
+# storage types
+# ---------------------------------------------------------------------------
+
+def f64_to_bf16_bits(x) -> np.ndarray:
+    """Round float64 to bfloat16 (nearest-even), returned as uint16 bit patterns."""
+    x = np.asarray(x, dtype=np.float64)
+    flat = x.reshape(-1)
+    out = np.empty(flat.shape, dtype=np.uint16)
+    for s0 in range(0, flat.size, _CHUNK):
+        xc = flat[s0:s0 + _CHUNK]
+        f = xc.astype(np.float32)
+        back = f.astype(np.float64)
+        inexact = back != xc
+        over = inexact & (np.abs(back) > np.abs(xc))
+        fb = f.view(np.uint32) - over.astype(np.uint32)   # truncate toward zero
+        fb |= inexact.astype(np.uint32)                   # sticky bit: round-to-odd
+        fb += ((fb >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+        out[s0:s0 + _CHUNK] = (fb >> np.uint32(16)).astype(np.uint16)
+    return out.reshape(x.shape)
+
+
+def bf16_bits_to_f64(b) -> np.ndarray:
+    b = np.asarray(b, dtype=np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+def to_storage(x64: np.ndarray, dtype: str) -> np.ndarray:
+    if dtype == "f32":
+        return np.asarray(x64, dtype=np.float64).astype(np.float32)
+    if dtype == "bf16":
+        return f64_to_bf16_bits(x64)
+    raise ValueError(dtype)
+
+
+def from_storage(a: np.ndarray, dtype: str) -> np.ndarray:
+    if dtype == "f32":
+        return np.asarray(a, dtype=np.float32).astype(np.float64)
+    if dtype == "bf16":
+        return bf16_bits_to_f64(a)
+    raise ValueError(dtype)
+
+
+def elem_bytes(dtype: str) -> int:
+    return {"f32": 4, "bf16": 2}[dtype]
+
+
+def _np_storage_type(dtype: str):
+    return {"f32": np.float32, "bf16": np.uint16}[dtype]
+
+
+# ---------------------------------------------------------------------------
+# specs
+# ---------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class CaseSpec:
+    name: str
+    batch: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    rank: int
+    top_k: int
+    context: int
+    n_prefix_anchors: int
+    window: int
+    span_dist: str          # "uniform" | "loguniform"
+    span_min: int
+    span_max: int
+    dtype: str              # "f32" | "bf16"
+    factor_kind: str        # "orthonormal" | "gaussian"
+    n_layers: int = 1
+    seed: int = 0
+    host_factors: bool = False   # factors live in pinned host memory (tier case)
+
+    @property
+    def group(self) -> int:
+        return self.n_q_heads // self.n_kv_heads
+
+    @property
+    def softmax_scale(self) -> float:
+        return 1.0 / math.sqrt(self.head_dim)
+
+
+CONFIGS = {
+    1: CaseSpec("tiny-f32", batch=1, n_q_heads=4, n_kv_heads=2, head_dim=64, rank=8,
+                top_k=2, context=2048, n_prefix_anchors=32, window=0,
+                span_dist="uniform", span_min=16, span_max=64, dtype="f32",
+                factor_kind="orthonormal", seed=1),
+    2: CaseSpec("llama3-8b-layer-32k", batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                rank=16, top_k=8, context=32768, n_prefix_anchors=256, window=512,
+                span_dist="uniform", span_min=32, span_max=256, dtype="bf16",
+                factor_kind="gaussian", seed=2),
+    3: CaseSpec("llama3-8b-layer-128k-b4", batch=4, n_q_heads=32, n_kv_heads=8, head_dim=128,
+                rank=32, top_k=16, context=131072, n_prefix_anchors=256, window=512,
+                span_dist="loguniform", span_min=32, span_max=512, dtype="bf16",
+                factor_kind="gaussian", seed=3),
+    4: CaseSpec("llama3-8b-32layer-32k-b32", batch=32, n_q_heads=32, n_kv_heads=8,
+                head_dim=128, rank=16, top_k=8, context=32768, n_prefix_anchors=256,
+                window=512, span_dist="uniform", span_min=32, span_max=256, dtype="bf16",
+                factor_kind="gaussian", n_layers=32, seed=4),
+    5: CaseSpec("llama3-8b-layer-128k-b4-hosttier", batch=4, n_q_heads=32, n_kv_heads=8,
+                head_dim=128, rank=32, top_k=16, context=131072, n_prefix_anchors=256,
+                window=512, span_dist="loguniform", span_min=32, span_max=512,
+                dtype="bf16", factor_kind="gaussian", seed=3, host_factors=True),
+}
+
+
+def custom_spec(**kw) -> CaseSpec:
+    """A small spec for tests; defaults follow the tiny fp32 case."""
+    base = dict(name="custom", batch=1, n_q_heads=4, n_kv_heads=2, head_dim=64, rank=8,
+                top_k=2, context=512, n_prefix_anchors=8, window=0, span_dist="uniform",
+                span_min=8, span_max=32, dtype="f32", factor_kind="gaussian", seed=99)
+    base.update(kw)
+    return CaseSpec(**base)
+
+
+# ---------------------------------------------------------------------------
+# case container
+# ---------------------------------------------------------------------------
+
+@dataclass
+class Case:
+    spec: CaseSpec
+    layer: int
+    variant: str
+    q: np.ndarray              # [B][Hq][d]            storage type
+    anchor_k: np.ndarray       # [B][Hkv][A_max][d]
+    anchor_v: np.ndarray
+    n_anchors: np.ndarray      # [B] int32
+    sum_k: np.ndarray          # [B][Hkv][M_max][d]
+    sum_v: np.ndarray
+    n_spans: np.ndarray        # [B] int32
+    span_len: np.ndarray       # [B][M_max] int32 (0 past n_spans)
+    span_logsize: np.ndarray   # [B][M_max] float64 ln|S| (0 past n_spans)
+    factors: np.ndarray        # uint8 arena
+    block_off: np.ndarray      # [B][Hkv][M_max] int64 byte offsets
+    needles: np.ndarray = field(default=None)   # [B][Hkv][n_p] planted spans (variant N)
+
+    @property
+    def dtype(self) -> str:
+        return self.spec.dtype
+
+    @property
+    def max_anchors(self) -> int:
+        return self.anchor_k.shape[2]
+
+    @property
+    def max_spans(self) -> int:
+        return self.sum_k.shape[2]
+
+    @property
+    def max_span_len(self) -> int:
+        return int(self.span_len.max()) if self.span_len.size else 1
+
+    def dims(self) -> dict:
+        s = self.spec
+        return dict(batch=s.batch, n_q_heads=s.n_q_heads, n_kv_heads=s.n_kv_heads,
+                    head_dim=s.head_dim, rank=s.rank, top_k=s.top_k,
+                    max_anchors=self.max_anchors, max_spans=self.max_spans,
+                    max_span_len=max(self.max_span_len, 1), dtype=s.dtype,
+                    softmax_scale=s.softmax_scale)
+
+
+# ---------------------------------------------------------------------------
+# partition
+# ---------------------------------------------------------------------------
+
+def span_lengths(spec: CaseSpec, b: int):
+    """Span lengths of sequence b and the short remainder kept at full resolution."""
+    middle = spec.context - spec.n_prefix_anchors - spec.window
+    if middle < 0:
+        raise ValueError("context shorter than anchors + window")
+    n_draw = middle // max(spec.span_min, 1) + 2
+    u = uniforms(stream_key(spec.seed, ST_PART, b), n_draw)
+    lo, hi = spec.span_min, spec.span_max
+    if spec.span_dist == "uniform":
+        drawn = lo + np.floor(u * (hi - lo + 1)).astype(np.int64)
+    elif spec.span_dist == "loguniform":
+        a, c = math.log(lo), math.log(hi + 1)
+        drawn = np.minimum(hi, np.floor(np.exp(a + u * (c - a))).astype(np.int64))
+    else:
+        raise ValueError(spec.span_dist)
+    lengths = []
+    pos = 0
+    for L in drawn:
+        rem = middle - pos
+        if rem < lo:
+            break
+        L = int(min(L, rem))
+        lengths.append(L)
+        pos += L
+    return lengths, middle - pos
+
+
+def block_bytes(length: int, rank: int, head_dim: int, dtype: str) -> int:
+    raw = (2 * length * rank + 2 * rank + 2 * rank * head_dim) * elem_bytes(dtype)
+    return (raw + 255) // 256 * 256
+
+
+# ---------------------------------------------------------------------------
+# factor synthesis
+# ---------------------------------------------------------------------------
+
+def _orthonormal_cols(mat: np.ndarray) -> np.ndarray:
+    """Q of a thin QR with a positive diagonal of R (first column keeps its direction)."""
+    qm, rm = np.linalg.qr(mat)
+    sgn = np.sign(np.diag(rm))
+    sgn[sgn == 0] = 1.0
+    return qm * sgn
+
+
+def _pair_factors(spec: CaseSpec, vkey, b, g, lens, planted, qbar):
+    """Float64 factors of every span of (b, g) before storage rounding."""
+    r, d, m = spec.rank, spec.head_dim, len(lens)
+    sum_l = int(sum(lens))
+    fs = 1.0 / math.sqrt(d)
+    out = {}
+    for side, (su, ss, sv) in (("K", (ST_UK, ST_SK, ST_VK)), ("V", (ST_UV, ST_SV, ST_VV))):
+        if spec.factor_kind == "gaussian":
+            scale = 1.0 if (side == "V" and planted) else fs
+            U = normals(stream_key(*vkey, su, b, g), sum_l * r).reshape(sum_l, r) * scale
+            s = np.abs(normals(stream_key(*vkey, ss, b, g), m * r).reshape(m, r))
+            s = -np.sort(-s, axis=1) * scale
+            Vt = normals(stream_key(*vkey, sv, b, g), m * r * d).reshape(m, r, d) * scale
+        elif spec.factor_kind == "orthonormal":
+            raw_u = normals(stream_key(*vkey, su, b, g), sum_l * r).reshape(sum_l, r)
+            raw_v = normals(stream_key(*vkey, sv, b, g), m * d * r).reshape(m, d, r)
+            uu = uniforms(stream_key(*vkey, ss, b, g), m * r).reshape(m, r)
+            expo = -np.log1p(-uu)                 # Exp(1) by inversion
+            s = -np.sort(-expo, axis=1)           # descending
+            U = np.empty_like(raw_u)
+            Vt = np.empty((m, r, d))
+            start = 0
+            for j, L in enumerate(lens):
+                U[start:start + L] = _orthonormal_cols(raw_u[start:start + L])
+                Vt[j] = _orthonormal_cols(raw_v[j]).T
+                start += L
+        else:
+            raise ValueError(spec.factor_kind)
+        out[side] = [U, s, Vt]
+    return out
+
+
+def _plant(spec: CaseSpec, fac, lens, needles, qbar):
+    """Make each needle span's keys align with the group's mean query (K side only)."""
+    r, d = spec.rank, spec.head_dim
+    U, s, Vt = fac["K"]
+    nq = float(np.linalg.norm(qbar))
+    direction = qbar / nq
+    starts = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.int64)
+    for j in needles:
+        L = lens[j]
+        rows = slice(starts[j], starts[j] + L)
+        if spec.factor_kind == "orthonormal":
+            mu = U[rows].copy()
+            mu[:, 0] = 1.0 / math.sqrt(L)
+            U[rows] = _orthonormal_cols(mu)
+            mv = Vt[j].T.copy()
+            mv[:, 0] = direction
+            Vt[j] = _orthonormal_cols(mv).T
+        else:
+            U[rows, 0] = 1.0 / math.sqrt(L)
+            Vt[j, 0] = direction
+        s[j, 0] = PLANT_DELTA * math.sqrt(L) / (spec.softmax_scale * nq)
+        s[j] = -np.sort(-s[j])
+
+
+def _write_pair(spec, arena_e, eoff, lens, fac_st):
+    """Copy the stored factors of one (b, g) into the arena (element view)."""
+    r, d = spec.rank, spec.head_dim
+    UK, sK, VK = fac_st["K"]
+    UV, sV, VV = fac_st["V"]
+    start = 0
+    for j, L in enumerate(lens):
+        o = int(eoff[j])
+        n_u = L * r
+        rows = slice(start, start + L)
+        arena_e[o:o + n_u] = UK[rows].reshape(-1)
+        o += n_u
+        arena_e[o:o + r] = sK[j]
+        o += r
+        arena_e[o:o + r * d] = VK[j].reshape(-1)
+        o += r * d
+        arena_e[o:o + n_u] = UV[rows].reshape(-1)
+        o += n_u
+        arena_e[o:o + r] = sV[j]
+        o += r
+        arena_e[o:o + r * d] = VV[j].reshape(-1)
+        start += L
+
+
+def _span_means(U, s, Vt, lens):
+    """(1/|S|) (1^T U) diag(sigma) V^T per span, float64."""
+    lens_a = np.asarray(lens, dtype=np.int64)
+    starts = np.concatenate([[0], np.cumsum(lens_a)[:-1]]).astype(np.int64)
+    colsum = np.add.reduceat(U, starts, axis=0)
+    coef = colsum / lens_a[:, None] * s
+    return np.einsum("mr,mrd->md", coef, Vt)
+
+
+def make_case(spec: CaseSpec, layer: int = 0, variant: str = "L", threads: int | None = None,
+              arena_out: np.ndarray | None = None) -> Case:
+    """Build the stored inputs of one layer of a decode step."""
+    if variant not in VARIANTS:
+        raise ValueError(variant)
+    planted = variant == "N"
+    B, Hq, Hkv, d, r = spec.batch, spec.n_q_heads, spec.n_kv_heads, spec.head_dim, spec.rank
+    if Hq % Hkv:
+        raise ValueError("n_q_heads must be a multiple of n_kv_heads")
+    G = Hq // Hkv
+    dt = spec.dtype
+    e = elem_bytes(dt)
+    vkey = (spec.seed, VARIANTS[variant], layer)
+
+    parts = [span_lengths(spec, b) for b in range(B)]
+    n_spans = np.array([len(p[0]) for p in parts], dtype=np.int32)
+    n_anch = np.array([spec.n_prefix_anchors + p[1] + spec.window for p in parts], dtype=np.int32)
+    M_max = max(int(n_spans.max()) if B else 0, 1)
+    A_max = max(int(n_anch.max()) if B else 0, 1)
+    span_len = np.zeros((B, M_max), dtype=np.int32)
+    for b, (lens, _) in enumerate(parts):
+        span_len[b, :len(lens)] = lens
+    span_logsize = np.zeros((B, M_max), dtype=np.float64)
+    nz = span_len > 0
+    span_logsize[nz] = np.log(span_len[nz].astype(np.float64))
+
+    qscale = 1.0 if spec.factor_kind == "orthonormal" else 1.0 / math.sqrt(d)
+    q64 = np.stack([normals(stream_key(*vkey, ST_Q, b), Hq * d).reshape(Hq, d)
+                    for b in range(B)]) * qscale if B else np.zeros((0, Hq, d))
+    q_st = to_storage(q64, dt)
+    q_dec = from_storage(q_st, dt)
+
+    # block offsets
+    block_off = np.zeros((B, Hkv, M_max), dtype=np.int64)
+    total = 0
+    for b, (lens, _) in enumerate(parts):
+        sizes = np.array([block_bytes(L, r, d, dt) for L in lens], dtype=np.int64)
+        for g in range(Hkv):
+            if len(lens):
+                block_off[b, g, :len(lens)] = total + np.concatenate([[0], np.cumsum(sizes)[:-1]])
+                total += int(sizes.sum())
+    total = max(total, 256)
+    if arena_out is not None:
+        if arena_out.nbytes < total or arena_out.dtype != np.uint8:
+            raise ValueError("arena_out too small or not uint8")
+        arena = arena_out[:total]
+    else:
+        arena = np.zeros(total, dtype=np.uint8)
+    arena_e = arena.view(_np_storage_type(dt))
+
+    st_t = _np_storage_type(dt)
+    anchor_k = np.zeros((B, Hkv, A_max, d), dtype=st_t)
+    anchor_v = np.zeros((B, Hkv, A_max, d), dtype=st_t)
+    sum_k = np.zeros((B, Hkv, M_max, d), dtype=st_t)
+    sum_v = np.zeros((B, Hkv, M_max, d), dtype=st_t)
+    n_p = max(1, spec.top_k // 2)
+    needles = np.full((B, Hkv, n_p), -1, dtype=np.int32) if planted else None
+
+    ascale = qscale
+    vscale_anchor = 1.0 if (planted and spec.factor_kind == "gaussian") else ascale
+
+    def work(bg):
+        b, g = bg
+        lens, _ = parts[b]
+        A = int(n_anch[b])
+        ak = normals(stream_key(*vkey, ST_AK, b, g), A * d).reshape(A, d) * ascale
+        av = normals(stream_key(*vkey, ST_AV, b, g), A * d).reshape(A, d) * vscale_anchor
+        anchor_k[b, g, :A] = to_storage(ak, dt)
+        anchor_v[b, g, :A] = to_storage(av, dt)
+        m = len(lens)
+        if m == 0:
+            return
+        qbar = q_dec[b, g * G:(g + 1) * G].mean(axis=0)
+        fac = _pair_factors(spec, vkey, b, g, lens, planted, qbar)
+        if planted:
+            h = uniforms(stream_key(*vkey, ST_NEEDLE, b, g), m)
+            chosen = np.sort(np.argsort(h, kind="stable")[:min(n_p, m)])
+            needles[b, g, :len(chosen)] = chosen
+            _plant(spec, fac, lens, chosen, qbar)
+        fac_st = {side: [to_storage(x, dt) for x in fac[side]] for side in fac}
+        _write_pair(spec, arena_e, block_off[b, g, :m] // e, lens, fac_st)
+        for side, dst in (("K", sum_k), ("V", sum_v)):
+            U, s, Vt = (from_storage(x, dt) for x in fac_st[side])
+            dst[b, g, :m] = to_storage(_span_means(U, s, Vt, lens), dt)
+
+    pairs = [(b, g) for b in range(B) for g in range(Hkv)]
+    nthreads = threads if threads is not None else min(16, os.cpu_count() or 1)
+    if nthreads > 1 and len(pairs) > 1:
+        with ThreadPoolExecutor(nthreads) as ex:
+            list(ex.map(work, pairs))
+    else:
+        for bg in pairs:
+            work(bg)
+
+    return Case(spec=spec, layer=layer, variant=variant, q=q_st, anchor_k=anchor_k,
+                anchor_v=anchor_v, n_anchors=n_anch, sum_k=sum_k, sum_v=sum_v,
+                n_spans=n_spans, span_len=span_len, span_logsize=span_logsize,
+                factors=arena, block_off=block_off, needles=needles)
+
+
+def with_top_k(case: Case, k: int) -> Case:
+    """The same stored cache with a different top-k."""
+    return replace(case, spec=replace(case.spec, top_k=k))
+
+
+def case_from_factors(q, anchor_k, anchor_v, span_factors, *, dtype: str, top_k: int,
+                      sum_k=None, sum_v=None) -> Case:
+    """Pack caller-given float64 arrays into a stored cache.
+
+    q: [B][Hq][d]; anchor_k/anchor_v: per sequence b an array [Hkv][A_b][d];
+    span_factors: per sequence b a list (over spans S) of per-KV-head lists of
+    dicts with keys UK [L][r], sK [r], VtK [r][d], UV, sV, VtV (all spans of a
+    sequence share L across heads; r is common).  Summaries are the span means
+    of the stored factors unless sum_k / sum_v ([B][Hkv][M][d]) are given.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    B, Hq, d = q.shape
+    Hkv = np.asarray(anchor_k[0]).shape[0] if B else 1
+    n_anch = np.array([np.asarray(a).shape[1] for a in anchor_k], dtype=np.int32)
+    n_spans = np.array([len(sf) for sf in span_factors], dtype=np.int32)
+    A_max = max(int(n_anch.max()) if B else 0, 1)
+    M_max = max(int(n_spans.max()) if B else 0, 1)
+    r = None
+    for sf in span_factors:
+        for per_head in sf:
+            r = per_head[0]["UK"].shape[1]
+            break
+        if r is not None:
+            break
+    r = r or 8
+    st_t = _np_storage_type(dtype)
+    e = elem_bytes(dtype)
+    spec = CaseSpec("packed", batch=B, n_q_heads=Hq, n_kv_heads=Hkv, head_dim=d, rank=r,
+                    top_k=top_k, context=0, n_prefix_anchors=0, window=0,
+                    span_dist="uniform", span_min=1, span_max=1, dtype=dtype,
+                    factor_kind="gaussian")
+    span_len = np.zeros((B, M_max), dtype=np.int32)
+    for b, sf in enumerate(span_factors):
+        for S, per_head in enumerate(sf):
+            span_len[b, S] = per_head[0]["UK"].shape[0]
+    span_logsize = np.zeros((B, M_max))
+    nz = span_len > 0
+    span_logsize[nz] = np.log(span_len[nz].astype(np.float64))
+    block_off = np.zeros((B, Hkv, M_max), dtype=np.int64)
+    total = 0
+    for b in range(B):
+        for g in range(Hkv):
+            for S in range(int(n_spans[b])):
+                block_off[b, g, S] = total
+                total += block_bytes(int(span_len[b, S]), r, d, dtype)
+    arena = np.zeros(max(total, 256), dtype=np.uint8)
+    arena_e = arena.view(st_t)
+    ak = np.zeros((B, Hkv, A_max, d), dtype=st_t)
+    av = np.zeros((B, Hkv, A_max, d), dtype=st_t)
+    sk = np.zeros((B, Hkv, M_max, d), dtype=st_t)
+    sv = np.zeros((B, Hkv, M_max, d), dtype=st_t)
+    for b in range(B):
+        A = int(n_anch[b])
+        ak[b, :, :A] = to_storage(np.asarray(anchor_k[b], np.float64), dtype)
+        av[b, :, :A] = to_storage(np.asarray(anchor_v[b], np.float64), dtype)
+        for g in range(Hkv):
+            m = int(n_spans[b])
+            if m == 0:
+                continue
+            lens = [int(span_len[b, S]) for S in range(m)]
+            fac_st = {}
+            for side in ("K", "V"):
+                U = np.concatenate([span_factors[b][S][g]["U" + side] for S in range(m)], axis=0)
+                s = np.stack([span_factors[b][S][g]["s" + side] for S in range(m)])
+                Vt = np.stack([span_factors[b][S][g]["Vt" + side] for S in range(m)])
+                fac_st[side] = [to_storage(U, dtype), to_storage(s, dtype), to_storage(Vt, dtype)]
+            _write_pair(spec, arena_e, block_off[b, g, :m] // e, lens, fac_st)
+            for side, dst, given in (("K", sk, sum_k), ("V", sv, sum_v)):
+                if given is not None:
+                    dst[b, g, :m] = to_storage(np.asarray(given)[b, g, :m], dtype)
+                else:
+                    U, s, Vt = (from_storage(x, dtype) for x in fac_st[side])
+                    dst[b, g, :m] = to_storage(_span_means(U, s, Vt, lens), dtype)
+    case = Case(spec=spec, layer=0, variant="L", q=to_storage(q, dtype), anchor_k=ak,
+                anchor_v=av, n_anchors=n_anch, sum_k=sk, sum_v=sv, n_spans=n_spans,
+                span_len=span_len, span_logsize=span_logsize, factors=arena,
+                block_off=block_off)
+    return case

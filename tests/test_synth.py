@@ -1,0 +1,98 @@
+"""The synthetic cache generator: partitions, storage rounding, determinism, planting."""
+
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import CONFIGS, custom_spec, make_case
+from synth.cases import (bf16_bits_to_f64, f64_to_bf16_bits, from_storage, span_lengths,
+                         uniforms)
+from tests.helpers import oracle_kwargs
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4])
+def test_partition_covers_context(cid):
+    spec = CONFIGS[cid]
+    for b in range(min(spec.batch, 4)):
+        lens, rem = span_lengths(spec, b)
+        assert all(spec.span_min <= L <= spec.span_max for L in lens)
+        assert 0 <= rem < spec.span_min
+        assert sum(lens) + rem + spec.n_prefix_anchors + spec.window == spec.context
+
+
+def test_loguniform_partition_statistics():
+    spec = CONFIGS[3]
+    lens = [L for b in range(4) for L in span_lengths(spec, b)[0]]
+    assert 165 < np.mean(lens) < 185          # E[min(512, floor(e^U))] ~ 173
+    assert 680 < len(lens) / 4 < 800          # about 700 spans per 128K sequence
+
+
+def test_bf16_rounding_is_nearest_even():
+    g = np.random.default_rng(0)
+    x = g.standard_normal(200_000) * 10.0 ** g.integers(-20, 20, 200_000)
+    b = f64_to_bf16_bits(x)
+    y = bf16_bits_to_f64(b)
+    up, dn = bf16_bits_to_f64(b + 1), bf16_bits_to_f64(b - 1)
+    assert np.all(np.abs(y - x) <= np.abs(up - x))
+    assert np.all(np.abs(y - x) <= np.abs(dn - x))
+    # exact halfway cases go to the even pattern
+    base = bf16_bits_to_f64(np.arange(0x3F80, 0x3F90, dtype=np.uint16))
+    mid = (base[:-1] + base[1:]) / 2
+    got = f64_to_bf16_bits(mid)
+    assert np.all(got % 2 == 0)
+
+
+def test_generation_is_deterministic_and_thread_independent():
+    spec = custom_spec(dtype="bf16", batch=2, n_q_heads=8, n_kv_heads=2, head_dim=64, rank=16,
+                       top_k=4, context=3000, seed=5)
+    a = make_case(spec, variant="N", threads=1)
+    b = make_case(spec, variant="N", threads=4)
+    for name in ("q", "anchor_k", "anchor_v", "sum_k", "sum_v", "factors", "block_off",
+                 "span_len", "span_logsize", "needles"):
+        assert np.array_equal(getattr(a, name), getattr(b, name)), name
+    c = make_case(spec, layer=1)
+    assert not np.array_equal(a.q, c.q)
+    assert np.array_equal(a.span_len, c.span_len)     # partition shared across layers
+
+
+def test_counter_stream_is_position_addressable():
+    full = uniforms(1234, 5000)
+    assert np.array_equal(full[:10], uniforms(1234, 10))
+    assert 0.0 <= full.min() and full.max() < 1.0
+    assert abs(full.mean() - 0.5) < 0.02
+
+
+def test_tiny_config_factors_are_orthonormal():
+    case = make_case(CONFIGS[1])
+    s = case.spec
+    for S in range(int(case.n_spans[0])):
+        f = oracle.read_span_block(case.factors, int(case.block_off[0, 1, S]),
+                                   int(case.span_len[0, S]), s.rank, s.head_dim, s.dtype)
+        for side in "KV":
+            U, Vt = f["U" + side], f["Vt" + side]
+            assert np.max(np.abs(U.T @ U - np.eye(s.rank))) < 1e-6
+            assert np.max(np.abs(Vt @ Vt.T - np.eye(s.rank))) < 1e-6
+            assert np.all(np.diff(f["s" + side]) <= 0)
+
+
+@pytest.mark.parametrize("cid", [1, 2])
+def test_planted_needles_are_selected(cid):
+    case = make_case(CONFIGS[cid], variant="N")
+    res = oracle.decode_step(**oracle_kwargs(case))
+    for b in range(case.spec.batch):
+        for g in range(case.spec.n_kv_heads):
+            needles = set(case.needles[b, g][case.needles[b, g] >= 0].tolist())
+            assert needles <= set(res["sel"][b, g].tolist())
+    if case.spec.factor_kind == "gaussian":
+        # planted outputs are O(1), literal ones tiny (the reason the planted variant exists)
+        assert np.abs(res["out"]).max() > 0.1
+
+
+def test_literal_layer_is_near_uniform():
+    case = make_case(CONFIGS[2])
+    qd = from_storage(case.q, "bf16")
+    kd = from_storage(case.sum_k[0, 0, :5], "bf16")
+    assert np.abs(qd[0, 0] @ kd.T * case.spec.softmax_scale).max() < 1e-3
+    assert math.isclose(case.spec.softmax_scale, 1 / math.sqrt(128))
