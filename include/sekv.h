@@ -1,0 +1,159 @@
+/*
+ * sekv.h -- C ABI of the SeKV decode-step library for AMD Instinct MI355X (gfx950).
+ *
+ * One decode step of SeKV (Abaskohi, Carenini, West, He: "SeKV: Resolution-Adaptive
+ * KV Cache with Hierarchical Semantic Memory for Long-Context LLM Inference"),
+ * for one attention layer, on one GPU:
+ *
+ *   1. routing: score every span of every sequence for every query head against the
+ *      span's coarse mean key (Sec. 3.2, eq. routing_gate, read with an identity
+ *      projection: score = scale * q.k_bar_S + ln|S|);
+ *   2. selection: per (sequence, KV head) keep the top_k spans in decreasing score
+ *      (Sec. 3.3, budget rule), the key of a span being the largest score over the
+ *      KV head's query heads; ties go to the lower span index;
+ *   3. zoom-in: rebuild the selected spans' keys and values from their low-rank
+ *      factors, K_hat = U diag(sigma) V^T (eq. key_reconstruction, gates folded into
+ *      sigma), in registers/LDS only -- reconstructed tokens never reach HBM;
+ *   4. one softmax over the mixed-resolution memory (Sec. 3.3): anchor tokens at full
+ *      resolution, one coarse entry (k_bar, v_bar, score + ln|S|) per unselected span,
+ *      and the reconstructed tokens of the selected spans.
+ *
+ * Conventions
+ *   - Every pointer in sekv_cache, and every sel/logits/out/workspace pointer, is a
+ *     DEVICE pointer owned by the caller, 16-byte aligned (the tier entry point is
+ *     the documented exception for the factor arena).  The library allocates nothing
+ *     on these calls.
+ *   - Calls enqueue work on the caller's stream and return; results are valid in
+ *     stream order.  Calls never synchronise the device unless documented.
+ *   - Errors found on the host (null or misaligned pointers, unsupported sizes, a small
+ *     workspace) are returned before anything is enqueued.  HIP launch failures return
+ *     SEKV_ERR_HIP.  sekv_last_error() gives a thread-local message for the last failure.
+ *   - Device-side tables must satisfy n_anchors[b] <= max_anchors, n_spans[b] <=
+ *     max_spans, 1 <= span_len <= max_span_len, every block inside the factor arena.
+ *     The kernels clamp counts and skip out-of-arena blocks (flagging the workspace
+ *     error word), so a bad table gives a wrong answer, never an out-of-bounds access.
+ *   - Results are bitwise deterministic: fixed reduction order, no floating-point atomics.
+ *   - Concurrent calls must use distinct workspaces.
+ */
+#ifndef SEKV_H
+#define SEKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SEKV_API __attribute__((visibility("default")))
+
+typedef enum {
+    SEKV_OK = 0,
+    SEKV_ERR_INVALID_ARG = 1,   /* null/misaligned pointer, inconsistent sizes      */
+    SEKV_ERR_UNSUPPORTED = 2,   /* head_dim, rank, group size or top_k not supported */
+    SEKV_ERR_WORKSPACE = 3,     /* workspace too small or not initialised            */
+    SEKV_ERR_HIP = 4            /* a HIP runtime call failed; see sekv_last_error()  */
+} sekv_status;
+
+typedef enum { SEKV_F32 = 0, SEKV_BF16 = 1 } sekv_dtype;
+
+/* Implementation choice for the zoomed spans (sekv_dims.flags bits 0..1). */
+#define SEKV_ZOOM_DEFAULT 0     /* library default (currently FACTORED)                     */
+#define SEKV_ZOOM_FACTORED 1    /* q.K_hat = U (sigma * (V^T q)), sum p V_hat = ((p^T U) sigma) V^T */
+
+/* Shapes and types of one layer's decode step.  Validated on the host before any launch. */
+typedef struct {
+    int32_t batch;          /* B >= 0 sequences                                          */
+    int32_t n_q_heads;      /* Hq; query head h reads KV head h / (Hq / Hkv)             */
+    int32_t n_kv_heads;     /* Hkv; Hq / Hkv in {1, 2, 4, 8}                             */
+    int32_t head_dim;       /* d in {64, 128}                                            */
+    int32_t rank;           /* r: factor rank, multiple of 8, 8 <= r <= 64               */
+    int32_t top_k;          /* k: spans expanded per (sequence, KV head), 0 <= k <= 64   */
+    int32_t max_anchors;    /* A_max >= 0: row stride of the anchor arrays               */
+    int32_t max_spans;      /* M_max >= 1: row stride of the span arrays                 */
+    int32_t max_span_len;   /* L_max >= 1: longest span                                  */
+    int32_t dtype;          /* sekv_dtype of q, anchors, summaries and factors           */
+    int32_t out_dtype;      /* sekv_dtype of out (F32 is allowed for BF16 storage)       */
+    int32_t flags;          /* bits 0..1: SEKV_ZOOM_*; other bits must be zero           */
+    double softmax_scale;   /* multiplies q.k everywhere, including the routing score    */
+} sekv_dims;
+
+/* The stored cache of one layer.  All device pointers, caller-owned.
+ *   q            [B][Hq][d]
+ *   anchor_k/v   [B][Hkv][A_max][d]       rows >= n_anchors[b] are ignored
+ *   n_anchors    int32 [B]                full-resolution tokens (anchors + local window)
+ *   sum_k/sum_v  [B][Hkv][M_max][d]       coarse mean key/value of each span
+ *   n_spans      int32 [B]
+ *   span_len     int32 [B][M_max]         |S| of span S of sequence b
+ *   span_logsize double [B][M_max]        ln|S|, computed once by the caller
+ *   factors      byte arena of span blocks, factors_bytes long
+ *   block_off    int64 [B][Hkv][M_max]    byte offset of block (b, g, S); multiple of 16
+ * A span block holds, in the storage dtype and in this order,
+ *   U_K[|S|][r] | sigma_K[r] | Vt_K[r][d] | U_V[|S|][r] | sigma_V[r] | Vt_V[r][d]
+ * i.e. the per-span factors of Sec. 3.2 (U, Sigma, V^T for keys, then for values). */
+typedef struct {
+    const void *q;
+    const void *anchor_k;
+    const void *anchor_v;
+    const int32_t *n_anchors;
+    const void *sum_k;
+    const void *sum_v;
+    const int32_t *n_spans;
+    const int32_t *span_len;
+    const double *span_logsize;
+    const void *factors;
+    int64_t factors_bytes;
+    const int64_t *block_off;
+} sekv_cache;
+
+/* Human-readable name of a status code (static storage). */
+SEKV_API const char *sekv_status_string(sekv_status status);
+
+/* Thread-local message describing the last failing call on this thread ("" if none). */
+SEKV_API const char *sekv_last_error(void);
+
+/* Host-only validation of a sekv_dims; SEKV_OK if every library call accepts it. */
+SEKV_API sekv_status sekv_check_dims(const sekv_dims *dims);
+
+/* Bytes of device workspace the calls below need for these dims (0 if dims are invalid). */
+SEKV_API size_t sekv_workspace_size(const sekv_dims *dims);
+
+/* Zero a workspace on `stream`.  Required once before the first call that uses it; every
+ * call leaves its counters zeroed again on completion.  ws: device, 256-byte aligned. */
+SEKV_API sekv_status sekv_workspace_init(void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Read and clear the workspace's device error word (synchronises `stream`).  Bits:
+ * 1 = a wait for a selection timed out, 2 = a factor block lay outside the arena,
+ * 4 = a selected index was out of range.  0 after every correct call. */
+SEKV_API sekv_status sekv_workspace_status(void *ws, size_t ws_bytes, hipStream_t stream,
+                                  int32_t *error_bits);
+
+/* Steps 1-2 (routing and selection; Sec. 3.2 eq. routing_gate, Sec. 3.3 budget rule).
+ *   sel    out, int32 [B][Hkv][top_k]: spans in decreasing key order, -1 past n_spans[b]
+ *   logits out, float [B][Hq][M_max] or NULL: the routing scores (score, not sigmoid);
+ *          entries past n_spans[b] are -inf.
+ * Reads q, sum_k, n_spans, span_logsize. */
+SEKV_API sekv_status sekv_route_topk(const sekv_dims *dims, const sekv_cache *cache, int32_t *sel,
+                            float *logits, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Steps 3-4 for a given selection (Sec. 3.3, mixed-resolution attention).
+ *   sel    in, int32 [B][Hkv][top_k] as produced by sekv_route_topk (-1 = empty slot)
+ *   logits in, float [B][Hq][M_max] routing scores, or NULL to recompute them from sum_k
+ *   out    out, [B][Hq][d] in out_dtype */
+SEKV_API sekv_status sekv_zoom_attend(const sekv_dims *dims, const sekv_cache *cache, const int32_t *sel,
+                             const float *logits, void *out, void *ws, size_t ws_bytes,
+                             hipStream_t stream);
+
+/* Steps 1-4 fused into one launch: sel and out as above; the routing scores stay in the
+ * workspace.  Summary rows are read once (keys for routing, values for the coarse
+ * entries in the same pass). */
+SEKV_API sekv_status sekv_decode_step(const sekv_dims *dims, const sekv_cache *cache, int32_t *sel,
+                             void *out, void *ws, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SEKV_H */

@@ -1,0 +1,276 @@
+// C ABI of the SeKV decode-step library: host-side validation, workspace layout and
+// launch set-up.  Every check that can be made on the host is made here, before
+// anything is enqueued; the kernels clamp device-side table values on their own.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+
+#include "sekv.h"
+#include "sekv_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+sekv_status fail(sekv_status st, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+sekv_status hip_fail(hipError_t e, const char *what) {
+    return fail(SEKV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+sekv_status check_dims_impl(const sekv_dims *d) {
+    if (!d) return fail(SEKV_ERR_INVALID_ARG, "dims is NULL");
+    if (d->batch < 0) return fail(SEKV_ERR_INVALID_ARG, "batch < 0");
+    if (d->n_q_heads <= 0 || d->n_kv_heads <= 0)
+        return fail(SEKV_ERR_INVALID_ARG, "head counts must be positive");
+    if (d->n_q_heads % d->n_kv_heads)
+        return fail(SEKV_ERR_INVALID_ARG, "n_q_heads %% n_kv_heads != 0");
+    const int G = d->n_q_heads / d->n_kv_heads;
+    if (G != 1 && G != 2 && G != 4 && G != 8)
+        return fail(SEKV_ERR_UNSUPPORTED, "group size %d not in {1,2,4,8}", G);
+    if (d->head_dim != 64 && d->head_dim != 128)
+        return fail(SEKV_ERR_UNSUPPORTED, "head_dim %d not in {64,128}", d->head_dim);
+    if (d->rank < 8 || d->rank > 64 || d->rank % 8)
+        return fail(SEKV_ERR_UNSUPPORTED, "rank %d: need a multiple of 8 in [8,64]", d->rank);
+    if (d->top_k < 0 || d->top_k > sekv::kMaxTopK)
+        return fail(SEKV_ERR_UNSUPPORTED, "top_k %d not in [0,%d]", d->top_k, sekv::kMaxTopK);
+    if (d->max_anchors < 0) return fail(SEKV_ERR_INVALID_ARG, "max_anchors < 0");
+    if (d->max_spans < 1) return fail(SEKV_ERR_INVALID_ARG, "max_spans < 1");
+    if (d->max_span_len < 1) return fail(SEKV_ERR_INVALID_ARG, "max_span_len < 1");
+    if (d->dtype != SEKV_F32 && d->dtype != SEKV_BF16)
+        return fail(SEKV_ERR_UNSUPPORTED, "dtype %d", d->dtype);
+    if (d->out_dtype != SEKV_F32 && d->out_dtype != SEKV_BF16)
+        return fail(SEKV_ERR_UNSUPPORTED, "out_dtype %d", d->out_dtype);
+    if (d->dtype == SEKV_F32 && d->out_dtype != SEKV_F32)
+        return fail(SEKV_ERR_UNSUPPORTED, "float32 storage needs float32 output");
+    const int zoom = d->flags & 3;
+    if ((d->flags & ~3) || zoom > SEKV_ZOOM_FACTORED)
+        return fail(SEKV_ERR_UNSUPPORTED, "flags 0x%x", unsigned(d->flags));
+    if (!(d->softmax_scale > 0.0) || !std::isfinite(d->softmax_scale))
+        return fail(SEKV_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
+    const sekv::Shape s = sekv::make_shape(*d);
+    if (s.n_slots > sekv::kMergeBuf)
+        return fail(SEKV_ERR_UNSUPPORTED, "too many partials per pair (%d > %d): max_spans or "
+                    "max_anchors too large", s.n_slots, sekv::kMergeBuf);
+    const long long rows = (long long)s.B * s.Hkv * std::max(s.M_max, s.A_max);
+    if (rows > (1ll << 31)) return fail(SEKV_ERR_UNSUPPORTED, "tables too large");
+    return SEKV_OK;
+}
+
+sekv_status check_cache(const sekv_dims *d, const sekv_cache *c, bool need_factors) {
+    if (!c) return fail(SEKV_ERR_INVALID_ARG, "cache is NULL");
+    if (d->batch == 0) return SEKV_OK;
+    struct { const void *p; const char *name; } ptrs[] = {
+        {c->q, "q"}, {c->sum_k, "sum_k"}, {c->sum_v, "sum_v"}, {c->n_spans, "n_spans"},
+        {c->span_len, "span_len"}, {c->span_logsize, "span_logsize"},
+        {c->n_anchors, "n_anchors"}};
+    for (auto &x : ptrs) {
+        if (!x.p) return fail(SEKV_ERR_INVALID_ARG, "cache.%s is NULL", x.name);
+        if (!aligned16(x.p)) return fail(SEKV_ERR_INVALID_ARG, "cache.%s not 16-byte aligned", x.name);
+    }
+    if (d->max_anchors > 0) {
+        if (!c->anchor_k || !c->anchor_v)
+            return fail(SEKV_ERR_INVALID_ARG, "cache.anchor_k/anchor_v is NULL");
+        if (!aligned16(c->anchor_k) || !aligned16(c->anchor_v))
+            return fail(SEKV_ERR_INVALID_ARG, "anchor arrays not 16-byte aligned");
+    }
+    if (need_factors && d->top_k > 0) {
+        if (!c->factors || !c->block_off)
+            return fail(SEKV_ERR_INVALID_ARG, "cache.factors/block_off is NULL");
+        if (!aligned16(c->factors) || !aligned16(c->block_off))
+            return fail(SEKV_ERR_INVALID_ARG, "factor arena or offsets not 16-byte aligned");
+        if (c->factors_bytes <= 0) return fail(SEKV_ERR_INVALID_ARG, "factors_bytes <= 0");
+    }
+    return SEKV_OK;
+}
+
+sekv_status check_ws(const sekv_dims *d, void *ws, size_t ws_bytes) {
+    const size_t need = sekv_workspace_size(d);
+    if (!ws) return fail(SEKV_ERR_WORKSPACE, "workspace is NULL");
+    if (reinterpret_cast<uintptr_t>(ws) & 255u)
+        return fail(SEKV_ERR_WORKSPACE, "workspace not 256-byte aligned");
+    if (ws_bytes < need)
+        return fail(SEKV_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    return SEKV_OK;
+}
+
+// Per-device cache of the resident-workgroup count of each kernel instantiation.
+struct OccKey { int dev, dtype, d, g; };
+std::mutex g_occ_mu;
+struct OccEntry { OccKey k; int n; };
+OccEntry g_occ[64];
+int g_occ_n = 0;
+
+int resident(int dtype, int head_dim, int group) {
+    int dev = 0;
+    (void)hipGetDevice(&dev);
+    std::lock_guard<std::mutex> lk(g_occ_mu);
+    for (int i = 0; i < g_occ_n; ++i) {
+        const OccKey &k = g_occ[i].k;
+        if (k.dev == dev && k.dtype == dtype && k.d == head_dim && k.g == group) return g_occ[i].n;
+    }
+    const int n = sekv::resident_workgroups(dtype, head_dim, group);
+    if (g_occ_n < 64) g_occ[g_occ_n++] = {{dev, dtype, head_dim, group}, n};
+    return n;
+}
+
+sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_out,
+                float *logits_out, const int32_t *sel_in, const float *logits_in, void *out,
+                void *ws, size_t ws_bytes, hipStream_t stream) {
+    sekv_status st = check_dims_impl(d);
+    if (st != SEKV_OK) return st;
+    st = check_cache(d, c, mode != sekv::kModeRoute);
+    if (st != SEKV_OK) return st;
+    st = check_ws(d, ws, ws_bytes);
+    if (st != SEKV_OK) return st;
+    if (d->batch == 0) return SEKV_OK;
+    if (mode != sekv::kModeAttend && d->top_k > 0 && !sel_out)
+        return fail(SEKV_ERR_INVALID_ARG, "sel is NULL");
+    if (mode == sekv::kModeAttend && d->top_k > 0 && !sel_in)
+        return fail(SEKV_ERR_INVALID_ARG, "sel is NULL");
+    if (mode != sekv::kModeRoute && !out) return fail(SEKV_ERR_INVALID_ARG, "out is NULL");
+    if ((sel_out && !aligned16(sel_out)) || (sel_in && !aligned16(sel_in)) ||
+        (out && !aligned16(out)) || (logits_out && !aligned16(logits_out)) ||
+        (logits_in && !aligned16(logits_in)))
+        return fail(SEKV_ERR_INVALID_ARG, "sel/logits/out not 16-byte aligned");
+
+    const sekv::Shape s = sekv::make_shape(*d);
+    const sekv::WsLayout L = sekv::make_layout(s);
+    unsigned char *w = static_cast<unsigned char *>(ws);
+
+    sekv::Params p{};
+    p.mode = mode;
+    p.B = s.B; p.Hq = s.Hq; p.Hkv = s.Hkv; p.r = s.r; p.k = s.k;
+    p.A_max = s.A_max; p.M_max = s.M_max;
+    p.n_rc = s.n_rc; p.n_ac = s.n_ac; p.kc = s.kc; p.n_slots = s.n_slots;
+    p.slot_route0 = s.n_ac;
+    p.slot_losers = s.n_ac + s.n_rc;
+    p.slot_zoom0 = s.n_ac + s.n_rc + 1;
+    const int n_route = s.P * s.n_rc;
+    const int n_anchor = (mode == sekv::kModeRoute) ? 0 : s.P * s.n_ac;
+    const int n_zoom = (mode == sekv::kModeRoute) ? 0 : s.P * s.k;
+    p.end_route = n_route;
+    p.end_anchor = n_route + n_anchor;
+    p.end_zoom = n_route + n_anchor + n_zoom;
+    p.out_f32 = d->out_dtype == SEKV_F32;
+    p.zoom_impl = (d->flags & 3) == SEKV_ZOOM_DEFAULT ? SEKV_ZOOM_FACTORED : (d->flags & 3);
+    p.scale = d->softmax_scale;
+    p.scale_log2 = float(d->softmax_scale * 1.4426950408889634074);
+    p.q = c->q; p.anchor_k = c->anchor_k; p.anchor_v = c->anchor_v; p.n_anchors = c->n_anchors;
+    p.sum_k = c->sum_k; p.sum_v = c->sum_v; p.n_spans = c->n_spans; p.span_len = c->span_len;
+    p.span_logsize = c->span_logsize;
+    p.factors = static_cast<const unsigned char *>(c->factors);
+    p.factors_bytes = c->factors_bytes;
+    p.block_off = c->block_off;
+    p.sel_out = sel_out; p.logits_out = logits_out; p.sel_in = sel_in; p.logits_in = logits_in;
+    p.out = out;
+    p.hdr = reinterpret_cast<sekv::WsHeader *>(w);
+    p.route_cnt = reinterpret_cast<uint32_t *>(w + L.route_cnt);
+    p.sel_ready = reinterpret_cast<uint32_t *>(w + L.sel_ready);
+    p.part_cnt = reinterpret_cast<uint32_t *>(w + L.part_cnt);
+    p.sel_ws = reinterpret_cast<int32_t *>(w + L.sel);
+    p.cand_key = reinterpret_cast<uint64_t *>(w + L.cand_key);
+    p.cand_idx = reinterpret_cast<int32_t *>(w + L.cand_idx);
+    p.cand_cnt = reinterpret_cast<int32_t *>(w + L.cand_cnt);
+    p.cand_lg = reinterpret_cast<float *>(w + L.cand_lg);
+    p.part_ml = reinterpret_cast<float *>(w + L.part_ml);
+    p.part_o = reinterpret_cast<float *>(w + L.part_o);
+
+    const int cap = resident(d->dtype, d->head_dim, s.G);
+    p.grid = std::max(1, std::min(p.end_zoom, cap));
+    if (p.end_zoom == 0) return SEKV_OK;
+    const hipError_t e = sekv::launch_step(p, d->dtype, d->head_dim, s.G, stream);
+    if (e != hipSuccess) return hip_fail(e, "kernel launch");
+    return SEKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *sekv_status_string(sekv_status status) {
+    switch (status) {
+        case SEKV_OK: return "SEKV_OK";
+        case SEKV_ERR_INVALID_ARG: return "SEKV_ERR_INVALID_ARG";
+        case SEKV_ERR_UNSUPPORTED: return "SEKV_ERR_UNSUPPORTED";
+        case SEKV_ERR_WORKSPACE: return "SEKV_ERR_WORKSPACE";
+        case SEKV_ERR_HIP: return "SEKV_ERR_HIP";
+    }
+    return "SEKV_ERR_UNKNOWN";
+}
+
+const char *sekv_last_error(void) { return g_err; }
+
+sekv_status sekv_check_dims(const sekv_dims *dims) { return check_dims_impl(dims); }
+
+size_t sekv_workspace_size(const sekv_dims *dims) {
+    char saved[sizeof(g_err)];
+    std::memcpy(saved, g_err, sizeof(g_err));
+    const sekv_status st = check_dims_impl(dims);
+    std::memcpy(g_err, saved, sizeof(g_err));
+    if (st != SEKV_OK) return 0;
+    return sekv::make_layout(sekv::make_shape(*dims)).total;
+}
+
+sekv_status sekv_workspace_init(void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (!ws) return fail(SEKV_ERR_WORKSPACE, "workspace is NULL");
+    if (reinterpret_cast<uintptr_t>(ws) & 255u)
+        return fail(SEKV_ERR_WORKSPACE, "workspace not 256-byte aligned");
+    if (ws_bytes % 16) return fail(SEKV_ERR_WORKSPACE, "workspace size not a multiple of 16");
+    const hipError_t e = sekv::launch_zero(ws, ws_bytes, stream);
+    if (e != hipSuccess) return hip_fail(e, "workspace zero kernel");
+    return SEKV_OK;
+}
+
+sekv_status sekv_workspace_status(void *ws, size_t ws_bytes, hipStream_t stream,
+                                  int32_t *error_bits) {
+    if (!ws || !error_bits) return fail(SEKV_ERR_INVALID_ARG, "NULL argument");
+    if (ws_bytes < sizeof(sekv::WsHeader)) return fail(SEKV_ERR_WORKSPACE, "workspace too small");
+    sekv::WsHeader *h = static_cast<sekv::WsHeader *>(ws);
+    int32_t v = 0;
+    hipError_t e = hipMemcpyAsync(&v, &h->error, sizeof(v), hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(e, "reading the workspace error word");
+    *error_bits = v;
+    if (v) {
+        const int32_t zero = 0;
+        e = hipMemcpyAsync(&h->error, &zero, sizeof(zero), hipMemcpyHostToDevice, stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);
+        if (e != hipSuccess) return hip_fail(e, "clearing the workspace error word");
+    }
+    return SEKV_OK;
+}
+
+sekv_status sekv_route_topk(const sekv_dims *dims, const sekv_cache *cache, int32_t *sel,
+                            float *logits, void *ws, size_t ws_bytes, hipStream_t stream) {
+    return run(sekv::kModeRoute, dims, cache, sel, logits, nullptr, nullptr, nullptr, ws,
+               ws_bytes, stream);
+}
+
+sekv_status sekv_zoom_attend(const sekv_dims *dims, const sekv_cache *cache, const int32_t *sel,
+                             const float *logits, void *out, void *ws, size_t ws_bytes,
+                             hipStream_t stream) {
+    return run(sekv::kModeAttend, dims, cache, nullptr, nullptr, sel, logits, out, ws, ws_bytes,
+               stream);
+}
+
+sekv_status sekv_decode_step(const sekv_dims *dims, const sekv_cache *cache, int32_t *sel,
+                             void *out, void *ws, size_t ws_bytes, hipStream_t stream) {
+    return run(sekv::kModeFused, dims, cache, sel, nullptr, nullptr, nullptr, out, ws, ws_bytes,
+               stream);
+}
+
+}  // extern "C"

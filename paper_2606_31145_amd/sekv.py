@@ -1,0 +1,248 @@
+"""ctypes binding of libsekv.so (the C ABI declared in include/sekv.h).
+
+Argument marshalling only: torch allocates device memory and provides the stream;
+every step of the decode path runs in the library's HIP kernels.  Importing this
+module loads the library and raises if it has not been built.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsekv.so")
+
+SEKV_OK, SEKV_ERR_INVALID_ARG, SEKV_ERR_UNSUPPORTED, SEKV_ERR_WORKSPACE, SEKV_ERR_HIP = range(5)
+SEKV_F32, SEKV_BF16 = 0, 1
+SEKV_ZOOM_DEFAULT, SEKV_ZOOM_FACTORED = 0, 1
+DTYPE_CODES = {"f32": SEKV_F32, "bf16": SEKV_BF16}
+
+EXPORTED = ("sekv_status_string", "sekv_last_error", "sekv_check_dims", "sekv_workspace_size",
+            "sekv_workspace_init", "sekv_workspace_status", "sekv_route_topk",
+            "sekv_zoom_attend", "sekv_decode_step")
+
+
+class SekvError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_status_name(status)}: {message}")
+        self.status = status
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("rank", ctypes.c_int32), ("top_k", ctypes.c_int32),
+                ("max_anchors", ctypes.c_int32), ("max_spans", ctypes.c_int32),
+                ("max_span_len", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("out_dtype", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_double)]
+
+
+class CacheStruct(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("anchor_k", ctypes.c_void_p),
+                ("anchor_v", ctypes.c_void_p), ("n_anchors", ctypes.c_void_p),
+                ("sum_k", ctypes.c_void_p), ("sum_v", ctypes.c_void_p),
+                ("n_spans", ctypes.c_void_p), ("span_len", ctypes.c_void_p),
+                ("span_logsize", ctypes.c_void_p), ("factors", ctypes.c_void_p),
+                ("factors_bytes", ctypes.c_int64), ("block_off", ctypes.c_void_p)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, VP, SZ, I32P = ctypes.POINTER, ctypes.c_void_p, ctypes.c_size_t, ctypes.POINTER(ctypes.c_int32)
+    lib.sekv_status_string.restype = ctypes.c_char_p
+    lib.sekv_status_string.argtypes = [ctypes.c_int]
+    lib.sekv_last_error.restype = ctypes.c_char_p
+    lib.sekv_last_error.argtypes = []
+    lib.sekv_check_dims.restype = ctypes.c_int
+    lib.sekv_check_dims.argtypes = [P(Dims)]
+    lib.sekv_workspace_size.restype = SZ
+    lib.sekv_workspace_size.argtypes = [P(Dims)]
+    lib.sekv_workspace_init.restype = ctypes.c_int
+    lib.sekv_workspace_init.argtypes = [VP, SZ, VP]
+    lib.sekv_workspace_status.restype = ctypes.c_int
+    lib.sekv_workspace_status.argtypes = [VP, SZ, VP, I32P]
+    lib.sekv_route_topk.restype = ctypes.c_int
+    lib.sekv_route_topk.argtypes = [P(Dims), P(CacheStruct), VP, VP, VP, SZ, VP]
+    lib.sekv_zoom_attend.restype = ctypes.c_int
+    lib.sekv_zoom_attend.argtypes = [P(Dims), P(CacheStruct), VP, VP, VP, VP, SZ, VP]
+    lib.sekv_decode_step.restype = ctypes.c_int
+    lib.sekv_decode_step.argtypes = [P(Dims), P(CacheStruct), VP, VP, VP, SZ, VP]
+    return lib
+
+
+LIB = _load()
+
+
+def _status_name(status: int) -> str:
+    try:
+        return LIB.sekv_status_string(int(status)).decode()
+    except Exception:
+        return f"status {status}"
+
+
+def _check(status: int):
+    if status != SEKV_OK:
+        raise SekvError(status, LIB.sekv_last_error().decode())
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("expected a torch tensor")
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to the library must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def make_dims(*, batch, n_q_heads, n_kv_heads, head_dim, rank, top_k, max_anchors, max_spans,
+              max_span_len, dtype, softmax_scale, out_dtype=None, zoom=SEKV_ZOOM_DEFAULT) -> Dims:
+    dt = DTYPE_CODES[dtype] if isinstance(dtype, str) else int(dtype)
+    if out_dtype is None:
+        odt = dt
+    else:
+        odt = DTYPE_CODES[out_dtype] if isinstance(out_dtype, str) else int(out_dtype)
+    return Dims(batch, n_q_heads, n_kv_heads, head_dim, rank, top_k, max_anchors, max_spans,
+                max_span_len, dt, odt, int(zoom), float(softmax_scale))
+
+
+def check_dims(dims: Dims):
+    _check(LIB.sekv_check_dims(ctypes.byref(dims)))
+
+
+def workspace_size(dims: Dims) -> int:
+    return int(LIB.sekv_workspace_size(ctypes.byref(dims)))
+
+
+class Workspace:
+    """A zero-initialised device workspace for a dims (256-byte aligned view of a torch buffer)."""
+
+    def __init__(self, dims: Dims, device="cuda", stream=None, nbytes: int | None = None):
+        need = workspace_size(dims) if nbytes is None else int(nbytes)
+        if need == 0:
+            check_dims(dims)
+        need = (need + 15) // 16 * 16
+        self._buf = torch.empty(need + 256, dtype=torch.uint8, device=device)
+        off = (-self._buf.data_ptr()) % 256
+        self.tensor = self._buf[off:off + need]
+        self.nbytes = need
+        _check(LIB.sekv_workspace_init(self.tensor.data_ptr(), need, _stream(stream)))
+
+    @property
+    def ptr(self) -> int:
+        return self.tensor.data_ptr()
+
+    def status(self, stream=None) -> int:
+        bits = ctypes.c_int32(0)
+        _check(LIB.sekv_workspace_status(self.ptr, self.nbytes, _stream(stream), ctypes.byref(bits)))
+        return int(bits.value)
+
+
+_TORCH_STORAGE = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def _to_device(arr: np.ndarray, dtype: str | None, device) -> torch.Tensor:
+    a = np.ascontiguousarray(arr)
+    if dtype == "bf16":
+        t = torch.from_numpy(a.view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(a)
+    return t.to(device)
+
+
+class DeviceCache:
+    """Device tensors of one layer's stored cache, laid out as sekv_cache describes."""
+
+    FIELDS = ("q", "anchor_k", "anchor_v", "n_anchors", "sum_k", "sum_v", "n_spans", "span_len",
+              "span_logsize", "factors", "block_off")
+
+    def __init__(self, tensors: dict, dtype: str):
+        missing = [f for f in self.FIELDS if f not in tensors]
+        if missing:
+            raise ValueError(f"missing cache fields: {missing}")
+        self.t = dict(tensors)
+        self.dtype = dtype
+        self._struct = None
+
+    @classmethod
+    def from_arrays(cls, arrays: dict, dtype: str, device="cuda", factors_device=None):
+        """Upload numpy arrays (storage-typed; bf16 as uint16 bit patterns)."""
+        t = {}
+        for f in ("q", "anchor_k", "anchor_v", "sum_k", "sum_v"):
+            t[f] = _to_device(arrays[f], dtype, device)
+        for f in ("n_anchors", "n_spans", "span_len"):
+            t[f] = torch.from_numpy(np.ascontiguousarray(arrays[f], dtype=np.int32)).to(device)
+        t["span_logsize"] = torch.from_numpy(np.ascontiguousarray(arrays["span_logsize"],
+                                                                  dtype=np.float64)).to(device)
+        t["block_off"] = torch.from_numpy(np.ascontiguousarray(arrays["block_off"],
+                                                               dtype=np.int64)).to(device)
+        t["factors"] = torch.from_numpy(np.ascontiguousarray(arrays["factors"],
+                                                             dtype=np.uint8)).to(
+            factors_device or device)
+        return cls(t, dtype)
+
+    def struct(self) -> CacheStruct:
+        t = self.t
+        return CacheStruct(_ptr(t["q"]), _ptr(t["anchor_k"]), _ptr(t["anchor_v"]),
+                           _ptr(t["n_anchors"]), _ptr(t["sum_k"]), _ptr(t["sum_v"]),
+                           _ptr(t["n_spans"]), _ptr(t["span_len"]), _ptr(t["span_logsize"]),
+                           _ptr(t["factors"]), int(t["factors"].numel()), _ptr(t["block_off"]))
+
+
+def _alloc(shape, dtype, device):
+    return torch.empty(shape, dtype=dtype, device=device)
+
+
+def route_topk(dims: Dims, cache: DeviceCache, ws: Workspace, sel=None, logits=None,
+               want_logits: bool = True, stream=None):
+    """sekv_route_topk: returns (sel int32 [B][Hkv][k], logits float [B][Hq][M_max] or None)."""
+    dev = cache.t["q"].device
+    if sel is None:
+        sel = _alloc((dims.batch, dims.n_kv_heads, max(dims.top_k, 0)), torch.int32, dev)
+    if logits is None and want_logits:
+        logits = _alloc((dims.batch, dims.n_q_heads, dims.max_spans), torch.float32, dev)
+    cs = cache.struct()
+    _check(LIB.sekv_route_topk(ctypes.byref(dims), ctypes.byref(cs), _ptr(sel), _ptr(logits),
+                               ws.ptr, ws.nbytes, _stream(stream)))
+    return sel, logits
+
+
+def _out_tensor(dims: Dims, dev):
+    dt = torch.float32 if dims.out_dtype == SEKV_F32 else torch.bfloat16
+    return _alloc((dims.batch, dims.n_q_heads, dims.head_dim), dt, dev)
+
+
+def zoom_attend(dims: Dims, cache: DeviceCache, sel, logits, ws: Workspace, out=None, stream=None):
+    """sekv_zoom_attend: returns out [B][Hq][d] in out_dtype."""
+    if out is None:
+        out = _out_tensor(dims, cache.t["q"].device)
+    cs = cache.struct()
+    _check(LIB.sekv_zoom_attend(ctypes.byref(dims), ctypes.byref(cs), _ptr(sel), _ptr(logits),
+                                _ptr(out), ws.ptr, ws.nbytes, _stream(stream)))
+    return out
+
+
+def decode_step(dims: Dims, cache: DeviceCache, ws: Workspace, sel=None, out=None, stream=None):
+    """sekv_decode_step: returns (sel, out)."""
+    dev = cache.t["q"].device
+    if sel is None:
+        sel = _alloc((dims.batch, dims.n_kv_heads, max(dims.top_k, 0)), torch.int32, dev)
+    if out is None:
+        out = _out_tensor(dims, dev)
+    cs = cache.struct()
+    _check(LIB.sekv_decode_step(ctypes.byref(dims), ctypes.byref(cs), _ptr(sel), _ptr(out),
+                                ws.ptr, ws.nbytes, _stream(stream)))
+    return sel, out

@@ -1,0 +1,102 @@
+"""The C-ABI library on the CPU: it loads, exports every declared symbol, and rejects
+bad arguments on the host before touching the GPU."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sekv.h")
+LIB = os.path.join(ROOT, "paper_2606_31145_amd", "libsekv.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"SEKV_API\s+[\w\s\*]*?\b(sekv_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def S():
+    if not os.path.exists(LIB):
+        from paper_2606_31145_amd.build import build
+        build()
+    from paper_2606_31145_amd import sekv
+    return sekv
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for fn in ("sekv_route_topk", "sekv_zoom_attend", "sekv_decode_step", "sekv_workspace_size"):
+        assert fn in names
+
+
+def test_library_exports_every_declared_symbol(S):
+    lib = ctypes.CDLL(LIB)
+    for fn in declared_functions():
+        assert hasattr(lib, fn), f"{fn} declared in sekv.h but not exported"
+    assert set(declared_functions()) == set(S.EXPORTED)
+
+
+def _dims(S, **kw):
+    base = dict(batch=1, n_q_heads=4, n_kv_heads=2, head_dim=64, rank=8, top_k=2, max_anchors=33,
+                max_spans=49, max_span_len=64, dtype="f32", softmax_scale=0.125)
+    base.update(kw)
+    return S.make_dims(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_q_heads=6, n_kv_heads=4), 1),          # Hq % Hkv
+    (dict(n_q_heads=12, n_kv_heads=4), 2),         # group 3
+    (dict(head_dim=96), 2),
+    (dict(rank=12), 2),
+    (dict(rank=72), 2),
+    (dict(top_k=65), 2),
+    (dict(max_spans=0), 1),
+    (dict(max_span_len=0), 1),
+    (dict(batch=-1), 1),
+    (dict(softmax_scale=0.0), 1),
+    (dict(dtype="f32", out_dtype="bf16"), 2),
+    (dict(max_spans=40000), 2),                    # too many partials per pair
+])
+def test_check_dims_rejects(S, kw, status):
+    d = _dims(S, **kw)
+    with pytest.raises(S.SekvError) as ei:
+        S.check_dims(d)
+    assert ei.value.status == status
+    assert S.workspace_size(d) == 0
+
+
+def test_check_dims_accepts_the_workload_shapes(S):
+    S.check_dims(_dims(S))
+    big = _dims(S, batch=4, n_q_heads=32, n_kv_heads=8, head_dim=128, rank=32, top_k=16,
+                max_anchors=800, max_spans=760, max_span_len=512, dtype="bf16",
+                softmax_scale=128 ** -0.5)
+    S.check_dims(big)
+    assert S.workspace_size(big) > 0
+
+
+def test_host_errors_before_any_launch(S):
+    """Null pointers and a short workspace are rejected without a HIP call."""
+    d = _dims(S)
+    cache = S.CacheStruct()              # all NULL
+    st = S.LIB.sekv_decode_step(ctypes.byref(d), ctypes.byref(cache), None, None, None, 0, None)
+    assert st == S.SEKV_ERR_INVALID_ARG
+    assert b"NULL" in S.LIB.sekv_last_error()
+    fake = ctypes.c_void_p(0x10000)      # aligned, never dereferenced on the host path below
+    c2 = S.CacheStruct(*([0x10000] * 10), 4096, 0x10000)
+    st = S.LIB.sekv_decode_step(ctypes.byref(d), ctypes.byref(c2), fake, fake, fake, 16, None)
+    assert st == S.SEKV_ERR_WORKSPACE
+    c3 = S.CacheStruct(0x10008, *([0x10000] * 9), 4096, 0x10000)
+    st = S.LIB.sekv_route_topk(ctypes.byref(d), ctypes.byref(c3), fake, None, fake, 1 << 20, None)
+    assert st == S.SEKV_ERR_INVALID_ARG and b"aligned" in S.LIB.sekv_last_error()
+    assert S.LIB.sekv_status_string(3) == b"SEKV_ERR_WORKSPACE"
+
+
+def test_empty_batch_is_a_no_op(S):
+    d = _dims(S, batch=0)
+    c = S.CacheStruct()
+    fake = ctypes.c_void_p(0x10000)
+    ws = S.workspace_size(d)
+    assert S.LIB.sekv_decode_step(ctypes.byref(d), ctypes.byref(c), None, None, fake, ws, None) == 0

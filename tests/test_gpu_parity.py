@@ -1,0 +1,177 @@
+"""GPU parity: every C-ABI entry point against the CPU oracle on the same seeded inputs.
+
+Selection must match bit for bit; outputs within max-abs 2e-2 (bf16 output) or 1e-4
+(float32 output), plus relative and cosine checks because the literal caches give
+tiny, near-uniform outputs.  Run on an MI355X with the library built in-tree.
+"""
+
+import numpy as np
+import pytest
+
+from synth import CONFIGS, custom_spec, make_case
+from synth.cases import Case
+from tests.gpu_common import (assert_out_close, banner, case_arrays, dims_for, min_boundary_gap,
+                              oracle_result, out_to_f64)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def S():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2606_31145_amd import sekv
+    return sekv
+
+
+def _ragged(case: Case) -> Case:
+    """Shrink some sequences: fewer spans, no spans, no anchors (tables only)."""
+    B = case.spec.batch
+    if B >= 2:
+        case.n_spans = case.n_spans.copy()
+        case.n_anchors = case.n_anchors.copy()
+        case.n_spans[1] = 0
+        if B >= 3:
+            case.n_anchors[2] = 0
+            case.n_spans[2] = max(1, int(case.n_spans[2]) // 3)
+        if B >= 4:
+            case.n_spans[3] = min(int(case.n_spans[3]), max(1, case.spec.top_k // 2))
+    return case
+
+
+def _custom(name, **kw):
+    variant = kw.pop("variant", "L")
+    ragged = kw.pop("ragged", False)
+    c = make_case(custom_spec(**kw), variant=variant)
+    if ragged:
+        c = _ragged(c)
+    return name, c
+
+
+def small_cases():
+    out = [("cfg1-L", make_case(CONFIGS[1], variant="L")),
+           ("cfg1-N", make_case(CONFIGS[1], variant="N")),
+           ("cfg2-L", make_case(CONFIGS[2], variant="L")),
+           ("cfg2-N", make_case(CONFIGS[2], variant="N"))]
+    out += [
+        _custom("g1-bf16-d128-r16", n_q_heads=4, n_kv_heads=4, head_dim=128, rank=16, top_k=3,
+                context=3000, dtype="bf16", seed=21, span_min=16, span_max=200),
+        _custom("g8-f32-d64-r64", n_q_heads=16, n_kv_heads=2, head_dim=64, rank=64, top_k=5,
+                context=5000, dtype="f32", seed=22, span_min=40, span_max=300, variant="N"),
+        _custom("g2-bf16-d64-r32-ragged", batch=4, n_q_heads=4, n_kv_heads=2, head_dim=64, rank=32,
+                top_k=6, context=4000, n_prefix_anchors=40, window=64, dtype="bf16", seed=23,
+                span_min=8, span_max=520, ragged=True, variant="N"),
+        _custom("g4-f32-d128-r8-k1", batch=2, n_q_heads=8, n_kv_heads=2, head_dim=128, rank=8,
+                top_k=1, context=2500, dtype="f32", seed=24, span_min=16, span_max=64),
+        _custom("k0-bf16", batch=2, n_q_heads=8, n_kv_heads=2, head_dim=128, rank=16, top_k=0,
+                context=2000, dtype="bf16", seed=25, span_min=32, span_max=128),
+        _custom("k-exceeds-spans", batch=2, n_q_heads=4, n_kv_heads=2, head_dim=64, rank=8,
+                top_k=64, context=600, n_prefix_anchors=0, window=0, dtype="f32", seed=26,
+                span_min=16, span_max=64),
+        _custom("long-spans-multiblock", batch=1, n_q_heads=8, n_kv_heads=2, head_dim=128,
+                rank=32, top_k=4, context=12000, dtype="bf16", seed=27, span_min=600,
+                span_max=1500, variant="N"),
+        _custom("many-spans-merge-rounds", batch=1, n_q_heads=4, n_kv_heads=1, head_dim=64,
+                rank=8, top_k=64, context=70000, dtype="bf16", seed=28, span_min=8, span_max=16),
+    ]
+    return out
+
+
+CASES = small_cases()
+
+
+@pytest.mark.parametrize("name,case", CASES, ids=[c[0] for c in CASES])
+def test_decode_step_matches_oracle(S, name, case):
+    import torch
+    banner(f"decode_step {name}")
+    ref = oracle_result(case)
+    dev = torch.device("cuda:0")
+    dc = S.DeviceCache.from_arrays(case_arrays(case), case.dtype, dev)
+    out_dtypes = [case.dtype] + (["f32"] if case.dtype == "bf16" else [])
+    for od in out_dtypes:
+        dims = dims_for(S, case, out_dtype=od)
+        ws = S.Workspace(dims, dev)
+        sel, out = S.decode_step(dims, dc, ws)
+        torch.cuda.synchronize()
+        assert ws.status() == 0
+        got_sel = sel.cpu().numpy()
+        if not np.array_equal(got_sel, ref["sel"]):
+            bad = np.argwhere(got_sel != ref["sel"])[:5]
+            raise AssertionError(f"{name}: selection differs at {bad.tolist()}; "
+                                 f"min boundary gap {min_boundary_gap(ref, case):.3e}")
+        assert_out_close(out_to_f64(out), ref["out"], od, where=f"{name} out={od}")
+        # bitwise determinism across launches (the workspace is reused as-is)
+        sel2, out2 = S.decode_step(dims, dc, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(sel, sel2) and torch.equal(out.view(torch.uint8) if out.dtype == torch.bfloat16
+                                                      else out, out2.view(torch.uint8)
+                                                      if out2.dtype == torch.bfloat16 else out2)
+        assert ws.status() == 0
+
+
+@pytest.mark.parametrize("name,case", CASES, ids=[c[0] for c in CASES])
+def test_route_then_attend_matches_oracle(S, name, case):
+    import torch
+    banner(f"route_topk + zoom_attend {name}")
+    ref = oracle_result(case)
+    dev = torch.device("cuda:0")
+    dc = S.DeviceCache.from_arrays(case_arrays(case), case.dtype, dev)
+    dims = dims_for(S, case)
+    ws = S.Workspace(dims, dev)
+    sel, logits = S.route_topk(dims, dc, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(sel.cpu().numpy(), ref["sel"]), f"{name}: route_topk selection differs"
+    lg = logits.cpu().numpy().astype(np.float64)
+    rl = ref["logits"]
+    fin = np.isfinite(rl)
+    assert np.array_equal(np.isfinite(lg), fin)
+    if fin.any():
+        assert np.max(np.abs(lg[fin] - rl[fin]) / np.maximum(np.abs(rl[fin]), 1e-30)) <= 2 ** -23
+    for given in (logits, None):
+        out = S.zoom_attend(dims, dc, sel, given, ws)
+        torch.cuda.synchronize()
+        assert_out_close(out_to_f64(out), ref["out"], case.dtype,
+                         where=f"{name} zoom_attend logits={'given' if given is not None else 'recomputed'}")
+    assert ws.status() == 0
+
+
+def test_workspace_reuse_across_shapes(S):
+    """One workspace serves calls of different sizes back to back (counters self-reset)."""
+    import torch
+    dev = torch.device("cuda:0")
+    big = make_case(custom_spec(batch=2, n_q_heads=8, n_kv_heads=2, head_dim=128, rank=16, top_k=4,
+                                context=6000, dtype="bf16", seed=31, span_min=32, span_max=256))
+    small = make_case(custom_spec(batch=1, n_q_heads=8, n_kv_heads=2, head_dim=128, rank=16,
+                                  top_k=2, context=1500, dtype="bf16", seed=32, span_min=32,
+                                  span_max=256))
+    dims_big = dims_for(S, big)
+    ws = S.Workspace(dims_big, dev)
+    for case in (big, small, big):
+        ref = oracle_result(case)
+        dc = S.DeviceCache.from_arrays(case_arrays(case), case.dtype, dev)
+        sel, out = S.decode_step(dims_for(S, case), dc, ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(sel.cpu().numpy(), ref["sel"])
+        assert_out_close(out_to_f64(out), ref["out"], case.dtype)
+    assert ws.status() == 0
+
+
+@pytest.mark.parametrize("variant", ["L", "N"])
+def test_config3_full_size(S, variant):
+    """The 128K-context, batch-4 layer at full size: every selection and every output row."""
+    import torch
+    banner(f"config 3 full size, variant {variant}: generating")
+    case = make_case(CONFIGS[3], variant=variant)
+    banner("config 3: oracle")
+    ref = oracle_result(case)
+    dev = torch.device("cuda:0")
+    dc = S.DeviceCache.from_arrays(case_arrays(case), case.dtype, dev)
+    dims = dims_for(S, case)
+    ws = S.Workspace(dims, dev)
+    banner("config 3: decode_step")
+    sel, out = S.decode_step(dims, dc, ws)
+    torch.cuda.synchronize()
+    assert ws.status() == 0
+    assert np.array_equal(sel.cpu().numpy(), ref["sel"]), \
+        f"selection differs; min boundary gap {min_boundary_gap(ref, case):.3e}"
+    assert_out_close(out_to_f64(out), ref["out"], "bf16", where=f"config 3 {variant}")
