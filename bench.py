@@ -1,0 +1,244 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused SeKV decode step on one MI355X.
+
+Workload: one attention layer of a Llama-3-8B-shaped model (32 query heads over 8 KV
+heads, head_dim 128) at 131,072 tokens of context, batch 4, rank-32 span factors,
+top-16 spans per KV head, bfloat16 storage, all factors device-resident.  A step is one
+call of sekv_decode_step (routing, selection, zoom-in, mixed-resolution attention).
+
+Inputs are synthetic and already resident in HBM when the timed region starts.  Steps
+rotate over several copies of the cache so that the 256 MB Infinity Cache cannot serve
+a step from the previous use of the same data (each step reads ~66 MB).
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "decode-step latency (µs) and achieved HBM GB/s, 128K context, batch 4"
+HBM_PEAK_GBS = 8000.0
+KERNEL_NAME = "sekv_step_kernel"
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_31145_amd", "csrc", "sekv_kernels.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(workload: str):
+    """HBM traffic per launch from a committed rocprofv3 counter summary, if it was taken
+    on the current kernel source; otherwise None."""
+    path = os.path.join(ROOT, "profiles", "sekv_step_kernel_counters.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except Exception:
+        return None
+    entry = rec.get(workload)
+    if not entry or entry.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return entry.get("hbm_bytes_per_launch")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--variant", choices=["L", "N"], default="L",
+                    help="L: literal synthetic values; N: planted needle spans")
+    ap.add_argument("--rotate", type=int, default=8, help="cache copies cycled through")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="approximate CPU time spent timing the oracle")
+    ap.add_argument("--calibration-copy-mib", type=int, default=0,
+                    help="also run one plain device copy of this size (counter calibration)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the decode step "
+              f"is not sharded across GPUs in this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2606_31145_amd import accounting
+    from paper_2606_31145_amd import sekv
+    from synth import CONFIGS, make_case
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    spec = CONFIGS[3]
+    log(f"[bench] generating the 128K x 4 cache (variant {args.variant})")
+    t0 = time.time()
+    case = make_case(spec, variant=args.variant)
+    log(f"[bench] generated in {time.time() - t0:.1f}s; factors {case.factors.nbytes / 1e6:.1f} MB")
+    arrays = dict(q=case.q, anchor_k=case.anchor_k, anchor_v=case.anchor_v,
+                  n_anchors=case.n_anchors, sum_k=case.sum_k, sum_v=case.sum_v,
+                  n_spans=case.n_spans, span_len=case.span_len, span_logsize=case.span_logsize,
+                  factors=case.factors, block_off=case.block_off)
+    base = sekv.DeviceCache.from_arrays(arrays, spec.dtype, dev)
+    caches = [base]
+    for _ in range(max(1, args.rotate) - 1):
+        caches.append(sekv.DeviceCache({k: v.clone() for k, v in base.t.items()}, spec.dtype))
+    dims = sekv.make_dims(batch=spec.batch, n_q_heads=spec.n_q_heads, n_kv_heads=spec.n_kv_heads,
+                          head_dim=spec.head_dim, rank=spec.rank, top_k=spec.top_k,
+                          max_anchors=case.max_anchors, max_spans=case.max_spans,
+                          max_span_len=case.max_span_len, dtype=spec.dtype,
+                          softmax_scale=spec.softmax_scale)
+    ws = sekv.Workspace(dims, dev)
+    B, Hq, Hkv, d = spec.batch, spec.n_q_heads, spec.n_kv_heads, spec.head_dim
+    sels = [torch.empty((B, Hkv, spec.top_k), dtype=torch.int32, device=dev) for _ in caches]
+    outs = [torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev) for _ in caches]
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        j = i % len(caches)
+        sekv.decode_step(dims, caches[j], ws, sel=sels[j], out=outs[j], stream=stream)
+
+    log(f"[bench] warmup {args.warmup}")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    assert ws.status() == 0, "device error word set during warmup"
+    sel_np = sels[0].cpu().numpy()
+    acct = accounting.step_bytes(n_q_heads=Hq, n_kv_heads=Hkv, head_dim=d, rank=spec.rank,
+                                 elem=2, out_elem=2, n_anchors=case.n_anchors,
+                                 n_spans=case.n_spans, span_len=case.span_len, sel=sel_np)
+    bytes_step = acct["total"]
+
+    # timed region: K steps, one event pair around each launch on the launch stream
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(K)]
+    log(f"[bench] timing {K} steps over {len(caches)} cache copies")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        ev[i][0].record(stream)
+        step(args.warmup + i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    assert ws.status() == 0, "device error word set during the timed steps"
+    us_step = wall / K * 1e6
+    kern_us = float(kern_ms.mean() * 1e3)
+    gbs = bytes_step * K / wall / 1e9
+    achieved = bytes_step / (kern_us * 1e-6) / 1e9
+
+    # same cache every step (Infinity-Cache warm), for context only
+    for _ in range(5):
+        sekv.decode_step(dims, caches[0], ws, sel=sels[0], out=outs[0], stream=stream)
+    torch.cuda.synchronize()
+    warm = []
+    for _ in range(50):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        sekv.decode_step(dims, caches[0], ws, sel=sels[0], out=outs[0], stream=stream)
+        b.record(stream)
+        warm.append((a, b))
+    torch.cuda.synchronize()
+    warm_us = float(np.mean([a.elapsed_time(b) for a, b in warm]) * 1e3)
+
+    if args.calibration_copy_mib > 0:
+        n = args.calibration_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {n} bytes done")
+
+    workload = "sekv-decode-step-128k-b4-r32-k16-bf16-" + args.variant
+    traffic = load_traffic(workload)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic, "kernel": KERNEL_NAME,
+                "kernel_us_mean": round(kern_us, 3),
+                "kernel_us_p50": round(float(np.median(kern_ms) * 1e3), 3),
+                "kernel_us_p90": round(float(np.percentile(kern_ms, 90) * 1e3), 3),
+                "algorithmic_bytes_per_launch": bytes_step}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(case, bytes_step, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": K, "warmup": args.warmup, "ms_per_step": round(wall / K * 1e3, 5),
+        "us_per_step": round(us_step, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": workload, "batch": B, "context": spec.context,
+                   "n_q_heads": Hq, "n_kv_heads": Hkv, "head_dim": d, "rank": spec.rank,
+                   "top_k": spec.top_k, "storage_dtype": "bf16", "routing_dtype": "f64",
+                   "variant": args.variant, "cache_copies": len(caches),
+                   "parallelism": "single-gpu"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "bytes": {k: v for k, v in acct.items()},
+        "warm_same_cache_kernel_us": round(warm_us, 3),
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(case, bytes_step, seconds):
+    """The oracle, as it stands, timed on the host on the same workload."""
+    import numpy as np
+
+    import oracle
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:  # pragma: no cover
+        threadpool_limits = None
+    s = case.spec
+    kw = dict(q=case.q, anchor_k=case.anchor_k, anchor_v=case.anchor_v, n_anchors=case.n_anchors,
+              sum_k=case.sum_k, sum_v=case.sum_v, n_spans=case.n_spans, span_len=case.span_len,
+              span_logsize=case.span_logsize, factors=case.factors, block_off=case.block_off,
+              rank=s.rank, top_k=s.top_k, softmax_scale=s.softmax_scale, dtype=s.dtype)
+    ctx = threadpool_limits(limits=1) if threadpool_limits else None
+    if ctx:
+        ctx.__enter__()
+    try:
+        times = []
+        t_end = time.perf_counter() + seconds
+        while True:
+            t0 = time.perf_counter()
+            oracle.decode_step(**kw)
+            times.append(time.perf_counter() - t0)
+            if time.perf_counter() > t_end or len(times) >= 100:
+                break
+    finally:
+        if ctx:
+            ctx.__exit__(None, None, None)
+    per = float(np.median(times))
+    log(f"[bench] oracle: {len(times)} steps, median {per:.3f}s")
+    return {"value": round(bytes_step / per / 1e9, 4), "unit": "GB/s", "cores": 1,
+            "kind": "oracle", "us_per_step": round(per * 1e6, 1),
+            "sample": f"{len(times)} full decode steps of the same 128K x 4 layer, median, "
+                      f"numpy float64, BLAS limited to 1 thread"}
+
+
+if __name__ == "__main__":
+    main()

@@ -181,7 +181,7 @@ sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_
     p.route_cnt = reinterpret_cast<uint32_t *>(w + L.route_cnt);
     p.sel_ready = reinterpret_cast<uint32_t *>(w + L.sel_ready);
     p.part_cnt = reinterpret_cast<uint32_t *>(w + L.part_cnt);
-    p.sel_ws = reinterpret_cast<int32_t *>(w + L.sel);
+    p.zrec = reinterpret_cast<int4 *>(w + L.zrec);
     p.cand_key = reinterpret_cast<uint64_t *>(w + L.cand_key);
     p.cand_idx = reinterpret_cast<int32_t *>(w + L.cand_idx);
     p.cand_cnt = reinterpret_cast<int32_t *>(w + L.cand_cnt);
@@ -189,6 +189,12 @@ sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_
     p.part_ml = reinterpret_cast<float *>(w + L.part_ml);
     p.part_o = reinterpret_cast<float *>(w + L.part_o);
 
+    // Fused mode ranks the candidates inside every zoom item when they fit its LDS
+    // buffers (<= kMergeBuf candidates and <= kLoserWin losing candidates per item);
+    // otherwise one workgroup per pair merges them.
+    const long long n_cand = (long long)s.n_rc * s.kc;
+    const bool per_item = n_cand <= sekv::kMergeBuf && n_cand <= (long long)s.k * (sekv::kLoserWin + 1);
+    p.merger = (mode == sekv::kModeRoute) || (mode == sekv::kModeFused && !per_item);
     const int cap = resident(d->dtype, d->head_dim, s.G);
     p.grid = std::max(1, std::min(p.end_zoom, cap));
     if (p.end_zoom == 0) return SEKV_OK;

@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include <hip/hip_runtime_api.h>
+#include <hip/hip_vector_types.h>
 
 #include "sekv.h"
 
@@ -14,10 +15,12 @@ namespace sekv {
 // Work decomposition (compile-time tile sizes).
 constexpr int kThreads = 256;      // threads per workgroup: 4 wave64s
 constexpr int kRouteChunk = 64;    // spans per routing / summary work item
-constexpr int kAnchorChunk = 128;  // anchor tokens per anchor work item
+// Anchor tokens per anchor work item: 8 key + 8 value vectors of 16 bytes per thread.
+constexpr int anchor_chunk(int elem_bytes, int head_dim) { return 32768 / (head_dim * elem_bytes); }
 constexpr int kZoomBlock = 512;    // tokens of a zoomed span scored per LDS pass
 constexpr int kMaxTopK = 64;
-constexpr int kMergeBuf = 512;     // candidate sort buffer of the selection merge
+constexpr int kMergeBuf = 512;     // candidates ranked in LDS
+constexpr int kLoserWin = 128;     // losing candidates folded per window
 
 enum Mode : int32_t { kModeRoute = 0, kModeAttend = 1, kModeFused = 2 };
 
@@ -36,7 +39,7 @@ struct WsHeader {
 // Byte offsets of the workspace sections for one dims.
 struct WsLayout {
     size_t route_cnt, sel_ready, part_cnt;    // uint32 [P]
-    size_t sel;                               // int32  [P][k]
+    size_t zrec;                              // int32x4 [P][k]: span, |S|, offset lo/hi
     size_t cand_key;                          // uint64 [P][n_rc][kc]
     size_t cand_idx;                          // int32  [P][n_rc][kc]
     size_t cand_cnt;                          // int32  [P][n_rc]
@@ -55,6 +58,8 @@ struct Shape {
     int n_slots;  // partials per pair (fused layout: anchors, summaries, losers, zoom)
 };
 
+inline int elem_bytes(int dtype) { return dtype == SEKV_BF16 ? 2 : 4; }
+
 inline Shape make_shape(const sekv_dims &d) {
     Shape s{};
     s.B = d.batch; s.Hq = d.n_q_heads; s.Hkv = d.n_kv_heads; s.G = s.Hq / s.Hkv;
@@ -62,7 +67,8 @@ inline Shape make_shape(const sekv_dims &d) {
     s.A_max = d.max_anchors; s.M_max = d.max_spans; s.L_max = d.max_span_len;
     s.P = s.B * s.Hkv;
     s.n_rc = (s.M_max + kRouteChunk - 1) / kRouteChunk;
-    s.n_ac = (s.A_max + kAnchorChunk - 1) / kAnchorChunk;
+    const int ca = anchor_chunk(elem_bytes(d.dtype), s.d);
+    s.n_ac = (s.A_max + ca - 1) / ca;
     s.kc = s.k < kRouteChunk ? s.k : kRouteChunk;
     s.n_slots = s.n_ac + s.n_rc + 1 + s.k;
     return s;
@@ -77,7 +83,7 @@ inline WsLayout make_layout(const Shape &s) {
     L.route_cnt = o; o = align256(o + 4 * P);
     L.sel_ready = o; o = align256(o + 4 * P);
     L.part_cnt = o;  o = align256(o + 4 * P);
-    L.sel = o;       o = align256(o + 4 * P * size_t(s.k > 0 ? s.k : 1));
+    L.zrec = o;      o = align256(o + 16 * P * size_t(s.k > 0 ? s.k : 1));
     const size_t nc = P * size_t(s.n_rc) * size_t(s.kc > 0 ? s.kc : 1);
     L.cand_key = o;  o = align256(o + 8 * nc);
     L.cand_idx = o;  o = align256(o + 4 * nc);
@@ -98,6 +104,9 @@ struct Params {
     int32_t slot_route0, slot_losers, slot_zoom0;   // first slot of each partial kind
     int32_t end_route, end_anchor, end_zoom;        // item-index ends of each item kind
     int32_t grid;                                   // workgroups in the launch
+    int32_t merger;                                 // 1: one workgroup per pair merges the
+                                                    // candidates (route mode, or too many
+                                                    // candidates for per-item ranking)
     int32_t out_f32;                                // 1: out is float, 0: bf16
     int32_t zoom_impl;
     double scale;                                   // softmax scale (routing score)
@@ -120,7 +129,7 @@ struct Params {
     // workspace
     WsHeader *hdr;
     uint32_t *route_cnt, *sel_ready, *part_cnt;
-    int32_t *sel_ws;
+    int4 *zrec;
     uint64_t *cand_key;
     int32_t *cand_idx, *cand_cnt;
     float *cand_lg;

@@ -2,26 +2,40 @@
 //
 // Work items (per (sequence b, KV head g) "pair"):
 //   route   chunk of 64 spans: routing scores in float64 (eq. routing_gate with the
-//           coarse mean key as summary), local top-k candidates, and -- fused mode --
-//           the coarse softmax partial of the chunk's non-candidate spans, so each
-//           summary row (k_bar, v_bar) is read from HBM once.  The last route item of a
-//           pair merges the candidates into the pair's selection (Sec. 3.3 budget rule)
-//           and adds the coarse partial of the candidates that lost.
-//   anchor  chunk of 128 full-resolution tokens: softmax partial.
-//   zoom    one selected span: its keys/values are U diag(sigma) V^T (eq.
-//           key_reconstruction); scores and the value sum are taken through the
-//           factors so no reconstructed token is ever written to memory.
+//           coarse mean key as summary), the chunk's local top-k as sorted candidates,
+//           and -- fused mode -- the coarse softmax partial of its non-candidate spans,
+//           so each summary row (k_bar, v_bar) is read from HBM once.
+//   anchor  chunk of full-resolution tokens: softmax partial.
+//   zoom    selection slot j of a pair: once every route chunk of the pair is done, the
+//           item ranks the pair's candidates (Sec. 3.3 budget rule: decreasing routing
+//           score, here top-k), takes the j-th span, and attends to its tokens through
+//           the factors, K_hat = U diag(sigma) V^T (eq. key_reconstruction), never
+//           forming K_hat in memory.  The same partial also covers every k-th losing
+//           candidate's coarse entry, so no span is dropped from the softmax.
 // Every partial (max, sum, weighted value sum) lands in a fixed slot; the item that
 // completes a pair's last slot merges them in slot order into the output (one softmax
 // over the mixed-resolution memory, Sec. 3.3).  No floating-point atomics: results are
 // bitwise deterministic.
 //
-// Scheduling: items [0, S) are taken statically by workgroups [0, S) where S counts
-// only items that never wait; the rest are handed out by an atomic ticket.  A zoom
-// item waits for its pair's selection, which is produced by route items whose index is
-// lower than any ticket, hence already running: the wait always ends (it is bounded
-// anyway and flags the workspace on timeout).  The last workgroup to leave zeroes the
-// counters, so the workspace is ready for the next launch.
+// Data movement: an item issues its global loads up front, as 16-byte vectors mapped
+// (row, column) onto the workgroup -- a wave reads 1 KB of contiguous rows per
+// instruction -- and keeps them in registers; row sums are lane shuffles inside a row
+// plus one cross-wave pass through LDS.
+//
+// Cross-workgroup protocol: data another workgroup reads (candidates, partials,
+// selection records) is stored with agent-scope relaxed atomic stores -- write-through
+// to the device coherence point on this chip -- every wave then waits for its stores to
+// complete (s_waitcnt vmcnt(0)), the workgroup synchronises, and one thread bumps the
+// pair's counter with a relaxed agent-scope atomic.  Readers use agent-scope relaxed
+// atomic loads, issued only after they have observed the counter.  This orders exactly
+// the data that is shared without writing back or invalidating whole L2 caches.
+//
+// Scheduling: workgroup w takes items w, w + grid, w + 2 grid, ... with grid no larger
+// than the number of workgroups the device holds at once.  Route items have the lowest
+// indices and never wait, so every route item a zoom item waits for is reached by its
+// workgroup after finitely many non-waiting items: the waits always end (they are
+// bounded anyway and flag the workspace on timeout).  The last workgroup to leave zeroes
+// the counters, so the workspace is ready for the next launch.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -67,6 +81,16 @@ struct F32 {
     }
 };
 
+// Row geometry of a d-row (one key/value/summary row) for a storage type.
+template <class T, int D>
+struct Geo {
+    static constexpr int VEC = T::kVec;             // values per 16-byte vector
+    static constexpr int RV = D * T::kBytes / 16;   // vectors per row: 8, 16 or 32
+    static constexpr int RPP = NT / RV;             // rows per workgroup pass
+    static constexpr int RB = D * T::kBytes;        // bytes per row
+    static constexpr int RS = RB + 16;              // padded LDS row stride
+};
+
 __device__ inline uint4 ld16(const void *p) { return *reinterpret_cast<const uint4 *>(p); }
 
 __device__ inline uint16_t f32_to_bf16_rne(float f) {
@@ -100,22 +124,24 @@ __device__ inline float wave_sum(float v) {
 __device__ inline float safe_exp2(float x) { return x == -INFINITY ? 0.0f : exp2f(x); }
 
 // ---------------------------------------------------------------------------
-// cross-workgroup signalling (agent scope)
+// cross-workgroup protocol (see the file comment)
 // ---------------------------------------------------------------------------
-__device__ inline uint32_t atomic_add_acqrel(uint32_t *p, uint32_t v) {
-    return __hip_atomic_fetch_add(p, v, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+template <class V>
+__device__ inline void st_shared(V *p, V v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ inline uint32_t atomic_add_relaxed(uint32_t *p, uint32_t v) {
+template <class V>
+__device__ inline V ld_shared(const V *p) {
+    return __hip_atomic_load(const_cast<V *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint32_t counter_add(uint32_t *p, uint32_t v) {
     return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ inline uint32_t load_acquire(const uint32_t *p) {
-    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+// Every wave waits for its own stores to complete; then the workgroup synchronises.
+__device__ inline void stores_done_barrier() {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
 }
-__device__ inline void store_release(uint32_t *p, uint32_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline void fence_acquire() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
-__device__ inline void fence_release() { __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent"); }
 __device__ inline void flag_error(const Params &p, int32_t bit) {
     __hip_atomic_fetch_or(&p.hdr->error, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -125,127 +151,166 @@ __device__ inline void flag_error(const Params &p, int32_t bit) {
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
 struct Smem {
-    static constexpr int kRowS = D * T::kBytes + 16;     // padded LDS row stride
-    struct Rows {                                        // route / summary / anchor items
-        union { double qd[G][D]; float qf[G][D]; } q;    // query: float64 (routing) / float32
-        unsigned char kb[CR * kRowS];                    // key rows
-        unsigned char vb[CR * kRowS];                    // value rows
+    using GE = Geo<T, D>;
+    static constexpr int CA = 8 * NT / GE::RV;           // anchor tokens per item
+    struct Route {                                       // route / summary item
+        double qd[G][D];                                 // query, float64
+        unsigned char kb[CR * GE::RS];                   // summary key rows (fp64 dots)
+        double lns[CR];                                  // ln|S| of the chunk's spans
         double lg[G][CR];                                // routing scores, natural units
-        float lw[G][CR];                                 // scores, base-2 units (-inf = excluded)
-        float pw[G][CR];                                 // exp2(lw - running max)
-        int32_t excl[CR];                                // excluded span / loser index
+        float pw[G][CR];                                 // coarse weights
+        int32_t excl[CR];                                // 1 = candidate / selected
     };
-    struct Zoom {                                        // zoom item
+    struct Anchor {
         float qf[G][D];
-        unsigned char vt[kMaxTopK * kRowS];              // Vt_V rows
-        float zs[G][kZoomBlock];                         // token scores, then weights
+        float sc[G][CA];                                 // scores, then weights
+    };
+    struct Zoom {
+        float qf[G][D];
+        uint4 cand[kMergeBuf];                           // {key lo, key hi, span, rank}
+        float cand_lg[kMergeBuf][G];                     // candidates' natural-unit scores
+        int32_t sel[kMaxTopK];                           // the pair's selection
+        int32_t loser[kLoserWin];                        // this item's losing candidates
+        float lw[G][kLoserWin];                          // their base-2 logits, then weights
         float w[G][kMaxTopK];                            // scale*log2e*sigma_K*(Vt_K q)
+        float zs[G][kZoomBlock];                         // token scores, then weights
+        float yr[4][G][kMaxTopK];                        // per-wave partial sums of p^T U_V
         float y[G][kMaxTopK];                            // (p^T U_V) * sigma_V
-        float red[4][G][kMaxTopK];                       // per-wave partial sums of y
         float sig[2][kMaxTopK];                          // sigma_K, sigma_V
     };
-    struct Merge {                                       // selection merge
+    struct Merge {                                       // single-merger selection
         uint64_t key[kMergeBuf];
         uint32_t idx[kMergeBuf];
         int32_t sel[kMaxTopK];
+        int32_t loser[kLoserWin];
+        float pw[G][kLoserWin];
     };
     struct Final {                                       // softmax merge
+        float ml[kMergeBuf][G][2];
         float wgt[kMergeBuf][G];
-        float M[G], L[G];
+        float L[G];
     };
     union {
-        Rows rows;
+        Route route;
+        Anchor anchor;
         Zoom zoom;
         Merge merge;
         Final fin;
     } u;
+    float red[4][G][D];                                  // per-wave row sums
     float m_run[G], l_run[G], scale_old[G];              // online softmax state
-    int32_t bcast[4];
+    int32_t bcast[8];
 };
 
 // ---------------------------------------------------------------------------
-// helpers on LDS rows
+// row-sum helpers: thread (rgrp = tid / RV, col = tid % RV) holds acc[G][VEC]
 // ---------------------------------------------------------------------------
-template <class T, int D>
-__device__ inline void copy_rows_to_lds(unsigned char *dst, const unsigned char *src, int nrows,
-                                        int tid) {
-    constexpr int RV = D * T::kBytes / 16;             // 16-byte vectors per row
-    constexpr int RS = D * T::kBytes + 16;
-    for (int v = tid; v < nrows * RV; v += NT) {
-        const int row = v / RV, col = v % RV;
-        *reinterpret_cast<uint4 *>(dst + size_t(row) * RS + col * 16) =
-            ld16(src + size_t(row) * (D * T::kBytes) + col * 16);
-    }
-}
-
-template <class T, int D>
-__device__ inline float lds_elem(const unsigned char *rows, int row, int col) {
-    constexpr int RS = D * T::kBytes + 16;
-    return T::load1(rows + size_t(row) * RS, col);
-}
-
-// Online coarse accumulation of one batch of <= CR rows held in LDS (vb, lw).
-// Each thread owns outputs o = tid + NT*u (head o / D, dim o % D), accumulated in acc[].
 template <class T, int D, int G>
-__device__ inline void online_batch(Smem<T, D, G> &sm, int nrows, float *acc, int tid) {
-    auto &R = sm.u.rows;
-    const int wave = tid >> 6, lane = tid & 63;
-    for (int hl = wave; hl < G; hl += 4) {
-        float x = (lane < nrows) ? R.lw[hl][lane] : -INFINITY;
-        const float mb = wave_max(x);
-        const float mo = sm.m_run[hl];
-        const float mn = fmaxf(mo, mb);
-        const float pw = (mn == -INFINITY) ? 0.0f : safe_exp2(x - mn);
-        if (lane < CR) R.pw[hl][lane] = pw;
-        const float lb = wave_sum(pw);
-        if (lane == 0) {
-            const float so = (mn == -INFINITY) ? 1.0f : safe_exp2(mo - mn);
-            sm.scale_old[hl] = so;
-            sm.l_run[hl] = sm.l_run[hl] * so + lb;
-            sm.m_run[hl] = mn;
-        }
-    }
-    __syncthreads();
-    constexpr int NOUT = (G * D + NT - 1) / NT;
+__device__ inline void acc_zero(float (&acc)[G][T::kVec]) {
 #pragma unroll
-    for (int u = 0; u < NOUT; ++u) {
-        const int o = tid + NT * u;
-        if (o < G * D) {
-            const int hl = o / D, d = o % D;
-            float a = acc[u] * sm.scale_old[hl];
-            for (int i = 0; i < nrows; ++i) a += R.pw[hl][i] * lds_elem<T, D>(R.vb, i, d);
-            acc[u] = a;
-        }
-    }
-    __syncthreads();
+    for (int hl = 0; hl < G; ++hl)
+#pragma unroll
+        for (int e = 0; e < T::kVec; ++e) acc[hl][e] = 0.0f;
 }
 
 template <class T, int D, int G>
-__device__ inline void online_reset(Smem<T, D, G> &sm, float *acc, int tid) {
-    auto &R = sm.u.rows;
-    if (tid < G) { sm.m_run[tid] = -INFINITY; sm.l_run[tid] = 0.0f; sm.scale_old[tid] = 1.0f; }
-    constexpr int NOUT = (G * D + NT - 1) / NT;
+__device__ inline void acc_scale(float (&acc)[G][T::kVec], const float *so) {
 #pragma unroll
-    for (int u = 0; u < NOUT; ++u) acc[u] = 0.0f;
-    __syncthreads();
+    for (int hl = 0; hl < G; ++hl) {
+        const float s = so[hl];
+#pragma unroll
+        for (int e = 0; e < T::kVec; ++e) acc[hl][e] *= s;
+    }
 }
 
-// Write a finished partial (m, l in LDS state; o in acc) to its slot.
+// acc += w[row] * row vector (rows of this thread: rgrp + RPP*j, j < NJ, row < nrows)
+template <class T, int D, int G, int NJ>
+__device__ inline void acc_rows(float (&acc)[G][T::kVec], const uint4 (&v)[NJ],
+                                const float *w, int wstride, int nrows, int rgrp) {
+    using GE = Geo<T, D>;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int row = rgrp + GE::RPP * j;
+        if (row < nrows) {
+            float f[GE::VEC];
+            T::unpack(v[j], f);
+#pragma unroll
+            for (int hl = 0; hl < G; ++hl) {
+                const float wt = w[hl * wstride + row];
+#pragma unroll
+                for (int e = 0; e < GE::VEC; ++e) acc[hl][e] += wt * f[e];
+            }
+        }
+    }
+}
+
+// Sum acc over the rows held by all threads into sm.red (caller syncs before reading).
+template <class T, int D, int G>
+__device__ inline void rows_to_red(Smem<T, D, G> &sm, float (&acc)[G][T::kVec], int tid) {
+    using GE = Geo<T, D>;
+    const int lane = tid & 63, wave = tid >> 6;
+#pragma unroll
+    for (int o = GE::RV; o < 64; o <<= 1)
+#pragma unroll
+        for (int hl = 0; hl < G; ++hl)
+#pragma unroll
+            for (int e = 0; e < GE::VEC; ++e) acc[hl][e] += __shfl_xor(acc[hl][e], o, 64);
+    if (lane < (GE::RV < 64 ? GE::RV : 64)) {
+        const int col = tid % GE::RV;
+#pragma unroll
+        for (int hl = 0; hl < G; ++hl)
+#pragma unroll
+            for (int e = 0; e < GE::VEC; ++e) sm.red[wave][hl][col * GE::VEC + e] = acc[hl][e];
+    }
+}
+
+// Write the partial of `slot`: m, l from the online state; o = the 4 wave rows of red.
 template <class T, int D, int G>
 __device__ inline void write_partial(const Params &p, Smem<T, D, G> &sm, int pair, int slot,
-                                     const float *acc, int tid) {
-    auto &R = sm.u.rows;
+                                     int tid) {
     const size_t base = (size_t(pair) * p.n_slots + slot) * G;
     if (tid < G) {
-        p.part_ml[(base + tid) * 2 + 0] = sm.m_run[tid];
-        p.part_ml[(base + tid) * 2 + 1] = sm.l_run[tid];
+        st_shared(&p.part_ml[(base + tid) * 2 + 0], sm.m_run[tid]);
+        st_shared(&p.part_ml[(base + tid) * 2 + 1], sm.l_run[tid]);
     }
-    constexpr int NOUT = (G * D + NT - 1) / NT;
-#pragma unroll
-    for (int u = 0; u < NOUT; ++u) {
-        const int o = tid + NT * u;
-        if (o < G * D) p.part_o[base * D + o] = acc[u];
+    for (int o = tid; o < G * D; o += NT) {
+        const int hl = o / D, d = o % D;
+        st_shared(&p.part_o[base * D + o],
+                  sm.red[0][hl][d] + sm.red[1][hl][d] + sm.red[2][hl][d] + sm.red[3][hl][d]);
     }
+}
+
+// Fold a batch of base-2 scores (LDS, -inf = excluded) into the online state: weights
+// are written in place relative to the new running max; scale_old gets the factor the
+// already accumulated sums must be multiplied by.
+__device__ inline void online_fold(float *sc, int stride, int n, int G, float *m_run,
+                                   float *l_run, float *scale_old, int tid) {
+    const int wave = tid >> 6, lane = tid & 63;
+    for (int hl = wave; hl < G; hl += 4) {
+        float *row = sc + hl * stride;
+        float mx = -INFINITY;
+        for (int i = lane; i < n; i += 64) mx = fmaxf(mx, row[i]);
+        mx = wave_max(mx);
+        const float mo = m_run[hl];
+        const float mn = fmaxf(mo, mx);
+        float ls = 0.0f;
+        for (int i = lane; i < n; i += 64) {
+            const float w = (mn == -INFINITY) ? 0.0f : safe_exp2(row[i] - mn);
+            row[i] = w;
+            ls += w;
+        }
+        ls = wave_sum(ls);
+        if (lane == 0) {
+            const float so = (mn == -INFINITY) ? 1.0f : safe_exp2(mo - mn);
+            scale_old[hl] = so;
+            l_run[hl] = l_run[hl] * so + ls;
+            m_run[hl] = mn;
+        }
+    }
+}
+
+__device__ inline void online_reset(int G, float *m_run, float *l_run, float *scale_old, int tid) {
+    if (tid < G) { m_run[tid] = -INFINITY; l_run[tid] = 0.0f; scale_old[tid] = 1.0f; }
 }
 
 // ---------------------------------------------------------------------------
@@ -256,103 +321,94 @@ __device__ void final_merge(const Params &p, Smem<T, D, G> &sm, int pair, int ti
     auto &F = sm.u.fin;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
     const int ns = p.n_slots;
-    const bool use_losers = (p.mode == kModeFused);
+    const bool use_losers = (p.mode == kModeFused) && p.merger;
     const float *ml = p.part_ml + size_t(pair) * ns * G * 2;
+    for (int i = tid; i < ns * G * 2; i += NT) (&F.ml[0][0][0])[i] = ld_shared(ml + i);
+    __syncthreads();
     const int wave = tid >> 6, lane = tid & 63;
     for (int hl = wave; hl < G; hl += 4) {
         float mx = -INFINITY;
         for (int s = lane; s < ns; s += 64) {
-            if (s == p.slot_losers && !use_losers) continue;
-            if (ml[(s * G + hl) * 2 + 1] > 0.0f) mx = fmaxf(mx, ml[(s * G + hl) * 2]);
+            const bool on = use_losers || s != p.slot_losers;
+            if (on && F.ml[s][hl][1] > 0.0f) mx = fmaxf(mx, F.ml[s][hl][0]);
         }
         mx = wave_max(mx);
         float lsum = 0.0f;
         for (int s = lane; s < ns; s += 64) {
+            const bool on = use_losers || s != p.slot_losers;
             float wgt = 0.0f;
-            const bool on = !(s == p.slot_losers && !use_losers);
-            if (on && ml[(s * G + hl) * 2 + 1] > 0.0f) {
-                wgt = exp2f(ml[(s * G + hl) * 2] - mx);
-                lsum += wgt * ml[(s * G + hl) * 2 + 1];
+            if (on && F.ml[s][hl][1] > 0.0f) {
+                wgt = exp2f(F.ml[s][hl][0] - mx);
+                lsum += wgt * F.ml[s][hl][1];
             }
             F.wgt[s][hl] = wgt;
         }
-        // fixed-order sum over lanes (deterministic for a given ns)
         lsum = wave_sum(lsum);
-        if (lane == 0) { F.M[hl] = mx; F.L[hl] = lsum; }
+        if (lane == 0) F.L[hl] = lsum;
     }
     __syncthreads();
     const float *po = p.part_o + size_t(pair) * ns * G * D;
-    constexpr int NOUT = (G * D + NT - 1) / NT;
+    for (int o = tid; o < G * D; o += NT) {
+        const int hl = o / D, d = o % D;
+        float a = 0.0f;
+        int s = 0;
+        for (; s + 8 <= ns; s += 8) {
+            float v[8];
 #pragma unroll
-    for (int u = 0; u < NOUT; ++u) {
-        const int o = tid + NT * u;
-        if (o < G * D) {
-            const int hl = o / D, d = o % D;
-            float a = 0.0f;
-            for (int s = 0; s < ns; ++s) {
-                const float wgt = F.wgt[s][hl];
-                if (wgt != 0.0f) a += wgt * po[(size_t(s) * G + hl) * D + d];
+            for (int u = 0; u < 8; ++u) v[u] = ld_shared(po + (size_t(s + u) * G + hl) * D + d);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const float wgt = F.wgt[s + u][hl];
+                a += (wgt != 0.0f) ? wgt * v[u] : 0.0f;
             }
-            const float L = F.L[hl];
-            const float r = (L > 0.0f) ? a / L : 0.0f;
-            const size_t oi = (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d;
-            if (p.out_f32) reinterpret_cast<float *>(p.out)[oi] = r;
-            else reinterpret_cast<uint16_t *>(p.out)[oi] = f32_to_bf16_rne(r);
         }
+        for (; s < ns; ++s) {
+            const float wgt = F.wgt[s][hl];
+            const float v = ld_shared(po + (size_t(s) * G + hl) * D + d);
+            a += (wgt != 0.0f) ? wgt * v : 0.0f;
+        }
+        const float L = F.L[hl];
+        const float r = (L > 0.0f) ? a / L : 0.0f;
+        const size_t oi = (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d;
+        if (p.out_f32) reinterpret_cast<float *>(p.out)[oi] = r;
+        else reinterpret_cast<uint16_t *>(p.out)[oi] = f32_to_bf16_rne(r);
     }
 }
 
-// Count one finished partial of `pair`; the item completing the pair merges.
+__device__ inline int parts_per_pair(const Params &p) {
+    int n = p.n_ac + p.n_rc + p.k;
+    if (p.mode == kModeFused && p.merger) n += 1;
+    return n;
+}
+
+// Count `n` finished partials of `pair` (written, stores completed by every wave); the
+// item completing the pair merges.
 template <class T, int D, int G>
-__device__ inline void finish_partial(const Params &p, Smem<T, D, G> &sm, int pair, int n_parts,
+__device__ inline void count_partials(const Params &p, Smem<T, D, G> &sm, int pair, uint32_t n,
                                       int tid) {
-    __syncthreads();
     if (tid == 0) {
-        fence_release();
-        const uint32_t prev = atomic_add_acqrel(&p.part_cnt[pair], 1u);
-        sm.bcast[0] = (prev == uint32_t(n_parts - 1));
+        const uint32_t prev = counter_add(&p.part_cnt[pair], n);
+        sm.bcast[0] = (prev + n == uint32_t(parts_per_pair(p)));
     }
     __syncthreads();
-    if (sm.bcast[0]) {
-        fence_acquire();
-        final_merge<T, D, G>(p, sm, pair, tid);
-    }
+    if (sm.bcast[0]) final_merge<T, D, G>(p, sm, pair, tid);
     __syncthreads();
 }
 
 // ---------------------------------------------------------------------------
-// selection merge: the last route item of a pair orders all candidates
+// selection by a single merger (route mode, or more candidates than kMergeBuf)
 // ---------------------------------------------------------------------------
-template <class T, int D, int G>
-__device__ inline void bitonic_sort_lds(Smem<T, D, G> &sm, int tid) {
-    auto &M = sm.u.merge;
-    for (int size = 2; size <= kMergeBuf; size <<= 1) {
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            for (int t = tid; t < kMergeBuf / 2; t += NT) {
-                const int i = (t / stride) * 2 * stride + (t % stride);
-                const int j = i + stride;
-                const bool up = (i & size) == 0;        // up: better elements first
-                const uint64_t ki = M.key[i], kj = M.key[j];
-                const uint32_t ii = M.idx[i], ij = M.idx[j];
-                const bool swap = up ? better(kj, ij, ki, ii) : better(ki, ii, kj, ij);
-                if (swap) { M.key[i] = kj; M.idx[i] = ij; M.key[j] = ki; M.idx[j] = ii; }
-            }
-            __syncthreads();
-        }
-    }
-}
-
 template <class T, int D, int G>
 __device__ void merge_selection(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
     auto &M = sm.u.merge;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
-    const int k = p.k;
+    const int k = p.k, kc = p.kc;
     int m_b = p.n_spans[b];
     m_b = m_b < 0 ? 0 : (m_b > p.M_max ? p.M_max : m_b);
-    const int kc = p.kc;
     const int n_cand = p.n_rc * kc;
-    constexpr int kHead = kMaxTopK;                       // running best occupies [0, 64)
+    constexpr int kHead = kMaxTopK;
     constexpr int kFill = kMergeBuf - kMaxTopK;
+    for (int j = tid; j < kMaxTopK; j += NT) M.sel[j] = -1;
     for (int i = tid; i < kMergeBuf; i += NT) { M.key[i] = 0; M.idx[i] = kInvalidIdx - i; }
     __syncthreads();
     for (int base = 0; base < n_cand; base += kFill) {
@@ -362,92 +418,109 @@ __device__ void merge_selection(const Params &p, Smem<T, D, G> &sm, int pair, in
             uint32_t idx = kInvalidIdx - (kHead + i);
             if (c < n_cand) {
                 const int chunk = c / kc, j = c % kc;
-                const int cnt = __hip_atomic_load(&p.cand_cnt[pair * p.n_rc + chunk],
-                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if (j < cnt) {
+                if (j < ld_shared(&p.cand_cnt[pair * p.n_rc + chunk])) {
                     const size_t ci = (size_t(pair) * p.n_rc + chunk) * kc + j;
-                    key = p.cand_key[ci];
-                    idx = uint32_t(p.cand_idx[ci]);
+                    key = ld_shared(&p.cand_key[ci]);
+                    idx = uint32_t(ld_shared(&p.cand_idx[ci]));
                 }
             }
             M.key[kHead + i] = key;
             M.idx[kHead + i] = idx;
         }
         __syncthreads();
-        bitonic_sort_lds<T, D, G>(sm, tid);
-        // keep the best k; invalidate [k, 64) so they cannot re-enter
+        for (int size = 2; size <= kMergeBuf; size <<= 1) {
+            for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                for (int t = tid; t < kMergeBuf / 2; t += NT) {
+                    const int i = (t / stride) * 2 * stride + (t % stride);
+                    const int j = i + stride;
+                    const bool up = (i & size) == 0;
+                    const uint64_t ki = M.key[i], kj = M.key[j];
+                    const uint32_t ii = M.idx[i], ij = M.idx[j];
+                    const bool swap = up ? better(kj, ij, ki, ii) : better(ki, ii, kj, ij);
+                    if (swap) { M.key[i] = kj; M.idx[i] = ij; M.key[j] = ki; M.idx[j] = ii; }
+                }
+                __syncthreads();
+            }
+        }
         for (int i = tid; i < kHead; i += NT)
             if (i >= k) { M.key[i] = 0; M.idx[i] = kInvalidIdx - i; }
         __syncthreads();
     }
     const int take = k < m_b ? k : m_b;
-    for (int j = tid; j < k; j += NT) {
-        const int s = (j < take && M.idx[j] < 0x80000000u) ? int(M.idx[j]) : -1;
-        M.sel[j] = s;
-        if (p.sel_out) p.sel_out[size_t(pair) * k + j] = s;
-        if (p.mode == kModeFused) p.sel_ws[size_t(pair) * k + j] = s;
-    }
+    for (int j = tid; j < take; j += NT)
+        if (M.idx[j] < 0x80000000u) M.sel[j] = int32_t(M.idx[j]);
     __syncthreads();
-    if (p.mode == kModeFused && tid == 0) {
-        fence_release();
-        store_release(&p.sel_ready[pair], 1u);
+    for (int j = tid; j < k; j += NT) {
+        const int s = M.sel[j];
+        if (p.sel_out) p.sel_out[size_t(pair) * k + j] = s;
+        if (p.mode == kModeFused) {
+            int L = 0;
+            int64_t off = 0;
+            if (s >= 0) {
+                L = p.span_len[size_t(b) * p.M_max + s];
+                off = p.block_off[(size_t(b) * p.Hkv + g) * p.M_max + s];
+            }
+            int32_t *rec = reinterpret_cast<int32_t *>(&p.zrec[size_t(pair) * k + j]);
+            st_shared(rec + 0, s);
+            st_shared(rec + 1, L);
+            st_shared(rec + 2, int32_t(off & 0xFFFFFFFF));
+            st_shared(rec + 3, int32_t(off >> 32));
+        }
     }
+    stores_done_barrier();
+    if (p.mode == kModeFused && tid == 0) st_shared(&p.sel_ready[pair], 1u);
 }
 
-// Coarse partial over the candidates that lost the selection (fused mode).
+// Coarse partial over the candidates that lost (single-merger fused mode).
 template <class T, int D, int G>
 __device__ void losers_partial(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
-    auto &R = sm.u.rows;
+    using GE = Geo<T, D>;
+    auto &M = sm.u.merge;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
     const int k = p.k, kc = p.kc;
-    // selection (from workspace; this workgroup wrote it)
-    __shared__ int32_t sel_l[kMaxTopK];
-    for (int j = tid; j < kMaxTopK; j += NT) sel_l[j] = (j < k) ? p.sel_ws[size_t(pair) * k + j] : -1;
-    __syncthreads();
-    constexpr int NOUT = (G * D + NT - 1) / NT;
-    float acc[NOUT];
-    online_reset<T, D, G>(sm, acc, tid);
+    const int rgrp = tid / GE::RV, col = tid % GE::RV;
+    constexpr int NJ = (kLoserWin + GE::RPP - 1) / GE::RPP;
     const unsigned char *sv = reinterpret_cast<const unsigned char *>(p.sum_v) +
-                              (size_t(b) * p.Hkv + g) * size_t(p.M_max) * D * T::kBytes;
+                              (size_t(b) * p.Hkv + g) * size_t(p.M_max) * GE::RB;
     const int n_cand = p.n_rc * kc;
-    for (int base = 0; base < n_cand; base += CR) {
-        // gather up to CR losers of this candidate window
-        if (tid < CR) {
-            const int c = base + tid;
+    float acc[G][GE::VEC];
+    acc_zero<T, D, G>(acc);
+    online_reset(G, sm.m_run, sm.l_run, sm.scale_old, tid);
+    for (int base = 0; base < n_cand; base += kLoserWin) {
+        for (int t = tid; t < kLoserWin; t += NT) {
+            const int c = base + t;
             int idx = -1;
+            size_t ci = 0;
             if (c < n_cand) {
                 const int chunk = c / kc, j = c % kc;
-                const int cnt = p.cand_cnt[pair * p.n_rc + chunk];
-                if (j < cnt) {
-                    const size_t ci = (size_t(pair) * p.n_rc + chunk) * kc + j;
-                    idx = p.cand_idx[ci];
-                    bool chosen = false;
-                    for (int q = 0; q < k; ++q) chosen |= (sel_l[q] == idx);
-                    if (chosen) idx = -1;
-                    else
-                        for (int hl = 0; hl < G; ++hl)
-                            R.lw[hl][tid] = p.cand_lg[ci * G + hl] * kLog2e;
+                if (j < ld_shared(&p.cand_cnt[pair * p.n_rc + chunk])) {
+                    ci = (size_t(pair) * p.n_rc + chunk) * kc + j;
+                    idx = ld_shared(&p.cand_idx[ci]);
+                    for (int q = 0; q < k; ++q) idx = (M.sel[q] == idx) ? -1 : idx;
                 }
             }
-            R.excl[tid] = idx;
-            if (idx < 0)
-                for (int hl = 0; hl < G; ++hl) R.lw[hl][tid] = -INFINITY;
+            M.loser[t] = idx;
+            for (int hl = 0; hl < G; ++hl)
+                M.pw[hl][t] = (idx >= 0) ? ld_shared(&p.cand_lg[ci * G + hl]) * kLog2e : -INFINITY;
         }
         __syncthreads();
-        // rows: v_bar of each loser (zero rows for empty slots are never weighted)
-        constexpr int RV = D * T::kBytes / 16;
-        constexpr int RS = D * T::kBytes + 16;
-        for (int v = tid; v < CR * RV; v += NT) {
-            const int row = v / RV, col = v % RV;
-            const int idx = R.excl[row];
-            uint4 val = make_uint4(0, 0, 0, 0);
-            if (idx >= 0) val = ld16(sv + size_t(idx) * D * T::kBytes + col * 16);
-            *reinterpret_cast<uint4 *>(R.vb + size_t(row) * RS + col * 16) = val;
+        uint4 v[NJ];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int row = rgrp + GE::RPP * j;
+            v[j] = make_uint4(0, 0, 0, 0);
+            if (row < kLoserWin && M.loser[row] >= 0)
+                v[j] = ld16(sv + size_t(M.loser[row]) * GE::RB + col * 16);
         }
+        online_fold(&M.pw[0][0], kLoserWin, kLoserWin, G, sm.m_run, sm.l_run, sm.scale_old, tid);
         __syncthreads();
-        online_batch<T, D, G>(sm, CR, acc, tid);
+        acc_scale<T, D, G>(acc, sm.scale_old);
+        acc_rows<T, D, G, NJ>(acc, v, &M.pw[0][0], kLoserWin, kLoserWin, rgrp);
+        __syncthreads();
     }
-    write_partial<T, D, G>(p, sm, pair, p.slot_losers, acc, tid);
+    rows_to_red<T, D, G>(sm, acc, tid);
+    __syncthreads();
+    write_partial<T, D, G>(p, sm, pair, p.slot_losers, tid);
 }
 
 // ---------------------------------------------------------------------------
@@ -455,7 +528,8 @@ __device__ void losers_partial(const Params &p, Smem<T, D, G> &sm, int pair, int
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
 __device__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chunk, int tid) {
-    auto &R = sm.u.rows;
+    using GE = Geo<T, D>;
+    auto &R = sm.u.route;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
     int m_b = p.n_spans[b];
     m_b = m_b < 0 ? 0 : (m_b > p.M_max ? p.M_max : m_b);
@@ -466,19 +540,38 @@ __device__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chu
     const bool have_logits = attend && p.logits_in != nullptr;
     const bool need_dots = !have_logits;
     const size_t row0 = (size_t(b) * p.Hkv + g) * size_t(p.M_max) + s0;
+    const int rgrp = tid / GE::RV, col = tid % GE::RV;
+    constexpr int NJ = (CR + GE::RPP - 1) / GE::RPP;
 
-    // 1. stage query (float64) and summary rows
+    // 1. issue every load: summary values (registers), summary keys (-> LDS), query, ln|S|
+    uint4 v[NJ];
+    if (need_coarse) {
+        const unsigned char *src = reinterpret_cast<const unsigned char *>(p.sum_v) + row0 * GE::RB;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int row = rgrp + GE::RPP * j;
+            if (row < nv) v[j] = ld16(src + size_t(row) * GE::RB + col * 16);
+        }
+    }
     if (need_dots) {
+        const unsigned char *src = reinterpret_cast<const unsigned char *>(p.sum_k) + row0 * GE::RB;
+        uint4 kv[NJ];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int row = rgrp + GE::RPP * j;
+            if (row < nv) kv[j] = ld16(src + size_t(row) * GE::RB + col * 16);
+        }
         for (int i = tid; i < G * D; i += NT) {
             const int hl = i / D, d = i % D;
-            R.q.qd[hl][d] = double(T::load1(p.q, (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d));
+            R.qd[hl][d] = double(T::load1(p.q, (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d));
         }
-        copy_rows_to_lds<T, D>(R.kb, reinterpret_cast<const unsigned char *>(p.sum_k) +
-                                         row0 * D * T::kBytes, nv, tid);
+        if (tid < nv) R.lns[tid] = p.span_logsize[size_t(b) * p.M_max + s0 + tid];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int row = rgrp + GE::RPP * j;
+            if (row < nv) *reinterpret_cast<uint4 *>(R.kb + size_t(row) * GE::RS + col * 16) = kv[j];
+        }
     }
-    if (need_coarse)
-        copy_rows_to_lds<T, D>(R.vb, reinterpret_cast<const unsigned char *>(p.sum_v) +
-                                         row0 * D * T::kBytes, nv, tid);
     __syncthreads();
 
     // 2. routing scores: float64, products exact, summed left to right over d,
@@ -488,21 +581,20 @@ __device__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chu
         double sc = -INFINITY;
         if (i < nv) {
             if (need_dots) {
-                constexpr int VEC = T::kVec;
-                constexpr int RS = D * T::kBytes + 16;
-                const unsigned char *row = R.kb + size_t(i) * RS;
+                const unsigned char *row = R.kb + size_t(i) * GE::RS;
                 double acc = 0.0;
 #pragma unroll 4
-                for (int c = 0; c < D / VEC; ++c) {
-                    float f[VEC];
+                for (int c = 0; c < GE::RV; ++c) {
+                    float f[GE::VEC];
                     T::unpack(*reinterpret_cast<const uint4 *>(row + c * 16), f);
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) acc = __builtin_fma(R.q.qd[hl][c * VEC + e], double(f[e]), acc);
+                    for (int e = 0; e < GE::VEC; ++e)
+                        acc = __builtin_fma(R.qd[hl][c * GE::VEC + e], double(f[e]), acc);
                 }
                 {
 #pragma clang fp contract(off)
                     const double scaled = acc * p.scale;
-                    sc = scaled + p.span_logsize[size_t(b) * p.M_max + s0 + i];
+                    sc = scaled + R.lns[i];
                 }
             } else {
                 sc = double(p.logits_in[(size_t(b) * p.Hq + size_t(g) * G + hl) * p.M_max + s0 + i]);
@@ -514,10 +606,10 @@ __device__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chu
     }
     __syncthreads();
 
-    // 3. exclusions: local top-k candidates (route/fused) or the given selection (attend)
+    // 3. exclusions: local top-k candidates, sorted (route/fused), or the given selection
     if (!attend) {
-        // one wave sorts the chunk's CR = 64 (key, idx) pairs with a bitonic network
         if (tid < 64) {
+            // one wave sorts the chunk's 64 (key, idx) pairs with a bitonic network
             const int i = tid;
             uint64_t key = 0;
             uint32_t idx = kInvalidIdx - uint32_t(i);
@@ -539,153 +631,266 @@ __device__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chu
                     if (take) { key = ok; idx = oi; }
                 }
             }
-            // lane j holds the j-th best
+            // lane j now holds the j-th best
             const int kc = min(p.kc, nv);
             R.excl[i] = 0;
             __builtin_amdgcn_wave_barrier();
             if (i < kc) {
                 const size_t ci = (size_t(pair) * p.n_rc + chunk) * p.kc + i;
-                p.cand_key[ci] = key;
-                p.cand_idx[ci] = int32_t(idx);
+                st_shared(&p.cand_key[ci], key);
+                st_shared(&p.cand_idx[ci], int32_t(idx));
                 const int li = int(idx) - s0;
-                for (int hl = 0; hl < G; ++hl) p.cand_lg[ci * G + hl] = float(R.lg[hl][li]);
+                for (int hl = 0; hl < G; ++hl) st_shared(&p.cand_lg[ci * G + hl], float(R.lg[hl][li]));
+                R.excl[li] = 1;
             }
-            if (i == 0) p.cand_cnt[pair * p.n_rc + chunk] = kc;
-            __builtin_amdgcn_wave_barrier();
-            if (i < kc) R.excl[int(idx) - s0] = 1;
+            if (i == 0) st_shared(&p.cand_cnt[pair * p.n_rc + chunk], kc);
         }
-    } else {
-        if (tid < CR) {
-            int ex = 0;
-            for (int j = 0; j < p.k; ++j) ex |= (p.sel_in[size_t(pair) * p.k + j] == s0 + tid);
-            R.excl[tid] = ex;
-        }
+    } else if (tid < CR) {
+        int ex = 0;
+        for (int j = 0; j < p.k; ++j) ex |= (p.sel_in[size_t(pair) * p.k + j] == s0 + tid);
+        R.excl[tid] = ex;
     }
     __syncthreads();
 
-    // 4. coarse partial over the chunk's remaining spans
+    // 4. coarse partial over the chunk's remaining spans (values already in registers)
     if (need_coarse) {
         for (int t = tid; t < G * CR; t += NT) {
             const int hl = t / CR, i = t % CR;
-            R.lw[hl][i] = (i < nv && !R.excl[i]) ? float(R.lg[hl][i] * kLog2eD) : -INFINITY;
+            R.pw[hl][i] = (i < nv && !R.excl[i]) ? float(R.lg[hl][i] * kLog2eD) : -INFINITY;
         }
-        constexpr int NOUT = (G * D + NT - 1) / NT;
-        float acc[NOUT];
-        online_reset<T, D, G>(sm, acc, tid);
-        online_batch<T, D, G>(sm, nv, acc, tid);
-        write_partial<T, D, G>(p, sm, pair, p.slot_route0 + chunk, acc, tid);
+        online_reset(G, sm.m_run, sm.l_run, sm.scale_old, tid);
+        __syncthreads();
+        online_fold(&R.pw[0][0], CR, CR, G, sm.m_run, sm.l_run, sm.scale_old, tid);
+        __syncthreads();
+        float acc[G][GE::VEC];
+        acc_zero<T, D, G>(acc);
+        acc_rows<T, D, G, NJ>(acc, v, &R.pw[0][0], CR, nv, rgrp);
+        rows_to_red<T, D, G>(sm, acc, tid);
+        __syncthreads();
+        write_partial<T, D, G>(p, sm, pair, p.slot_route0 + chunk, tid);
     }
 
-    // 5. the last route item of the pair merges the candidates into the selection
-    if (!attend) {
-        __syncthreads();
-        if (tid == 0) {
-            fence_release();
-            const uint32_t prev = atomic_add_acqrel(&p.route_cnt[pair], 1u);
-            sm.bcast[1] = (prev == uint32_t(p.n_rc - 1));
+    // 5. publish (candidates and partial complete), then count
+    stores_done_barrier();
+    if (tid == 0) {
+        sm.bcast[1] = 0;
+        if (!attend) {
+            const uint32_t prev = counter_add(&p.route_cnt[pair], 1u);
+            sm.bcast[1] = p.merger && (prev == uint32_t(p.n_rc - 1));
         }
-        __syncthreads();
-        if (sm.bcast[1]) {
-            fence_acquire();
-            merge_selection<T, D, G>(p, sm, pair, tid);
-            __syncthreads();
-            if (p.mode == kModeFused) {
-                losers_partial<T, D, G>(p, sm, pair, tid);
-            }
-        }
+    }
+    __syncthreads();
+    uint32_t n_done = need_coarse ? 1u : 0u;
+    if (sm.bcast[1]) {
+        merge_selection<T, D, G>(p, sm, pair, tid);
         __syncthreads();
         if (p.mode == kModeFused) {
-            const int n_parts = p.n_ac + p.n_rc + 1 + p.k;
-            // this chunk's coarse partial, plus the losers partial if this item merged
-            finish_partial<T, D, G>(p, sm, pair, n_parts, tid);
-            if (sm.bcast[1]) finish_partial<T, D, G>(p, sm, pair, n_parts, tid);
+            losers_partial<T, D, G>(p, sm, pair, tid);
+            stores_done_barrier();
+            n_done += 1;
         }
-    } else {
-        finish_partial<T, D, G>(p, sm, pair, p.n_ac + p.n_rc + p.k, tid);
     }
+    if (n_done) count_partials<T, D, G>(p, sm, pair, n_done, tid);
 }
 
 // ---------------------------------------------------------------------------
-// anchor item: kAnchorChunk full-resolution tokens of a pair, in batches of CR rows
+// anchor item: CA full-resolution tokens of a pair
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
 __device__ void anchor_item(const Params &p, Smem<T, D, G> &sm, int pair, int chunk, int tid) {
-    auto &R = sm.u.rows;
+    using GE = Geo<T, D>;
+    constexpr int CA = Smem<T, D, G>::CA;
+    constexpr int NJ = CA / GE::RPP;                     // 8
+    auto &A = sm.u.anchor;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
-    int A = p.n_anchors[b];
-    A = A < 0 ? 0 : (A > p.A_max ? p.A_max : A);
-    const int a0 = chunk * kAnchorChunk;
-    const int na = max(0, min(kAnchorChunk, A - a0));
-    for (int i = tid; i < G * D; i += NT) {
-        const int hl = i / D, d = i % D;
-        R.q.qf[hl][d] = T::load1(p.q, (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d);
-    }
-    constexpr int NOUT = (G * D + NT - 1) / NT;
-    float acc[NOUT];
-    online_reset<T, D, G>(sm, acc, tid);
-    const size_t base = ((size_t(b) * p.Hkv + g) * size_t(p.A_max) + a0) * D * T::kBytes;
+    int An = p.n_anchors[b];
+    An = An < 0 ? 0 : (An > p.A_max ? p.A_max : An);
+    const int a0 = chunk * CA;
+    const int na = max(0, min(CA, An - a0));
+    const int rgrp = tid / GE::RV, col = tid % GE::RV;
+    const size_t base = ((size_t(b) * p.Hkv + g) * size_t(p.A_max) + a0) * GE::RB;
     const unsigned char *ak = reinterpret_cast<const unsigned char *>(p.anchor_k) + base;
     const unsigned char *av = reinterpret_cast<const unsigned char *>(p.anchor_v) + base;
-    for (int t0 = 0; t0 < na; t0 += CR) {
-        const int nb = min(CR, na - t0);
-        copy_rows_to_lds<T, D>(R.kb, ak + size_t(t0) * D * T::kBytes, nb, tid);
-        copy_rows_to_lds<T, D>(R.vb, av + size_t(t0) * D * T::kBytes, nb, tid);
-        __syncthreads();
-        for (int t = tid; t < G * CR; t += NT) {
-            const int hl = t / CR, i = t % CR;
-            float s = -INFINITY;
-            if (i < nb) {
-                constexpr int VEC = T::kVec;
-                constexpr int RS = D * T::kBytes + 16;
-                const unsigned char *row = R.kb + size_t(i) * RS;
-                float a = 0.0f;
-#pragma unroll 4
-                for (int c = 0; c < D / VEC; ++c) {
-                    float f[VEC];
-                    T::unpack(*reinterpret_cast<const uint4 *>(row + c * 16), f);
+    uint4 kv[NJ], vv[NJ];
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) a += R.q.qf[hl][c * VEC + e] * f[e];
-                }
-                s = a * p.scale_log2;
-            }
-            R.lw[hl][i] = s;
+    for (int j = 0; j < NJ; ++j) {
+        const int row = rgrp + GE::RPP * j;
+        if (row < na) {
+            kv[j] = ld16(ak + size_t(row) * GE::RB + col * 16);
+            vv[j] = ld16(av + size_t(row) * GE::RB + col * 16);
         }
-        __syncthreads();
-        online_batch<T, D, G>(sm, nb, acc, tid);
     }
-    write_partial<T, D, G>(p, sm, pair, chunk, acc, tid);
-    const int n_parts = (p.mode == kModeFused) ? p.n_ac + p.n_rc + 1 + p.k : p.n_ac + p.n_rc + p.k;
-    finish_partial<T, D, G>(p, sm, pair, n_parts, tid);
+    for (int i = tid; i < G * D; i += NT) {
+        const int hl = i / D, d = i % D;
+        A.qf[hl][d] = T::load1(p.q, (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d);
+    }
+    online_reset(G, sm.m_run, sm.l_run, sm.scale_old, tid);
+    __syncthreads();
+    // scores: partial dots over this thread's VEC columns, summed across the row's lanes
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int row = rgrp + GE::RPP * j;
+        float part[G];
+#pragma unroll
+        for (int hl = 0; hl < G; ++hl) part[hl] = 0.0f;
+        if (row < na) {
+            float f[GE::VEC];
+            T::unpack(kv[j], f);
+#pragma unroll
+            for (int hl = 0; hl < G; ++hl)
+#pragma unroll
+                for (int e = 0; e < GE::VEC; ++e) part[hl] += A.qf[hl][col * GE::VEC + e] * f[e];
+        }
+#pragma unroll
+        for (int o = 1; o < GE::RV; o <<= 1)
+#pragma unroll
+            for (int hl = 0; hl < G; ++hl) part[hl] += __shfl_xor(part[hl], o, 64);
+        if (col == 0)
+#pragma unroll
+            for (int hl = 0; hl < G; ++hl)
+                A.sc[hl][row] = (row < na) ? part[hl] * p.scale_log2 : -INFINITY;
+    }
+    __syncthreads();
+    online_fold(&A.sc[0][0], CA, CA, G, sm.m_run, sm.l_run, sm.scale_old, tid);
+    __syncthreads();
+    float acc[G][GE::VEC];
+    acc_zero<T, D, G>(acc);
+    acc_rows<T, D, G, NJ>(acc, vv, &A.sc[0][0], CA, na, rgrp);
+    rows_to_red<T, D, G>(sm, acc, tid);
+    __syncthreads();
+    write_partial<T, D, G>(p, sm, pair, chunk, tid);
+    stores_done_barrier();
+    count_partials<T, D, G>(p, sm, pair, 1u, tid);
 }
 
 // ---------------------------------------------------------------------------
-// zoom item: one selected span, attended through its factors
+// zoom item, fused per-item selection: rank the pair's candidates (LDS)
+// ---------------------------------------------------------------------------
+template <class T, int D, int G>
+__device__ void rank_candidates(const Params &p, Smem<T, D, G> &sm, int pair, int j, int m_b,
+                                int tid, int &n_loser) {
+    auto &Z = sm.u.zoom;
+    const int k = p.k, kc = p.kc;
+    const int n_cand = p.n_rc * kc;
+    for (int c = tid; c < kMergeBuf; c += NT) {
+        uint4 e = make_uint4(0, 0, kInvalidIdx - uint32_t(c), 0);
+        if (c < n_cand) {
+            const int chunk = c / kc, jj = c % kc;
+            if (jj < ld_shared(&p.cand_cnt[pair * p.n_rc + chunk])) {
+                const size_t ci = (size_t(pair) * p.n_rc + chunk) * kc + jj;
+                const uint64_t key = ld_shared(&p.cand_key[ci]);
+                e = make_uint4(uint32_t(key), uint32_t(key >> 32), uint32_t(ld_shared(&p.cand_idx[ci])), 0);
+#pragma unroll
+                for (int hl = 0; hl < G; ++hl) Z.cand_lg[c][hl] = ld_shared(&p.cand_lg[ci * G + hl]);
+            }
+        }
+        Z.cand[c] = e;
+    }
+    if (tid < kMaxTopK) Z.sel[tid] = -1;
+    if (tid == 0) sm.bcast[3] = 0;
+    __syncthreads();
+    // rank = number of candidates ahead in (key desc, span asc); reads stay independent
+    int n_valid_local = 0;
+    for (int c = tid; c < n_cand; c += NT) {
+        const uint4 me = Z.cand[c];
+        if (me.z >= 0x80000000u) continue;
+        ++n_valid_local;
+        const uint64_t mk = (uint64_t(me.y) << 32) | me.x;
+        int rank = 0;
+        int o = 0;
+        for (; o + 8 <= n_cand; o += 8) {
+            uint4 e[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) e[u] = Z.cand[o + u];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                rank += better((uint64_t(e[u].y) << 32) | e[u].x, e[u].z, mk, me.z) ? 1 : 0;
+        }
+        for (; o < n_cand; ++o) {
+            const uint4 e = Z.cand[o];
+            rank += better((uint64_t(e.y) << 32) | e.x, e.z, mk, me.z) ? 1 : 0;
+        }
+        Z.cand[c].w = uint32_t(rank);
+        if (rank < k && rank < m_b) Z.sel[rank] = int32_t(me.z);
+    }
+    // number of valid candidates (wave sums, then LDS)
+    int nvl = n_valid_local;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) nvl += __shfl_xor(nvl, o, 64);
+    if ((tid & 63) == 0) atomicAdd(&sm.bcast[3], nvl);
+    __syncthreads();
+    // losing candidates of this item: ranks k + j, 2k + j, ...  (deterministic slots)
+    const int n_valid = sm.bcast[3];
+    const int n_lose_all = max(0, n_valid - k);
+    n_loser = (n_lose_all > j) ? (n_lose_all - j + k - 1) / k : 0;
+    for (int c = tid; c < n_cand; c += NT) {
+        const uint4 me = Z.cand[c];
+        if (me.z >= 0x80000000u) continue;
+        const int rank = int(me.w);
+        if (rank >= k && ((rank - k) % k) == j) {
+            const int slot = (rank - k) / k;
+            if (slot < kLoserWin) {
+                Z.loser[slot] = int32_t(me.z);
+#pragma unroll
+                for (int hl = 0; hl < G; ++hl) Z.lw[hl][slot] = Z.cand_lg[c][hl] * kLog2e;
+            }
+        }
+    }
+    __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// zoom item: one selection slot of a pair, attended through the span's factors
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
 __device__ void zoom_item(const Params &p, Smem<T, D, G> &sm, int pair, int j, int tid) {
+    using GE = Geo<T, D>;
     auto &Z = sm.u.zoom;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
     const int r = p.r;
-    // which span
+    int m_b = p.n_spans[b];
+    m_b = m_b < 0 ? 0 : (m_b > p.M_max ? p.M_max : m_b);
+    const bool per_item_select = (p.mode == kModeFused) && !p.merger;
+    const int rgrp = tid / GE::RV, col = tid % GE::RV;
+    // the query does not depend on the selection: stage it first
+    for (int i = tid; i < G * D; i += NT) {
+        const int hl = i / D, d = i % D;
+        Z.qf[hl][d] = T::load1(p.q, (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d);
+    }
+    online_reset(G, sm.m_run, sm.l_run, sm.scale_old, tid);
+    // wait for the pair's routing (fused mode)
     if (tid == 0) {
-        int S;
+        bool ok = true;
         if (p.mode == kModeFused) {
             uint32_t n = 0;
-            while (load_acquire(&p.sel_ready[pair]) == 0u) {
-                __builtin_amdgcn_s_sleep(2);
-                if (++n > kSpinLimit) { flag_error(p, kErrSpinTimeout); break; }
+            const uint32_t *flag = per_item_select ? &p.route_cnt[pair] : &p.sel_ready[pair];
+            const uint32_t target = per_item_select ? uint32_t(p.n_rc) : 1u;
+            while (ld_shared(flag) < target) {
+                __builtin_amdgcn_s_sleep(1);
+                if (++n > kSpinLimit) { flag_error(p, kErrSpinTimeout); ok = false; break; }
             }
-            S = __hip_atomic_load(&p.sel_ws[size_t(pair) * p.k + j], __ATOMIC_RELAXED,
-                                  __HIP_MEMORY_SCOPE_AGENT);
-            if (n > kSpinLimit) S = -1;
+        }
+        sm.bcast[2] = ok;
+    }
+    __syncthreads();
+    int n_loser = 0;
+    int S = -1;
+    if (sm.bcast[2]) {
+        if (per_item_select) {
+            rank_candidates<T, D, G>(p, sm, pair, j, m_b, tid, n_loser);
+            S = Z.sel[j];
+            if (tid == 0 && p.sel_out) p.sel_out[size_t(pair) * p.k + j] = S;
+        } else if (p.mode == kModeFused) {
+            const int32_t *rec = reinterpret_cast<const int32_t *>(&p.zrec[size_t(pair) * p.k + j]);
+            S = ld_shared(rec);
         } else {
             S = p.sel_in[size_t(pair) * p.k + j];
         }
-        int m_b = p.n_spans[b];
-        m_b = m_b < 0 ? 0 : (m_b > p.M_max ? p.M_max : m_b);
-        if (S >= m_b) { flag_error(p, kErrSelRange); S = -1; }
+    }
+    if (tid == 0) {
         int L = 0;
         int64_t off = 0;
+        if (S >= m_b) { flag_error(p, kErrSelRange); S = -1; }
         if (S >= 0) {
             L = p.span_len[size_t(b) * p.M_max + S];
             off = p.block_off[(size_t(b) * p.Hkv + g) * p.M_max + S];
@@ -695,153 +900,163 @@ __device__ void zoom_item(const Params &p, Smem<T, D, G> &sm, int pair, int j, i
                 S = -1;
             }
         }
-        sm.bcast[0] = S;
-        sm.bcast[1] = L;
-        sm.bcast[2] = int32_t(off & 0xFFFFFFFF);
-        sm.bcast[3] = int32_t(off >> 32);
+        sm.bcast[4] = S;
+        sm.bcast[5] = L;
+        sm.bcast[6] = int32_t(off & 0xFFFFFFFF);
+        sm.bcast[7] = int32_t(off >> 32);
     }
-    if (p.mode == kModeFused) fence_acquire();
     __syncthreads();
-    const int S = sm.bcast[0];
-    const int L = sm.bcast[1];
-    const int64_t off = int64_t(uint32_t(sm.bcast[2])) | (int64_t(sm.bcast[3]) << 32);
-    __syncthreads();
-
-    constexpr int NOUT = (G * D + NT - 1) / NT;
-    float acc[NOUT];
-    online_reset<T, D, G>(sm, acc, tid);
+    S = sm.bcast[4];
+    const int L = sm.bcast[5];
+    const int64_t off = int64_t(uint32_t(sm.bcast[6])) | (int64_t(sm.bcast[7]) << 32);
     const int slot = p.slot_zoom0 + j;
-    if (S >= 0) {
-        constexpr int VEC = T::kVec;
-        constexpr int RV = D * T::kBytes / 16;          // vectors per d-row
-        constexpr int RS = D * T::kBytes + 16;
-        const int RU = r * T::kBytes / 16;              // vectors per U row
-        const unsigned char *UK = p.factors + off;
-        const unsigned char *sK = UK + size_t(L) * r * T::kBytes;
-        const unsigned char *VtK = sK + size_t(r) * T::kBytes;
-        const unsigned char *UV = VtK + size_t(r) * D * T::kBytes;
-        const unsigned char *sV = UV + size_t(L) * r * T::kBytes;
-        const unsigned char *VtV = sV + size_t(r) * T::kBytes;
+    float acc[G][GE::VEC];
+    acc_zero<T, D, G>(acc);
 
-        // stage q (float), sigmas, and Vt_V rows (into kb) for the final projection
-        for (int i = tid; i < G * D; i += NT) {
-            const int hl = i / D, d = i % D;
-            Z.qf[hl][d] = T::load1(p.q, (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d);
+    constexpr int VEC = GE::VEC;
+    constexpr int RV = GE::RV;
+    constexpr int NVT = (kMaxTopK * RV + NT - 1) / NT;   // Vt vectors per thread at r = 64
+    const int RU = r * T::kBytes / 16;                  // vectors per U row
+    const unsigned char *UK = p.factors + off;
+    const unsigned char *sK = UK + size_t(L) * r * T::kBytes;
+    const unsigned char *VtK = sK + size_t(r) * T::kBytes;
+    const unsigned char *UV = VtK + size_t(r) * D * T::kBytes;
+    const unsigned char *sV = UV + size_t(L) * r * T::kBytes;
+    const unsigned char *VtV = sV + size_t(r) * T::kBytes;
+    const int ucol = tid % RU;                          // fixed per thread (NT % RU == 0)
+    int nb_max = (8 * NT) / RU;
+    if (nb_max > kZoomBlock) nb_max = kZoomBlock;
+    const int nb0 = min(nb_max, L);
+
+    // issue: Vt_K, Vt_V (row i, column c) and the first token block of U_K, U_V
+    uint4 vk[NVT], vvt[NVT], uk[8], uv[8];
+    if (S >= 0) {
+#pragma unroll
+        for (int u = 0; u < NVT; ++u) {
+            const int vi = tid + NT * u;
+            if (vi < r * RV) {
+                vk[u] = ld16(VtK + size_t(vi / RV) * GE::RB + (vi % RV) * 16);
+                vvt[u] = ld16(VtV + size_t(vi / RV) * GE::RB + (vi % RV) * 16);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int tok = (tid + NT * u) / RU;
+            if (tok < nb0) {
+                uk[u] = ld16(UK + size_t(tok) * r * T::kBytes + ucol * 16);
+                uv[u] = ld16(UV + size_t(tok) * r * T::kBytes + ucol * 16);
+            }
         }
         if (tid < r) {
             Z.sig[0][tid] = T::load1(sK, tid);
             Z.sig[1][tid] = T::load1(sV, tid);
         }
-        copy_rows_to_lds<T, D>(Z.vt, VtV, r, tid);
-        __syncthreads();
+    }
 
+    // losing candidates of this item: coarse entries (v_bar rows, routing scores)
+    if (n_loser > 0) {
+        constexpr int NJL = (kLoserWin + GE::RPP - 1) / GE::RPP;
+        const unsigned char *sv = reinterpret_cast<const unsigned char *>(p.sum_v) +
+                                  (size_t(b) * p.Hkv + g) * size_t(p.M_max) * GE::RB;
+        const int nl = min(n_loser, kLoserWin);
+        uint4 lv[NJL];
+#pragma unroll
+        for (int jj = 0; jj < NJL; ++jj) {
+            const int row = rgrp + GE::RPP * jj;
+            if (row < nl) lv[jj] = ld16(sv + size_t(Z.loser[row]) * GE::RB + col * 16);
+        }
+        if (tid < G)
+            for (int i = nl; i < kLoserWin; ++i) Z.lw[tid][i] = -INFINITY;
+        __syncthreads();
+        online_fold(&Z.lw[0][0], kLoserWin, nl, G, sm.m_run, sm.l_run, sm.scale_old, tid);
+        __syncthreads();
+        acc_rows<T, D, G, NJL>(acc, lv, &Z.lw[0][0], kLoserWin, nl, rgrp);
+    }
+
+    if (S >= 0) {
+        __syncthreads();
         // w[h][i] = scale*log2e * sigma_K[i] * (Vt_K[i] . q_h)
-        for (int v0 = 0; v0 < r * RV; v0 += NT) {
-            const int v = v0 + tid;
+#pragma unroll
+        for (int u = 0; u < NVT; ++u) {
+            const int vi = tid + NT * u;
+            const int row = vi / RV, c = vi % RV;
             float part[G];
 #pragma unroll
             for (int hl = 0; hl < G; ++hl) part[hl] = 0.0f;
-            const int row = v / RV, col = v % RV;
-            if (v < r * RV) {
+            if (vi < r * RV) {
                 float f[VEC];
-                T::unpack(ld16(VtK + size_t(row) * D * T::kBytes + col * 16), f);
+                T::unpack(vk[u], f);
 #pragma unroll
                 for (int hl = 0; hl < G; ++hl)
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) part[hl] += Z.qf[hl][col * VEC + e] * f[e];
+                    for (int e = 0; e < VEC; ++e) part[hl] += Z.qf[hl][c * VEC + e] * f[e];
             }
 #pragma unroll
             for (int o = 1; o < RV; o <<= 1)
 #pragma unroll
                 for (int hl = 0; hl < G; ++hl) part[hl] += __shfl_xor(part[hl], o, 64);
-            if (v < r * RV && col == 0)
+            if (vi < r * RV && c == 0)
 #pragma unroll
-                for (int hl = 0; hl < G; ++hl) Z.w[hl][row] = part[hl] * Z.sig[0][row] * p.scale_log2;
+                for (int hl = 0; hl < G; ++hl)
+                    Z.w[hl][row] = part[hl] * Z.sig[0][row] * p.scale_log2;
         }
         __syncthreads();
 
-        // token blocks: scores via U_K, online softmax, y accumulation via U_V
+        // token blocks: scores via U_K, online softmax, y = p^T U_V accumulated per lane
         float yacc[G][VEC];
 #pragma unroll
         for (int hl = 0; hl < G; ++hl)
 #pragma unroll
             for (int e = 0; e < VEC; ++e) yacc[hl][e] = 0.0f;
-        const int col = tid % RU;                       // fixed per thread (NT % RU == 0)
-        int nb_max = (8 * NT) / RU;
-        if (nb_max > kZoomBlock) nb_max = kZoomBlock;
         const int wave = tid >> 6, lane = tid & 63;
         for (int t0 = 0; t0 < L; t0 += nb_max) {
             const int nb = min(nb_max, L - t0);
-            uint4 uv[8];
-            {
-                uint4 uk[8];
+            if (t0 > 0) {
 #pragma unroll
                 for (int u = 0; u < 8; ++u) {
                     const int tok = (tid + NT * u) / RU;
-                    if (tok < nb) uk[u] = ld16(UK + (size_t(t0 + tok) * r) * T::kBytes + col * 16);
-                }
-                // scores of the block's tokens
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int tok = (tid + NT * u) / RU;
-                    float part[G];
-#pragma unroll
-                    for (int hl = 0; hl < G; ++hl) part[hl] = 0.0f;
                     if (tok < nb) {
-                        float f[VEC];
-                        T::unpack(uk[u], f);
-#pragma unroll
-                        for (int hl = 0; hl < G; ++hl)
-#pragma unroll
-                            for (int e = 0; e < VEC; ++e) part[hl] += f[e] * Z.w[hl][col * VEC + e];
+                        uk[u] = ld16(UK + size_t(t0 + tok) * r * T::kBytes + ucol * 16);
+                        uv[u] = ld16(UV + size_t(t0 + tok) * r * T::kBytes + ucol * 16);
                     }
-                    for (int o = 1; o < RU; o <<= 1)
-#pragma unroll
-                        for (int hl = 0; hl < G; ++hl) part[hl] += __shfl_xor(part[hl], o, 64);
-                    if (tok < nb && col == 0)
-#pragma unroll
-                        for (int hl = 0; hl < G; ++hl) Z.zs[hl][tok] = part[hl];
                 }
             }
-            // value-side rows: in flight while the block's softmax weights are formed
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
                 const int tok = (tid + NT * u) / RU;
-                if (tok < nb) uv[u] = ld16(UV + (size_t(t0 + tok) * r) * T::kBytes + col * 16);
+                float part[G];
+#pragma unroll
+                for (int hl = 0; hl < G; ++hl) part[hl] = 0.0f;
+                if (tok < nb) {
+                    float f[VEC];
+                    T::unpack(uk[u], f);
+#pragma unroll
+                    for (int hl = 0; hl < G; ++hl)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) part[hl] += f[e] * Z.w[hl][ucol * VEC + e];
+                }
+                for (int o = 1; o < RU; o <<= 1)
+#pragma unroll
+                    for (int hl = 0; hl < G; ++hl) part[hl] += __shfl_xor(part[hl], o, 64);
+                if (tok < nb && ucol == 0)
+#pragma unroll
+                    for (int hl = 0; hl < G; ++hl) Z.zs[hl][tok] = part[hl];
             }
             __syncthreads();
-            // block max and weights (wave hl handles head hl)
-            for (int hl = wave; hl < G; hl += 4) {
-                float mx = -INFINITY;
-                for (int t = lane; t < nb; t += 64) mx = fmaxf(mx, Z.zs[hl][t]);
-                mx = wave_max(mx);
-                const float mo = sm.m_run[hl];
-                const float mn = fmaxf(mo, mx);
-                float ls = 0.0f;
-                for (int t = lane; t < nb; t += 64) {
-                    const float w = exp2f(Z.zs[hl][t] - mn);
-                    Z.zs[hl][t] = w;
-                    ls += w;
-                }
-                ls = wave_sum(ls);
-                if (lane == 0) {
-                    const float so = safe_exp2(mo - mn);
-                    sm.scale_old[hl] = so;
-                    sm.l_run[hl] = sm.l_run[hl] * so + ls;
-                    sm.m_run[hl] = mn;
-                }
-            }
+            online_fold(&Z.zs[0][0], kZoomBlock, nb, G, sm.m_run, sm.l_run, sm.scale_old, tid);
             __syncthreads();
 #pragma unroll
             for (int hl = 0; hl < G; ++hl) {
                 const float so = sm.scale_old[hl];
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) yacc[hl][e] *= so;
+                for (int e = 0; e < VEC; ++e) {
+                    yacc[hl][e] *= so;
+                    acc[hl][e] *= so;
+                }
             }
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
-                const int v = tid + NT * u;
-                const int tok = v / RU;
+                const int tok = (tid + NT * u) / RU;
                 if (tok < nb) {
                     float f[VEC];
                     T::unpack(uv[u], f);
@@ -855,7 +1070,7 @@ __device__ void zoom_item(const Params &p, Smem<T, D, G> &sm, int pair, int j, i
             }
             __syncthreads();
         }
-        // reduce yacc over the lanes sharing `col` (lane ^ RU, 2RU, ... within a wave)
+        // y[h][i]: sum yacc over the lanes sharing ucol, then over the waves
         for (int o = RU; o < 64; o <<= 1)
 #pragma unroll
             for (int hl = 0; hl < G; ++hl)
@@ -865,30 +1080,37 @@ __device__ void zoom_item(const Params &p, Smem<T, D, G> &sm, int pair, int j, i
 #pragma unroll
             for (int hl = 0; hl < G; ++hl)
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) Z.red[wave][hl][col * VEC + e] = yacc[hl][e];
+                for (int e = 0; e < VEC; ++e) Z.yr[wave][hl][ucol * VEC + e] = yacc[hl][e];
         __syncthreads();
         for (int t = tid; t < G * r; t += NT) {
             const int hl = t / r, i = t % r;
-            const float y = Z.red[0][hl][i] + Z.red[1][hl][i] + Z.red[2][hl][i] + Z.red[3][hl][i];
-            Z.y[hl][i] = y * Z.sig[1][i];
+            Z.y[hl][i] = (Z.yr[0][hl][i] + Z.yr[1][hl][i] + Z.yr[2][hl][i] + Z.yr[3][hl][i]) *
+                         Z.sig[1][i];
         }
         __syncthreads();
-        // o[h][d] = sum_i y~[h][i] Vt_V[i][d]
+        // o[h][:] += sum_i y~[h][i] Vt_V[i][:]; Vt_V rows of column c sit RV lanes apart,
+        // exactly like summary rows
 #pragma unroll
-        for (int u = 0; u < NOUT; ++u) {
-            const int o = tid + NT * u;
-            if (o < G * D) {
-                const int hl = o / D, d = o % D;
-                float a = 0.0f;
-                for (int i = 0; i < r; ++i) a += Z.y[hl][i] * lds_elem<T, D>(Z.vt, i, d);
-                acc[u] = a;
+        for (int u = 0; u < NVT; ++u) {
+            const int vi = tid + NT * u;
+            if (vi < r * RV) {
+                const int row = vi / RV;
+                float f[VEC];
+                T::unpack(vvt[u], f);
+#pragma unroll
+                for (int hl = 0; hl < G; ++hl) {
+                    const float y = Z.y[hl][row];
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) acc[hl][e] += y * f[e];
+                }
             }
         }
-        (void)RS;
     }
-    write_partial<T, D, G>(p, sm, pair, slot, acc, tid);
-    const int n_parts = (p.mode == kModeFused) ? p.n_ac + p.n_rc + 1 + p.k : p.n_ac + p.n_rc + p.k;
-    finish_partial<T, D, G>(p, sm, pair, n_parts, tid);
+    rows_to_red<T, D, G>(sm, acc, tid);
+    __syncthreads();
+    write_partial<T, D, G>(p, sm, pair, slot, tid);
+    stores_done_barrier();
+    count_partials<T, D, G>(p, sm, pair, 1u, tid);
 }
 
 // ---------------------------------------------------------------------------
@@ -899,41 +1121,29 @@ __global__ void __launch_bounds__(NT, 2) sekv_step_kernel(Params p) {
     __shared__ Smem<T, D, G> sm;
     const int tid = threadIdx.x;
     const int n_items = p.end_zoom;
-    // items that never wait are taken statically by the first workgroups
-    const int n_static = min(p.grid, p.end_anchor);
-    int item;
-    if (int(blockIdx.x) < n_static) {
-        item = blockIdx.x;
-    } else {
-        if (tid == 0) sm.bcast[2] = n_static + int(atomic_add_relaxed(&p.hdr->ticket, 1u));
-        __syncthreads();
-        item = sm.bcast[2];
-        __syncthreads();
-    }
-    while (item < n_items) {
+    for (int item = blockIdx.x; item < n_items; item += p.grid) {
+        // an opaque copy of the thread index keeps per-thread address arithmetic inside
+        // each item instead of alive across the whole loop (register pressure)
+        int t;
+        asm volatile("v_mov_b32 %0, %1" : "=v"(t) : "v"(tid));
         if (item < p.end_route) {
-            route_item<T, D, G>(p, sm, item / p.n_rc, item % p.n_rc, tid);
+            route_item<T, D, G>(p, sm, item / p.n_rc, item % p.n_rc, t);
         } else if (item < p.end_anchor) {
             const int i = item - p.end_route;
-            anchor_item<T, D, G>(p, sm, i / p.n_ac, i % p.n_ac, tid);
+            anchor_item<T, D, G>(p, sm, i / p.n_ac, i % p.n_ac, t);
         } else {
             const int i = item - p.end_anchor;
-            zoom_item<T, D, G>(p, sm, i / p.k, i % p.k, tid);
+            zoom_item<T, D, G>(p, sm, i / p.k, i % p.k, t);
         }
-        __syncthreads();
-        if (tid == 0) sm.bcast[2] = n_static + int(atomic_add_relaxed(&p.hdr->ticket, 1u));
-        __syncthreads();
-        item = sm.bcast[2];
         __syncthreads();
     }
     // shutdown: the last workgroup out zeroes the counters for the next launch
     if (tid == 0) {
-        const uint32_t prev = atomic_add_acqrel(&p.hdr->exit_count, 1u);
+        const uint32_t prev = counter_add(&p.hdr->exit_count, 1u);
         sm.bcast[3] = (prev == uint32_t(p.grid - 1));
     }
     __syncthreads();
     if (sm.bcast[3]) {
-        fence_acquire();
         const int P = p.B * p.Hkv;
         for (int i = tid; i < P; i += NT) {
             p.route_cnt[i] = 0u;
