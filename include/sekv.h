@@ -69,7 +69,7 @@ typedef struct {
     int32_t n_q_heads;      /* Hq; query head h reads KV head h / (Hq / Hkv)             */
     int32_t n_kv_heads;     /* Hkv; Hq / Hkv in {1, 2, 4, 8}                             */
     int32_t head_dim;       /* d in {64, 128}                                            */
-    int32_t rank;           /* r: factor rank, multiple of 8, 8 <= r <= 64               */
+    int32_t rank;           /* r: factor rank, one of 8, 16, 32, 64                      */
     int32_t top_k;          /* k: spans expanded per (sequence, KV head), 0 <= k <= 64   */
     int32_t max_anchors;    /* A_max >= 0: row stride of the anchor arrays               */
     int32_t max_spans;      /* M_max >= 1: row stride of the span arrays                 */

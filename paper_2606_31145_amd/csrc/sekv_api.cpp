@@ -43,8 +43,8 @@ sekv_status check_dims_impl(const sekv_dims *d) {
         return fail(SEKV_ERR_UNSUPPORTED, "group size %d not in {1,2,4,8}", G);
     if (d->head_dim != 64 && d->head_dim != 128)
         return fail(SEKV_ERR_UNSUPPORTED, "head_dim %d not in {64,128}", d->head_dim);
-    if (d->rank < 8 || d->rank > 64 || d->rank % 8)
-        return fail(SEKV_ERR_UNSUPPORTED, "rank %d: need a multiple of 8 in [8,64]", d->rank);
+    if (d->rank != 8 && d->rank != 16 && d->rank != 32 && d->rank != 64)
+        return fail(SEKV_ERR_UNSUPPORTED, "rank %d: need 8, 16, 32 or 64", d->rank);
     if (d->top_k < 0 || d->top_k > sekv::kMaxTopK)
         return fail(SEKV_ERR_UNSUPPORTED, "top_k %d not in [0,%d]", d->top_k, sekv::kMaxTopK);
     if (d->max_anchors < 0) return fail(SEKV_ERR_INVALID_ARG, "max_anchors < 0");
@@ -184,16 +184,18 @@ sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_
     p.zrec = reinterpret_cast<int4 *>(w + L.zrec);
     p.cand_key = reinterpret_cast<uint64_t *>(w + L.cand_key);
     p.cand_idx = reinterpret_cast<int32_t *>(w + L.cand_idx);
+    p.cand_len = reinterpret_cast<int32_t *>(w + L.cand_len);
+    p.cand_off = reinterpret_cast<int64_t *>(w + L.cand_off);
     p.cand_cnt = reinterpret_cast<int32_t *>(w + L.cand_cnt);
     p.cand_lg = reinterpret_cast<float *>(w + L.cand_lg);
     p.part_ml = reinterpret_cast<float *>(w + L.part_ml);
     p.part_o = reinterpret_cast<float *>(w + L.part_o);
 
     // Fused mode ranks the candidates inside every zoom item when they fit its LDS
-    // buffers (<= kMergeBuf candidates and <= kLoserWin losing candidates per item);
+    // buffers (<= kMergeBuf candidates and <= kZoomLosers losing candidates per item);
     // otherwise one workgroup per pair merges them.
     const long long n_cand = (long long)s.n_rc * s.kc;
-    const bool per_item = n_cand <= sekv::kMergeBuf && n_cand <= (long long)s.k * (sekv::kLoserWin + 1);
+    const bool per_item = n_cand <= sekv::kMergeBuf && n_cand <= (long long)s.k * (sekv::kZoomLosers + 1);
     p.merger = (mode == sekv::kModeRoute) || (mode == sekv::kModeFused && !per_item);
     const int cap = resident(d->dtype, d->head_dim, s.G);
     p.grid = std::max(1, std::min(p.end_zoom, cap));

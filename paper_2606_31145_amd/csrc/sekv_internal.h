@@ -14,13 +14,14 @@ namespace sekv {
 
 // Work decomposition (compile-time tile sizes).
 constexpr int kThreads = 256;      // threads per workgroup: 4 wave64s
-constexpr int kRouteChunk = 64;    // spans per routing / summary work item
+constexpr int kRouteChunk = 128;   // spans per routing / summary work item
 // Anchor tokens per anchor work item: 8 key + 8 value vectors of 16 bytes per thread.
 constexpr int anchor_chunk(int elem_bytes, int head_dim) { return 32768 / (head_dim * elem_bytes); }
 constexpr int kZoomBlock = 512;    // tokens of a zoomed span scored per LDS pass
 constexpr int kMaxTopK = 64;
 constexpr int kMergeBuf = 512;     // candidates ranked in LDS
-constexpr int kLoserWin = 128;     // losing candidates folded per window
+constexpr int kLoserWin = 128;     // losing candidates folded per window (single merger)
+constexpr int kZoomLosers = 32;    // losing candidates folded by one zoom item, at most
 
 enum Mode : int32_t { kModeRoute = 0, kModeAttend = 1, kModeFused = 2 };
 
@@ -42,6 +43,8 @@ struct WsLayout {
     size_t zrec;                              // int32x4 [P][k]: span, |S|, offset lo/hi
     size_t cand_key;                          // uint64 [P][n_rc][kc]
     size_t cand_idx;                          // int32  [P][n_rc][kc]
+    size_t cand_len;                          // int32  [P][n_rc][kc]  |S|
+    size_t cand_off;                          // int64  [P][n_rc][kc]  block offset
     size_t cand_cnt;                          // int32  [P][n_rc]
     size_t cand_lg;                           // float  [P][n_rc][kc][G]
     size_t part_ml;                           // float  [P][n_slots][G][2]
@@ -87,6 +90,8 @@ inline WsLayout make_layout(const Shape &s) {
     const size_t nc = P * size_t(s.n_rc) * size_t(s.kc > 0 ? s.kc : 1);
     L.cand_key = o;  o = align256(o + 8 * nc);
     L.cand_idx = o;  o = align256(o + 4 * nc);
+    L.cand_len = o;  o = align256(o + 4 * nc);
+    L.cand_off = o;  o = align256(o + 8 * nc);
     L.cand_cnt = o;  o = align256(o + 4 * P * size_t(s.n_rc));
     L.cand_lg = o;   o = align256(o + 4 * nc * size_t(s.G));
     const size_t ns = P * size_t(s.n_slots) * size_t(s.G);
@@ -131,7 +136,8 @@ struct Params {
     uint32_t *route_cnt, *sel_ready, *part_cnt;
     int4 *zrec;
     uint64_t *cand_key;
-    int32_t *cand_idx, *cand_cnt;
+    int32_t *cand_idx, *cand_len, *cand_cnt;
+    int64_t *cand_off;
     float *cand_lg;
     float *part_ml, *part_o;
 };

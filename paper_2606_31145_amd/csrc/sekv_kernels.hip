@@ -1,7 +1,7 @@
 // SeKV decode step for gfx950: one persistent kernel over typed work items.
 //
 // Work items (per (sequence b, KV head g) "pair"):
-//   route   chunk of 64 spans: routing scores in float64 (eq. routing_gate with the
+//   route   chunk of 128 spans: routing scores in float64 (eq. routing_gate with the
 //           coarse mean key as summary), the chunk's local top-k as sorted candidates,
 //           and -- fused mode -- the coarse softmax partial of its non-candidate spans,
 //           so each summary row (k_bar, v_bar) is read from HBM once.
@@ -111,15 +111,110 @@ __device__ inline bool better(uint64_t ka, uint32_t ia, uint64_t kb, uint32_t ib
     return ka > kb || (ka == kb && ia < ib);
 }
 
-__device__ inline float wave_max(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+// ---------------------------------------------------------------------------
+// lane reductions without LDS: DPP row operations inside 16-lane rows and the
+// gfx950 permlane swaps across rows.  With both operands equal, permlane16_swap /
+// permlane32_swap return the two halves whose sum is the xor-16 / xor-32 butterfly.
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ inline float dpp_mov(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ inline uint32_t dpp_mov_u(uint32_t v) {
+    return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppRor4 = 0x124;       // row_ror:4
+constexpr int kDppRor8 = 0x128;       // row_ror:8  (= xor 8 inside a row)
+constexpr int kDppHalfMirror = 0x141; // row_half_mirror
+
+struct OpSum { __device__ static float f(float a, float b) { return a + b; } };
+struct OpMax { __device__ static float f(float a, float b) { return fmaxf(a, b); } };
+
+template <class Op>
+__device__ inline float perm16(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return Op::f(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+template <class Op>
+__device__ inline float perm32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return Op::f(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Reduce over the lanes whose index differs only in bits [LO, HI); every lane gets
+// the result.  Bit 2 alone (without bits 2 and 3 together) needs bits 0 and 1 reduced.
+template <int LO, int HI, class Op = OpSum>
+__device__ inline float lane_reduce(float v) {
+    static_assert(!(HI == 3 && LO != 0), "bit 2 alone needs bits 0-1 reduced first");
+    if constexpr (LO <= 0 && 0 < HI) v = Op::f(v, dpp_mov<kDppXor1>(v));
+    if constexpr (LO <= 1 && 1 < HI) v = Op::f(v, dpp_mov<kDppXor2>(v));
+    if constexpr (LO <= 2 && 3 < HI) {
+        v = Op::f(v, dpp_mov<kDppRor4>(v));
+        v = Op::f(v, dpp_mov<kDppRor8>(v));
+    } else if constexpr (LO <= 2 && 2 < HI) {
+        v = Op::f(v, dpp_mov<kDppHalfMirror>(v));
+    } else if constexpr (LO <= 3 && 3 < HI) {
+        v = Op::f(v, dpp_mov<kDppRor8>(v));
+    }
+    if constexpr (LO <= 4 && 4 < HI) v = perm16<Op>(v);
+    if constexpr (LO <= 5 && 5 < HI) v = perm32<Op>(v);
     return v;
 }
-__device__ inline float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
+
+__device__ inline float wave_max(float v) { return lane_reduce<0, 6, OpMax>(v); }
+__device__ inline float wave_sum(float v) { return lane_reduce<0, 6, OpSum>(v); }
+
+// Sum over the n lanes of an aligned group of n (n in {1,2,4,8,16}); runtime n.
+__device__ inline float group_sum(float v, int n) {
+    switch (n) {
+        case 1: return v;
+        case 2: return lane_reduce<0, 1>(v);
+        case 4: return lane_reduce<0, 2>(v);
+        case 8: return lane_reduce<0, 3>(v);
+        default: return lane_reduce<0, 4>(v);
+    }
+}
+// Sum over the lanes that share lane % n (n in {1,2,4,8,16}); runtime n.
+__device__ inline float stride_sum(float v, int n) {
+    switch (n) {
+        case 1: return lane_reduce<0, 6>(v);
+        case 2: return lane_reduce<1, 6>(v);
+        case 4: return lane_reduce<2, 6>(v);
+        case 8: return lane_reduce<3, 6>(v);
+        default: return lane_reduce<4, 6>(v);
+    }
+}
+template <int RV>
+__device__ inline float row_sum(float v) {     // sum over an aligned group of RV lanes
+    if constexpr (RV == 8) return lane_reduce<0, 3>(v);
+    else if constexpr (RV == 16) return lane_reduce<0, 4>(v);
+    else return lane_reduce<0, 5>(v);
+}
+template <int RV>
+__device__ inline float col_sum(float v) {     // sum over the lanes sharing lane % RV
+    if constexpr (RV == 8) return lane_reduce<3, 6>(v);
+    else if constexpr (RV == 16) return lane_reduce<4, 6>(v);
+    else return lane_reduce<5, 6>(v);
+}
+
+// Value of the lane at index ^ S (bitonic partner), 32-bit.
+template <int S>
+__device__ inline uint32_t lane_xor(uint32_t v, int lane) {
+    if constexpr (S == 1) return dpp_mov_u<kDppXor1>(v);
+    else if constexpr (S == 2) return dpp_mov_u<kDppXor2>(v);
+    else if constexpr (S == 8) return dpp_mov_u<kDppRor8>(v);
+    else if constexpr (S == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        return (lane & 16) ? r[0] : r[1];
+    } else if constexpr (S == 32) {
+        const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+        return (lane & 32) ? r[0] : r[1];
+    } else {
+        return uint32_t(__shfl_xor(int(v), S, 64));
+    }
 }
 __device__ inline float safe_exp2(float x) { return x == -INFINITY ? 0.0f : exp2f(x); }
 
@@ -160,6 +255,10 @@ struct Smem {
         double lg[G][CR];                                // routing scores, natural units
         float pw[G][CR];                                 // coarse weights
         int32_t excl[CR];                                // 1 = candidate / selected
+        int32_t slen[CR];                                // |S| of the chunk's spans
+        int64_t boff[CR];                                // their block offsets
+        uint64_t skey[2][64];                            // two sorted halves of the chunk
+        uint32_t sidx[2][64];
     };
     struct Anchor {
         float qf[G][D];
@@ -167,16 +266,13 @@ struct Smem {
     };
     struct Zoom {
         float qf[G][D];
-        uint4 cand[kMergeBuf];                           // {key lo, key hi, span, rank}
-        float cand_lg[kMergeBuf][G];                     // candidates' natural-unit scores
-        int32_t sel[kMaxTopK];                           // the pair's selection
-        int32_t loser[kLoserWin];                        // this item's losing candidates
-        float lw[G][kLoserWin];                          // their base-2 logits, then weights
+        uint4 cand[kMergeBuf];                           // {key lo, key hi, span, -}
+        int32_t loser[kZoomLosers];                      // this item's losing candidates
+        float lw[G][kZoomLosers];                        // their base-2 logits, then weights
         float w[G][kMaxTopK];                            // scale*log2e*sigma_K*(Vt_K q)
         float zs[G][kZoomBlock];                         // token scores, then weights
         float yr[4][G][kMaxTopK];                        // per-wave partial sums of p^T U_V
         float y[G][kMaxTopK];                            // (p^T U_V) * sigma_V
-        float sig[2][kMaxTopK];                          // sigma_K, sigma_V
     };
     struct Merge {                                       // single-merger selection
         uint64_t key[kMergeBuf];
@@ -250,12 +346,10 @@ __device__ inline void rows_to_red(Smem<T, D, G> &sm, float (&acc)[G][T::kVec], 
     using GE = Geo<T, D>;
     const int lane = tid & 63, wave = tid >> 6;
 #pragma unroll
-    for (int o = GE::RV; o < 64; o <<= 1)
+    for (int hl = 0; hl < G; ++hl)
 #pragma unroll
-        for (int hl = 0; hl < G; ++hl)
-#pragma unroll
-            for (int e = 0; e < GE::VEC; ++e) acc[hl][e] += __shfl_xor(acc[hl][e], o, 64);
-    if (lane < (GE::RV < 64 ? GE::RV : 64)) {
+        for (int e = 0; e < GE::VEC; ++e) acc[hl][e] = col_sum<GE::RV>(acc[hl][e]);
+    if (lane < GE::RV) {
         const int col = tid % GE::RV;
 #pragma unroll
         for (int hl = 0; hl < G; ++hl)
@@ -317,13 +411,26 @@ __device__ inline void online_reset(int G, float *m_run, float *l_run, float *sc
 // final softmax merge of one pair (slot order fixed => deterministic)
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
-__device__ void final_merge(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
+__device__ __forceinline__ void final_merge(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
     auto &F = sm.u.fin;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
     const int ns = p.n_slots;
     const bool use_losers = (p.mode == kModeFused) && p.merger;
     const float *ml = p.part_ml + size_t(pair) * ns * G * 2;
+    const float *po = p.part_o + size_t(pair) * ns * G * D;
+    constexpr int NOUT = (G * D + NT - 1) / NT;
+    // every load first: the (m, l) of all slots to LDS, this thread's o values to registers
+    constexpr int kBatch = 32;                          // slots whose o values are in flight
+    float ov[NOUT][kBatch];
     for (int i = tid; i < ns * G * 2; i += NT) (&F.ml[0][0][0])[i] = ld_shared(ml + i);
+#pragma unroll
+    for (int u = 0; u < NOUT; ++u) {
+        const int o = tid + NT * u;
+        const int hl = o / D, d = o % D;
+#pragma unroll
+        for (int s = 0; s < kBatch; ++s)
+            ov[u][s] = (o < G * D && s < ns) ? ld_shared(po + (size_t(s) * G + hl) * D + d) : 0.0f;
+    }
     __syncthreads();
     const int wave = tid >> 6, lane = tid & 63;
     for (int hl = wave; hl < G; hl += 4) {
@@ -347,22 +454,18 @@ __device__ void final_merge(const Params &p, Smem<T, D, G> &sm, int pair, int ti
         if (lane == 0) F.L[hl] = lsum;
     }
     __syncthreads();
-    const float *po = p.part_o + size_t(pair) * ns * G * D;
-    for (int o = tid; o < G * D; o += NT) {
+#pragma unroll
+    for (int u = 0; u < NOUT; ++u) {
+        const int o = tid + NT * u;
+        if (o >= G * D) continue;
         const int hl = o / D, d = o % D;
         float a = 0.0f;
-        int s = 0;
-        for (; s + 8 <= ns; s += 8) {
-            float v[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = ld_shared(po + (size_t(s + u) * G + hl) * D + d);
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const float wgt = F.wgt[s + u][hl];
-                a += (wgt != 0.0f) ? wgt * v[u] : 0.0f;
-            }
+        for (int s = 0; s < kBatch; ++s) {
+            const float wgt = (s < ns) ? F.wgt[s][hl] : 0.0f;
+            a += (wgt != 0.0f) ? wgt * ov[u][s] : 0.0f;
         }
-        for (; s < ns; ++s) {
+        for (int s = kBatch; s < ns; ++s) {              // rare: more slots than the batch
             const float wgt = F.wgt[s][hl];
             const float v = ld_shared(po + (size_t(s) * G + hl) * D + d);
             a += (wgt != 0.0f) ? wgt * v : 0.0f;
@@ -399,7 +502,7 @@ __device__ inline void count_partials(const Params &p, Smem<T, D, G> &sm, int pa
 // selection by a single merger (route mode, or more candidates than kMergeBuf)
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
-__device__ void merge_selection(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
+__device__ __forceinline__ void merge_selection(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
     auto &M = sm.u.merge;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
     const int k = p.k, kc = p.kc;
@@ -473,7 +576,7 @@ __device__ void merge_selection(const Params &p, Smem<T, D, G> &sm, int pair, in
 
 // Coarse partial over the candidates that lost (single-merger fused mode).
 template <class T, int D, int G>
-__device__ void losers_partial(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
+__device__ __forceinline__ void losers_partial(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
     using GE = Geo<T, D>;
     auto &M = sm.u.merge;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
@@ -527,7 +630,7 @@ __device__ void losers_partial(const Params &p, Smem<T, D, G> &sm, int pair, int
 // route / summary item: one chunk of CR spans of a pair
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
-__device__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chunk, int tid) {
+__device__ __forceinline__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chunk, int tid) {
     using GE = Geo<T, D>;
     auto &R = sm.u.route;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
@@ -541,18 +644,11 @@ __device__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chu
     const bool need_dots = !have_logits;
     const size_t row0 = (size_t(b) * p.Hkv + g) * size_t(p.M_max) + s0;
     const int rgrp = tid / GE::RV, col = tid % GE::RV;
+    const int wave = tid >> 6, lane = tid & 63;
     constexpr int NJ = (CR + GE::RPP - 1) / GE::RPP;
 
-    // 1. issue every load: summary values (registers), summary keys (-> LDS), query, ln|S|
-    uint4 v[NJ];
-    if (need_coarse) {
-        const unsigned char *src = reinterpret_cast<const unsigned char *>(p.sum_v) + row0 * GE::RB;
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            const int row = rgrp + GE::RPP * j;
-            if (row < nv) v[j] = ld16(src + size_t(row) * GE::RB + col * 16);
-        }
-    }
+    // 1. issue the loads routing needs: summary keys (-> LDS), query, ln|S|, and
+    //    |S| / block offsets for the candidate records
     if (need_dots) {
         const unsigned char *src = reinterpret_cast<const unsigned char *>(p.sum_k) + row0 * GE::RB;
         uint4 kv[NJ];
@@ -572,45 +668,67 @@ __device__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chu
             if (row < nv) *reinterpret_cast<uint4 *>(R.kb + size_t(row) * GE::RS + col * 16) = kv[j];
         }
     }
-    __syncthreads();
-
-    // 2. routing scores: float64, products exact, summed left to right over d,
-    //    then (s * scale) + ln|S| as two separately rounded operations.
-    for (int t = tid; t < G * CR; t += NT) {
-        const int hl = t / CR, i = t % CR;
-        double sc = -INFINITY;
-        if (i < nv) {
-            if (need_dots) {
-                const unsigned char *row = R.kb + size_t(i) * GE::RS;
-                double acc = 0.0;
-#pragma unroll 4
-                for (int c = 0; c < GE::RV; ++c) {
-                    float f[GE::VEC];
-                    T::unpack(*reinterpret_cast<const uint4 *>(row + c * 16), f);
-#pragma unroll
-                    for (int e = 0; e < GE::VEC; ++e)
-                        acc = __builtin_fma(R.qd[hl][c * GE::VEC + e], double(f[e]), acc);
-                }
-                {
-#pragma clang fp contract(off)
-                    const double scaled = acc * p.scale;
-                    sc = scaled + R.lns[i];
-                }
-            } else {
-                sc = double(p.logits_in[(size_t(b) * p.Hq + size_t(g) * G + hl) * p.M_max + s0 + i]);
-            }
+    if (tid < CR) {
+        R.excl[tid] = 0;
+        if (!attend && tid < nv) {
+            R.slen[tid] = p.span_len[size_t(b) * p.M_max + s0 + tid];
+            R.boff[tid] = p.block_off[row0 + tid];
         }
-        R.lg[hl][i] = sc;
-        if (p.logits_out && s0 + i < p.M_max)
-            p.logits_out[(size_t(b) * p.Hq + size_t(g) * G + hl) * p.M_max + s0 + i] = float(sc);
     }
     __syncthreads();
 
-    // 3. exclusions: local top-k candidates, sorted (route/fused), or the given selection
+    // 2. routing scores: float64, products exact, summed left to right over d,
+    //    then (s * scale) + ln|S| as two separately rounded operations.  Each thread
+    //    runs two independent chains (same head within a wave, different spans).
+    for (int c0 = tid; c0 < G * CR; c0 += 2 * NT) {
+        const int c1 = c0 + NT;
+        const bool has1 = c1 < G * CR;
+        const int h0 = c0 / CR, i0 = c0 % CR;
+        const int h1 = has1 ? c1 / CR : h0, i1 = has1 ? c1 % CR : i0;
+        double sc0 = -INFINITY, sc1 = -INFINITY;
+        if (need_dots) {
+            const unsigned char *r0 = R.kb + size_t(i0) * GE::RS;
+            const unsigned char *r1 = R.kb + size_t(i1) * GE::RS;
+            double a0 = 0.0, a1 = 0.0;
+#pragma unroll 2
+            for (int c = 0; c < GE::RV; ++c) {
+                float f0[GE::VEC], f1[GE::VEC];
+                T::unpack(*reinterpret_cast<const uint4 *>(r0 + c * 16), f0);
+                T::unpack(*reinterpret_cast<const uint4 *>(r1 + c * 16), f1);
+#pragma unroll
+                for (int e = 0; e < GE::VEC; ++e) {
+                    a0 = __builtin_fma(R.qd[h0][c * GE::VEC + e], double(f0[e]), a0);
+                    a1 = __builtin_fma(R.qd[h1][c * GE::VEC + e], double(f1[e]), a1);
+                }
+            }
+            {
+#pragma clang fp contract(off)
+                const double m0 = a0 * p.scale;
+                const double m1 = a1 * p.scale;
+                if (i0 < nv) sc0 = m0 + R.lns[i0];
+                if (has1 && i1 < nv) sc1 = m1 + R.lns[i1];
+            }
+        } else {
+            const size_t lbase = (size_t(b) * p.Hq + size_t(g) * G) * p.M_max + s0;
+            if (i0 < nv) sc0 = double(p.logits_in[lbase + size_t(h0) * p.M_max + i0]);
+            if (has1 && i1 < nv) sc1 = double(p.logits_in[lbase + size_t(h1) * p.M_max + i1]);
+        }
+        R.lg[h0][i0] = sc0;
+        if (has1) R.lg[h1][i1] = sc1;
+        if (p.logits_out) {
+            const size_t lbase = (size_t(b) * p.Hq + size_t(g) * G) * p.M_max;
+            if (s0 + i0 < p.M_max) p.logits_out[lbase + size_t(h0) * p.M_max + s0 + i0] = float(sc0);
+            if (has1 && s0 + i1 < p.M_max) p.logits_out[lbase + size_t(h1) * p.M_max + s0 + i1] = float(sc1);
+        }
+    }
+    __syncthreads();
+
+    // 3. candidates: waves 0 and 1 each sort 64 (key, span) pairs with a bitonic network;
+    //    a span's rank in the chunk is its position plus the number of better entries of
+    //    the other half (binary search); the best kc become the chunk's sorted candidates.
     if (!attend) {
-        if (tid < 64) {
-            // one wave sorts the chunk's 64 (key, idx) pairs with a bitonic network
-            const int i = tid;
+        if (wave < 2) {
+            const int i = wave * 64 + lane;
             uint64_t key = 0;
             uint32_t idx = kInvalidIdx - uint32_t(i);
             if (i < nv) {
@@ -619,40 +737,90 @@ __device__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chu
                 key = order_key(x);
                 idx = uint32_t(s0 + i);
             }
-            for (int size = 2; size <= 64; size <<= 1) {
-                for (int stride = size >> 1; stride > 0; stride >>= 1) {
-                    const uint32_t klo = __shfl_xor(uint32_t(key), stride, 64);
-                    const uint32_t khi = __shfl_xor(uint32_t(key >> 32), stride, 64);
-                    const uint32_t oi = __shfl_xor(idx, stride, 64);
-                    const uint64_t ok = (uint64_t(khi) << 32) | klo;
-                    const bool lower = (i & stride) == 0;
-                    const bool up = (i & size) == 0;
-                    const bool take = (lower == up) ? better(ok, oi, key, idx) : better(key, idx, ok, oi);
-                    if (take) { key = ok; idx = oi; }
-                }
+#define SEKV_BITONIC_STEP(STRIDE)                                                          \
+            {                                                                              \
+                const uint32_t klo = lane_xor<STRIDE>(uint32_t(key), lane);                \
+                const uint32_t khi = lane_xor<STRIDE>(uint32_t(key >> 32), lane);          \
+                const uint32_t oi = lane_xor<STRIDE>(idx, lane);                           \
+                const uint64_t ok = (uint64_t(khi) << 32) | klo;                           \
+                const bool lower = (lane & (STRIDE)) == 0;                                 \
+                const bool take = (lower == up) ? better(ok, oi, key, idx)                 \
+                                                : better(key, idx, ok, oi);                \
+                if (take) { key = ok; idx = oi; }                                          \
             }
-            // lane j now holds the j-th best
-            const int kc = min(p.kc, nv);
-            R.excl[i] = 0;
-            __builtin_amdgcn_wave_barrier();
-            if (i < kc) {
-                const size_t ci = (size_t(pair) * p.n_rc + chunk) * p.kc + i;
+#pragma unroll
+            for (int size = 2; size <= 64; size <<= 1) {
+                const bool up = (lane & size) == 0;
+                if (size >= 64) SEKV_BITONIC_STEP(32)
+                if (size >= 32) SEKV_BITONIC_STEP(16)
+                if (size >= 16) SEKV_BITONIC_STEP(8)
+                if (size >= 8) SEKV_BITONIC_STEP(4)
+                if (size >= 4) SEKV_BITONIC_STEP(2)
+                SEKV_BITONIC_STEP(1)
+            }
+#undef SEKV_BITONIC_STEP
+            R.skey[wave][lane] = key;
+            R.sidx[wave][lane] = idx;
+        }
+        __syncthreads();
+        const int kc = min(p.kc, nv);
+        if (wave < 2) {
+            const uint64_t key = R.skey[wave][lane];
+            const uint32_t idx = R.sidx[wave][lane];
+            const int other = 1 - wave;
+            int lo = 0, hi = 64;
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (better(R.skey[other][mid], R.sidx[other][mid], key, idx)) lo = mid + 1;
+                else hi = mid;
+            }
+            const int rank = lane + lo;
+            if (idx < 0x80000000u && rank < kc) {
+                const int li = int(idx) - s0;
+                const size_t ci = (size_t(pair) * p.n_rc + chunk) * p.kc + rank;
                 st_shared(&p.cand_key[ci], key);
                 st_shared(&p.cand_idx[ci], int32_t(idx));
-                const int li = int(idx) - s0;
+                st_shared(&p.cand_len[ci], R.slen[li]);
+                st_shared(&p.cand_off[ci], R.boff[li]);
                 for (int hl = 0; hl < G; ++hl) st_shared(&p.cand_lg[ci * G + hl], float(R.lg[hl][li]));
                 R.excl[li] = 1;
             }
-            if (i == 0) st_shared(&p.cand_cnt[pair * p.n_rc + chunk], kc);
         }
-    } else if (tid < CR) {
-        int ex = 0;
-        for (int j = 0; j < p.k; ++j) ex |= (p.sel_in[size_t(pair) * p.k + j] == s0 + tid);
-        R.excl[tid] = ex;
+        if (tid == 0) st_shared(&p.cand_cnt[pair * p.n_rc + chunk], kc);
+        // publish the candidates before the coarse partial: zoom items wait on them
+        stores_done_barrier();
+        if (tid == 0) {
+            sm.bcast[1] = 0;
+            if (p.merger) {
+                const uint32_t prev = counter_add(&p.route_cnt[pair], 1u);
+                sm.bcast[1] = (prev == uint32_t(p.n_rc - 1));
+            } else {
+                (void)counter_add(&p.route_cnt[pair], 1u);     // no return value awaited
+            }
+        }
+        __syncthreads();
+    } else {
+        if (tid < CR) {
+            int ex = 0;
+            for (int j = 0; j < p.k; ++j) ex |= (p.sel_in[size_t(pair) * p.k + j] == s0 + tid);
+            R.excl[tid] = ex;
+        }
+        if (tid == 0) sm.bcast[1] = 0;
+        __syncthreads();
     }
-    __syncthreads();
+    const bool merger = sm.bcast[1] != 0;
 
-    // 4. coarse partial over the chunk's remaining spans (values already in registers)
+    // 4. coarse partial over the chunk's remaining spans
+    uint32_t n_done = 0;
+    uint4 v[NJ];
+    if (need_coarse) {
+        const unsigned char *src = reinterpret_cast<const unsigned char *>(p.sum_v) + row0 * GE::RB;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int row = rgrp + GE::RPP * j;
+            if (row < nv) v[j] = ld16(src + size_t(row) * GE::RB + col * 16);
+        }
+    }
     if (need_coarse) {
         for (int t = tid; t < G * CR; t += NT) {
             const int hl = t / CR, i = t % CR;
@@ -668,36 +836,28 @@ __device__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chu
         rows_to_red<T, D, G>(sm, acc, tid);
         __syncthreads();
         write_partial<T, D, G>(p, sm, pair, p.slot_route0 + chunk, tid);
+        n_done = 1;
     }
-
-    // 5. publish (candidates and partial complete), then count
-    stores_done_barrier();
-    if (tid == 0) {
-        sm.bcast[1] = 0;
-        if (!attend) {
-            const uint32_t prev = counter_add(&p.route_cnt[pair], 1u);
-            sm.bcast[1] = p.merger && (prev == uint32_t(p.n_rc - 1));
-        }
-    }
-    __syncthreads();
-    uint32_t n_done = need_coarse ? 1u : 0u;
-    if (sm.bcast[1]) {
+    if (merger) {
+        __syncthreads();
         merge_selection<T, D, G>(p, sm, pair, tid);
         __syncthreads();
         if (p.mode == kModeFused) {
             losers_partial<T, D, G>(p, sm, pair, tid);
-            stores_done_barrier();
             n_done += 1;
         }
     }
-    if (n_done) count_partials<T, D, G>(p, sm, pair, n_done, tid);
+    if (n_done) {
+        stores_done_barrier();
+        count_partials<T, D, G>(p, sm, pair, n_done, tid);
+    }
 }
 
 // ---------------------------------------------------------------------------
 // anchor item: CA full-resolution tokens of a pair
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
-__device__ void anchor_item(const Params &p, Smem<T, D, G> &sm, int pair, int chunk, int tid) {
+__device__ __forceinline__ void anchor_item(const Params &p, Smem<T, D, G> &sm, int pair, int chunk, int tid) {
     using GE = Geo<T, D>;
     constexpr int CA = Smem<T, D, G>::CA;
     constexpr int NJ = CA / GE::RPP;                     // 8
@@ -742,9 +902,7 @@ __device__ void anchor_item(const Params &p, Smem<T, D, G> &sm, int pair, int ch
                 for (int e = 0; e < GE::VEC; ++e) part[hl] += A.qf[hl][col * GE::VEC + e] * f[e];
         }
 #pragma unroll
-        for (int o = 1; o < GE::RV; o <<= 1)
-#pragma unroll
-            for (int hl = 0; hl < G; ++hl) part[hl] += __shfl_xor(part[hl], o, 64);
+        for (int hl = 0; hl < G; ++hl) part[hl] = row_sum<GE::RV>(part[hl]);
         if (col == 0)
 #pragma unroll
             for (int hl = 0; hl < G; ++hl)
@@ -767,72 +925,88 @@ __device__ void anchor_item(const Params &p, Smem<T, D, G> &sm, int pair, int ch
 // zoom item, fused per-item selection: rank the pair's candidates (LDS)
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
-__device__ void rank_candidates(const Params &p, Smem<T, D, G> &sm, int pair, int j, int m_b,
+__device__ __forceinline__ void rank_candidates(const Params &p, Smem<T, D, G> &sm, int pair, int j, int m_b,
                                 int tid, int &n_loser) {
     auto &Z = sm.u.zoom;
     const int k = p.k, kc = p.kc;
     const int n_cand = p.n_rc * kc;
-    for (int c = tid; c < kMergeBuf; c += NT) {
-        uint4 e = make_uint4(0, 0, kInvalidIdx - uint32_t(c), 0);
+    // each thread owns candidates tid and tid + NT: records stay in its registers
+    constexpr int OWN = kMergeBuf / NT;
+    uint64_t okey[OWN];
+    uint32_t oidx[OWN];
+    int32_t olen[OWN];
+    int64_t ooff[OWN];
+    float olg[OWN][G];
+#pragma unroll
+    for (int u = 0; u < OWN; ++u) {
+        const int c = tid + NT * u;
+        okey[u] = 0;
+        oidx[u] = kInvalidIdx - uint32_t(c);
+        olen[u] = 0;
+        ooff[u] = 0;
         if (c < n_cand) {
             const int chunk = c / kc, jj = c % kc;
             if (jj < ld_shared(&p.cand_cnt[pair * p.n_rc + chunk])) {
                 const size_t ci = (size_t(pair) * p.n_rc + chunk) * kc + jj;
-                const uint64_t key = ld_shared(&p.cand_key[ci]);
-                e = make_uint4(uint32_t(key), uint32_t(key >> 32), uint32_t(ld_shared(&p.cand_idx[ci])), 0);
+                okey[u] = ld_shared(&p.cand_key[ci]);
+                oidx[u] = uint32_t(ld_shared(&p.cand_idx[ci]));
+                olen[u] = ld_shared(&p.cand_len[ci]);
+                ooff[u] = ld_shared(&p.cand_off[ci]);
 #pragma unroll
-                for (int hl = 0; hl < G; ++hl) Z.cand_lg[c][hl] = ld_shared(&p.cand_lg[ci * G + hl]);
+                for (int hl = 0; hl < G; ++hl) olg[u][hl] = ld_shared(&p.cand_lg[ci * G + hl]);
             }
         }
-        Z.cand[c] = e;
+        Z.cand[c] = make_uint4(uint32_t(okey[u]), uint32_t(okey[u] >> 32), oidx[u], 0);
     }
-    if (tid < kMaxTopK) Z.sel[tid] = -1;
-    if (tid == 0) sm.bcast[3] = 0;
+    if (tid == 0) { sm.bcast[3] = 0; sm.bcast[4] = -1; sm.bcast[5] = 0; sm.bcast[6] = 0; sm.bcast[7] = 0; }
     __syncthreads();
-    // rank = number of candidates ahead in (key desc, span asc); reads stay independent
+    // rank = number of candidates ahead in (key desc, span asc); LDS reads batched by 8
+    int rank[OWN];
     int n_valid_local = 0;
-    for (int c = tid; c < n_cand; c += NT) {
-        const uint4 me = Z.cand[c];
-        if (me.z >= 0x80000000u) continue;
+#pragma unroll
+    for (int u = 0; u < OWN; ++u) {
+        rank[u] = -1;
+        const int c = tid + NT * u;
+        if (c >= n_cand || oidx[u] >= 0x80000000u) continue;
         ++n_valid_local;
-        const uint64_t mk = (uint64_t(me.y) << 32) | me.x;
-        int rank = 0;
+        int rk = 0;
         int o = 0;
         for (; o + 8 <= n_cand; o += 8) {
             uint4 e[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) e[u] = Z.cand[o + u];
+            for (int w = 0; w < 8; ++w) e[w] = Z.cand[o + w];
 #pragma unroll
-            for (int u = 0; u < 8; ++u)
-                rank += better((uint64_t(e[u].y) << 32) | e[u].x, e[u].z, mk, me.z) ? 1 : 0;
+            for (int w = 0; w < 8; ++w)
+                rk += better((uint64_t(e[w].y) << 32) | e[w].x, e[w].z, okey[u], oidx[u]) ? 1 : 0;
         }
         for (; o < n_cand; ++o) {
             const uint4 e = Z.cand[o];
-            rank += better((uint64_t(e.y) << 32) | e.x, e.z, mk, me.z) ? 1 : 0;
+            rk += better((uint64_t(e.y) << 32) | e.x, e.z, okey[u], oidx[u]) ? 1 : 0;
         }
-        Z.cand[c].w = uint32_t(rank);
-        if (rank < k && rank < m_b) Z.sel[rank] = int32_t(me.z);
+        rank[u] = rk;
+        if (rk == j && rk < k && rk < m_b) {        // this item's span
+            sm.bcast[4] = int32_t(oidx[u]);
+            sm.bcast[5] = olen[u];
+            sm.bcast[6] = int32_t(ooff[u] & 0xFFFFFFFF);
+            sm.bcast[7] = int32_t(ooff[u] >> 32);
+        }
     }
-    // number of valid candidates (wave sums, then LDS)
-    int nvl = n_valid_local;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) nvl += __shfl_xor(nvl, o, 64);
-    if ((tid & 63) == 0) atomicAdd(&sm.bcast[3], nvl);
+    const float nvl = wave_sum(float(n_valid_local));
+    if ((tid & 63) == 0) atomicAdd(&sm.bcast[3], int(nvl));
     __syncthreads();
     // losing candidates of this item: ranks k + j, 2k + j, ...  (deterministic slots)
     const int n_valid = sm.bcast[3];
     const int n_lose_all = max(0, n_valid - k);
     n_loser = (n_lose_all > j) ? (n_lose_all - j + k - 1) / k : 0;
-    for (int c = tid; c < n_cand; c += NT) {
-        const uint4 me = Z.cand[c];
-        if (me.z >= 0x80000000u) continue;
-        const int rank = int(me.w);
-        if (rank >= k && ((rank - k) % k) == j) {
-            const int slot = (rank - k) / k;
-            if (slot < kLoserWin) {
-                Z.loser[slot] = int32_t(me.z);
 #pragma unroll
-                for (int hl = 0; hl < G; ++hl) Z.lw[hl][slot] = Z.cand_lg[c][hl] * kLog2e;
+    for (int u = 0; u < OWN; ++u) {
+        const int rk = rank[u];
+        if (rk >= k && ((rk - k) % k) == j) {
+            const int slot = (rk - k) / k;
+            if (slot < kZoomLosers) {
+                Z.loser[slot] = int32_t(oidx[u]);
+#pragma unroll
+                for (int hl = 0; hl < G; ++hl) Z.lw[hl][slot] = olg[u][hl] * kLog2e;
             }
         }
     }
@@ -840,10 +1014,227 @@ __device__ void rank_candidates(const Params &p, Smem<T, D, G> &sm, int pair, in
 }
 
 // ---------------------------------------------------------------------------
+// zoom item body for one span, RU = 16-byte vectors per factor row U[t][:]
+// ---------------------------------------------------------------------------
+template <class T, int D, int G, int RU>
+__device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, int pair, int S,
+                                          int L, int64_t off, int nl,
+                                          float (&acc)[G][T::kVec], int tid) {
+    using GE = Geo<T, D>;
+    auto &Z = sm.u.zoom;
+    constexpr int VEC = GE::VEC;
+    constexpr int RV = GE::RV;
+    constexpr int NVT = (kMaxTopK * RV + NT - 1) / NT;   // Vt vectors per thread at r = 64
+    constexpr int NSV = (G * kMaxTopK + NT - 1) / NT;    // y entries per thread at r = 64
+    constexpr int NB = (8 * NT / RU) < kZoomBlock ? (8 * NT / RU) : kZoomBlock;  // tokens/block
+    constexpr int NU = NB * RU / NT;                     // U vectors per thread per block
+    constexpr int LG_RU = RU == 1 ? 0 : RU == 2 ? 1 : RU == 4 ? 2 : RU == 8 ? 3 : 4;
+    const int b = pair / p.Hkv, g = pair % p.Hkv;
+    const int r = p.r;
+    const int rgrp = tid / GE::RV, col = tid % GE::RV;
+    const int ucol = tid % RU;
+    const int wave = tid >> 6, lane = tid & 63;
+    const unsigned char *UK = p.factors + off;
+    const unsigned char *sK = UK + size_t(L) * r * T::kBytes;
+    const unsigned char *VtK = sK + size_t(r) * T::kBytes;
+    const unsigned char *UV = VtK + size_t(r) * D * T::kBytes;
+    const unsigned char *sV = UV + size_t(L) * r * T::kBytes;
+    const unsigned char *VtV = sV + size_t(r) * T::kBytes;
+    const bool zoom = S >= 0;
+    const int nb0 = min(NB, L);
+
+    // issue in the order of use: sigmas, Vt_K, losers' value rows, U_K, then U_V.
+    // Addresses are clamped into the block, validity is applied where values are used.
+    float sk_reg[NVT], sv_reg[NSV];
+    uint4 vk[NVT], vvt[NVT], uk[NU], uv[NU];
+    constexpr int NJL = (kZoomLosers + GE::RPP - 1) / GE::RPP;
+    uint4 lv[NJL];
+    if (zoom) {
+#pragma unroll
+        for (int u = 0; u < NVT; ++u) {
+            const int vi = min(tid + NT * u, r * RV - 1);
+            sk_reg[u] = T::load1(sK, vi / RV);
+        }
+#pragma unroll
+        for (int u = 0; u < NSV; ++u) sv_reg[u] = T::load1(sV, (tid + NT * u) % r);
+#pragma unroll
+        for (int u = 0; u < NVT; ++u) {
+            const int vi = min(tid + NT * u, r * RV - 1);
+            vk[u] = ld16(VtK + size_t(vi / RV) * GE::RB + (vi % RV) * 16);
+        }
+    }
+    if (nl > 0) {
+        const unsigned char *sv = reinterpret_cast<const unsigned char *>(p.sum_v) +
+                                  (size_t(b) * p.Hkv + g) * size_t(p.M_max) * GE::RB;
+#pragma unroll
+        for (int jj = 0; jj < NJL; ++jj) {
+            const int row = min(rgrp + GE::RPP * jj, nl - 1);
+            lv[jj] = ld16(sv + size_t(Z.loser[row]) * GE::RB + col * 16);
+        }
+        if (tid < G)
+            for (int i = nl; i < kZoomLosers; ++i) Z.lw[tid][i] = -INFINITY;
+    }
+    if (zoom) {
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            const int tok = min((tid + NT * u) / RU, nb0 - 1);
+            uk[u] = ld16(UK + size_t(tok) * r * T::kBytes + ucol * 16);
+        }
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            const int tok = min((tid + NT * u) / RU, nb0 - 1);
+            uv[u] = ld16(UV + size_t(tok) * r * T::kBytes + ucol * 16);
+        }
+    }
+    __syncthreads();
+
+    if (zoom) {
+        // w[h][i] = scale*log2e * sigma_K[i] * (Vt_K[i] . q_h)
+#pragma unroll
+        for (int u = 0; u < NVT; ++u) {
+            const int vi = tid + NT * u;
+            const int row = vi / RV, c = vi % RV;
+            float part[G];
+            float f[VEC];
+            T::unpack(vk[u], f);
+#pragma unroll
+            for (int hl = 0; hl < G; ++hl) {
+                part[hl] = 0.0f;
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) part[hl] += Z.qf[hl][c * VEC + e] * f[e];
+                part[hl] = row_sum<RV>(part[hl]);
+            }
+            if (vi < r * RV && c == 0)
+#pragma unroll
+                for (int hl = 0; hl < G; ++hl) Z.w[hl][row] = part[hl] * sk_reg[u] * p.scale_log2;
+        }
+        // Vt_V rows take the registers Vt_K has released
+#pragma unroll
+        for (int u = 0; u < NVT; ++u) {
+            const int vi = min(tid + NT * u, r * RV - 1);
+            vvt[u] = ld16(VtV + size_t(vi / RV) * GE::RB + (vi % RV) * 16);
+        }
+    }
+
+    // this item's losing candidates: coarse entries (v_bar rows, routing scores)
+    if (nl > 0) {
+        online_fold(&Z.lw[0][0], kZoomLosers, nl, G, sm.m_run, sm.l_run, sm.scale_old, tid);
+        __syncthreads();
+        acc_rows<T, D, G, NJL>(acc, lv, &Z.lw[0][0], kZoomLosers, nl, rgrp);
+    }
+    if (!zoom) return;
+    __syncthreads();
+
+    // token blocks: scores via U_K, online softmax, y = p^T U_V accumulated per lane
+    float yacc[G][VEC];
+#pragma unroll
+    for (int hl = 0; hl < G; ++hl)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) yacc[hl][e] = 0.0f;
+    for (int t0 = 0; t0 < L; t0 += NB) {
+        const int nb = min(NB, L - t0);
+        if (t0 > 0) {
+#pragma unroll
+            for (int u = 0; u < NU; ++u) {
+                const int tok = min((tid + NT * u) / RU, nb - 1);
+                uk[u] = ld16(UK + size_t(t0 + tok) * r * T::kBytes + ucol * 16);
+            }
+#pragma unroll
+            for (int u = 0; u < NU; ++u) {
+                const int tok = min((tid + NT * u) / RU, nb - 1);
+                uv[u] = ld16(UV + size_t(t0 + tok) * r * T::kBytes + ucol * 16);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            const int tok = (tid + NT * u) / RU;
+            float f[VEC];
+            T::unpack(uk[u], f);
+            float part[G];
+#pragma unroll
+            for (int hl = 0; hl < G; ++hl) {
+                part[hl] = 0.0f;
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) part[hl] += f[e] * Z.w[hl][ucol * VEC + e];
+                part[hl] = lane_reduce<0, LG_RU>(part[hl]);
+            }
+            if (tok < nb && ucol == 0)
+#pragma unroll
+                for (int hl = 0; hl < G; ++hl) Z.zs[hl][tok] = part[hl];
+        }
+        __syncthreads();
+        online_fold(&Z.zs[0][0], kZoomBlock, nb, G, sm.m_run, sm.l_run, sm.scale_old, tid);
+        __syncthreads();
+#pragma unroll
+        for (int hl = 0; hl < G; ++hl) {
+            const float so = sm.scale_old[hl];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) {
+                yacc[hl][e] *= so;
+                acc[hl][e] *= so;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            const int tok = (tid + NT * u) / RU;
+            if (tok < nb) {
+                float f[VEC];
+                T::unpack(uv[u], f);
+#pragma unroll
+                for (int hl = 0; hl < G; ++hl) {
+                    const float pw = Z.zs[hl][tok];
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) yacc[hl][e] += pw * f[e];
+                }
+            }
+        }
+        __syncthreads();
+    }
+    // y[h][i]: sum yacc over the lanes sharing ucol, then over the waves
+#pragma unroll
+    for (int hl = 0; hl < G; ++hl)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) yacc[hl][e] = lane_reduce<LG_RU, 6>(yacc[hl][e]);
+    if (lane < RU)
+#pragma unroll
+        for (int hl = 0; hl < G; ++hl)
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) Z.yr[wave][hl][ucol * VEC + e] = yacc[hl][e];
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < NSV; ++u) {
+        const int t = tid + NT * u;
+        if (t < G * r) {
+            const int hl = t / r, i = t % r;
+            Z.y[hl][i] = (Z.yr[0][hl][i] + Z.yr[1][hl][i] + Z.yr[2][hl][i] + Z.yr[3][hl][i]) *
+                         sv_reg[u];
+        }
+    }
+    __syncthreads();
+    // o[h][:] += sum_i y~[h][i] Vt_V[i][:]; Vt_V rows of column c sit RV lanes apart,
+    // exactly like summary rows
+#pragma unroll
+    for (int u = 0; u < NVT; ++u) {
+        const int vi = tid + NT * u;
+        if (vi < r * RV) {
+            const int row = vi / RV;
+            float f[VEC];
+            T::unpack(vvt[u], f);
+#pragma unroll
+            for (int hl = 0; hl < G; ++hl) {
+                const float y = Z.y[hl][row];
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) acc[hl][e] += y * f[e];
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // zoom item: one selection slot of a pair, attended through the span's factors
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
-__device__ void zoom_item(const Params &p, Smem<T, D, G> &sm, int pair, int j, int tid) {
+__device__ __forceinline__ void zoom_item(const Params &p, Smem<T, D, G> &sm, int pair, int j, int tid) {
     using GE = Geo<T, D>;
     auto &Z = sm.u.zoom;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
@@ -875,25 +1266,33 @@ __device__ void zoom_item(const Params &p, Smem<T, D, G> &sm, int pair, int j, i
     __syncthreads();
     int n_loser = 0;
     int S = -1;
-    if (sm.bcast[2]) {
-        if (per_item_select) {
-            rank_candidates<T, D, G>(p, sm, pair, j, m_b, tid, n_loser);
-            S = Z.sel[j];
-            if (tid == 0 && p.sel_out) p.sel_out[size_t(pair) * p.k + j] = S;
-        } else if (p.mode == kModeFused) {
-            const int32_t *rec = reinterpret_cast<const int32_t *>(&p.zrec[size_t(pair) * p.k + j]);
-            S = ld_shared(rec);
-        } else {
-            S = p.sel_in[size_t(pair) * p.k + j];
-        }
+    if (sm.bcast[2] && per_item_select) {
+        // ranks the pair's candidates; the owner of rank j leaves {span, |S|, offset} in bcast
+        rank_candidates<T, D, G>(p, sm, pair, j, m_b, tid, n_loser);
     }
     if (tid == 0) {
         int L = 0;
         int64_t off = 0;
-        if (S >= m_b) { flag_error(p, kErrSelRange); S = -1; }
+        if (!sm.bcast[2]) {
+            S = -1;
+        } else if (per_item_select) {
+            S = sm.bcast[4];
+            L = sm.bcast[5];
+            off = int64_t(uint32_t(sm.bcast[6])) | (int64_t(sm.bcast[7]) << 32);
+            if (p.sel_out) p.sel_out[size_t(pair) * p.k + j] = S;
+        } else {
+            if (p.mode == kModeFused) {
+                S = ld_shared(reinterpret_cast<const int32_t *>(&p.zrec[size_t(pair) * p.k + j]));
+            } else {
+                S = p.sel_in[size_t(pair) * p.k + j];
+            }
+            if (S >= m_b) { flag_error(p, kErrSelRange); S = -1; }
+            if (S >= 0) {
+                L = p.span_len[size_t(b) * p.M_max + S];
+                off = p.block_off[(size_t(b) * p.Hkv + g) * p.M_max + S];
+            }
+        }
         if (S >= 0) {
-            L = p.span_len[size_t(b) * p.M_max + S];
-            off = p.block_off[(size_t(b) * p.Hkv + g) * p.M_max + S];
             const int64_t bytes = (2 * int64_t(L) * r + 2 * r + 2 * int64_t(r) * D) * T::kBytes;
             if (L < 1 || off < 0 || (off & 15) || off + bytes > p.factors_bytes) {
                 flag_error(p, kErrBlockRange);
@@ -912,198 +1311,14 @@ __device__ void zoom_item(const Params &p, Smem<T, D, G> &sm, int pair, int j, i
     const int slot = p.slot_zoom0 + j;
     float acc[G][GE::VEC];
     acc_zero<T, D, G>(acc);
-
-    constexpr int VEC = GE::VEC;
-    constexpr int RV = GE::RV;
-    constexpr int NVT = (kMaxTopK * RV + NT - 1) / NT;   // Vt vectors per thread at r = 64
-    const int RU = r * T::kBytes / 16;                  // vectors per U row
-    const unsigned char *UK = p.factors + off;
-    const unsigned char *sK = UK + size_t(L) * r * T::kBytes;
-    const unsigned char *VtK = sK + size_t(r) * T::kBytes;
-    const unsigned char *UV = VtK + size_t(r) * D * T::kBytes;
-    const unsigned char *sV = UV + size_t(L) * r * T::kBytes;
-    const unsigned char *VtV = sV + size_t(r) * T::kBytes;
-    const int ucol = tid % RU;                          // fixed per thread (NT % RU == 0)
-    int nb_max = (8 * NT) / RU;
-    if (nb_max > kZoomBlock) nb_max = kZoomBlock;
-    const int nb0 = min(nb_max, L);
-
-    // issue: Vt_K, Vt_V (row i, column c) and the first token block of U_K, U_V
-    uint4 vk[NVT], vvt[NVT], uk[8], uv[8];
-    if (S >= 0) {
-#pragma unroll
-        for (int u = 0; u < NVT; ++u) {
-            const int vi = tid + NT * u;
-            if (vi < r * RV) {
-                vk[u] = ld16(VtK + size_t(vi / RV) * GE::RB + (vi % RV) * 16);
-                vvt[u] = ld16(VtV + size_t(vi / RV) * GE::RB + (vi % RV) * 16);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int tok = (tid + NT * u) / RU;
-            if (tok < nb0) {
-                uk[u] = ld16(UK + size_t(tok) * r * T::kBytes + ucol * 16);
-                uv[u] = ld16(UV + size_t(tok) * r * T::kBytes + ucol * 16);
-            }
-        }
-        if (tid < r) {
-            Z.sig[0][tid] = T::load1(sK, tid);
-            Z.sig[1][tid] = T::load1(sV, tid);
-        }
-    }
-
-    // losing candidates of this item: coarse entries (v_bar rows, routing scores)
-    if (n_loser > 0) {
-        constexpr int NJL = (kLoserWin + GE::RPP - 1) / GE::RPP;
-        const unsigned char *sv = reinterpret_cast<const unsigned char *>(p.sum_v) +
-                                  (size_t(b) * p.Hkv + g) * size_t(p.M_max) * GE::RB;
-        const int nl = min(n_loser, kLoserWin);
-        uint4 lv[NJL];
-#pragma unroll
-        for (int jj = 0; jj < NJL; ++jj) {
-            const int row = rgrp + GE::RPP * jj;
-            if (row < nl) lv[jj] = ld16(sv + size_t(Z.loser[row]) * GE::RB + col * 16);
-        }
-        if (tid < G)
-            for (int i = nl; i < kLoserWin; ++i) Z.lw[tid][i] = -INFINITY;
-        __syncthreads();
-        online_fold(&Z.lw[0][0], kLoserWin, nl, G, sm.m_run, sm.l_run, sm.scale_old, tid);
-        __syncthreads();
-        acc_rows<T, D, G, NJL>(acc, lv, &Z.lw[0][0], kLoserWin, nl, rgrp);
-    }
-
-    if (S >= 0) {
-        __syncthreads();
-        // w[h][i] = scale*log2e * sigma_K[i] * (Vt_K[i] . q_h)
-#pragma unroll
-        for (int u = 0; u < NVT; ++u) {
-            const int vi = tid + NT * u;
-            const int row = vi / RV, c = vi % RV;
-            float part[G];
-#pragma unroll
-            for (int hl = 0; hl < G; ++hl) part[hl] = 0.0f;
-            if (vi < r * RV) {
-                float f[VEC];
-                T::unpack(vk[u], f);
-#pragma unroll
-                for (int hl = 0; hl < G; ++hl)
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) part[hl] += Z.qf[hl][c * VEC + e] * f[e];
-            }
-#pragma unroll
-            for (int o = 1; o < RV; o <<= 1)
-#pragma unroll
-                for (int hl = 0; hl < G; ++hl) part[hl] += __shfl_xor(part[hl], o, 64);
-            if (vi < r * RV && c == 0)
-#pragma unroll
-                for (int hl = 0; hl < G; ++hl)
-                    Z.w[hl][row] = part[hl] * Z.sig[0][row] * p.scale_log2;
-        }
-        __syncthreads();
-
-        // token blocks: scores via U_K, online softmax, y = p^T U_V accumulated per lane
-        float yacc[G][VEC];
-#pragma unroll
-        for (int hl = 0; hl < G; ++hl)
-#pragma unroll
-            for (int e = 0; e < VEC; ++e) yacc[hl][e] = 0.0f;
-        const int wave = tid >> 6, lane = tid & 63;
-        for (int t0 = 0; t0 < L; t0 += nb_max) {
-            const int nb = min(nb_max, L - t0);
-            if (t0 > 0) {
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int tok = (tid + NT * u) / RU;
-                    if (tok < nb) {
-                        uk[u] = ld16(UK + size_t(t0 + tok) * r * T::kBytes + ucol * 16);
-                        uv[u] = ld16(UV + size_t(t0 + tok) * r * T::kBytes + ucol * 16);
-                    }
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int tok = (tid + NT * u) / RU;
-                float part[G];
-#pragma unroll
-                for (int hl = 0; hl < G; ++hl) part[hl] = 0.0f;
-                if (tok < nb) {
-                    float f[VEC];
-                    T::unpack(uk[u], f);
-#pragma unroll
-                    for (int hl = 0; hl < G; ++hl)
-#pragma unroll
-                        for (int e = 0; e < VEC; ++e) part[hl] += f[e] * Z.w[hl][ucol * VEC + e];
-                }
-                for (int o = 1; o < RU; o <<= 1)
-#pragma unroll
-                    for (int hl = 0; hl < G; ++hl) part[hl] += __shfl_xor(part[hl], o, 64);
-                if (tok < nb && ucol == 0)
-#pragma unroll
-                    for (int hl = 0; hl < G; ++hl) Z.zs[hl][tok] = part[hl];
-            }
-            __syncthreads();
-            online_fold(&Z.zs[0][0], kZoomBlock, nb, G, sm.m_run, sm.l_run, sm.scale_old, tid);
-            __syncthreads();
-#pragma unroll
-            for (int hl = 0; hl < G; ++hl) {
-                const float so = sm.scale_old[hl];
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) {
-                    yacc[hl][e] *= so;
-                    acc[hl][e] *= so;
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const int tok = (tid + NT * u) / RU;
-                if (tok < nb) {
-                    float f[VEC];
-                    T::unpack(uv[u], f);
-#pragma unroll
-                    for (int hl = 0; hl < G; ++hl) {
-                        const float pw = Z.zs[hl][tok];
-#pragma unroll
-                        for (int e = 0; e < VEC; ++e) yacc[hl][e] += pw * f[e];
-                    }
-                }
-            }
-            __syncthreads();
-        }
-        // y[h][i]: sum yacc over the lanes sharing ucol, then over the waves
-        for (int o = RU; o < 64; o <<= 1)
-#pragma unroll
-            for (int hl = 0; hl < G; ++hl)
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) yacc[hl][e] += __shfl_xor(yacc[hl][e], o, 64);
-        if (lane < RU)
-#pragma unroll
-            for (int hl = 0; hl < G; ++hl)
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) Z.yr[wave][hl][ucol * VEC + e] = yacc[hl][e];
-        __syncthreads();
-        for (int t = tid; t < G * r; t += NT) {
-            const int hl = t / r, i = t % r;
-            Z.y[hl][i] = (Z.yr[0][hl][i] + Z.yr[1][hl][i] + Z.yr[2][hl][i] + Z.yr[3][hl][i]) *
-                         Z.sig[1][i];
-        }
-        __syncthreads();
-        // o[h][:] += sum_i y~[h][i] Vt_V[i][:]; Vt_V rows of column c sit RV lanes apart,
-        // exactly like summary rows
-#pragma unroll
-        for (int u = 0; u < NVT; ++u) {
-            const int vi = tid + NT * u;
-            if (vi < r * RV) {
-                const int row = vi / RV;
-                float f[VEC];
-                T::unpack(vvt[u], f);
-#pragma unroll
-                for (int hl = 0; hl < G; ++hl) {
-                    const float y = Z.y[hl][row];
-#pragma unroll
-                    for (int e = 0; e < VEC; ++e) acc[hl][e] += y * f[e];
-                }
-            }
+    const int nl = min(n_loser, kZoomLosers);
+    if (S >= 0 || nl > 0) {
+        switch (r * T::kBytes / 16) {                   // 16-byte vectors per U row
+            case 1: zoom_span<T, D, G, 1>(p, sm, pair, S, L, off, nl, acc, tid); break;
+            case 2: zoom_span<T, D, G, 2>(p, sm, pair, S, L, off, nl, acc, tid); break;
+            case 4: zoom_span<T, D, G, 4>(p, sm, pair, S, L, off, nl, acc, tid); break;
+            case 8: zoom_span<T, D, G, 8>(p, sm, pair, S, L, off, nl, acc, tid); break;
+            default: zoom_span<T, D, G, 16>(p, sm, pair, S, L, off, nl, acc, tid); break;
         }
     }
     rows_to_red<T, D, G>(sm, acc, tid);

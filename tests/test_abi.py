@@ -51,6 +51,7 @@ def _dims(S, **kw):
     (dict(n_q_heads=12, n_kv_heads=4), 2),         # group 3
     (dict(head_dim=96), 2),
     (dict(rank=12), 2),
+    (dict(rank=24), 2),
     (dict(rank=72), 2),
     (dict(top_k=65), 2),
     (dict(max_spans=0), 1),
@@ -58,7 +59,7 @@ def _dims(S, **kw):
     (dict(batch=-1), 1),
     (dict(softmax_scale=0.0), 1),
     (dict(dtype="f32", out_dtype="bf16"), 2),
-    (dict(max_spans=40000), 2),                    # too many partials per pair
+    (dict(max_spans=80000), 2),                    # too many partials per pair
 ])
 def test_check_dims_rejects(S, kw, status):
     d = _dims(S, **kw)
