@@ -61,11 +61,9 @@ sekv_status check_dims_impl(const sekv_dims *d) {
         return fail(SEKV_ERR_UNSUPPORTED, "flags 0x%x", unsigned(d->flags));
     if (!(d->softmax_scale > 0.0) || !std::isfinite(d->softmax_scale))
         return fail(SEKV_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
-    const sekv::Shape s = sekv::make_shape(*d);
-    if (s.n_slots > sekv::kMergeBuf)
-        return fail(SEKV_ERR_UNSUPPORTED, "too many partials per pair (%d > %d): max_spans or "
-                    "max_anchors too large", s.n_slots, sekv::kMergeBuf);
-    const long long rows = (long long)s.B * s.Hkv * std::max(s.M_max, s.A_max);
+    if (d->max_spans > sekv::kMaxSpans)
+        return fail(SEKV_ERR_UNSUPPORTED, "max_spans %d > %d", d->max_spans, sekv::kMaxSpans);
+    const long long rows = (long long)d->batch * d->n_kv_heads * std::max(d->max_spans, d->max_anchors);
     if (rows > (1ll << 31)) return fail(SEKV_ERR_UNSUPPORTED, "tables too large");
     return SEKV_OK;
 }
@@ -155,16 +153,14 @@ sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_
     p.mode = mode;
     p.B = s.B; p.Hq = s.Hq; p.Hkv = s.Hkv; p.r = s.r; p.k = s.k;
     p.A_max = s.A_max; p.M_max = s.M_max;
-    p.n_rc = s.n_rc; p.n_ac = s.n_ac; p.kc = s.kc; p.n_slots = s.n_slots;
-    p.slot_route0 = s.n_ac;
-    p.slot_losers = s.n_ac + s.n_rc;
-    p.slot_zoom0 = s.n_ac + s.n_rc + 1;
-    const int n_route = s.P * s.n_rc;
-    const int n_anchor = (mode == sekv::kModeRoute) ? 0 : s.P * s.n_ac;
-    const int n_zoom = (mode == sekv::kModeRoute) ? 0 : s.P * s.k;
+    p.n_rc = s.n_rc; p.kc = s.kc; p.n_cand = s.n_cand; p.n_zi = s.n_zi;
+    // routing items run unless the caller hands in the routing scores; share items run
+    // unless only the selection is asked for
+    const bool scores = !(mode == sekv::kModeAttend && logits_in != nullptr);
+    const int n_route = scores ? s.P * s.n_rc : 0;
+    const int n_share = (mode == sekv::kModeRoute) ? 0 : s.P * s.n_zi;
     p.end_route = n_route;
-    p.end_anchor = n_route + n_anchor;
-    p.end_zoom = n_route + n_anchor + n_zoom;
+    p.end_share = n_route + n_share;
     p.out_f32 = d->out_dtype == SEKV_F32;
     p.zoom_impl = (d->flags & 3) == SEKV_ZOOM_DEFAULT ? SEKV_ZOOM_FACTORED : (d->flags & 3);
     p.scale = d->softmax_scale;
@@ -182,24 +178,18 @@ sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_
     p.sel_ready = reinterpret_cast<uint32_t *>(w + L.sel_ready);
     p.part_cnt = reinterpret_cast<uint32_t *>(w + L.part_cnt);
     p.zrec = reinterpret_cast<int4 *>(w + L.zrec);
-    p.cand_key = reinterpret_cast<uint64_t *>(w + L.cand_key);
-    p.cand_idx = reinterpret_cast<int32_t *>(w + L.cand_idx);
-    p.cand_len = reinterpret_cast<int32_t *>(w + L.cand_len);
-    p.cand_off = reinterpret_cast<int64_t *>(w + L.cand_off);
-    p.cand_cnt = reinterpret_cast<int32_t *>(w + L.cand_cnt);
-    p.cand_lg = reinterpret_cast<float *>(w + L.cand_lg);
-    p.part_ml = reinterpret_cast<float *>(w + L.part_ml);
-    p.part_o = reinterpret_cast<float *>(w + L.part_o);
+    p.cand = reinterpret_cast<uint64_t *>(w + L.cand);
+    p.tlg = reinterpret_cast<uint64_t *>(w + L.tlg);
+    p.part_ml = reinterpret_cast<uint64_t *>(w + L.part_ml);
+    p.part_o = reinterpret_cast<uint64_t *>(w + L.part_o);
 
-    // Fused mode ranks the candidates inside every zoom item when they fit its LDS
-    // buffers (<= kMergeBuf candidates and <= kZoomLosers losing candidates per item);
-    // otherwise one workgroup per pair merges them.
-    const long long n_cand = (long long)s.n_rc * s.kc;
-    const bool per_item = n_cand <= sekv::kMergeBuf && n_cand <= (long long)s.k * (sekv::kZoomLosers + 1);
+    // Fused mode ranks the candidates inside every share item when they fit its LDS
+    // buffer; otherwise one workgroup per pair merges them.
+    const bool per_item = s.n_cand <= sekv::kMergeBuf;
     p.merger = (mode == sekv::kModeRoute) || (mode == sekv::kModeFused && !per_item);
     const int cap = resident(d->dtype, d->head_dim, s.G);
-    p.grid = std::max(1, std::min(p.end_zoom, cap));
-    if (p.end_zoom == 0) return SEKV_OK;
+    p.grid = std::max(1, std::min(p.end_share, cap));
+    if (p.end_share == 0) return SEKV_OK;
     const hipError_t e = sekv::launch_step(p, d->dtype, d->head_dim, s.G, stream);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     return SEKV_OK;

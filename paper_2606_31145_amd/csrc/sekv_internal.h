@@ -14,51 +14,49 @@ namespace sekv {
 
 // Work decomposition (compile-time tile sizes).
 constexpr int kThreads = 256;      // threads per workgroup: 4 wave64s
-constexpr int kRouteChunk = 128;   // spans per routing / summary work item
-// Anchor tokens per anchor work item: 8 key + 8 value vectors of 16 bytes per thread.
-constexpr int anchor_chunk(int elem_bytes, int head_dim) { return 32768 / (head_dim * elem_bytes); }
+constexpr int kRouteChunk = 128;   // spans per routing work item
 constexpr int kZoomBlock = 512;    // tokens of a zoomed span scored per LDS pass
 constexpr int kMaxTopK = 64;
-constexpr int kMergeBuf = 512;     // candidates ranked in LDS
-constexpr int kLoserWin = 128;     // losing candidates folded per window (single merger)
-constexpr int kZoomLosers = 32;    // losing candidates folded by one zoom item, at most
+constexpr int kMergeBuf = 512;     // candidates ranked in LDS by one workgroup
+constexpr int kMaxSpans = 65536;   // max_spans limit (span indices and record sizes)
 
 enum Mode : int32_t { kModeRoute = 0, kModeAttend = 1, kModeFused = 2 };
 
 // Device error bits (workspace header word `error`).
 enum : int32_t { kErrSpinTimeout = 1, kErrBlockRange = 2, kErrSelRange = 4 };
 
-// Workspace header: dynamic work counter and shutdown counter, then per-(b, kv head)
-// counters.  The last workgroup to finish a launch zeroes every counter it used.
+// Fields of a tagged candidate record (one 64-bit word each, 32-bit payload).
+enum : int32_t { kCandKeyHi = 0, kCandKeyLo, kCandIdx, kCandLen, kCandOffLo, kCandOffHi, kCandFields };
+
+// Workspace header.  `epoch` is the tag of the next launch: that launch marks the words
+// it publishes with it, and its last workgroup out advances it (skipping 0, the value
+// of never-written words; initialisation sets 1) and zeroes every counter it used.
 struct WsHeader {
     uint32_t ticket;
     uint32_t exit_count;
     int32_t error;
-    uint32_t pad[61];
+    uint32_t epoch;
+    uint32_t pad[60];
 };
 
 // Byte offsets of the workspace sections for one dims.
 struct WsLayout {
     size_t route_cnt, sel_ready, part_cnt;    // uint32 [P]
     size_t zrec;                              // int32x4 [P][k]: span, |S|, offset lo/hi
-    size_t cand_key;                          // uint64 [P][n_rc][kc]
-    size_t cand_idx;                          // int32  [P][n_rc][kc]
-    size_t cand_len;                          // int32  [P][n_rc][kc]  |S|
-    size_t cand_off;                          // int64  [P][n_rc][kc]  block offset
-    size_t cand_cnt;                          // int32  [P][n_rc]
-    size_t cand_lg;                           // float  [P][n_rc][kc][G]
-    size_t part_ml;                           // float  [P][n_slots][G][2]
-    size_t part_o;                            // float  [P][n_slots][G][d]
+    size_t cand;                              // tagged uint64 [kCandFields][P][n_cand]
+    size_t tlg;                               // tagged uint64 [P][G][M_max]: base-2 logits
+    size_t part_ml;                           // float pairs (m, l) [P][n_zi][G]
+    size_t part_o;                            // float pairs [P][n_zi][G][d/2]
     size_t total;
 };
 
 struct Shape {
     int B, Hq, Hkv, G, d, r, k, A_max, M_max, L_max;
     int P;        // B * Hkv pairs
-    int n_rc;     // routing/summary chunks per pair
-    int n_ac;     // anchor chunks per pair
+    int n_rc;     // routing chunks per pair
     int kc;       // candidates kept per routing chunk = min(k, kRouteChunk)
-    int n_slots;  // partials per pair (fused layout: anchors, summaries, losers, zoom)
+    int n_cand;   // candidates per pair = n_rc * kc
+    int n_zi;     // share items (and partials) per pair = max(k, 1)
 };
 
 inline int elem_bytes(int dtype) { return dtype == SEKV_BF16 ? 2 : 4; }
@@ -70,10 +68,9 @@ inline Shape make_shape(const sekv_dims &d) {
     s.A_max = d.max_anchors; s.M_max = d.max_spans; s.L_max = d.max_span_len;
     s.P = s.B * s.Hkv;
     s.n_rc = (s.M_max + kRouteChunk - 1) / kRouteChunk;
-    const int ca = anchor_chunk(elem_bytes(d.dtype), s.d);
-    s.n_ac = (s.A_max + ca - 1) / ca;
     s.kc = s.k < kRouteChunk ? s.k : kRouteChunk;
-    s.n_slots = s.n_ac + s.n_rc + 1 + s.k;
+    s.n_cand = s.n_rc * s.kc;
+    s.n_zi = s.k > 1 ? s.k : 1;
     return s;
 }
 
@@ -87,14 +84,9 @@ inline WsLayout make_layout(const Shape &s) {
     L.sel_ready = o; o = align256(o + 4 * P);
     L.part_cnt = o;  o = align256(o + 4 * P);
     L.zrec = o;      o = align256(o + 16 * P * size_t(s.k > 0 ? s.k : 1));
-    const size_t nc = P * size_t(s.n_rc) * size_t(s.kc > 0 ? s.kc : 1);
-    L.cand_key = o;  o = align256(o + 8 * nc);
-    L.cand_idx = o;  o = align256(o + 4 * nc);
-    L.cand_len = o;  o = align256(o + 4 * nc);
-    L.cand_off = o;  o = align256(o + 8 * nc);
-    L.cand_cnt = o;  o = align256(o + 4 * P * size_t(s.n_rc));
-    L.cand_lg = o;   o = align256(o + 4 * nc * size_t(s.G));
-    const size_t ns = P * size_t(s.n_slots) * size_t(s.G);
+    L.cand = o;      o = align256(o + 8 * size_t(kCandFields) * P * size_t(s.n_cand > 0 ? s.n_cand : 1));
+    L.tlg = o;       o = align256(o + 8 * P * size_t(s.G) * size_t(s.M_max));
+    const size_t ns = P * size_t(s.n_zi) * size_t(s.G);
     L.part_ml = o;   o = align256(o + 8 * ns);
     L.part_o = o;    o = align256(o + 4 * ns * size_t(s.d));
     L.total = o;
@@ -105,13 +97,12 @@ inline WsLayout make_layout(const Shape &s) {
 struct Params {
     int32_t mode;
     int32_t B, Hq, Hkv, r, k, A_max, M_max;
-    int32_t n_rc, n_ac, kc, n_slots;
-    int32_t slot_route0, slot_losers, slot_zoom0;   // first slot of each partial kind
-    int32_t end_route, end_anchor, end_zoom;        // item-index ends of each item kind
+    int32_t n_rc, kc, n_cand, n_zi;
+    int32_t end_route, end_share;                   // item-index ends of each item kind
     int32_t grid;                                   // workgroups in the launch
     int32_t merger;                                 // 1: one workgroup per pair merges the
-                                                    // candidates (route mode, or too many
-                                                    // candidates for per-item ranking)
+                                                    // candidates (route mode, or more than
+                                                    // kMergeBuf candidates)
     int32_t out_f32;                                // 1: out is float, 0: bf16
     int32_t zoom_impl;
     double scale;                                   // softmax scale (routing score)
@@ -135,11 +126,9 @@ struct Params {
     WsHeader *hdr;
     uint32_t *route_cnt, *sel_ready, *part_cnt;
     int4 *zrec;
-    uint64_t *cand_key;
-    int32_t *cand_idx, *cand_len, *cand_cnt;
-    int64_t *cand_off;
-    float *cand_lg;
-    float *part_ml, *part_o;
+    uint64_t *cand;
+    uint64_t *tlg;
+    uint64_t *part_ml, *part_o;
 };
 
 // Launchers (sekv_kernels.hip).  Return the HIP error of the launch.

@@ -2,37 +2,41 @@
 //
 // Work items (per (sequence b, KV head g) "pair"):
 //   route   chunk of 128 spans: routing scores in float64 (eq. routing_gate with the
-//           coarse mean key as summary), the chunk's local top-k as sorted candidates,
-//           and -- fused mode -- the coarse softmax partial of its non-candidate spans,
-//           so each summary row (k_bar, v_bar) is read from HBM once.
-//   anchor  chunk of full-resolution tokens: softmax partial.
-//   zoom    selection slot j of a pair: once every route chunk of the pair is done, the
-//           item ranks the pair's candidates (Sec. 3.3 budget rule: decreasing routing
-//           score, here top-k), takes the j-th span, and attends to its tokens through
-//           the factors, K_hat = U diag(sigma) V^T (eq. key_reconstruction), never
-//           forming K_hat in memory.  The same partial also covers every k-th losing
-//           candidate's coarse entry, so no span is dropped from the softmax.
-// Every partial (max, sum, weighted value sum) lands in a fixed slot; the item that
-// completes a pair's last slot merges them in slot order into the output (one softmax
-// over the mixed-resolution memory, Sec. 3.3).  No floating-point atomics: results are
-// bitwise deterministic.
+//           coarse mean key as summary).  It publishes every span's score (the coarse
+//           logit) and, when the step selects, the chunk's local top-k as sorted
+//           candidate records.  It waits for nothing.
+//   share   selection slot j of a pair (j < max(k, 1)).  While routing runs it attends
+//           to its share of the anchor tokens; then it ranks the pair's candidates
+//           (Sec. 3.3 budget rule: decreasing routing score, here top-k), takes the j-th
+//           span and attends to its tokens through the factors, K_hat = U diag(sigma) V^T
+//           (eq. key_reconstruction), never forming K_hat in memory; while the factor
+//           loads are in flight it folds its share of the summaries, skipping the
+//           selected spans, so every span enters the softmax once: zoomed or coarse.
+// Each share item leaves one partial (max, sum, weighted value sum per head) in a fixed
+// slot; the item that completes a pair merges the slots in order into the output (one
+// softmax over the mixed-resolution memory, Sec. 3.3).  No floating-point atomics:
+// results are bitwise deterministic.
 //
 // Data movement: an item issues its global loads up front, as 16-byte vectors mapped
 // (row, column) onto the workgroup -- a wave reads 1 KB of contiguous rows per
 // instruction -- and keeps them in registers; row sums are lane shuffles inside a row
 // plus one cross-wave pass through LDS.
 //
-// Cross-workgroup protocol: data another workgroup reads (candidates, partials,
-// selection records) is stored with agent-scope relaxed atomic stores -- write-through
-// to the device coherence point on this chip -- every wave then waits for its stores to
+// Cross-workgroup protocol.  Routing results travel as tagged words: 32 bits of payload
+// and the launch's 32-bit tag in one 64-bit relaxed agent-scope atomic store
+// (write-through to the device coherence point on this chip).  A reader polls them with
+// relaxed agent-scope atomic loads until every tag it needs is the current launch's, so
+// the writer neither waits for its stores nor bumps a counter.  The tag is the
+// workspace epoch (1 after initialisation, never 0, which unwritten words hold); the last
+// workgroup out advances it.  Partials (and the
+// single-merger selection) use counters instead: every wave waits for its stores to
 // complete (s_waitcnt vmcnt(0)), the workgroup synchronises, and one thread bumps the
-// pair's counter with a relaxed agent-scope atomic.  Readers use agent-scope relaxed
-// atomic loads, issued only after they have observed the counter.  This orders exactly
-// the data that is shared without writing back or invalidating whole L2 caches.
+// pair's counter with a relaxed agent-scope atomic; readers load the data only after
+// observing the counter.  No fence writes back or invalidates whole L2 caches.
 //
 // Scheduling: workgroup w takes items w, w + grid, w + 2 grid, ... with grid no larger
 // than the number of workgroups the device holds at once.  Route items have the lowest
-// indices and never wait, so every route item a zoom item waits for is reached by its
+// indices and never wait, so every route item a share item waits for is reached by its
 // workgroup after finitely many non-waiting items: the waits always end (they are
 // bounded anyway and flag the workspace on timeout).  The last workgroup to leave zeroes
 // the counters, so the workspace is ready for the next launch.
@@ -241,34 +245,41 @@ __device__ inline void flag_error(const Params &p, int32_t bit) {
     __hip_atomic_fetch_or(&p.hdr->error, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Tagged words: payload in the low half, the launch tag in the high half.
+__device__ inline uint64_t tagged(uint32_t tag, uint32_t v) { return (uint64_t(tag) << 32) | v; }
+__device__ inline bool tag_is(uint64_t w, uint32_t tag) { return uint32_t(w >> 32) == tag; }
+__device__ inline uint64_t pack2(float lo, float hi) {
+    return uint64_t(__float_as_uint(lo)) | (uint64_t(__float_as_uint(hi)) << 32);
+}
+__device__ inline float lo_f(uint64_t w) { return __uint_as_float(uint32_t(w)); }
+__device__ inline float hi_f(uint64_t w) { return __uint_as_float(uint32_t(w >> 32)); }
+
 // ---------------------------------------------------------------------------
 // shared memory
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
 struct Smem {
     using GE = Geo<T, D>;
-    static constexpr int CA = 8 * NT / GE::RV;           // anchor tokens per item
-    struct Route {                                       // route / summary item
-        double qd[G][D];                                 // query, float64
-        unsigned char kb[CR * GE::RS];                   // summary key rows (fp64 dots)
+    static constexpr int HPT = (G + 1) / 2;              // routing heads per thread
+    static constexpr int NJ = 4;                          // rows per thread in a block
+    static constexpr int AB = NJ * GE::RPP;               // anchor tokens per block
+    static constexpr int CB = NJ * GE::RPP;               // summary rows per block
+    struct Route {                                       // routing item
+        unsigned char kb[CR * GE::RS];                   // summary key rows
         double lns[CR];                                  // ln|S| of the chunk's spans
-        double lg[G][CR];                                // routing scores, natural units
-        float pw[G][CR];                                 // coarse weights
-        int32_t excl[CR];                                // 1 = candidate / selected
+        double pmax[2][CR];                              // per head group max score
         int32_t slen[CR];                                // |S| of the chunk's spans
         int64_t boff[CR];                                // their block offsets
         uint64_t skey[2][64];                            // two sorted halves of the chunk
         uint32_t sidx[2][64];
     };
-    struct Anchor {
+    struct Share {                                       // share item
         float qf[G][D];
-        float sc[G][CA];                                 // scores, then weights
-    };
-    struct Zoom {
-        float qf[G][D];
-        uint4 cand[kMergeBuf];                           // {key lo, key hi, span, -}
-        int32_t loser[kZoomLosers];                      // this item's losing candidates
-        float lw[G][kZoomLosers];                        // their base-2 logits, then weights
+        float sc[G][AB];                                 // anchor scores, then weights
+        float cw[G][CB];                                 // summary logits, then weights
+        uint4 cand[kMergeBuf];                           // {~span, key lo, key hi, -}
+        uint32_t rk[NT];                                 // partial ranks (two scanners)
+        int32_t sel[kMaxTopK];                           // the pair's selected spans
         float w[G][kMaxTopK];                            // scale*log2e*sigma_K*(Vt_K q)
         float zs[G][kZoomBlock];                         // token scores, then weights
         float yr[4][G][kMaxTopK];                        // per-wave partial sums of p^T U_V
@@ -278,18 +289,15 @@ struct Smem {
         uint64_t key[kMergeBuf];
         uint32_t idx[kMergeBuf];
         int32_t sel[kMaxTopK];
-        int32_t loser[kLoserWin];
-        float pw[G][kLoserWin];
     };
     struct Final {                                       // softmax merge
-        float ml[kMergeBuf][G][2];
-        float wgt[kMergeBuf][G];
+        float m[kMaxTopK][G], l[kMaxTopK][G];
+        float wgt[kMaxTopK][G];
         float L[G];
     };
     union {
         Route route;
-        Anchor anchor;
-        Zoom zoom;
+        Share share;
         Merge merge;
         Final fin;
     } u;
@@ -307,16 +315,6 @@ __device__ inline void acc_zero(float (&acc)[G][T::kVec]) {
     for (int hl = 0; hl < G; ++hl)
 #pragma unroll
         for (int e = 0; e < T::kVec; ++e) acc[hl][e] = 0.0f;
-}
-
-template <class T, int D, int G>
-__device__ inline void acc_scale(float (&acc)[G][T::kVec], const float *so) {
-#pragma unroll
-    for (int hl = 0; hl < G; ++hl) {
-        const float s = so[hl];
-#pragma unroll
-        for (int e = 0; e < T::kVec; ++e) acc[hl][e] *= s;
-    }
 }
 
 // acc += w[row] * row vector (rows of this thread: rgrp + RPP*j, j < NJ, row < nrows)
@@ -340,9 +338,30 @@ __device__ inline void acc_rows(float (&acc)[G][T::kVec], const uint4 (&v)[NJ],
     }
 }
 
-// Sum acc over the rows held by all threads into sm.red (caller syncs before reading).
+// Write the partial of share slot `slot`: (m, l) from the online state; o = the 4 wave
+// rows of red, as float pairs.
 template <class T, int D, int G>
-__device__ inline void rows_to_red(Smem<T, D, G> &sm, float (&acc)[G][T::kVec], int tid) {
+__device__ inline void write_partial(const Params &p, Smem<T, D, G> &sm, int pair, int slot,
+                                     int tid) {
+    constexpr int NO = G * D / 2;
+    const size_t base = size_t(pair) * p.n_zi + slot;
+    if (tid < G) st_shared(&p.part_ml[base * G + tid], pack2(sm.m_run[tid], sm.l_run[tid]));
+    uint64_t *po = p.part_o + base * NO;
+    for (int o2 = tid; o2 < NO; o2 += NT) {
+        const int hl = (2 * o2) / D, d = (2 * o2) % D;
+        const float v0 = sm.red[0][hl][d] + sm.red[1][hl][d] + sm.red[2][hl][d] + sm.red[3][hl][d];
+        const float v1 = sm.red[0][hl][d + 1] + sm.red[1][hl][d + 1] + sm.red[2][hl][d + 1] +
+                         sm.red[3][hl][d + 1];
+        st_shared(&po[o2], pack2(v0, v1));
+    }
+}
+
+// Add acc, summed over this wave's rows, into the wave's row of sm.red after scaling that
+// row by pend (the rescale factors of the folds since the previous flush); pend becomes 1.
+// Each wave touches only its own row, so no synchronisation is needed here.
+template <class T, int D, int G>
+__device__ inline void acc_flush(Smem<T, D, G> &sm, float (&acc)[G][T::kVec], float (&pend)[G],
+                                 int tid) {
     using GE = Geo<T, D>;
     const int lane = tid & 63, wave = tid >> 6;
 #pragma unroll
@@ -350,28 +369,23 @@ __device__ inline void rows_to_red(Smem<T, D, G> &sm, float (&acc)[G][T::kVec], 
 #pragma unroll
         for (int e = 0; e < GE::VEC; ++e) acc[hl][e] = col_sum<GE::RV>(acc[hl][e]);
     if (lane < GE::RV) {
-        const int col = tid % GE::RV;
 #pragma unroll
         for (int hl = 0; hl < G; ++hl)
 #pragma unroll
-            for (int e = 0; e < GE::VEC; ++e) sm.red[wave][hl][col * GE::VEC + e] = acc[hl][e];
+            for (int e = 0; e < GE::VEC; ++e) {
+                float &r = sm.red[wave][hl][lane * GE::VEC + e];
+                r = r * pend[hl] + acc[hl][e];
+            }
     }
+#pragma unroll
+    for (int hl = 0; hl < G; ++hl) pend[hl] = 1.0f;
 }
 
-// Write the partial of `slot`: m, l from the online state; o = the 4 wave rows of red.
-template <class T, int D, int G>
-__device__ inline void write_partial(const Params &p, Smem<T, D, G> &sm, int pair, int slot,
-                                     int tid) {
-    const size_t base = (size_t(pair) * p.n_slots + slot) * G;
-    if (tid < G) {
-        st_shared(&p.part_ml[(base + tid) * 2 + 0], sm.m_run[tid]);
-        st_shared(&p.part_ml[(base + tid) * 2 + 1], sm.l_run[tid]);
-    }
-    for (int o = tid; o < G * D; o += NT) {
-        const int hl = o / D, d = o % D;
-        st_shared(&p.part_o[base * D + o],
-                  sm.red[0][hl][d] + sm.red[1][hl][d] + sm.red[2][hl][d] + sm.red[3][hl][d]);
-    }
+// Multiply the pending rescale factors by those of the fold that just finished.
+template <int G>
+__device__ inline void pend_fold(float (&pend)[G], const float *so) {
+#pragma unroll
+    for (int hl = 0; hl < G; ++hl) pend[hl] *= so[hl];
 }
 
 // Fold a batch of base-2 scores (LDS, -inf = excluded) into the online state: weights
@@ -414,39 +428,38 @@ template <class T, int D, int G>
 __device__ __forceinline__ void final_merge(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
     auto &F = sm.u.fin;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
-    const int ns = p.n_slots;
-    const bool use_losers = (p.mode == kModeFused) && p.merger;
-    const float *ml = p.part_ml + size_t(pair) * ns * G * 2;
-    const float *po = p.part_o + size_t(pair) * ns * G * D;
-    constexpr int NOUT = (G * D + NT - 1) / NT;
-    // every load first: the (m, l) of all slots to LDS, this thread's o values to registers
-    constexpr int kBatch = 32;                          // slots whose o values are in flight
-    float ov[NOUT][kBatch];
-    for (int i = tid; i < ns * G * 2; i += NT) (&F.ml[0][0][0])[i] = ld_shared(ml + i);
+    const int ns = p.n_zi;
+    constexpr int NO = G * D / 2;                       // float pairs per slot
+    constexpr int NP = (NO + NT - 1) / NT;              // float pairs per thread
+    constexpr int kBatch = 16;                          // slots whose values are in flight
+    const uint64_t *ml = p.part_ml + size_t(pair) * ns * G;
+    const uint64_t *po = p.part_o + size_t(pair) * ns * NO;
+    // every load first: (m, l) of all slots to LDS, this thread's o values to registers
+    for (int i = tid; i < ns * G; i += NT) {
+        const uint64_t w = ld_shared(ml + i);
+        F.m[i / G][i % G] = lo_f(w);
+        F.l[i / G][i % G] = hi_f(w);
+    }
+    uint64_t ov[NP][kBatch];
 #pragma unroll
-    for (int u = 0; u < NOUT; ++u) {
-        const int o = tid + NT * u;
-        const int hl = o / D, d = o % D;
+    for (int u = 0; u < NP; ++u) {
+        const int o2 = min(tid + NT * u, NO - 1);
 #pragma unroll
-        for (int s = 0; s < kBatch; ++s)
-            ov[u][s] = (o < G * D && s < ns) ? ld_shared(po + (size_t(s) * G + hl) * D + d) : 0.0f;
+        for (int s = 0; s < kBatch; ++s) ov[u][s] = ld_shared(po + size_t(min(s, ns - 1)) * NO + o2);
     }
     __syncthreads();
     const int wave = tid >> 6, lane = tid & 63;
     for (int hl = wave; hl < G; hl += 4) {
         float mx = -INFINITY;
-        for (int s = lane; s < ns; s += 64) {
-            const bool on = use_losers || s != p.slot_losers;
-            if (on && F.ml[s][hl][1] > 0.0f) mx = fmaxf(mx, F.ml[s][hl][0]);
-        }
+        for (int s = lane; s < ns; s += 64)
+            if (F.l[s][hl] > 0.0f) mx = fmaxf(mx, F.m[s][hl]);
         mx = wave_max(mx);
         float lsum = 0.0f;
         for (int s = lane; s < ns; s += 64) {
-            const bool on = use_losers || s != p.slot_losers;
             float wgt = 0.0f;
-            if (on && F.ml[s][hl][1] > 0.0f) {
-                wgt = exp2f(F.ml[s][hl][0] - mx);
-                lsum += wgt * F.ml[s][hl][1];
+            if (F.l[s][hl] > 0.0f) {
+                wgt = exp2f(F.m[s][hl] - mx);
+                lsum += wgt * F.l[s][hl];
             }
             F.wgt[s][hl] = wgt;
         }
@@ -455,43 +468,47 @@ __device__ __forceinline__ void final_merge(const Params &p, Smem<T, D, G> &sm, 
     }
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < NOUT; ++u) {
-        const int o = tid + NT * u;
-        if (o >= G * D) continue;
-        const int hl = o / D, d = o % D;
-        float a = 0.0f;
+    for (int u = 0; u < NP; ++u) {
+        const int o2 = tid + NT * u;
+        if (o2 >= NO) continue;
+        const int hl = (2 * o2) / D, d = (2 * o2) % D;
+        float a0 = 0.0f, a1 = 0.0f;
 #pragma unroll
         for (int s = 0; s < kBatch; ++s) {
             const float wgt = (s < ns) ? F.wgt[s][hl] : 0.0f;
-            a += (wgt != 0.0f) ? wgt * ov[u][s] : 0.0f;
+            if (wgt != 0.0f) {
+                a0 += wgt * lo_f(ov[u][s]);
+                a1 += wgt * hi_f(ov[u][s]);
+            }
         }
-        for (int s = kBatch; s < ns; ++s) {              // rare: more slots than the batch
+        for (int s = kBatch; s < ns; ++s) {              // more slots than the batch
             const float wgt = F.wgt[s][hl];
-            const float v = ld_shared(po + (size_t(s) * G + hl) * D + d);
-            a += (wgt != 0.0f) ? wgt * v : 0.0f;
+            const uint64_t v = ld_shared(po + size_t(s) * NO + o2);
+            if (wgt != 0.0f) {
+                a0 += wgt * lo_f(v);
+                a1 += wgt * hi_f(v);
+            }
         }
         const float L = F.L[hl];
-        const float r = (L > 0.0f) ? a / L : 0.0f;
+        const float r0 = (L > 0.0f) ? a0 / L : 0.0f;
+        const float r1 = (L > 0.0f) ? a1 / L : 0.0f;
         const size_t oi = (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d;
-        if (p.out_f32) reinterpret_cast<float *>(p.out)[oi] = r;
-        else reinterpret_cast<uint16_t *>(p.out)[oi] = f32_to_bf16_rne(r);
+        if (p.out_f32) {
+            *reinterpret_cast<float2 *>(reinterpret_cast<float *>(p.out) + oi) = make_float2(r0, r1);
+        } else {
+            *reinterpret_cast<uint32_t *>(reinterpret_cast<uint16_t *>(p.out) + oi) =
+                uint32_t(f32_to_bf16_rne(r0)) | (uint32_t(f32_to_bf16_rne(r1)) << 16);
+        }
     }
 }
 
-__device__ inline int parts_per_pair(const Params &p) {
-    int n = p.n_ac + p.n_rc + p.k;
-    if (p.mode == kModeFused && p.merger) n += 1;
-    return n;
-}
-
-// Count `n` finished partials of `pair` (written, stores completed by every wave); the
+// Count one finished partial of `pair` (written, stores completed by every wave); the
 // item completing the pair merges.
 template <class T, int D, int G>
-__device__ inline void count_partials(const Params &p, Smem<T, D, G> &sm, int pair, uint32_t n,
-                                      int tid) {
+__device__ inline void count_partial(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
     if (tid == 0) {
-        const uint32_t prev = counter_add(&p.part_cnt[pair], n);
-        sm.bcast[0] = (prev + n == uint32_t(parts_per_pair(p)));
+        const uint32_t prev = counter_add(&p.part_cnt[pair], 1u);
+        sm.bcast[0] = (prev + 1u == uint32_t(p.n_zi));
     }
     __syncthreads();
     if (sm.bcast[0]) final_merge<T, D, G>(p, sm, pair, tid);
@@ -499,16 +516,19 @@ __device__ inline void count_partials(const Params &p, Smem<T, D, G> &sm, int pa
 }
 
 // ---------------------------------------------------------------------------
-// selection by a single merger (route mode, or more candidates than kMergeBuf)
+// selection by a single merger (route mode, or more than kMergeBuf candidates).  Runs
+// in the last route item of the pair, after every route item's records are complete.
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
 __device__ __forceinline__ void merge_selection(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
     auto &M = sm.u.merge;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
-    const int k = p.k, kc = p.kc;
+    const int k = p.k;
     int m_b = p.n_spans[b];
     m_b = m_b < 0 ? 0 : (m_b > p.M_max ? p.M_max : m_b);
-    const int n_cand = p.n_rc * kc;
+    const int n_cand = p.n_cand;
+    const size_t FS = size_t(p.B) * p.Hkv * size_t(n_cand);
+    const uint64_t *rec = p.cand + size_t(pair) * n_cand;
     constexpr int kHead = kMaxTopK;
     constexpr int kFill = kMergeBuf - kMaxTopK;
     for (int j = tid; j < kMaxTopK; j += NT) M.sel[j] = -1;
@@ -520,11 +540,11 @@ __device__ __forceinline__ void merge_selection(const Params &p, Smem<T, D, G> &
             uint64_t key = 0;
             uint32_t idx = kInvalidIdx - (kHead + i);
             if (c < n_cand) {
-                const int chunk = c / kc, j = c % kc;
-                if (j < ld_shared(&p.cand_cnt[pair * p.n_rc + chunk])) {
-                    const size_t ci = (size_t(pair) * p.n_rc + chunk) * kc + j;
-                    key = ld_shared(&p.cand_key[ci]);
-                    idx = uint32_t(ld_shared(&p.cand_idx[ci]));
+                const uint32_t ci = uint32_t(ld_shared(rec + kCandIdx * FS + c));
+                if (ci < 0x80000000u) {
+                    key = (uint64_t(uint32_t(ld_shared(rec + kCandKeyHi * FS + c))) << 32) |
+                          uint32_t(ld_shared(rec + kCandKeyLo * FS + c));
+                    idx = ci;
                 }
             }
             M.key[kHead + i] = key;
@@ -563,450 +583,604 @@ __device__ __forceinline__ void merge_selection(const Params &p, Smem<T, D, G> &
                 L = p.span_len[size_t(b) * p.M_max + s];
                 off = p.block_off[(size_t(b) * p.Hkv + g) * p.M_max + s];
             }
-            int32_t *rec = reinterpret_cast<int32_t *>(&p.zrec[size_t(pair) * k + j]);
-            st_shared(rec + 0, s);
-            st_shared(rec + 1, L);
-            st_shared(rec + 2, int32_t(off & 0xFFFFFFFF));
-            st_shared(rec + 3, int32_t(off >> 32));
+            int32_t *zr = reinterpret_cast<int32_t *>(&p.zrec[size_t(pair) * k + j]);
+            st_shared(zr + 0, s);
+            st_shared(zr + 1, L);
+            st_shared(zr + 2, int32_t(off & 0xFFFFFFFF));
+            st_shared(zr + 3, int32_t(off >> 32));
         }
     }
     stores_done_barrier();
     if (p.mode == kModeFused && tid == 0) st_shared(&p.sel_ready[pair], 1u);
 }
 
-// Coarse partial over the candidates that lost (single-merger fused mode).
-template <class T, int D, int G>
-__device__ __forceinline__ void losers_partial(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
-    using GE = Geo<T, D>;
-    auto &M = sm.u.merge;
-    const int b = pair / p.Hkv, g = pair % p.Hkv;
-    const int k = p.k, kc = p.kc;
-    const int rgrp = tid / GE::RV, col = tid % GE::RV;
-    constexpr int NJ = (kLoserWin + GE::RPP - 1) / GE::RPP;
-    const unsigned char *sv = reinterpret_cast<const unsigned char *>(p.sum_v) +
-                              (size_t(b) * p.Hkv + g) * size_t(p.M_max) * GE::RB;
-    const int n_cand = p.n_rc * kc;
-    float acc[G][GE::VEC];
-    acc_zero<T, D, G>(acc);
-    online_reset(G, sm.m_run, sm.l_run, sm.scale_old, tid);
-    for (int base = 0; base < n_cand; base += kLoserWin) {
-        for (int t = tid; t < kLoserWin; t += NT) {
-            const int c = base + t;
-            int idx = -1;
-            size_t ci = 0;
-            if (c < n_cand) {
-                const int chunk = c / kc, j = c % kc;
-                if (j < ld_shared(&p.cand_cnt[pair * p.n_rc + chunk])) {
-                    ci = (size_t(pair) * p.n_rc + chunk) * kc + j;
-                    idx = ld_shared(&p.cand_idx[ci]);
-                    for (int q = 0; q < k; ++q) idx = (M.sel[q] == idx) ? -1 : idx;
-                }
-            }
-            M.loser[t] = idx;
-            for (int hl = 0; hl < G; ++hl)
-                M.pw[hl][t] = (idx >= 0) ? ld_shared(&p.cand_lg[ci * G + hl]) * kLog2e : -INFINITY;
-        }
-        __syncthreads();
-        uint4 v[NJ];
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            const int row = rgrp + GE::RPP * j;
-            v[j] = make_uint4(0, 0, 0, 0);
-            if (row < kLoserWin && M.loser[row] >= 0)
-                v[j] = ld16(sv + size_t(M.loser[row]) * GE::RB + col * 16);
-        }
-        online_fold(&M.pw[0][0], kLoserWin, kLoserWin, G, sm.m_run, sm.l_run, sm.scale_old, tid);
-        __syncthreads();
-        acc_scale<T, D, G>(acc, sm.scale_old);
-        acc_rows<T, D, G, NJ>(acc, v, &M.pw[0][0], kLoserWin, kLoserWin, rgrp);
-        __syncthreads();
+// Compile-time loop: f(IC<I>{}) for I in [B, E).
+template <int V> struct IC { static constexpr int value = V; };
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(IC<B>{});
+        static_for<B + 1, E>(f);
     }
-    rows_to_red<T, D, G>(sm, acc, tid);
-    __syncthreads();
-    write_partial<T, D, G>(p, sm, pair, p.slot_losers, tid);
 }
 
 // ---------------------------------------------------------------------------
-// route / summary item: one chunk of CR spans of a pair
+// float64 FMA chains with the query broadcast by DPP: lane l of every 16-lane row holds
+// q[d] for d = 16 m + l in qv[m]; `v_fmac_f64` with row_newbcast:n reads lane n of the
+// lane's own row, so each FMA takes the query value of column d straight from a
+// register.  One 16-byte key vector (VEC consecutive columns starting at column N0,
+// N0 % 16 + VEC <= 16) is folded into the HPT chains a[u] += q_u[d] * k[e], column by
+// column, in increasing d: the same left-to-right sum as a plain loop.  A DPP source
+// must not be written by a VALU instruction in the two preceding wait states; the
+// s_nop at the top of every block guarantees it whatever the compiler placed before.
+// ---------------------------------------------------------------------------
+template <int HPT, int VEC, int N0>
+__device__ __forceinline__ void dpp_fma_block(double (&a)[HPT], const double (&q)[HPT], const double (&k)[VEC]) {
+    if constexpr (HPT == 1 && VEC == 4) {
+        asm("s_nop 1\n\t"
+            "v_fmac_f64_dpp %0, %1, %2 row_newbcast:%6 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %1, %3 row_newbcast:%7 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %1, %4 row_newbcast:%8 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %1, %5 row_newbcast:%9 row_mask:0xf bank_mask:0xf\n\t"
+            : "+v"(a[0])
+            : "v"(q[0]), "v"(k[0]), "v"(k[1]), "v"(k[2]), "v"(k[3]), "n"(N0 + 0), "n"(N0 + 1), "n"(N0 + 2), "n"(N0 + 3));
+    }
+    else if constexpr (HPT == 1 && VEC == 8) {
+        asm("s_nop 1\n\t"
+            "v_fmac_f64_dpp %0, %1, %2 row_newbcast:%10 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %1, %3 row_newbcast:%11 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %1, %4 row_newbcast:%12 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %1, %5 row_newbcast:%13 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %1, %6 row_newbcast:%14 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %1, %7 row_newbcast:%15 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %1, %8 row_newbcast:%16 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %1, %9 row_newbcast:%17 row_mask:0xf bank_mask:0xf\n\t"
+            : "+v"(a[0])
+            : "v"(q[0]), "v"(k[0]), "v"(k[1]), "v"(k[2]), "v"(k[3]), "v"(k[4]), "v"(k[5]), "v"(k[6]), "v"(k[7]), "n"(N0 + 0), "n"(N0 + 1), "n"(N0 + 2), "n"(N0 + 3), "n"(N0 + 4), "n"(N0 + 5), "n"(N0 + 6), "n"(N0 + 7));
+    }
+    else if constexpr (HPT == 2 && VEC == 4) {
+        asm("s_nop 1\n\t"
+            "v_fmac_f64_dpp %0, %2, %4 row_newbcast:%8 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %3, %4 row_newbcast:%8 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %2, %5 row_newbcast:%9 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %3, %5 row_newbcast:%9 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %2, %6 row_newbcast:%10 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %3, %6 row_newbcast:%10 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %2, %7 row_newbcast:%11 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %3, %7 row_newbcast:%11 row_mask:0xf bank_mask:0xf\n\t"
+            : "+v"(a[0]), "+v"(a[1])
+            : "v"(q[0]), "v"(q[1]), "v"(k[0]), "v"(k[1]), "v"(k[2]), "v"(k[3]), "n"(N0 + 0), "n"(N0 + 1), "n"(N0 + 2), "n"(N0 + 3));
+    }
+    else if constexpr (HPT == 2 && VEC == 8) {
+        asm("s_nop 1\n\t"
+            "v_fmac_f64_dpp %0, %2, %4 row_newbcast:%12 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %3, %4 row_newbcast:%12 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %2, %5 row_newbcast:%13 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %3, %5 row_newbcast:%13 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %2, %6 row_newbcast:%14 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %3, %6 row_newbcast:%14 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %2, %7 row_newbcast:%15 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %3, %7 row_newbcast:%15 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %2, %8 row_newbcast:%16 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %3, %8 row_newbcast:%16 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %2, %9 row_newbcast:%17 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %3, %9 row_newbcast:%17 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %2, %10 row_newbcast:%18 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %3, %10 row_newbcast:%18 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %2, %11 row_newbcast:%19 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %3, %11 row_newbcast:%19 row_mask:0xf bank_mask:0xf\n\t"
+            : "+v"(a[0]), "+v"(a[1])
+            : "v"(q[0]), "v"(q[1]), "v"(k[0]), "v"(k[1]), "v"(k[2]), "v"(k[3]), "v"(k[4]), "v"(k[5]), "v"(k[6]), "v"(k[7]), "n"(N0 + 0), "n"(N0 + 1), "n"(N0 + 2), "n"(N0 + 3), "n"(N0 + 4), "n"(N0 + 5), "n"(N0 + 6), "n"(N0 + 7));
+    }
+    else if constexpr (HPT == 4 && VEC == 4) {
+        asm("s_nop 1\n\t"
+            "v_fmac_f64_dpp %0, %4, %8 row_newbcast:%12 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %5, %8 row_newbcast:%12 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %2, %6, %8 row_newbcast:%12 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %3, %7, %8 row_newbcast:%12 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %4, %9 row_newbcast:%13 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %5, %9 row_newbcast:%13 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %2, %6, %9 row_newbcast:%13 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %3, %7, %9 row_newbcast:%13 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %4, %10 row_newbcast:%14 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %5, %10 row_newbcast:%14 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %2, %6, %10 row_newbcast:%14 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %3, %7, %10 row_newbcast:%14 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %4, %11 row_newbcast:%15 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %5, %11 row_newbcast:%15 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %2, %6, %11 row_newbcast:%15 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %3, %7, %11 row_newbcast:%15 row_mask:0xf bank_mask:0xf\n\t"
+            : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3])
+            : "v"(q[0]), "v"(q[1]), "v"(q[2]), "v"(q[3]), "v"(k[0]), "v"(k[1]), "v"(k[2]), "v"(k[3]), "n"(N0 + 0), "n"(N0 + 1), "n"(N0 + 2), "n"(N0 + 3));
+    }
+    else if constexpr (HPT == 4 && VEC == 8) {
+        asm("s_nop 1\n\t"
+            "v_fmac_f64_dpp %0, %4, %8 row_newbcast:%16 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %5, %8 row_newbcast:%16 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %2, %6, %8 row_newbcast:%16 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %3, %7, %8 row_newbcast:%16 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %4, %9 row_newbcast:%17 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %5, %9 row_newbcast:%17 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %2, %6, %9 row_newbcast:%17 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %3, %7, %9 row_newbcast:%17 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %4, %10 row_newbcast:%18 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %5, %10 row_newbcast:%18 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %2, %6, %10 row_newbcast:%18 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %3, %7, %10 row_newbcast:%18 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %4, %11 row_newbcast:%19 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %5, %11 row_newbcast:%19 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %2, %6, %11 row_newbcast:%19 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %3, %7, %11 row_newbcast:%19 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %4, %12 row_newbcast:%20 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %5, %12 row_newbcast:%20 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %2, %6, %12 row_newbcast:%20 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %3, %7, %12 row_newbcast:%20 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %4, %13 row_newbcast:%21 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %5, %13 row_newbcast:%21 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %2, %6, %13 row_newbcast:%21 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %3, %7, %13 row_newbcast:%21 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %4, %14 row_newbcast:%22 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %5, %14 row_newbcast:%22 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %2, %6, %14 row_newbcast:%22 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %3, %7, %14 row_newbcast:%22 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %0, %4, %15 row_newbcast:%23 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %1, %5, %15 row_newbcast:%23 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %2, %6, %15 row_newbcast:%23 row_mask:0xf bank_mask:0xf\n\t"
+            "v_fmac_f64_dpp %3, %7, %15 row_newbcast:%23 row_mask:0xf bank_mask:0xf\n\t"
+            : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3])
+            : "v"(q[0]), "v"(q[1]), "v"(q[2]), "v"(q[3]), "v"(k[0]), "v"(k[1]), "v"(k[2]), "v"(k[3]), "v"(k[4]), "v"(k[5]), "v"(k[6]), "v"(k[7]), "n"(N0 + 0), "n"(N0 + 1), "n"(N0 + 2), "n"(N0 + 3), "n"(N0 + 4), "n"(N0 + 5), "n"(N0 + 6), "n"(N0 + 7));
+    }
+    else {
+        static_assert(HPT == 1 || HPT == 2 || HPT == 4, "heads per thread");
+    }
+}
+
+// ---------------------------------------------------------------------------
+// route item: one chunk of CR spans of a pair
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
-__device__ __forceinline__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chunk, int tid) {
+__device__ __forceinline__ void route_item(const Params &p, Smem<T, D, G> &sm, int pair, int chunk,
+                                           uint32_t tag, int tid) {
     using GE = Geo<T, D>;
+    constexpr int HPT = Smem<T, D, G>::HPT;
     auto &R = sm.u.route;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
     int m_b = p.n_spans[b];
     m_b = m_b < 0 ? 0 : (m_b > p.M_max ? p.M_max : m_b);
     const int s0 = chunk * CR;
     const int nv = max(0, min(CR, m_b - s0));
-    const bool attend = (p.mode == kModeAttend);
-    const bool need_coarse = (p.mode != kModeRoute);
-    const bool have_logits = attend && p.logits_in != nullptr;
-    const bool need_dots = !have_logits;
+    const bool select = (p.mode != kModeAttend);       // candidates for the selection
+    const bool publish = (p.mode != kModeRoute);       // coarse logits for the share items
     const size_t row0 = (size_t(b) * p.Hkv + g) * size_t(p.M_max) + s0;
     const int rgrp = tid / GE::RV, col = tid % GE::RV;
     const int wave = tid >> 6, lane = tid & 63;
     constexpr int NJ = (CR + GE::RPP - 1) / GE::RPP;
 
-    // 1. issue the loads routing needs: summary keys (-> LDS), query, ln|S|, and
-    //    |S| / block offsets for the candidate records
-    if (need_dots) {
+    // 1. loads: summary keys (-> LDS), query (-> registers, float64), ln|S|, and
+    //    |S| / block offsets for the candidate records.  Every load is issued before any
+    //    value is used; addresses are clamped to the chunk's rows inside the arrays, so
+    //    none waits for n_spans (validity is applied where the values are used).
+    const int nr = min(CR, p.M_max - s0);               // rows of this chunk in the arrays
+    double qv[D / 16][HPT];
+    {
         const unsigned char *src = reinterpret_cast<const unsigned char *>(p.sum_k) + row0 * GE::RB;
         uint4 kv[NJ];
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
-            const int row = rgrp + GE::RPP * j;
-            if (row < nv) kv[j] = ld16(src + size_t(row) * GE::RB + col * 16);
+            const int row = min(rgrp + GE::RPP * j, nr - 1);
+            kv[j] = ld16(src + size_t(row) * GE::RB + col * 16);
         }
-        for (int i = tid; i < G * D; i += NT) {
-            const int hl = i / D, d = i % D;
-            R.qd[hl][d] = double(T::load1(p.q, (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d));
+        // the query of the thread's head group: lane l of each 16-lane row holds
+        // q_u[16 m + l] in qv[m][u]
+        const int l16 = lane & 15, hgq = tid / CR;
+        float qr[D / 16][HPT];
+#pragma unroll
+        for (int m = 0; m < D / 16; ++m)
+#pragma unroll
+            for (int u = 0; u < HPT; ++u) {
+                const int h = min(hgq * HPT + u, G - 1);
+                qr[m][u] = T::load1(p.q, (size_t(b) * p.Hq + size_t(g) * G + h) * D + m * 16 + l16);
+            }
+        const int ti = min(tid, nr - 1);
+        const double lns = p.span_logsize[size_t(b) * p.M_max + s0 + ti];
+        int32_t slen = 0;
+        int64_t boff = 0;
+        if (select) {
+            slen = p.span_len[size_t(b) * p.M_max + s0 + ti];
+            boff = p.block_off[row0 + ti];
         }
-        if (tid < nv) R.lns[tid] = p.span_logsize[size_t(b) * p.M_max + s0 + tid];
+#pragma unroll
+        for (int m = 0; m < D / 16; ++m)
+#pragma unroll
+            for (int u = 0; u < HPT; ++u) qv[m][u] = (hgq * HPT + u < G) ? double(qr[m][u]) : 0.0;
+        if (tid < CR) {
+            R.lns[tid] = lns;
+            R.slen[tid] = slen;
+            R.boff[tid] = boff;
+        }
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
             const int row = rgrp + GE::RPP * j;
-            if (row < nv) *reinterpret_cast<uint4 *>(R.kb + size_t(row) * GE::RS + col * 16) = kv[j];
-        }
-    }
-    if (tid < CR) {
-        R.excl[tid] = 0;
-        if (!attend && tid < nv) {
-            R.slen[tid] = p.span_len[size_t(b) * p.M_max + s0 + tid];
-            R.boff[tid] = p.block_off[row0 + tid];
+            if (row < nr) *reinterpret_cast<uint4 *>(R.kb + size_t(row) * GE::RS + col * 16) = kv[j];
         }
     }
     __syncthreads();
 
-    // 2. routing scores: float64, products exact, summed left to right over d,
-    //    then (s * scale) + ln|S| as two separately rounded operations.  Each thread
-    //    runs two independent chains (same head within a wave, different spans).
-    for (int c0 = tid; c0 < G * CR; c0 += 2 * NT) {
-        const int c1 = c0 + NT;
-        const bool has1 = c1 < G * CR;
-        const int h0 = c0 / CR, i0 = c0 % CR;
-        const int h1 = has1 ? c1 / CR : h0, i1 = has1 ? c1 % CR : i0;
-        double sc0 = -INFINITY, sc1 = -INFINITY;
-        if (need_dots) {
-            const unsigned char *r0 = R.kb + size_t(i0) * GE::RS;
-            const unsigned char *r1 = R.kb + size_t(i1) * GE::RS;
-            double a0 = 0.0, a1 = 0.0;
-#pragma unroll 2
-            for (int c = 0; c < GE::RV; ++c) {
-                float f0[GE::VEC], f1[GE::VEC];
-                T::unpack(*reinterpret_cast<const uint4 *>(r0 + c * 16), f0);
-                T::unpack(*reinterpret_cast<const uint4 *>(r1 + c * 16), f1);
+    // 2. routing scores: float64, products exact, summed left to right over d, then
+    //    (s * scale) + ln|S| as two separately rounded operations.  Thread (span i, head
+    //    group hg) runs HPT chains that share each converted key element; the head group
+    //    is uniform per wave and the query comes from registers by DPP broadcast.
+    const int i = tid % CR, hg = tid / CR;
+    double sc[HPT];
+    {
+        double a[HPT];
 #pragma unroll
-                for (int e = 0; e < GE::VEC; ++e) {
-                    a0 = __builtin_fma(R.qd[h0][c * GE::VEC + e], double(f0[e]), a0);
-                    a1 = __builtin_fma(R.qd[h1][c * GE::VEC + e], double(f1[e]), a1);
-                }
-            }
-            {
+        for (int u = 0; u < HPT; ++u) a[u] = 0.0;
+        const unsigned char *rowp = R.kb + size_t(i) * GE::RS;
+        static_for<0, GE::RV>([&](auto cc) {
+            constexpr int c = decltype(cc)::value;
+            constexpr int d0 = c * GE::VEC;
+            float f[GE::VEC];
+            T::unpack(*reinterpret_cast<const uint4 *>(rowp + c * 16), f);
+            double kd[GE::VEC];
+#pragma unroll
+            for (int e = 0; e < GE::VEC; ++e) kd[e] = double(f[e]);
+            double qq[HPT];
+#pragma unroll
+            for (int u = 0; u < HPT; ++u) qq[u] = qv[d0 / 16][u];
+            dpp_fma_block<HPT, GE::VEC, d0 % 16>(a, qq, kd);
+        });
+        {
 #pragma clang fp contract(off)
-                const double m0 = a0 * p.scale;
-                const double m1 = a1 * p.scale;
-                if (i0 < nv) sc0 = m0 + R.lns[i0];
-                if (has1 && i1 < nv) sc1 = m1 + R.lns[i1];
+#pragma unroll
+            for (int u = 0; u < HPT; ++u) {
+                const double m = a[u] * p.scale;
+                sc[u] = (i < nv) ? m + R.lns[i] : -INFINITY;
             }
-        } else {
-            const size_t lbase = (size_t(b) * p.Hq + size_t(g) * G) * p.M_max + s0;
-            if (i0 < nv) sc0 = double(p.logits_in[lbase + size_t(h0) * p.M_max + i0]);
-            if (has1 && i1 < nv) sc1 = double(p.logits_in[lbase + size_t(h1) * p.M_max + i1]);
         }
-        R.lg[h0][i0] = sc0;
-        if (has1) R.lg[h1][i1] = sc1;
-        if (p.logits_out) {
-            const size_t lbase = (size_t(b) * p.Hq + size_t(g) * G) * p.M_max;
-            if (s0 + i0 < p.M_max) p.logits_out[lbase + size_t(h0) * p.M_max + s0 + i0] = float(sc0);
-            if (has1 && s0 + i1 < p.M_max) p.logits_out[lbase + size_t(h1) * p.M_max + s0 + i1] = float(sc1);
-        }
+    }
+    // 3. per (head, span) outputs: the tagged base-2 logit for the share items, the
+    //    natural-unit logit for the caller
+#pragma unroll
+    for (int u = 0; u < HPT; ++u) {
+        const int h = hg * HPT + u;
+        if (h >= G) continue;
+        if (publish && i < nv)
+            st_shared(&p.tlg[(size_t(pair) * G + h) * p.M_max + s0 + i],
+                      tagged(tag, __float_as_uint(float(sc[u] * kLog2eD))));
+        if (p.logits_out && s0 + i < p.M_max)
+            p.logits_out[(size_t(b) * p.Hq + size_t(g) * G + h) * p.M_max + s0 + i] = float(sc[u]);
+    }
+    if (!select) return;
+    {
+        double mx = -INFINITY;
+#pragma unroll
+        for (int u = 0; u < HPT; ++u)
+            if (hg * HPT + u < G) mx = fmax(mx, sc[u]);
+        R.pmax[hg][i] = mx;
     }
     __syncthreads();
 
-    // 3. candidates: waves 0 and 1 each sort 64 (key, span) pairs with a bitonic network;
+    // 4. candidates: waves 0 and 1 each sort 64 (key, span) pairs with a bitonic network;
     //    a span's rank in the chunk is its position plus the number of better entries of
-    //    the other half (binary search); the best kc become the chunk's sorted candidates.
-    if (!attend) {
-        if (wave < 2) {
-            const int i = wave * 64 + lane;
-            uint64_t key = 0;
-            uint32_t idx = kInvalidIdx - uint32_t(i);
-            if (i < nv) {
-                double x = R.lg[0][i];
-                for (int hl = 1; hl < G; ++hl) x = fmax(x, R.lg[hl][i]);
-                key = order_key(x);
-                idx = uint32_t(s0 + i);
-            }
+    //    the other half (binary search); the best kc become the chunk's candidate records.
+    if (wave < 2) {
+        const int ii = wave * 64 + lane;
+        uint64_t key = 0;
+        uint32_t idx = kInvalidIdx - uint32_t(ii);
+        if (ii < nv) {
+            key = order_key(fmax(R.pmax[0][ii], R.pmax[1][ii]));
+            idx = uint32_t(s0 + ii);
+        }
 #define SEKV_BITONIC_STEP(STRIDE)                                                          \
-            {                                                                              \
-                const uint32_t klo = lane_xor<STRIDE>(uint32_t(key), lane);                \
-                const uint32_t khi = lane_xor<STRIDE>(uint32_t(key >> 32), lane);          \
-                const uint32_t oi = lane_xor<STRIDE>(idx, lane);                           \
-                const uint64_t ok = (uint64_t(khi) << 32) | klo;                           \
-                const bool lower = (lane & (STRIDE)) == 0;                                 \
-                const bool take = (lower == up) ? better(ok, oi, key, idx)                 \
-                                                : better(key, idx, ok, oi);                \
-                if (take) { key = ok; idx = oi; }                                          \
-            }
+        {                                                                                  \
+            const uint32_t klo = lane_xor<STRIDE>(uint32_t(key), lane);                    \
+            const uint32_t khi = lane_xor<STRIDE>(uint32_t(key >> 32), lane);              \
+            const uint32_t oi = lane_xor<STRIDE>(idx, lane);                               \
+            const uint64_t ok = (uint64_t(khi) << 32) | klo;                               \
+            const bool lower = (lane & (STRIDE)) == 0;                                     \
+            const bool take = (lower == up) ? better(ok, oi, key, idx)                     \
+                                            : better(key, idx, ok, oi);                    \
+            if (take) { key = ok; idx = oi; }                                              \
+        }
 #pragma unroll
-            for (int size = 2; size <= 64; size <<= 1) {
-                const bool up = (lane & size) == 0;
-                if (size >= 64) SEKV_BITONIC_STEP(32)
-                if (size >= 32) SEKV_BITONIC_STEP(16)
-                if (size >= 16) SEKV_BITONIC_STEP(8)
-                if (size >= 8) SEKV_BITONIC_STEP(4)
-                if (size >= 4) SEKV_BITONIC_STEP(2)
-                SEKV_BITONIC_STEP(1)
-            }
+        for (int size = 2; size <= 64; size <<= 1) {
+            const bool up = (lane & size) == 0;
+            if (size >= 64) SEKV_BITONIC_STEP(32)
+            if (size >= 32) SEKV_BITONIC_STEP(16)
+            if (size >= 16) SEKV_BITONIC_STEP(8)
+            if (size >= 8) SEKV_BITONIC_STEP(4)
+            if (size >= 4) SEKV_BITONIC_STEP(2)
+            SEKV_BITONIC_STEP(1)
+        }
 #undef SEKV_BITONIC_STEP
-            R.skey[wave][lane] = key;
-            R.sidx[wave][lane] = idx;
+        R.skey[wave][lane] = key;
+        R.sidx[wave][lane] = idx;
+    }
+    __syncthreads();
+    const int kc = p.kc;
+    if (wave < 2) {
+        const uint64_t key = R.skey[wave][lane];
+        const uint32_t idx = R.sidx[wave][lane];
+        const int other = 1 - wave;
+        int lo = 0, hi = 64;
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (better(R.skey[other][mid], R.sidx[other][mid], key, idx)) lo = mid + 1;
+            else hi = mid;
         }
-        __syncthreads();
-        const int kc = min(p.kc, nv);
-        if (wave < 2) {
-            const uint64_t key = R.skey[wave][lane];
-            const uint32_t idx = R.sidx[wave][lane];
-            const int other = 1 - wave;
-            int lo = 0, hi = 64;
-            while (lo < hi) {
-                const int mid = (lo + hi) >> 1;
-                if (better(R.skey[other][mid], R.sidx[other][mid], key, idx)) lo = mid + 1;
-                else hi = mid;
-            }
-            const int rank = lane + lo;
-            if (idx < 0x80000000u && rank < kc) {
-                const int li = int(idx) - s0;
-                const size_t ci = (size_t(pair) * p.n_rc + chunk) * p.kc + rank;
-                st_shared(&p.cand_key[ci], key);
-                st_shared(&p.cand_idx[ci], int32_t(idx));
-                st_shared(&p.cand_len[ci], R.slen[li]);
-                st_shared(&p.cand_off[ci], R.boff[li]);
-                for (int hl = 0; hl < G; ++hl) st_shared(&p.cand_lg[ci * G + hl], float(R.lg[hl][li]));
-                R.excl[li] = 1;
-            }
+        const int rank = lane + lo;
+        if (rank < kc) {
+            // every position of every chunk is written each launch (invalid entries too),
+            // so a reader never has to know which ones exist
+            const bool valid = idx < 0x80000000u;
+            const int li = valid ? int(idx) - s0 : 0;
+            const int32_t len = valid ? R.slen[li] : 0;
+            const uint64_t off = valid ? uint64_t(R.boff[li]) : 0;
+            const size_t FS = size_t(p.B) * p.Hkv * size_t(p.n_cand);
+            uint64_t *rec = p.cand + size_t(pair) * p.n_cand + size_t(chunk) * kc + rank;
+            st_shared(rec + kCandKeyHi * FS, tagged(tag, valid ? uint32_t(key >> 32) : 0u));
+            st_shared(rec + kCandKeyLo * FS, tagged(tag, valid ? uint32_t(key) : 0u));
+            st_shared(rec + kCandIdx * FS, tagged(tag, valid ? idx : kInvalidIdx));
+            st_shared(rec + kCandLen * FS, tagged(tag, uint32_t(len)));
+            st_shared(rec + kCandOffLo * FS, tagged(tag, uint32_t(off)));
+            st_shared(rec + kCandOffHi * FS, tagged(tag, uint32_t(off >> 32)));
         }
-        if (tid == 0) st_shared(&p.cand_cnt[pair * p.n_rc + chunk], kc);
-        // publish the candidates before the coarse partial: zoom items wait on them
+    }
+    if (p.merger) {
+        // single merger: the last route item of the pair (counted after its records are
+        // complete) selects for the whole pair
         stores_done_barrier();
         if (tid == 0) {
-            sm.bcast[1] = 0;
-            if (p.merger) {
-                const uint32_t prev = counter_add(&p.route_cnt[pair], 1u);
-                sm.bcast[1] = (prev == uint32_t(p.n_rc - 1));
-            } else {
-                (void)counter_add(&p.route_cnt[pair], 1u);     // no return value awaited
-            }
+            const uint32_t prev = counter_add(&p.route_cnt[pair], 1u);
+            sm.bcast[1] = (prev == uint32_t(p.n_rc - 1));
         }
         __syncthreads();
-    } else {
-        if (tid < CR) {
-            int ex = 0;
-            for (int j = 0; j < p.k; ++j) ex |= (p.sel_in[size_t(pair) * p.k + j] == s0 + tid);
-            R.excl[tid] = ex;
-        }
-        if (tid == 0) sm.bcast[1] = 0;
-        __syncthreads();
-    }
-    const bool merger = sm.bcast[1] != 0;
-
-    // 4. coarse partial over the chunk's remaining spans
-    uint32_t n_done = 0;
-    uint4 v[NJ];
-    if (need_coarse) {
-        const unsigned char *src = reinterpret_cast<const unsigned char *>(p.sum_v) + row0 * GE::RB;
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-            const int row = rgrp + GE::RPP * j;
-            if (row < nv) v[j] = ld16(src + size_t(row) * GE::RB + col * 16);
-        }
-    }
-    if (need_coarse) {
-        for (int t = tid; t < G * CR; t += NT) {
-            const int hl = t / CR, i = t % CR;
-            R.pw[hl][i] = (i < nv && !R.excl[i]) ? float(R.lg[hl][i] * kLog2eD) : -INFINITY;
-        }
-        online_reset(G, sm.m_run, sm.l_run, sm.scale_old, tid);
-        __syncthreads();
-        online_fold(&R.pw[0][0], CR, CR, G, sm.m_run, sm.l_run, sm.scale_old, tid);
-        __syncthreads();
-        float acc[G][GE::VEC];
-        acc_zero<T, D, G>(acc);
-        acc_rows<T, D, G, NJ>(acc, v, &R.pw[0][0], CR, nv, rgrp);
-        rows_to_red<T, D, G>(sm, acc, tid);
-        __syncthreads();
-        write_partial<T, D, G>(p, sm, pair, p.slot_route0 + chunk, tid);
-        n_done = 1;
-    }
-    if (merger) {
-        __syncthreads();
-        merge_selection<T, D, G>(p, sm, pair, tid);
-        __syncthreads();
-        if (p.mode == kModeFused) {
-            losers_partial<T, D, G>(p, sm, pair, tid);
-            n_done += 1;
-        }
-    }
-    if (n_done) {
-        stores_done_barrier();
-        count_partials<T, D, G>(p, sm, pair, n_done, tid);
+        if (sm.bcast[1]) merge_selection<T, D, G>(p, sm, pair, tid);
     }
 }
 
 // ---------------------------------------------------------------------------
-// anchor item: CA full-resolution tokens of a pair
+// share item pieces
 // ---------------------------------------------------------------------------
-template <class T, int D, int G>
-__device__ __forceinline__ void anchor_item(const Params &p, Smem<T, D, G> &sm, int pair, int chunk, int tid) {
+// Rows rgrp + RPP*j (j < NJ) of a block of n rows; addresses are clamped to the last
+// row, so every vector is loaded (validity is applied where the values are used).
+template <class T, int D, int NJ>
+__device__ inline void load_rows(uint4 (&v)[NJ], const unsigned char *base, int n, int rgrp, int col) {
     using GE = Geo<T, D>;
-    constexpr int CA = Smem<T, D, G>::CA;
-    constexpr int NJ = CA / GE::RPP;                     // 8
-    auto &A = sm.u.anchor;
-    const int b = pair / p.Hkv, g = pair % p.Hkv;
-    int An = p.n_anchors[b];
-    An = An < 0 ? 0 : (An > p.A_max ? p.A_max : An);
-    const int a0 = chunk * CA;
-    const int na = max(0, min(CA, An - a0));
-    const int rgrp = tid / GE::RV, col = tid % GE::RV;
-    const size_t base = ((size_t(b) * p.Hkv + g) * size_t(p.A_max) + a0) * GE::RB;
-    const unsigned char *ak = reinterpret_cast<const unsigned char *>(p.anchor_k) + base;
-    const unsigned char *av = reinterpret_cast<const unsigned char *>(p.anchor_v) + base;
-    uint4 kv[NJ], vv[NJ];
+    if (n <= 0) return;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int row = min(rgrp + GE::RPP * j, n - 1);
+        v[j] = ld16(base + size_t(row) * GE::RB + col * 16);
+    }
+}
+
+// One block of na anchor tokens: scores, online softmax, weighted values into sm.red.
+template <class T, int D, int G, int NJ>
+__device__ inline void anchor_block(const Params &p, Smem<T, D, G> &sm, const uint4 (&kr)[NJ],
+                                    const uint4 (&vr)[NJ], int na, float (&pend)[G], int rgrp,
+                                    int col, int tid) {
+    using GE = Geo<T, D>;
+    constexpr int AB = Smem<T, D, G>::AB;
+    auto &Z = sm.u.share;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
         const int row = rgrp + GE::RPP * j;
-        if (row < na) {
-            kv[j] = ld16(ak + size_t(row) * GE::RB + col * 16);
-            vv[j] = ld16(av + size_t(row) * GE::RB + col * 16);
-        }
-    }
-    for (int i = tid; i < G * D; i += NT) {
-        const int hl = i / D, d = i % D;
-        A.qf[hl][d] = T::load1(p.q, (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d);
-    }
-    online_reset(G, sm.m_run, sm.l_run, sm.scale_old, tid);
-    __syncthreads();
-    // scores: partial dots over this thread's VEC columns, summed across the row's lanes
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-        const int row = rgrp + GE::RPP * j;
+        float f[GE::VEC];
+        T::unpack(kr[j], f);
         float part[G];
 #pragma unroll
-        for (int hl = 0; hl < G; ++hl) part[hl] = 0.0f;
-        if (row < na) {
-            float f[GE::VEC];
-            T::unpack(kv[j], f);
+        for (int hl = 0; hl < G; ++hl) {
+            part[hl] = 0.0f;
 #pragma unroll
-            for (int hl = 0; hl < G; ++hl)
-#pragma unroll
-                for (int e = 0; e < GE::VEC; ++e) part[hl] += A.qf[hl][col * GE::VEC + e] * f[e];
+            for (int e = 0; e < GE::VEC; ++e) part[hl] += Z.qf[hl][col * GE::VEC + e] * f[e];
+            part[hl] = row_sum<GE::RV>(part[hl]);
         }
+        if (col == 0 && row < na)
 #pragma unroll
-        for (int hl = 0; hl < G; ++hl) part[hl] = row_sum<GE::RV>(part[hl]);
-        if (col == 0)
-#pragma unroll
-            for (int hl = 0; hl < G; ++hl)
-                A.sc[hl][row] = (row < na) ? part[hl] * p.scale_log2 : -INFINITY;
+            for (int hl = 0; hl < G; ++hl) Z.sc[hl][row] = part[hl] * p.scale_log2;
     }
     __syncthreads();
-    online_fold(&A.sc[0][0], CA, CA, G, sm.m_run, sm.l_run, sm.scale_old, tid);
+    online_fold(&Z.sc[0][0], AB, na, G, sm.m_run, sm.l_run, sm.scale_old, tid);
     __syncthreads();
+    pend_fold<G>(pend, sm.scale_old);
     float acc[G][GE::VEC];
     acc_zero<T, D, G>(acc);
-    acc_rows<T, D, G, NJ>(acc, vv, &A.sc[0][0], CA, na, rgrp);
-    rows_to_red<T, D, G>(sm, acc, tid);
+    acc_rows<T, D, G, NJ>(acc, vr, &Z.sc[0][0], AB, na, rgrp);
+    acc_flush<T, D, G>(sm, acc, pend, tid);
     __syncthreads();
-    write_partial<T, D, G>(p, sm, pair, chunk, tid);
-    stores_done_barrier();
-    count_partials<T, D, G>(p, sm, pair, 1u, tid);
 }
 
-// ---------------------------------------------------------------------------
-// zoom item, fused per-item selection: rank the pair's candidates (LDS)
-// ---------------------------------------------------------------------------
-template <class T, int D, int G>
-__device__ __forceinline__ void rank_candidates(const Params &p, Smem<T, D, G> &sm, int pair, int j, int m_b,
-                                int tid, int &n_loser) {
-    auto &Z = sm.u.zoom;
-    const int k = p.k, kc = p.kc;
-    const int n_cand = p.n_rc * kc;
-    // each thread owns candidates tid and tid + NT: records stay in its registers
-    constexpr int OWN = kMergeBuf / NT;
-    uint64_t okey[OWN];
-    uint32_t oidx[OWN];
-    int32_t olen[OWN];
-    int64_t ooff[OWN];
-    float olg[OWN][G];
+// One block of nc summary rows starting at span c0; Z.cw holds their base-2 logits.
+// Spans among the pair's k selected ones (Z.sel) are skipped: they are zoomed.
+template <class T, int D, int G, int NJ>
+__device__ inline void coarse_block(Smem<T, D, G> &sm, const uint4 (&cv)[NJ], int c0, int nc,
+                                    int k, float (&pend)[G], int rgrp, int tid) {
+    using GE = Geo<T, D>;
+    constexpr int CB = Smem<T, D, G>::CB;
+    static_assert(CB <= NT, "one thread per summary row");
+    auto &Z = sm.u.share;
+    if (tid < nc) {
+        bool ex = false;
+        for (int t = 0; t < k; ++t) ex |= (Z.sel[t] == c0 + tid);
+        if (ex)
 #pragma unroll
-    for (int u = 0; u < OWN; ++u) {
+            for (int hl = 0; hl < G; ++hl) Z.cw[hl][tid] = -INFINITY;
+    }
+    __syncthreads();
+    online_fold(&Z.cw[0][0], CB, nc, G, sm.m_run, sm.l_run, sm.scale_old, tid);
+    __syncthreads();
+    pend_fold<G>(pend, sm.scale_old);
+    float acc[G][GE::VEC];
+    acc_zero<T, D, G>(acc);
+    acc_rows<T, D, G, NJ>(acc, cv, &Z.cw[0][0], CB, nc, rgrp);
+    acc_flush<T, D, G>(sm, acc, pend, tid);
+    __syncthreads();
+}
+
+// Base-2 logits of summary rows [c0, c0 + nc) into Z.cw: one polling attempt on this
+// launch's tagged words (returns whether every tag was current), or the caller's logits.
+template <class T, int D, int G>
+__device__ inline bool coarse_logits(const Params &p, Smem<T, D, G> &sm, int pair, int c0, int nc,
+                                     uint32_t tag, int tid) {
+    constexpr int CB = Smem<T, D, G>::CB;
+    auto &Z = sm.u.share;
+    bool ok = true;
+    if (p.logits_in) {
+        const int b = pair / p.Hkv, g = pair % p.Hkv;
+        for (int t = tid; t < G * CB; t += NT) {
+            const int hl = t / CB, i = t % CB;
+            if (i < nc)
+                Z.cw[hl][i] = p.logits_in[(size_t(b) * p.Hq + size_t(g) * G + hl) * p.M_max + c0 + i] * kLog2e;
+        }
+        return true;
+    }
+    for (int t = tid; t < G * CB; t += NT) {
+        const int hl = t / CB, i = t % CB;
+        if (i < nc) {
+            const uint64_t w = ld_shared(&p.tlg[(size_t(pair) * G + hl) * p.M_max + c0 + i]);
+            ok &= tag_is(w, tag);
+            Z.cw[hl][i] = lo_f(w);
+        }
+    }
+    return ok;
+}
+
+// Poll until the logits of summary block [c0, c0 + nc) are this launch's.
+template <class T, int D, int G>
+__device__ inline void wait_coarse_logits(const Params &p, Smem<T, D, G> &sm, int pair, int c0,
+                                          int nc, uint32_t tag, int tid) {
+    for (uint32_t it = 0;; ++it) {
+        const bool ok = coarse_logits<T, D, G>(p, sm, pair, c0, nc, tag, tid);
+        if (__syncthreads_and(ok)) return;
+        if (it >= kSpinLimit) {
+            if (tid == 0) flag_error(p, kErrSpinTimeout);
+            return;
+        }
+        __builtin_amdgcn_s_sleep(2);
+    }
+}
+
+constexpr int kOwn = kMergeBuf / NT;                   // candidates per thread when ranking
+
+// One polling attempt on the pair's candidate records; thread tid owns candidates tid
+// and tid + NT.  Returns whether every tag was current.
+__device__ inline bool load_candidates(const Params &p, int pair, uint32_t tag, uint64_t (&okey)[kOwn],
+                                       uint32_t (&oidx)[kOwn], int32_t (&olen)[kOwn],
+                                       int64_t (&ooff)[kOwn], int tid) {
+    const size_t FS = size_t(p.B) * p.Hkv * size_t(p.n_cand);
+    const uint64_t *rec = p.cand + size_t(pair) * p.n_cand;
+    bool ok = true;
+#pragma unroll
+    for (int u = 0; u < kOwn; ++u) {
         const int c = tid + NT * u;
         okey[u] = 0;
-        oidx[u] = kInvalidIdx - uint32_t(c);
+        oidx[u] = kInvalidIdx;
         olen[u] = 0;
         ooff[u] = 0;
-        if (c < n_cand) {
-            const int chunk = c / kc, jj = c % kc;
-            if (jj < ld_shared(&p.cand_cnt[pair * p.n_rc + chunk])) {
-                const size_t ci = (size_t(pair) * p.n_rc + chunk) * kc + jj;
-                okey[u] = ld_shared(&p.cand_key[ci]);
-                oidx[u] = uint32_t(ld_shared(&p.cand_idx[ci]));
-                olen[u] = ld_shared(&p.cand_len[ci]);
-                ooff[u] = ld_shared(&p.cand_off[ci]);
+        if (c < p.n_cand) {
+            uint64_t w[kCandFields];
 #pragma unroll
-                for (int hl = 0; hl < G; ++hl) olg[u][hl] = ld_shared(&p.cand_lg[ci * G + hl]);
+            for (int f = 0; f < kCandFields; ++f) w[f] = ld_shared(rec + f * FS + c);
+#pragma unroll
+            for (int f = 0; f < kCandFields; ++f) ok &= tag_is(w[f], tag);
+            okey[u] = (uint64_t(uint32_t(w[kCandKeyHi])) << 32) | uint32_t(w[kCandKeyLo]);
+            oidx[u] = uint32_t(w[kCandIdx]);
+            olen[u] = int32_t(uint32_t(w[kCandLen]));
+            ooff[u] = int64_t(uint64_t(uint32_t(w[kCandOffLo])) | (uint64_t(uint32_t(w[kCandOffHi])) << 32));
+        }
+    }
+    return ok;
+}
+
+// rk += 1 if (key_o, ~idx_o) > (key_c, ~idx_c) as 96-bit unsigned numbers, i.e. if
+// candidate o is ahead of candidate c in (key desc, span asc): the borrow out of
+// mine - other.  Words are {~idx, key lo, key hi}.
+__device__ __forceinline__ void count_ahead(uint32_t &rk, const uint4 &o, uint32_t m0, uint32_t m1,
+                                            uint32_t m2) {
+    uint32_t t;
+    asm("v_sub_co_u32 %0, vcc, %2, %3\n\t"
+        "v_subb_co_u32 %0, vcc, %4, %5, vcc\n\t"
+        "v_subb_co_u32 %0, vcc, %6, %7, vcc\n\t"
+        "v_addc_co_u32 %1, vcc, 0, %1, vcc"
+        : "=&v"(t), "+v"(rk)
+        : "v"(m0), "v"(o.x), "v"(m1), "v"(o.y), "v"(m2), "v"(o.z)
+        : "vcc");
+}
+
+// Rank the pair's candidates (LDS): rank = number of candidates ahead in (key desc,
+// span asc).  Ranks below k fill Z.sel; the owner of rank j leaves {span, |S|, offset}
+// in bcast[4..7].  Up to NT/2 candidates, two threads scan half the list each.
+template <class T, int D, int G>
+__device__ __forceinline__ void rank_candidates(const Params &p, Smem<T, D, G> &sm, int j, int m_b,
+                                                const uint64_t (&okey)[kOwn], const uint32_t (&oidx)[kOwn],
+                                                const int32_t (&olen)[kOwn], const int64_t (&ooff)[kOwn],
+                                                int tid) {
+    auto &Z = sm.u.share;
+    const int k = p.k, n_cand = p.n_cand;
+#pragma unroll
+    for (int u = 0; u < kOwn; ++u) {
+        const int c = tid + NT * u;
+        if (c < n_cand) Z.cand[c] = make_uint4(~oidx[u], uint32_t(okey[u]), uint32_t(okey[u] >> 32), 0);
+    }
+    __syncthreads();
+    const bool split = n_cand <= NT / 2;
+    if (split) {
+        // thread c and c + NT/2 rank candidate c over the two halves of the list
+        const int c = tid % (NT / 2), half = tid / (NT / 2);
+        const int o0 = half ? n_cand / 2 : 0, o1 = half ? n_cand : n_cand / 2;
+        uint32_t rk = 0;
+        if (c < n_cand) {
+            const uint4 me = Z.cand[c];
+            int o = o0;
+            for (; o + 8 <= o1; o += 8) {
+                uint4 e[8];
+#pragma unroll
+                for (int w = 0; w < 8; ++w) e[w] = Z.cand[o + w];
+#pragma unroll
+                for (int w = 0; w < 8; ++w) count_ahead(rk, e[w], me.x, me.y, me.z);
+            }
+            for (; o < o1; ++o) count_ahead(rk, Z.cand[o], me.x, me.y, me.z);
+        }
+        Z.rk[tid] = rk;
+        __syncthreads();
+        if (tid < n_cand && oidx[0] < 0x80000000u) {
+            const int r = int(Z.rk[tid] + Z.rk[tid + NT / 2]);
+            if (r < k && r < m_b) {
+                Z.sel[r] = int32_t(oidx[0]);
+                if (r == j) {
+                    sm.bcast[4] = int32_t(oidx[0]);
+                    sm.bcast[5] = olen[0];
+                    sm.bcast[6] = int32_t(ooff[0] & 0xFFFFFFFF);
+                    sm.bcast[7] = int32_t(ooff[0] >> 32);
+                }
             }
         }
-        Z.cand[c] = make_uint4(uint32_t(okey[u]), uint32_t(okey[u] >> 32), oidx[u], 0);
-    }
-    if (tid == 0) { sm.bcast[3] = 0; sm.bcast[4] = -1; sm.bcast[5] = 0; sm.bcast[6] = 0; sm.bcast[7] = 0; }
-    __syncthreads();
-    // rank = number of candidates ahead in (key desc, span asc); LDS reads batched by 8
-    int rank[OWN];
-    int n_valid_local = 0;
+    } else {
 #pragma unroll
-    for (int u = 0; u < OWN; ++u) {
-        rank[u] = -1;
-        const int c = tid + NT * u;
-        if (c >= n_cand || oidx[u] >= 0x80000000u) continue;
-        ++n_valid_local;
-        int rk = 0;
-        int o = 0;
-        for (; o + 8 <= n_cand; o += 8) {
-            uint4 e[8];
+        for (int u = 0; u < kOwn; ++u) {
+            const int c = tid + NT * u;
+            if (c >= n_cand || oidx[u] >= 0x80000000u) continue;
+            const uint32_t m0 = ~oidx[u], m1 = uint32_t(okey[u]), m2 = uint32_t(okey[u] >> 32);
+            uint32_t rk = 0;
+            int o = 0;
+            for (; o + 8 <= n_cand; o += 8) {
+                uint4 e[8];
 #pragma unroll
-            for (int w = 0; w < 8; ++w) e[w] = Z.cand[o + w];
+                for (int w = 0; w < 8; ++w) e[w] = Z.cand[o + w];
 #pragma unroll
-            for (int w = 0; w < 8; ++w)
-                rk += better((uint64_t(e[w].y) << 32) | e[w].x, e[w].z, okey[u], oidx[u]) ? 1 : 0;
-        }
-        for (; o < n_cand; ++o) {
-            const uint4 e = Z.cand[o];
-            rk += better((uint64_t(e.y) << 32) | e.x, e.z, okey[u], oidx[u]) ? 1 : 0;
-        }
-        rank[u] = rk;
-        if (rk == j && rk < k && rk < m_b) {        // this item's span
-            sm.bcast[4] = int32_t(oidx[u]);
-            sm.bcast[5] = olen[u];
-            sm.bcast[6] = int32_t(ooff[u] & 0xFFFFFFFF);
-            sm.bcast[7] = int32_t(ooff[u] >> 32);
-        }
-    }
-    const float nvl = wave_sum(float(n_valid_local));
-    if ((tid & 63) == 0) atomicAdd(&sm.bcast[3], int(nvl));
-    __syncthreads();
-    // losing candidates of this item: ranks k + j, 2k + j, ...  (deterministic slots)
-    const int n_valid = sm.bcast[3];
-    const int n_lose_all = max(0, n_valid - k);
-    n_loser = (n_lose_all > j) ? (n_lose_all - j + k - 1) / k : 0;
-#pragma unroll
-    for (int u = 0; u < OWN; ++u) {
-        const int rk = rank[u];
-        if (rk >= k && ((rk - k) % k) == j) {
-            const int slot = (rk - k) / k;
-            if (slot < kZoomLosers) {
-                Z.loser[slot] = int32_t(oidx[u]);
-#pragma unroll
-                for (int hl = 0; hl < G; ++hl) Z.lw[hl][slot] = olg[u][hl] * kLog2e;
+                for (int w = 0; w < 8; ++w) count_ahead(rk, e[w], m0, m1, m2);
+            }
+            for (; o < n_cand; ++o) count_ahead(rk, Z.cand[o], m0, m1, m2);
+            if (int(rk) < k && int(rk) < m_b) {
+                Z.sel[rk] = int32_t(oidx[u]);
+                if (int(rk) == j) {
+                    sm.bcast[4] = int32_t(oidx[u]);
+                    sm.bcast[5] = olen[u];
+                    sm.bcast[6] = int32_t(ooff[u] & 0xFFFFFFFF);
+                    sm.bcast[7] = int32_t(ooff[u] >> 32);
+                }
             }
         }
     }
@@ -1014,115 +1188,88 @@ __device__ __forceinline__ void rank_candidates(const Params &p, Smem<T, D, G> &
 }
 
 // ---------------------------------------------------------------------------
-// zoom item body for one span, RU = 16-byte vectors per factor row U[t][:]
+// zoom of one span through its factors, RU = 16-byte vectors per factor row U[t][:].
+// `mid` runs once the first factor loads are issued: work that needs none of them.
 // ---------------------------------------------------------------------------
-template <class T, int D, int G, int RU>
-__device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, int pair, int S,
-                                          int L, int64_t off, int nl,
-                                          float (&acc)[G][T::kVec], int tid) {
+template <class T, int D, int G, int RU, class Mid>
+__device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, int L, int64_t off,
+                                          float (&pend)[G], int tid, Mid &&mid) {
     using GE = Geo<T, D>;
-    auto &Z = sm.u.zoom;
+    auto &Z = sm.u.share;
     constexpr int VEC = GE::VEC;
     constexpr int RV = GE::RV;
-    constexpr int NVT = (kMaxTopK * RV + NT - 1) / NT;   // Vt vectors per thread at r = 64
-    constexpr int NSV = (G * kMaxTopK + NT - 1) / NT;    // y entries per thread at r = 64
+    constexpr int R = RU * 16 / T::kBytes;               // rank of the factors
+    constexpr int NVT = (R * RV + NT - 1) / NT;          // Vt vectors per thread
+    constexpr int NSV = (G * R + NT - 1) / NT;           // y entries per thread
     constexpr int NB = (8 * NT / RU) < kZoomBlock ? (8 * NT / RU) : kZoomBlock;  // tokens/block
     constexpr int NU = NB * RU / NT;                     // U vectors per thread per block
     constexpr int LG_RU = RU == 1 ? 0 : RU == 2 ? 1 : RU == 4 ? 2 : RU == 8 ? 3 : 4;
-    const int b = pair / p.Hkv, g = pair % p.Hkv;
-    const int r = p.r;
     const int rgrp = tid / GE::RV, col = tid % GE::RV;
     const int ucol = tid % RU;
     const int wave = tid >> 6, lane = tid & 63;
     const unsigned char *UK = p.factors + off;
-    const unsigned char *sK = UK + size_t(L) * r * T::kBytes;
-    const unsigned char *VtK = sK + size_t(r) * T::kBytes;
-    const unsigned char *UV = VtK + size_t(r) * D * T::kBytes;
-    const unsigned char *sV = UV + size_t(L) * r * T::kBytes;
-    const unsigned char *VtV = sV + size_t(r) * T::kBytes;
-    const bool zoom = S >= 0;
+    const unsigned char *sK = UK + size_t(L) * R * T::kBytes;
+    const unsigned char *VtK = sK + size_t(R) * T::kBytes;
+    const unsigned char *UV = VtK + size_t(R) * D * T::kBytes;
+    const unsigned char *sV = UV + size_t(L) * R * T::kBytes;
+    const unsigned char *VtV = sV + size_t(R) * T::kBytes;
     const int nb0 = min(NB, L);
 
-    // issue in the order of use: sigmas, Vt_K, losers' value rows, U_K, then U_V.
-    // Addresses are clamped into the block, validity is applied where values are used.
+    // issue in the order of use: sigmas, Vt_K, U_K, then (after `mid`) U_V.  Addresses
+    // are clamped into the block, validity is applied where values are used.
     float sk_reg[NVT], sv_reg[NSV];
     uint4 vk[NVT], vvt[NVT], uk[NU], uv[NU];
-    constexpr int NJL = (kZoomLosers + GE::RPP - 1) / GE::RPP;
-    uint4 lv[NJL];
-    if (zoom) {
 #pragma unroll
-        for (int u = 0; u < NVT; ++u) {
-            const int vi = min(tid + NT * u, r * RV - 1);
-            sk_reg[u] = T::load1(sK, vi / RV);
-        }
-#pragma unroll
-        for (int u = 0; u < NSV; ++u) sv_reg[u] = T::load1(sV, (tid + NT * u) % r);
-#pragma unroll
-        for (int u = 0; u < NVT; ++u) {
-            const int vi = min(tid + NT * u, r * RV - 1);
-            vk[u] = ld16(VtK + size_t(vi / RV) * GE::RB + (vi % RV) * 16);
-        }
+    for (int u = 0; u < NVT; ++u) {
+        const int vi = min(tid + NT * u, R * RV - 1);
+        sk_reg[u] = T::load1(sK, vi / RV);
     }
-    if (nl > 0) {
-        const unsigned char *sv = reinterpret_cast<const unsigned char *>(p.sum_v) +
-                                  (size_t(b) * p.Hkv + g) * size_t(p.M_max) * GE::RB;
 #pragma unroll
-        for (int jj = 0; jj < NJL; ++jj) {
-            const int row = min(rgrp + GE::RPP * jj, nl - 1);
-            lv[jj] = ld16(sv + size_t(Z.loser[row]) * GE::RB + col * 16);
-        }
-        if (tid < G)
-            for (int i = nl; i < kZoomLosers; ++i) Z.lw[tid][i] = -INFINITY;
+    for (int u = 0; u < NSV; ++u) sv_reg[u] = T::load1(sV, (tid + NT * u) % R);
+#pragma unroll
+    for (int u = 0; u < NVT; ++u) {
+        const int vi = min(tid + NT * u, R * RV - 1);
+        vk[u] = ld16(VtK + size_t(vi / RV) * GE::RB + (vi % RV) * 16);
     }
-    if (zoom) {
 #pragma unroll
-        for (int u = 0; u < NU; ++u) {
-            const int tok = min((tid + NT * u) / RU, nb0 - 1);
-            uk[u] = ld16(UK + size_t(tok) * r * T::kBytes + ucol * 16);
-        }
+    for (int u = 0; u < NU; ++u) {
+        const int tok = min((tid + NT * u) / RU, nb0 - 1);
+        uk[u] = ld16(UK + size_t(tok) * R * T::kBytes + ucol * 16);
+    }
+    mid();
 #pragma unroll
-        for (int u = 0; u < NU; ++u) {
-            const int tok = min((tid + NT * u) / RU, nb0 - 1);
-            uv[u] = ld16(UV + size_t(tok) * r * T::kBytes + ucol * 16);
-        }
+    for (int u = 0; u < NU; ++u) {
+        const int tok = min((tid + NT * u) / RU, nb0 - 1);
+        uv[u] = ld16(UV + size_t(tok) * R * T::kBytes + ucol * 16);
     }
     __syncthreads();
 
-    if (zoom) {
-        // w[h][i] = scale*log2e * sigma_K[i] * (Vt_K[i] . q_h)
+    // w[h][i] = scale*log2e * sigma_K[i] * (Vt_K[i] . q_h)
 #pragma unroll
-        for (int u = 0; u < NVT; ++u) {
-            const int vi = tid + NT * u;
-            const int row = vi / RV, c = vi % RV;
-            float part[G];
-            float f[VEC];
-            T::unpack(vk[u], f);
+    for (int u = 0; u < NVT; ++u) {
+        const int vi = tid + NT * u;
+        const int row = vi / RV, c = vi % RV;
+        float part[G];
+        float f[VEC];
+        T::unpack(vk[u], f);
 #pragma unroll
-            for (int hl = 0; hl < G; ++hl) {
-                part[hl] = 0.0f;
+        for (int hl = 0; hl < G; ++hl) {
+            part[hl] = 0.0f;
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) part[hl] += Z.qf[hl][c * VEC + e] * f[e];
-                part[hl] = row_sum<RV>(part[hl]);
-            }
-            if (vi < r * RV && c == 0)
-#pragma unroll
-                for (int hl = 0; hl < G; ++hl) Z.w[hl][row] = part[hl] * sk_reg[u] * p.scale_log2;
+            for (int e = 0; e < VEC; ++e) part[hl] += Z.qf[hl][c * VEC + e] * f[e];
+            part[hl] = row_sum<RV>(part[hl]);
         }
-        // Vt_V rows take the registers Vt_K has released
+        if (vi < R * RV && c == 0)
 #pragma unroll
-        for (int u = 0; u < NVT; ++u) {
-            const int vi = min(tid + NT * u, r * RV - 1);
-            vvt[u] = ld16(VtV + size_t(vi / RV) * GE::RB + (vi % RV) * 16);
-        }
+            for (int hl = 0; hl < G; ++hl) Z.w[hl][row] = part[hl] * sk_reg[u] * p.scale_log2;
+    }
+    // Vt_V rows take the registers Vt_K has released
+#pragma unroll
+    for (int u = 0; u < NVT; ++u) {
+        const int vi = min(tid + NT * u, R * RV - 1);
+        vvt[u] = ld16(VtV + size_t(vi / RV) * GE::RB + (vi % RV) * 16);
     }
 
-    // this item's losing candidates: coarse entries (v_bar rows, routing scores)
-    if (nl > 0) {
-        online_fold(&Z.lw[0][0], kZoomLosers, nl, G, sm.m_run, sm.l_run, sm.scale_old, tid);
-        __syncthreads();
-        acc_rows<T, D, G, NJL>(acc, lv, &Z.lw[0][0], kZoomLosers, nl, rgrp);
-    }
-    if (!zoom) return;
     __syncthreads();
 
     // token blocks: scores via U_K, online softmax, y = p^T U_V accumulated per lane
@@ -1137,12 +1284,12 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
 #pragma unroll
             for (int u = 0; u < NU; ++u) {
                 const int tok = min((tid + NT * u) / RU, nb - 1);
-                uk[u] = ld16(UK + size_t(t0 + tok) * r * T::kBytes + ucol * 16);
+                uk[u] = ld16(UK + size_t(t0 + tok) * R * T::kBytes + ucol * 16);
             }
 #pragma unroll
             for (int u = 0; u < NU; ++u) {
                 const int tok = min((tid + NT * u) / RU, nb - 1);
-                uv[u] = ld16(UV + size_t(t0 + tok) * r * T::kBytes + ucol * 16);
+                uv[u] = ld16(UV + size_t(t0 + tok) * R * T::kBytes + ucol * 16);
             }
         }
 #pragma unroll
@@ -1169,11 +1316,9 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
         for (int hl = 0; hl < G; ++hl) {
             const float so = sm.scale_old[hl];
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) {
-                yacc[hl][e] *= so;
-                acc[hl][e] *= so;
-            }
+            for (int e = 0; e < VEC; ++e) yacc[hl][e] *= so;
         }
+        pend_fold<G>(pend, sm.scale_old);
 #pragma unroll
         for (int u = 0; u < NU; ++u) {
             const int tok = (tid + NT * u) / RU;
@@ -1204,8 +1349,8 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
 #pragma unroll
     for (int u = 0; u < NSV; ++u) {
         const int t = tid + NT * u;
-        if (t < G * r) {
-            const int hl = t / r, i = t % r;
+        if (t < G * R) {
+            const int hl = t / R, i = t % R;
             Z.y[hl][i] = (Z.yr[0][hl][i] + Z.yr[1][hl][i] + Z.yr[2][hl][i] + Z.yr[3][hl][i]) *
                          sv_reg[u];
         }
@@ -1213,10 +1358,12 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
     __syncthreads();
     // o[h][:] += sum_i y~[h][i] Vt_V[i][:]; Vt_V rows of column c sit RV lanes apart,
     // exactly like summary rows
+    float acc[G][VEC];
+    acc_zero<T, D, G>(acc);
 #pragma unroll
     for (int u = 0; u < NVT; ++u) {
         const int vi = tid + NT * u;
-        if (vi < r * RV) {
+        if (vi < R * RV) {
             const int row = vi / RV;
             float f[VEC];
             T::unpack(vvt[u], f);
@@ -1228,71 +1375,137 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
             }
         }
     }
+    acc_flush<T, D, G>(sm, acc, pend, tid);
 }
 
 // ---------------------------------------------------------------------------
-// zoom item: one selection slot of a pair, attended through the span's factors
+// share item: anchors share, selection slot j, summaries share of one pair
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
-__device__ __forceinline__ void zoom_item(const Params &p, Smem<T, D, G> &sm, int pair, int j, int tid) {
+__device__ __forceinline__ void share_item(const Params &p, Smem<T, D, G> &sm, int pair, int j,
+                                           uint32_t tag, int tid) {
     using GE = Geo<T, D>;
-    auto &Z = sm.u.zoom;
+    using SM = Smem<T, D, G>;
+    constexpr int NJ = SM::NJ, AB = SM::AB, CB = SM::CB;
+    auto &Z = sm.u.share;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
-    const int r = p.r;
+    const int k = p.k, r = p.r, nz = p.n_zi;
+    // this item's shares: contiguous ranges of the anchor and span index spaces up to
+    // the maxima, so the first loads need no table value; the sequence's own counts
+    // (n_anchors, n_spans) mask rows where the values are used
+    const int as = (p.A_max + nz - 1) / nz;
+    const int a_lo = min(p.A_max, j * as), a_hi = min(p.A_max, a_lo + as);
+    const int cs = (p.M_max + nz - 1) / nz;
+    const int c_lo = min(p.M_max, j * cs), c_hi = min(p.M_max, c_lo + cs);
+    const int rgrp = tid / GE::RV, col = tid % GE::RV;
+    const size_t pr = size_t(b) * p.Hkv + g;
+    const unsigned char *ak = reinterpret_cast<const unsigned char *>(p.anchor_k) + pr * p.A_max * GE::RB;
+    const unsigned char *av = reinterpret_cast<const unsigned char *>(p.anchor_v) + pr * p.A_max * GE::RB;
+    const unsigned char *sv = reinterpret_cast<const unsigned char *>(p.sum_v) + pr * p.M_max * GE::RB;
+
+    // 1. loads that depend on nothing: the first anchor block, the first summary block
+    //    (values only; its logits come from routing), the query
+    uint4 kr[NJ], vr[NJ], cv[NJ];
+    load_rows<T, D, NJ>(kr, ak + size_t(a_lo) * GE::RB, min(AB, a_hi - a_lo), rgrp, col);
+    load_rows<T, D, NJ>(vr, av + size_t(a_lo) * GE::RB, min(AB, a_hi - a_lo), rgrp, col);
+    load_rows<T, D, NJ>(cv, sv + size_t(c_lo) * GE::RB, min(CB, c_hi - c_lo), rgrp, col);
     int m_b = p.n_spans[b];
     m_b = m_b < 0 ? 0 : (m_b > p.M_max ? p.M_max : m_b);
-    const bool per_item_select = (p.mode == kModeFused) && !p.merger;
-    const int rgrp = tid / GE::RV, col = tid % GE::RV;
-    // the query does not depend on the selection: stage it first
+    int An = p.n_anchors[b];
+    An = An < 0 ? 0 : (An > p.A_max ? p.A_max : An);
     for (int i = tid; i < G * D; i += NT) {
         const int hl = i / D, d = i % D;
         Z.qf[hl][d] = T::load1(p.q, (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d);
     }
     online_reset(G, sm.m_run, sm.l_run, sm.scale_old, tid);
-    // wait for the pair's routing (fused mode)
-    if (tid == 0) {
-        bool ok = true;
-        if (p.mode == kModeFused) {
-            uint32_t n = 0;
-            const uint32_t *flag = per_item_select ? &p.route_cnt[pair] : &p.sel_ready[pair];
-            const uint32_t target = per_item_select ? uint32_t(p.n_rc) : 1u;
-            while (ld_shared(flag) < target) {
-                __builtin_amdgcn_s_sleep(1);
-                if (++n > kSpinLimit) { flag_error(p, kErrSpinTimeout); ok = false; break; }
-            }
-        }
-        sm.bcast[2] = ok;
-    }
+    for (int t = tid; t < kMaxTopK; t += NT) Z.sel[t] = -1;
+    for (int i = tid; i < 4 * G * D; i += NT) (&sm.red[0][0][0])[i] = 0.0f;
+    if (tid == 0) { sm.bcast[4] = -1; sm.bcast[5] = 0; sm.bcast[6] = 0; sm.bcast[7] = 0; }
     __syncthreads();
-    int n_loser = 0;
-    int S = -1;
-    if (sm.bcast[2] && per_item_select) {
-        // ranks the pair's candidates; the owner of rank j leaves {span, |S|, offset} in bcast
-        rank_candidates<T, D, G>(p, sm, pair, j, m_b, tid, n_loser);
+    // valid rows of the prefetched blocks
+    const int nc0 = max(0, min(min(CB, c_hi - c_lo), m_b - c_lo));
+    // the weighted value sums live in sm.red (one row per wave); pend holds the rescale
+    // factors not yet applied to them
+    float pend[G];
+#pragma unroll
+    for (int hl = 0; hl < G; ++hl) pend[hl] = 1.0f;
+
+    // 2. the anchor share, while routing runs elsewhere
+    for (int a0 = a_lo; a0 < a_hi && a0 < An; a0 += AB) {
+        const int na = min(min(AB, a_hi - a0), An - a0);
+        if (a0 != a_lo) {
+            load_rows<T, D, NJ>(kr, ak + size_t(a0) * GE::RB, na, rgrp, col);
+            load_rows<T, D, NJ>(vr, av + size_t(a0) * GE::RB, na, rgrp, col);
+        }
+        anchor_block<T, D, G, NJ>(p, sm, kr, vr, na, pend, rgrp, col, tid);
     }
-    if (tid == 0) {
-        int L = 0;
-        int64_t off = 0;
-        if (!sm.bcast[2]) {
-            S = -1;
-        } else if (per_item_select) {
-            S = sm.bcast[4];
-            L = sm.bcast[5];
-            off = int64_t(uint32_t(sm.bcast[6])) | (int64_t(sm.bcast[7]) << 32);
-            if (p.sel_out) p.sel_out[size_t(pair) * p.k + j] = S;
-        } else {
-            if (p.mode == kModeFused) {
-                S = ld_shared(reinterpret_cast<const int32_t *>(&p.zrec[size_t(pair) * p.k + j]));
-            } else {
-                S = p.sel_in[size_t(pair) * p.k + j];
+
+    // 3. the selection (Z.sel, this slot's span in bcast) and the first block's logits
+    const bool per_item = (p.mode == kModeFused) && !p.merger;
+    if (per_item) {
+        uint64_t okey[kOwn];
+        uint32_t oidx[kOwn];
+        int32_t olen[kOwn];
+        int64_t ooff[kOwn];
+        bool done = false;
+        for (uint32_t it = 0;; ++it) {
+            bool ok = load_candidates(p, pair, tag, okey, oidx, olen, ooff, tid);
+            ok &= coarse_logits<T, D, G>(p, sm, pair, c_lo, nc0, tag, tid);
+            if (__syncthreads_and(ok)) { done = true; break; }
+            if (it >= kSpinLimit) {
+                if (tid == 0) flag_error(p, kErrSpinTimeout);
+                break;
             }
-            if (S >= m_b) { flag_error(p, kErrSelRange); S = -1; }
-            if (S >= 0) {
-                L = p.span_len[size_t(b) * p.M_max + S];
-                off = p.block_off[(size_t(b) * p.Hkv + g) * p.M_max + S];
+            __builtin_amdgcn_s_sleep(2);
+        }
+        if (done) rank_candidates<T, D, G>(p, sm, j, m_b, okey, oidx, olen, ooff, tid);
+        if (tid == 0 && j < k && p.sel_out) p.sel_out[size_t(pair) * k + j] = sm.bcast[4];
+    } else {
+        if (p.mode == kModeFused) {
+            // single merger: wait for the pair's selection records
+            if (tid == 0) {
+                bool ok = true;
+                uint32_t n = 0;
+                while (ld_shared(&p.sel_ready[pair]) == 0u) {
+                    __builtin_amdgcn_s_sleep(2);
+                    if (++n > kSpinLimit) { flag_error(p, kErrSpinTimeout); ok = false; break; }
+                }
+                sm.bcast[2] = ok;
+            }
+            __syncthreads();
+            if (sm.bcast[2] && tid < k) {
+                const int32_t *zr = reinterpret_cast<const int32_t *>(&p.zrec[size_t(pair) * k + tid]);
+                const int s = ld_shared(zr);
+                Z.sel[tid] = s;
+                if (tid == j) {
+                    sm.bcast[4] = s;
+                    sm.bcast[5] = ld_shared(zr + 1);
+                    sm.bcast[6] = ld_shared(zr + 2);
+                    sm.bcast[7] = ld_shared(zr + 3);
+                }
+            }
+        } else if (tid < k) {
+            // the caller's selection
+            int s = p.sel_in[size_t(pair) * k + tid];
+            if (s >= m_b) { flag_error(p, kErrSelRange); s = -1; }
+            Z.sel[tid] = s;
+            if (tid == j && s >= 0) {
+                const int64_t off = p.block_off[pr * p.M_max + s];
+                sm.bcast[4] = s;
+                sm.bcast[5] = p.span_len[size_t(b) * p.M_max + s];
+                sm.bcast[6] = int32_t(off & 0xFFFFFFFF);
+                sm.bcast[7] = int32_t(off >> 32);
             }
         }
+        if (nc0 > 0) wait_coarse_logits<T, D, G>(p, sm, pair, c_lo, nc0, tag, tid);
+        else __syncthreads();
+    }
+    // the zoomed span's block must lie inside the factor arena
+    if (tid == 0) {
+        int S = sm.bcast[4];
         if (S >= 0) {
+            const int L = sm.bcast[5];
+            const int64_t off = int64_t(uint32_t(sm.bcast[6])) | (int64_t(sm.bcast[7]) << 32);
             const int64_t bytes = (2 * int64_t(L) * r + 2 * r + 2 * int64_t(r) * D) * T::kBytes;
             if (L < 1 || off < 0 || (off & 15) || off + bytes > p.factors_bytes) {
                 flag_error(p, kErrBlockRange);
@@ -1300,32 +1513,49 @@ __device__ __forceinline__ void zoom_item(const Params &p, Smem<T, D, G> &sm, in
             }
         }
         sm.bcast[4] = S;
-        sm.bcast[5] = L;
-        sm.bcast[6] = int32_t(off & 0xFFFFFFFF);
-        sm.bcast[7] = int32_t(off >> 32);
     }
     __syncthreads();
-    S = sm.bcast[4];
+    const int S = sm.bcast[4];
     const int L = sm.bcast[5];
     const int64_t off = int64_t(uint32_t(sm.bcast[6])) | (int64_t(sm.bcast[7]) << 32);
-    const int slot = p.slot_zoom0 + j;
-    float acc[G][GE::VEC];
-    acc_zero<T, D, G>(acc);
-    const int nl = min(n_loser, kZoomLosers);
-    if (S >= 0 || nl > 0) {
-        switch (r * T::kBytes / 16) {                   // 16-byte vectors per U row
-            case 1: zoom_span<T, D, G, 1>(p, sm, pair, S, L, off, nl, acc, tid); break;
-            case 2: zoom_span<T, D, G, 2>(p, sm, pair, S, L, off, nl, acc, tid); break;
-            case 4: zoom_span<T, D, G, 4>(p, sm, pair, S, L, off, nl, acc, tid); break;
-            case 8: zoom_span<T, D, G, 8>(p, sm, pair, S, L, off, nl, acc, tid); break;
-            default: zoom_span<T, D, G, 16>(p, sm, pair, S, L, off, nl, acc, tid); break;
+
+    // 4. zoom the slot's span; its factor loads are in flight while the first summary
+    //    block is folded
+    auto coarse0 = [&]() {
+        if (nc0 > 0) coarse_block<T, D, G, NJ>(sm, cv, c_lo, nc0, k, pend, rgrp, tid);
+    };
+    if (S >= 0) {
+        // 16-byte vectors per U row: rank 8..64 gives 1..8 (bf16) or 2..16 (f32)
+        const int ru = r * T::kBytes / 16;
+        if constexpr (T::kBytes == 2) {
+            switch (ru) {
+                case 1: zoom_span<T, D, G, 1>(p, sm, L, off, pend, tid, coarse0); break;
+                case 2: zoom_span<T, D, G, 2>(p, sm, L, off, pend, tid, coarse0); break;
+                case 4: zoom_span<T, D, G, 4>(p, sm, L, off, pend, tid, coarse0); break;
+                default: zoom_span<T, D, G, 8>(p, sm, L, off, pend, tid, coarse0); break;
+            }
+        } else {
+            switch (ru) {
+                case 2: zoom_span<T, D, G, 2>(p, sm, L, off, pend, tid, coarse0); break;
+                case 4: zoom_span<T, D, G, 4>(p, sm, L, off, pend, tid, coarse0); break;
+                case 8: zoom_span<T, D, G, 8>(p, sm, L, off, pend, tid, coarse0); break;
+                default: zoom_span<T, D, G, 16>(p, sm, L, off, pend, tid, coarse0); break;
+            }
         }
+    } else {
+        coarse0();
     }
-    rows_to_red<T, D, G>(sm, acc, tid);
+    // 5. the rest of the summary share (several blocks only when k is small)
+    for (int c0 = c_lo + CB; c0 < c_hi && c0 < m_b; c0 += CB) {
+        const int nc = min(min(CB, c_hi - c0), m_b - c0);
+        load_rows<T, D, NJ>(cv, sv + size_t(c0) * GE::RB, nc, rgrp, col);
+        wait_coarse_logits<T, D, G>(p, sm, pair, c0, nc, tag, tid);
+        coarse_block<T, D, G, NJ>(sm, cv, c0, nc, k, pend, rgrp, tid);
+    }
     __syncthreads();
-    write_partial<T, D, G>(p, sm, pair, slot, tid);
+    write_partial<T, D, G>(p, sm, pair, j, tid);
     stores_done_barrier();
-    count_partials<T, D, G>(p, sm, pair, 1u, tid);
+    count_partial<T, D, G>(p, sm, pair, tid);
 }
 
 // ---------------------------------------------------------------------------
@@ -1335,24 +1565,24 @@ template <class T, int D, int G>
 __global__ void __launch_bounds__(NT, 2) sekv_step_kernel(Params p) {
     __shared__ Smem<T, D, G> sm;
     const int tid = threadIdx.x;
-    const int n_items = p.end_zoom;
+    // the tag of this launch's published words, used as loaded: its first use is when
+    // an item publishes or polls, so the load overlaps the first item's own loads
+    const uint32_t tag = ld_shared(&p.hdr->epoch);
+    const int n_items = p.end_share;
     for (int item = blockIdx.x; item < n_items; item += p.grid) {
         // an opaque copy of the thread index keeps per-thread address arithmetic inside
         // each item instead of alive across the whole loop (register pressure)
         int t;
         asm volatile("v_mov_b32 %0, %1" : "=v"(t) : "v"(tid));
         if (item < p.end_route) {
-            route_item<T, D, G>(p, sm, item / p.n_rc, item % p.n_rc, t);
-        } else if (item < p.end_anchor) {
-            const int i = item - p.end_route;
-            anchor_item<T, D, G>(p, sm, i / p.n_ac, i % p.n_ac, t);
+            route_item<T, D, G>(p, sm, item / p.n_rc, item % p.n_rc, tag, t);
         } else {
-            const int i = item - p.end_anchor;
-            zoom_item<T, D, G>(p, sm, i / p.k, i % p.k, t);
+            const int i = item - p.end_route;
+            share_item<T, D, G>(p, sm, i / p.n_zi, i % p.n_zi, tag, t);
         }
         __syncthreads();
     }
-    // shutdown: the last workgroup out zeroes the counters for the next launch
+    // shutdown: the last workgroup out zeroes the counters and advances the epoch
     if (tid == 0) {
         const uint32_t prev = counter_add(&p.hdr->exit_count, 1u);
         sm.bcast[3] = (prev == uint32_t(p.grid - 1));
@@ -1368,14 +1598,17 @@ __global__ void __launch_bounds__(NT, 2) sekv_step_kernel(Params p) {
         if (tid == 0) {
             p.hdr->ticket = 0u;
             p.hdr->exit_count = 0u;
+            st_shared(&p.hdr->epoch, tag + 1u == 0u ? 1u : tag + 1u);   // 0 marks unwritten words
         }
     }
 }
 
+// Workspace initialisation: everything zero except the header's epoch, which starts at
+// 1 (the first {ticket, exit_count, error, epoch} vector).
 __global__ void zero_kernel(uint4 *p, size_t n16) {
     for (size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n16;
          i += size_t(gridDim.x) * blockDim.x)
-        p[i] = make_uint4(0, 0, 0, 0);
+        p[i] = make_uint4(0, 0, 0, i == 0 ? 1u : 0u);
 }
 
 template <class T, int D, int G>
