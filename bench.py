@@ -69,6 +69,12 @@ def parse():
                     help="approximate CPU time spent timing the oracle")
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (counter calibration)")
+    ap.add_argument("--workload", choices=["layer128k", "layers32"], default="layer128k",
+                    help="layer128k: one 128K x 4 layer (the headline); layers32: the 32-layer, "
+                         "batch-32, 32K-context step replayed as one HIP graph")
+    ap.add_argument("--distinct-layers", type=int, default=4,
+                    help="layers32: independently seeded layers generated on the host; the "
+                         "32 device-resident layers cycle through them, each in its own memory")
     return ap.parse_args()
 
 
@@ -88,6 +94,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
+    if args.workload == "layers32":
+        return bench_layers32(args, dev)
     spec = CONFIGS[3]
     log(f"[bench] generating the 128K x 4 cache (variant {args.variant})")
     t0 = time.time()
@@ -203,7 +211,101 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def cpu_baseline(case, bytes_step, seconds):
+def bench_layers32(args, dev):
+    """32 layers x (batch 32, 32K context, rank 16, top-8), one HIP graph per step."""
+    import numpy as np
+    import torch
+
+    from paper_2606_31145_amd import accounting
+    from paper_2606_31145_amd import sekv
+    from synth import CONFIGS, make_case
+
+    spec = CONFIGS[4]
+    L = spec.n_layers
+    D = max(1, min(args.distinct_layers, L))
+    t0 = time.time()
+    cases = []
+    for l in range(D):
+        cases.append(make_case(spec, layer=l, variant=args.variant))
+        log(f"[bench] layer {l} generated ({time.time() - t0:.1f}s)")
+    base = [sekv.DeviceCache.from_arrays(dict(
+        q=c.q, anchor_k=c.anchor_k, anchor_v=c.anchor_v, n_anchors=c.n_anchors, sum_k=c.sum_k,
+        sum_v=c.sum_v, n_spans=c.n_spans, span_len=c.span_len, span_logsize=c.span_logsize,
+        factors=c.factors, block_off=c.block_off), spec.dtype, dev) for c in cases]
+    caches = []
+    for l in range(L):
+        src = base[l % D]
+        caches.append(src if l < D else
+                      sekv.DeviceCache({k: v.clone() for k, v in src.t.items()}, spec.dtype))
+    torch.cuda.synchronize()
+    c0 = cases[0]
+    dims = sekv.make_dims(batch=spec.batch, n_q_heads=spec.n_q_heads, n_kv_heads=spec.n_kv_heads,
+                          head_dim=spec.head_dim, rank=spec.rank, top_k=spec.top_k,
+                          max_anchors=c0.max_anchors, max_spans=c0.max_spans,
+                          max_span_len=max(c.max_span_len for c in cases), dtype=spec.dtype,
+                          softmax_scale=spec.softmax_scale)
+    ws = sekv.Workspace(dims, dev)
+    graph = sekv.LayerGraph(dims, caches, ws)
+    stream = torch.cuda.current_stream()
+    log(f"[bench] 32-layer graph built; warmup {args.warmup}")
+    for _ in range(args.warmup):
+        graph.launch(stream)
+    torch.cuda.synchronize()
+    assert ws.status() == 0, "device error word set during warmup"
+    sel_np = graph.sel.cpu().numpy()
+    per_layer = [accounting.step_bytes(n_q_heads=spec.n_q_heads, n_kv_heads=spec.n_kv_heads,
+                                       head_dim=spec.head_dim, rank=spec.rank, elem=2,
+                                       out_elem=2, n_anchors=cases[l % D].n_anchors,
+                                       n_spans=cases[l % D].n_spans,
+                                       span_len=cases[l % D].span_len, sel=sel_np[l])
+                 for l in range(L)]
+    bytes_step = int(sum(a["total"] for a in per_layer))
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        ev[i][0].record(stream)
+        graph.launch(stream)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    assert ws.status() == 0, "device error word set during the timed steps"
+    step_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    step_us = float(step_ms.mean() * 1e3)
+    achieved = bytes_step / (step_us * 1e-6) / 1e9
+    graph.destroy()
+    workload = f"sekv-decode-step-32layer-32k-b32-r16-k8-bf16-{args.variant}"
+    line = {
+        "metric": "decode-step latency (µs) and achieved HBM GB/s, 32 layers, 32K context, batch 32",
+        "value": round(bytes_step * K / wall / 1e9, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": K, "warmup": args.warmup, "ms_per_step": round(wall / K * 1e3, 5),
+        "us_per_step": round(wall / K * 1e6, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": workload, "layers": L, "distinct_layer_seeds": D,
+                   "batch": spec.batch, "context": spec.context, "n_q_heads": spec.n_q_heads,
+                   "n_kv_heads": spec.n_kv_heads, "head_dim": spec.head_dim, "rank": spec.rank,
+                   "top_k": spec.top_k, "storage_dtype": "bf16", "routing_dtype": "f64",
+                   "variant": args.variant, "graph": "hipGraph, one kernel node per layer",
+                   "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": KERNEL_NAME, "graph_us_mean": round(step_us, 3),
+                     "graph_us_p50": round(float(np.median(step_ms) * 1e3), 3),
+                     "graph_us_p90": round(float(np.percentile(step_ms, 90) * 1e3), 3),
+                     "algorithmic_bytes_per_step": bytes_step},
+        "cpu_baseline": None,
+        "bytes_per_layer_mean": {k: float(np.mean([a[k] for a in per_layer])) for k in per_layer[0]},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cases[0], per_layer[0]["total"], args.cpu_seconds,
+                                            what="full decode steps of one layer of the 32-layer "
+                                                 "workload (batch 32, 32K)")
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(case, bytes_step, seconds, what="full decode steps of the same 128K x 4 layer"):
     """The oracle, as it stands, timed on the host on the same workload."""
     import numpy as np
 
@@ -236,8 +338,7 @@ def cpu_baseline(case, bytes_step, seconds):
     log(f"[bench] oracle: {len(times)} steps, median {per:.3f}s")
     return {"value": round(bytes_step / per / 1e9, 4), "unit": "GB/s", "cores": 1,
             "kind": "oracle", "us_per_step": round(per * 1e6, 1),
-            "sample": f"{len(times)} full decode steps of the same 128K x 4 layer, median, "
-                      f"numpy float64, BLAS limited to 1 thread"}
+            "sample": f"{len(times)} {what}, median, numpy float64, BLAS limited to 1 thread"}
 
 
 if __name__ == "__main__":

@@ -152,6 +152,35 @@ SEKV_API sekv_status sekv_zoom_attend(const sekv_dims *dims, const sekv_cache *c
 SEKV_API sekv_status sekv_decode_step(const sekv_dims *dims, const sekv_cache *cache, int32_t *sel,
                              void *out, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* ----------------------------------------------------------------------------------
+ * Several layers in one HIP graph.  A decode step of an L-layer model runs the step
+ * above once per layer (each attention layer keeps its own span cache, Sec. 3.2; the
+ * per-layer cost analysis of App. D sums over layers).  sekv_graph_create validates
+ * every layer and captures one sekv_decode_step per layer, in layer order, into an
+ * executable HIP graph; sekv_graph_launch replays it on any stream.
+ *   layers  host array [n_layers] of sekv_cache (device pointers as above); every
+ *           layer has the shapes of `dims`
+ *   sel     device int32 [n_layers][B][Hkv][top_k], may be NULL when top_k == 0
+ *   out     device [n_layers][B][Hq][d] in out_dtype
+ *   ws      one workspace for all layers (the launches run one after another)
+ * The graph keeps the pointers it was created with: the caller keeps every buffer
+ * alive and in place until sekv_graph_destroy.  Launches of one graph, or of graphs
+ * and calls sharing its workspace, must be ordered (one stream); concurrent replays
+ * race on the workspace.  The handle is host memory owned by the library; the graph
+ * itself records only kernel launches.
+ * -------------------------------------------------------------------------------- */
+typedef struct sekv_graph sekv_graph;
+
+SEKV_API sekv_status sekv_graph_create(const sekv_dims *dims, const sekv_cache *layers,
+                                       int32_t n_layers, int32_t *sel, void *out, void *ws,
+                                       size_t ws_bytes, sekv_graph **graph);
+
+/* Enqueue one replay of the graph (all layers) on `stream`. */
+SEKV_API sekv_status sekv_graph_launch(sekv_graph *graph, hipStream_t stream);
+
+/* Free the graph and its handle (NULL is a no-op).  No replay may be pending. */
+SEKV_API sekv_status sekv_graph_destroy(sekv_graph *graph);
+
 #ifdef __cplusplus
 }
 #endif

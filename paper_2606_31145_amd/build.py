@@ -34,7 +34,8 @@ def build(verbose: bool = False) -> str:
     a_obj = os.path.join(bdir, "sekv_api.o")
     _run([HIPCC, *COMMON, f"--offload-arch={ARCH}", *DEVICE_FLAGS, "-c",
           os.path.join(CSRC, "sekv_kernels.hip"), "-o", k_obj], verbose)
-    _run([HIPCC, *COMMON, "-c", os.path.join(CSRC, "sekv_api.cpp"), "-o", a_obj], verbose)
+    _run([HIPCC, *COMMON, f"--offload-arch={ARCH}", "-c", os.path.join(CSRC, "sekv_api.cpp"), "-o", a_obj],
+         verbose)
     tmp = LIB_PATH + ".tmp"
     _run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", k_obj, a_obj, "-o", tmp], verbose)
     os.replace(tmp, LIB_PATH)

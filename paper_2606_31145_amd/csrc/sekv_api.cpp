@@ -9,6 +9,8 @@
 #include <cstdio>
 #include <cstring>
 #include <mutex>
+#include <new>
+#include <vector>
 
 #include "sekv.h"
 #include "sekv_internal.h"
@@ -125,9 +127,12 @@ int resident(int dtype, int head_dim, int group) {
     return n;
 }
 
-sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_out,
-                float *logits_out, const int32_t *sel_in, const float *logits_in, void *out,
-                void *ws, size_t ws_bytes, hipStream_t stream) {
+// Validate one call and fill its launch parameters.  *launch is false when there is
+// nothing to run (empty batch, or no work items).
+sekv_status prepare(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_out,
+                    float *logits_out, const int32_t *sel_in, const float *logits_in, void *out,
+                    void *ws, size_t ws_bytes, sekv::Params *pp, bool *launch) {
+    *launch = false;
     sekv_status st = check_dims_impl(d);
     if (st != SEKV_OK) return st;
     st = check_cache(d, c, mode != sekv::kModeRoute);
@@ -189,8 +194,21 @@ sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_
     p.merger = (mode == sekv::kModeRoute) || (mode == sekv::kModeFused && !per_item);
     const int cap = resident(d->dtype, d->head_dim, s.G);
     p.grid = std::max(1, std::min(p.end_share, cap));
-    if (p.end_share == 0) return SEKV_OK;
-    const hipError_t e = sekv::launch_step(p, d->dtype, d->head_dim, s.G, stream);
+    *pp = p;
+    *launch = p.end_share > 0;
+    return SEKV_OK;
+}
+
+sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_out,
+                float *logits_out, const int32_t *sel_in, const float *logits_in, void *out,
+                void *ws, size_t ws_bytes, hipStream_t stream) {
+    sekv::Params p{};
+    bool launch = false;
+    const sekv_status st = prepare(mode, d, c, sel_out, logits_out, sel_in, logits_in, out, ws,
+                                   ws_bytes, &p, &launch);
+    if (st != SEKV_OK || !launch) return st;
+    const hipError_t e = sekv::launch_step(p, d->dtype, d->head_dim, d->n_q_heads / d->n_kv_heads,
+                                           stream);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     return SEKV_OK;
 }
@@ -269,6 +287,94 @@ sekv_status sekv_decode_step(const sekv_dims *dims, const sekv_cache *cache, int
                              void *out, void *ws, size_t ws_bytes, hipStream_t stream) {
     return run(sekv::kModeFused, dims, cache, sel, nullptr, nullptr, nullptr, out, ws, ws_bytes,
                stream);
+}
+
+struct sekv_graph {
+    hipGraph_t graph;
+    hipGraphExec_t exec;
+    int32_t n_layers;
+};
+
+sekv_status sekv_graph_create(const sekv_dims *dims, const sekv_cache *layers, int32_t n_layers,
+                              int32_t *sel, void *out, void *ws, size_t ws_bytes,
+                              sekv_graph **graph) {
+    if (!graph) return fail(SEKV_ERR_INVALID_ARG, "graph is NULL");
+    *graph = nullptr;
+    if (n_layers < 1) return fail(SEKV_ERR_INVALID_ARG, "n_layers < 1");
+    if (!layers) return fail(SEKV_ERR_INVALID_ARG, "layers is NULL");
+    sekv_status st = check_dims_impl(dims);
+    if (st != SEKV_OK) return st;
+    // every layer is validated before anything is captured
+    const size_t sel_stride = size_t(dims->batch) * dims->n_kv_heads * size_t(dims->top_k);
+    const size_t out_stride = size_t(dims->batch) * dims->n_q_heads * size_t(dims->head_dim) *
+                              (dims->out_dtype == SEKV_F32 ? 4 : 2);
+    std::vector<sekv::Params> ps(static_cast<size_t>(n_layers));
+    std::vector<char> go(static_cast<size_t>(n_layers));
+    for (int32_t l = 0; l < n_layers; ++l) {
+        bool launch = false;
+        int32_t *sel_l = sel ? sel + size_t(l) * sel_stride : nullptr;
+        void *out_l = out ? static_cast<unsigned char *>(out) + size_t(l) * out_stride : nullptr;
+        st = prepare(sekv::kModeFused, dims, &layers[l], sel_l, nullptr, nullptr, nullptr, out_l,
+                     ws, ws_bytes, &ps[size_t(l)], &launch);
+        if (st != SEKV_OK) {
+            char msg[sizeof(g_err)];
+            std::snprintf(msg, sizeof(msg), "%s", g_err);
+            return fail(st, "layer %d: %s", int(l), msg);
+        }
+        go[size_t(l)] = launch;
+    }
+    const int G = dims->n_q_heads / dims->n_kv_heads;
+    // capture on a private stream (the legacy default stream cannot be captured); the
+    // launches form one chain, so the layers share the workspace in order
+    hipStream_t cs = nullptr;
+    hipError_t e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+    if (e != hipSuccess) return hip_fail(e, "capture stream");
+    e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) {
+        (void)hipStreamDestroy(cs);
+        return hip_fail(e, "begin capture");
+    }
+    hipError_t le = hipSuccess;
+    for (int32_t l = 0; l < n_layers && le == hipSuccess; ++l)
+        if (go[size_t(l)]) le = sekv::launch_step(ps[size_t(l)], dims->dtype, dims->head_dim, G, cs);
+    hipGraph_t g = nullptr;
+    e = hipStreamEndCapture(cs, &g);
+    (void)hipStreamDestroy(cs);
+    if (le != hipSuccess || e != hipSuccess) {
+        if (g) (void)hipGraphDestroy(g);
+        return hip_fail(le != hipSuccess ? le : e, "capturing the layer launches");
+    }
+    hipGraphExec_t x = nullptr;
+    e = hipGraphInstantiate(&x, g, nullptr, nullptr, 0);
+    if (e != hipSuccess) {
+        (void)hipGraphDestroy(g);
+        return hip_fail(e, "instantiating the graph");
+    }
+    sekv_graph *h = new (std::nothrow) sekv_graph{g, x, n_layers};
+    if (!h) {
+        (void)hipGraphExecDestroy(x);
+        (void)hipGraphDestroy(g);
+        return fail(SEKV_ERR_INVALID_ARG, "out of host memory");
+    }
+    *graph = h;
+    return SEKV_OK;
+}
+
+sekv_status sekv_graph_launch(sekv_graph *graph, hipStream_t stream) {
+    if (!graph) return fail(SEKV_ERR_INVALID_ARG, "graph is NULL");
+    const hipError_t e = hipGraphLaunch(graph->exec, stream);
+    if (e != hipSuccess) return hip_fail(e, "graph launch");
+    return SEKV_OK;
+}
+
+sekv_status sekv_graph_destroy(sekv_graph *graph) {
+    if (!graph) return SEKV_OK;
+    hipError_t e = hipGraphExecDestroy(graph->exec);
+    const hipError_t e2 = hipGraphDestroy(graph->graph);
+    delete graph;
+    if (e == hipSuccess) e = e2;
+    if (e != hipSuccess) return hip_fail(e, "destroying the graph");
+    return SEKV_OK;
 }
 
 }  // extern "C"

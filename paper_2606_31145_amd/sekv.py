@@ -23,7 +23,8 @@ DTYPE_CODES = {"f32": SEKV_F32, "bf16": SEKV_BF16}
 
 EXPORTED = ("sekv_status_string", "sekv_last_error", "sekv_check_dims", "sekv_workspace_size",
             "sekv_workspace_init", "sekv_workspace_status", "sekv_route_topk",
-            "sekv_zoom_attend", "sekv_decode_step")
+            "sekv_zoom_attend", "sekv_decode_step", "sekv_graph_create", "sekv_graph_launch",
+            "sekv_graph_destroy")
 
 
 class SekvError(RuntimeError):
@@ -74,6 +75,13 @@ def _load():
     lib.sekv_zoom_attend.argtypes = [P(Dims), P(CacheStruct), VP, VP, VP, VP, SZ, VP]
     lib.sekv_decode_step.restype = ctypes.c_int
     lib.sekv_decode_step.argtypes = [P(Dims), P(CacheStruct), VP, VP, VP, SZ, VP]
+    lib.sekv_graph_create.restype = ctypes.c_int
+    lib.sekv_graph_create.argtypes = [P(Dims), P(CacheStruct), ctypes.c_int32, VP, VP, VP, SZ,
+                                      P(VP)]
+    lib.sekv_graph_launch.restype = ctypes.c_int
+    lib.sekv_graph_launch.argtypes = [VP, VP]
+    lib.sekv_graph_destroy.restype = ctypes.c_int
+    lib.sekv_graph_destroy.argtypes = [VP]
     return lib
 
 
@@ -246,3 +254,47 @@ def decode_step(dims: Dims, cache: DeviceCache, ws: Workspace, sel=None, out=Non
     _check(LIB.sekv_decode_step(ctypes.byref(dims), ctypes.byref(cs), _ptr(sel), _ptr(out),
                                 ws.ptr, ws.nbytes, _stream(stream)))
     return sel, out
+
+
+class LayerGraph:
+    """sekv_graph_*: one decode step over several layers, captured once as a HIP graph.
+
+    caches: one DeviceCache per layer (same shapes).  sel [L][B][Hkv][k] and out
+    [L][B][Hq][d] are allocated here unless given.  The graph holds raw pointers, so this
+    object keeps every tensor it was built from alive.
+    """
+
+    def __init__(self, dims: Dims, caches, ws: Workspace, sel=None, out=None):
+        caches = list(caches)
+        if not caches:
+            raise ValueError("need at least one layer")
+        L = len(caches)
+        dev = caches[0].t["q"].device
+        if sel is None:
+            sel = _alloc((L, dims.batch, dims.n_kv_heads, max(dims.top_k, 0)), torch.int32, dev)
+        if out is None:
+            dt = torch.float32 if dims.out_dtype == SEKV_F32 else torch.bfloat16
+            out = _alloc((L, dims.batch, dims.n_q_heads, dims.head_dim), dt, dev)
+        self.dims, self.caches, self.ws, self.sel, self.out = dims, caches, ws, sel, out
+        self._structs = (CacheStruct * L)(*[c.struct() for c in caches])
+        h = ctypes.c_void_p(0)
+        _check(LIB.sekv_graph_create(ctypes.byref(dims), self._structs, L, _ptr(sel), _ptr(out),
+                                     ws.ptr, ws.nbytes, ctypes.byref(h)))
+        self._h = h
+
+    def launch(self, stream=None):
+        if not self._h:
+            raise RuntimeError("graph destroyed")
+        _check(LIB.sekv_graph_launch(self._h, _stream(stream)))
+        return self.sel, self.out
+
+    def destroy(self):
+        if self._h:
+            h, self._h = self._h, ctypes.c_void_p(0)
+            _check(LIB.sekv_graph_destroy(h))
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
