@@ -69,9 +69,11 @@ def parse():
                     help="approximate CPU time spent timing the oracle")
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (counter calibration)")
-    ap.add_argument("--workload", choices=["layer128k", "layers32"], default="layer128k",
+    ap.add_argument("--workload", choices=["layer128k", "layers32", "hosttier"],
+                    default="layer128k",
                     help="layer128k: one 128K x 4 layer (the headline); layers32: the 32-layer, "
-                         "batch-32, 32K-context step replayed as one HIP graph")
+                         "batch-32, 32K-context step replayed as one HIP graph; hosttier: the "
+                         "128K x 4 layer with its factors in pinned host memory")
     ap.add_argument("--distinct-layers", type=int, default=4,
                     help="layers32: independently seeded layers generated on the host; the "
                          "32 device-resident layers cycle through them, each in its own memory")
@@ -96,6 +98,8 @@ def main():
     dev = torch.device("cuda:0")
     if args.workload == "layers32":
         return bench_layers32(args, dev)
+    if args.workload == "hosttier":
+        return bench_hosttier(args, dev)
     spec = CONFIGS[3]
     log(f"[bench] generating the 128K x 4 cache (variant {args.variant})")
     t0 = time.time()
@@ -302,6 +306,88 @@ def bench_layers32(args, dev):
         line["cpu_baseline"] = cpu_baseline(cases[0], per_layer[0]["total"], args.cpu_seconds,
                                             what="full decode steps of one layer of the 32-layer "
                                                  "workload (batch 32, 32K)")
+    print(json.dumps(line), flush=True)
+
+
+def bench_hosttier(args, dev):
+    """128K x 4 layer; factors in pinned host memory, selected blocks copied per step."""
+    import numpy as np
+    import torch
+
+    from paper_2606_31145_amd import accounting
+    from paper_2606_31145_amd import sekv
+    from synth import CONFIGS, make_case
+
+    spec = CONFIGS[5]
+    t0 = time.time()
+    case = make_case(spec, variant=args.variant)
+    log(f"[bench] generated in {time.time() - t0:.1f}s")
+    dummy = np.zeros(256, dtype=np.uint8)       # the device cache carries no factors
+    arrays = dict(q=case.q, anchor_k=case.anchor_k, anchor_v=case.anchor_v,
+                  n_anchors=case.n_anchors, sum_k=case.sum_k, sum_v=case.sum_v,
+                  n_spans=case.n_spans, span_len=case.span_len, span_logsize=case.span_logsize,
+                  factors=dummy, block_off=np.zeros_like(case.block_off))
+    dc = sekv.DeviceCache.from_arrays(arrays, spec.dtype, dev)
+    host = sekv.HostFactors(case.factors, case.block_off, case.span_len)
+    dims = sekv.make_dims(batch=spec.batch, n_q_heads=spec.n_q_heads, n_kv_heads=spec.n_kv_heads,
+                          head_dim=spec.head_dim, rank=spec.rank, top_k=spec.top_k,
+                          max_anchors=case.max_anchors, max_spans=case.max_spans,
+                          max_span_len=case.max_span_len, dtype=spec.dtype,
+                          softmax_scale=spec.softmax_scale)
+    ws = sekv.Workspace(dims, dev)
+    tier = sekv.Tier(dims)
+    side = torch.cuda.Stream()
+    stream = torch.cuda.current_stream()
+    B, Hq, Hkv, d = spec.batch, spec.n_q_heads, spec.n_kv_heads, spec.head_dim
+    sel = torch.empty((B, Hkv, spec.top_k), dtype=torch.int32, device=dev)
+    out = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
+    for _ in range(args.warmup):
+        sekv.decode_step_tiered(dims, dc, host, tier, ws, sel=sel, out=out, stream=stream, side=side)
+    torch.cuda.synchronize()
+    assert ws.status() == 0
+    K = args.steps
+    walls, copy_ms, copy_bytes, n_copies = [], [], [], []
+    for _ in range(K):
+        t1 = time.perf_counter()
+        sekv.decode_step_tiered(dims, dc, host, tier, ws, sel=sel, out=out, stream=stream, side=side)
+        torch.cuda.synchronize()
+        walls.append(time.perf_counter() - t1)
+        nb, nc, ms = tier.last_copy()
+        copy_ms.append(ms)
+        copy_bytes.append(nb)
+        n_copies.append(nc)
+    assert ws.status() == 0
+    sel_np = sel.cpu().numpy()
+    acct = accounting.step_bytes(n_q_heads=Hq, n_kv_heads=Hkv, head_dim=d, rank=spec.rank,
+                                 elem=2, out_elem=2, n_anchors=case.n_anchors,
+                                 n_spans=case.n_spans, span_len=case.span_len, sel=sel_np)
+    step_s = float(np.median(walls))
+    link = float(np.mean(copy_bytes)) / (float(np.mean(copy_ms)) * 1e-3) / 1e9
+    # HBM held by the tiered step vs a dense bf16 cache of the same tokens
+    resident = int(sum(t.numel() * t.element_size() for k, t in dc.t.items()
+                       if k not in ("factors", "block_off")) + tier.staging_bytes)
+    full = accounting.full_kv_bytes_same_shapes(n_kv_heads=Hkv, head_dim=d, elem=2,
+                                                n_anchors=case.n_anchors, span_len=case.span_len)
+    tier.destroy()
+    line = {
+        "metric": "decode-step latency (µs), host-link GB/s and HBM saved, 128K context, batch 4, "
+                  "factors in pinned host memory",
+        "value": round(step_s * 1e6, 1), "unit": "us", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(step_s * 1e3, 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"sekv-decode-step-128k-b4-r32-k16-bf16-hosttier-{args.variant}",
+                   "batch": B, "context": spec.context, "rank": spec.rank, "top_k": spec.top_k,
+                   "variant": args.variant, "parallelism": "single-gpu"},
+        "host_link": {"bytes_per_step": int(np.mean(copy_bytes)),
+                      "copies_per_step": float(np.mean(n_copies)),
+                      "copy_ms_per_step": round(float(np.mean(copy_ms)), 4),
+                      "GB_s": round(link, 2)},
+        "hbm": {"resident_bytes": resident, "full_bf16_kv_bytes": full,
+                "saved_frac": round(1.0 - resident / full, 4),
+                "algorithmic_bytes_per_step": acct["total"]},
+        "step_us_p90": round(float(np.percentile(walls, 90)) * 1e6, 1),
+    }
     print(json.dumps(line), flush=True)
 
 

@@ -20,9 +20,11 @@
  *
  * Conventions
  *   - Every pointer in sekv_cache, and every sel/logits/out/workspace pointer, is a
- *     DEVICE pointer owned by the caller, 16-byte aligned (the tier entry point is
- *     the documented exception for the factor arena).  The library allocates nothing
- *     on these calls.
+ *     DEVICE pointer owned by the caller.  Data arrays (q, anchors, summaries, factor
+ *     arena) are 16-byte aligned, out 8-byte; sel, logits and the tables n_anchors,
+ *     n_spans, span_len 4-byte; span_logsize and block_off 8-byte (the tiered step reads the
+ *     factor arena from pinned host memory instead).  The step calls allocate nothing;
+ *     only the set-up calls (sekv_graph_create, sekv_tier_create) do.
  *   - Calls enqueue work on the caller's stream and return; results are valid in
  *     stream order.  Calls never synchronise the device unless documented.
  *   - Errors found on the host (null or misaligned pointers, unsupported sizes, a small
@@ -180,6 +182,72 @@ SEKV_API sekv_status sekv_graph_launch(sekv_graph *graph, hipStream_t stream);
 
 /* Free the graph and its handle (NULL is a no-op).  No replay may be pending. */
 SEKV_API sekv_status sekv_graph_destroy(sekv_graph *graph);
+
+/* ----------------------------------------------------------------------------------
+ * Pinned-host tier.  The paper keeps every span's low-rank factors in CPU memory and
+ * moves only the zoomed spans' factors to the GPU at each step, overlapped with the
+ * rest of the step (Sec. 3.2, last paragraph; App. D: the per-step transfer is the
+ * sum over the zoomed spans of 2 H_kv r (|S| + d_h + 1) elements, independent of the
+ * context length).  Here anchors, summaries and span tables stay in HBM and the factor
+ * arena lives in pinned host memory.
+ *
+ * sekv_decode_step_tiered, per sequence b in order:
+ *   1. routing and selection of b on `main` (steps 1-2); the selection is read back to
+ *      a pinned mirror;
+ *   2. the host waits for that selection only, then enqueues one hipMemcpyAsync per run
+ *      of selected blocks that are neighbours in the arena, on `side`, into the tier's
+ *      device staging area, plus the staging offset table of b;
+ *   3. `main` waits for those copies (an event) and runs steps 3-4 of b from staging.
+ * Copies of sequence b overlap the routing of later sequences and the attention of
+ * earlier ones.  The call returns after enqueuing the last attention; it blocks the
+ * host only on the per-sequence selection readbacks.  Results are those of
+ * sekv_route_topk followed by sekv_zoom_attend with the routing scores, on a
+ * device-resident copy of the arena.
+ * -------------------------------------------------------------------------------- */
+
+/* The factor arena in pinned host memory (hipHostMalloc), and host copies of the span
+ * tables the host needs to address it. */
+typedef struct {
+    const void *arena;              /* pinned host bytes, span blocks as in sekv_cache       */
+    int64_t arena_bytes;
+    const int64_t *block_off;       /* host int64 [B][Hkv][M_max]: byte offset of each block */
+    const int32_t *span_len;        /* host int32 [B][M_max]: |S|                            */
+} sekv_host_factors;
+
+typedef struct sekv_tier sekv_tier;
+
+/* Set-up (allocates): pinned mirrors of the selection and of the staging offsets,
+ * device staging for batch * Hkv * top_k blocks of max_span_len tokens, a routing-score
+ * buffer, and events, on the current device.  dims is copied; every step must pass
+ * identical dims. */
+SEKV_API sekv_status sekv_tier_create(const sekv_dims *dims, sekv_tier **tier);
+
+/* Free everything the tier holds (NULL is a no-op).  No step may be pending. */
+SEKV_API sekv_status sekv_tier_destroy(sekv_tier *tier);
+
+/* Device staging bytes the tier holds (0 for NULL). */
+SEKV_API size_t sekv_tier_staging_size(const sekv_tier *tier);
+
+/* Host-link figures of the last tiered step: bytes copied host to device, number of
+ * copies, and the time from the first copy's start to the last copy's end on the side
+ * stream (valid once that step has completed). */
+SEKV_API sekv_status sekv_tier_last_copy(sekv_tier *tier, int64_t *bytes, int32_t *copies,
+                                         float *ms);
+
+/* One decode step with the factors in pinned host memory.
+ *   cache   device arrays as for sekv_decode_step; cache->factors and cache->block_off
+ *           are not read (the host arena replaces them)
+ *   host    the pinned arena and host tables; a block outside the arena, or an arena
+ *           that is not pinned, is an SEKV_ERR_INVALID_ARG
+ *   sel     device int32 [B][Hkv][top_k]; out device [B][Hq][d] in out_dtype
+ *   ws      workspace of sekv_workspace_size(dims)
+ *   main    stream of the kernels; side: stream of the host-to-device copies (both at the
+ *           default priority; side must differ from main for the overlap)
+ * The tier must not be shared by concurrent steps. */
+SEKV_API sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_cache *cache,
+                                             const sekv_host_factors *host, sekv_tier *tier,
+                                             int32_t *sel, void *out, void *ws, size_t ws_bytes,
+                                             hipStream_t main, hipStream_t side);
 
 #ifdef __cplusplus
 }

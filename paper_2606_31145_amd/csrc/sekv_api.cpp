@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdint>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -73,13 +74,15 @@ sekv_status check_dims_impl(const sekv_dims *d) {
 sekv_status check_cache(const sekv_dims *d, const sekv_cache *c, bool need_factors) {
     if (!c) return fail(SEKV_ERR_INVALID_ARG, "cache is NULL");
     if (d->batch == 0) return SEKV_OK;
-    struct { const void *p; const char *name; } ptrs[] = {
-        {c->q, "q"}, {c->sum_k, "sum_k"}, {c->sum_v, "sum_v"}, {c->n_spans, "n_spans"},
-        {c->span_len, "span_len"}, {c->span_logsize, "span_logsize"},
-        {c->n_anchors, "n_anchors"}};
+    // data rows are read as 16-byte vectors; tables element by element
+    struct { const void *p; const char *name; uintptr_t align; } ptrs[] = {
+        {c->q, "q", 16}, {c->sum_k, "sum_k", 16}, {c->sum_v, "sum_v", 16},
+        {c->n_spans, "n_spans", 4}, {c->span_len, "span_len", 4},
+        {c->span_logsize, "span_logsize", 8}, {c->n_anchors, "n_anchors", 4}};
     for (auto &x : ptrs) {
         if (!x.p) return fail(SEKV_ERR_INVALID_ARG, "cache.%s is NULL", x.name);
-        if (!aligned16(x.p)) return fail(SEKV_ERR_INVALID_ARG, "cache.%s not 16-byte aligned", x.name);
+        if (reinterpret_cast<uintptr_t>(x.p) & (x.align - 1))
+            return fail(SEKV_ERR_INVALID_ARG, "cache.%s not %d-byte aligned", x.name, int(x.align));
     }
     if (d->max_anchors > 0) {
         if (!c->anchor_k || !c->anchor_v)
@@ -90,8 +93,8 @@ sekv_status check_cache(const sekv_dims *d, const sekv_cache *c, bool need_facto
     if (need_factors && d->top_k > 0) {
         if (!c->factors || !c->block_off)
             return fail(SEKV_ERR_INVALID_ARG, "cache.factors/block_off is NULL");
-        if (!aligned16(c->factors) || !aligned16(c->block_off))
-            return fail(SEKV_ERR_INVALID_ARG, "factor arena or offsets not 16-byte aligned");
+        if (!aligned16(c->factors) || (reinterpret_cast<uintptr_t>(c->block_off) & 7))
+            return fail(SEKV_ERR_INVALID_ARG, "factor arena not 16-byte or offsets not 8-byte aligned");
         if (c->factors_bytes <= 0) return fail(SEKV_ERR_INVALID_ARG, "factors_bytes <= 0");
     }
     return SEKV_OK;
@@ -145,10 +148,10 @@ sekv_status prepare(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *
     if (mode == sekv::kModeAttend && d->top_k > 0 && !sel_in)
         return fail(SEKV_ERR_INVALID_ARG, "sel is NULL");
     if (mode != sekv::kModeRoute && !out) return fail(SEKV_ERR_INVALID_ARG, "out is NULL");
-    if ((sel_out && !aligned16(sel_out)) || (sel_in && !aligned16(sel_in)) ||
-        (out && !aligned16(out)) || (logits_out && !aligned16(logits_out)) ||
-        (logits_in && !aligned16(logits_in)))
-        return fail(SEKV_ERR_INVALID_ARG, "sel/logits/out not 16-byte aligned");
+    // element accesses: sel and logits 4-byte, out in pairs of values (8-byte)
+    auto mis = [](const void *q, uintptr_t a) { return (reinterpret_cast<uintptr_t>(q) & (a - 1)) != 0; };
+    if (mis(sel_out, 4) || mis(sel_in, 4) || mis(logits_out, 4) || mis(logits_in, 4) || mis(out, 8))
+        return fail(SEKV_ERR_INVALID_ARG, "sel/logits not 4-byte or out not 8-byte aligned");
 
     const sekv::Shape s = sekv::make_shape(*d);
     const sekv::WsLayout L = sekv::make_layout(s);
@@ -211,6 +214,16 @@ sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_
                                            stream);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     return SEKV_OK;
+}
+
+// Bytes of one span block of length L (U|sigma|Vt for keys, then values; every segment
+// starts on a 16-byte boundary, the block on a 256-byte boundary).
+size_t tier_block_bytes(const sekv_dims &d, int L) {
+    const size_t e = size_t(sekv::elem_bytes(d.dtype));
+    auto a16 = [](size_t x) { return (x + 15) & ~size_t(15); };
+    const size_t side = a16(size_t(L) * d.rank * e) + a16(size_t(d.rank) * e) +
+                        a16(size_t(d.rank) * d.head_dim * e);
+    return 2 * side;
 }
 
 }  // namespace
@@ -374,6 +387,243 @@ sekv_status sekv_graph_destroy(sekv_graph *graph) {
     delete graph;
     if (e == hipSuccess) e = e2;
     if (e != hipSuccess) return hip_fail(e, "destroying the graph");
+    return SEKV_OK;
+}
+
+
+// ------------------------------------------------------------------------------------
+// pinned-host tier
+// ------------------------------------------------------------------------------------
+struct sekv_tier {
+    sekv_dims dims;
+    int device;
+    size_t slot_bytes;          // staging bytes per selection slot (largest block, aligned)
+    size_t staging_bytes;
+    int32_t *h_sel;             // pinned [B][Hkv][k]: selection read back per sequence
+    int64_t *h_off;             // pinned [B][Hkv][M_max]: staging offsets of the selected blocks
+    void *d_mem;                // one device allocation: offsets | logits | staging
+    int64_t *d_off;             // [B][Hkv][M_max]
+    float *d_logits;            // [B][Hq][M_max]
+    unsigned char *d_staging;   // [B][Hkv][k] slots
+    hipEvent_t *ev_sel;         // [B] selection of sequence b is on the host
+    hipEvent_t *ev_copy;        // [B] factors of sequence b are in staging
+    hipEvent_t ev_t0, ev_t1;    // timing of the last step's copies (side stream)
+    int64_t last_bytes;
+    int32_t last_copies;
+};
+
+sekv_status sekv_tier_create(const sekv_dims *dims, sekv_tier **tier) {
+    if (!tier) return fail(SEKV_ERR_INVALID_ARG, "tier is NULL");
+    *tier = nullptr;
+    sekv_status st = check_dims_impl(dims);
+    if (st != SEKV_OK) return st;
+    if (dims->batch < 1) return fail(SEKV_ERR_INVALID_ARG, "the tier needs batch >= 1");
+    sekv_tier *t = new (std::nothrow) sekv_tier{};
+    if (!t) return fail(SEKV_ERR_INVALID_ARG, "out of host memory");
+    t->dims = *dims;
+    const size_t B = size_t(dims->batch), Hkv = size_t(dims->n_kv_heads), Hq = size_t(dims->n_q_heads);
+    const size_t M = size_t(dims->max_spans), k = size_t(std::max(dims->top_k, 1));
+    t->slot_bytes = sekv::align256(tier_block_bytes(*dims, dims->max_span_len));
+    t->staging_bytes = B * Hkv * k * t->slot_bytes;
+    auto cleanup = [&](hipError_t e, const char *what) {
+        sekv_tier_destroy(t);
+        return hip_fail(e, what);
+    };
+    hipError_t e = hipGetDevice(&t->device);
+    if (e != hipSuccess) return cleanup(e, "hipGetDevice");
+    e = hipHostMalloc(reinterpret_cast<void **>(&t->h_sel), B * Hkv * k * sizeof(int32_t), hipHostMallocDefault);
+    if (e != hipSuccess) return cleanup(e, "pinned selection mirror");
+    e = hipHostMalloc(reinterpret_cast<void **>(&t->h_off), B * Hkv * M * sizeof(int64_t), hipHostMallocDefault);
+    if (e != hipSuccess) return cleanup(e, "pinned offset table");
+    std::memset(t->h_off, 0, B * Hkv * M * sizeof(int64_t));
+    const size_t off_bytes = sekv::align256(B * Hkv * M * sizeof(int64_t));
+    const size_t lg_bytes = sekv::align256(B * Hq * M * sizeof(float));
+    e = hipMalloc(&t->d_mem, off_bytes + lg_bytes + t->staging_bytes);
+    if (e != hipSuccess) return cleanup(e, "device staging");
+    t->d_off = static_cast<int64_t *>(t->d_mem);
+    t->d_logits = reinterpret_cast<float *>(static_cast<unsigned char *>(t->d_mem) + off_bytes);
+    t->d_staging = static_cast<unsigned char *>(t->d_mem) + off_bytes + lg_bytes;
+    e = hipMemset(t->d_off, 0, off_bytes);
+    if (e != hipSuccess) return cleanup(e, "clearing the offset table");
+    t->ev_sel = new (std::nothrow) hipEvent_t[B]();
+    t->ev_copy = new (std::nothrow) hipEvent_t[B]();
+    if (!t->ev_sel || !t->ev_copy) {
+        sekv_tier_destroy(t);
+        return fail(SEKV_ERR_INVALID_ARG, "out of host memory");
+    }
+    for (size_t b = 0; b < B; ++b) {
+        e = hipEventCreateWithFlags(&t->ev_sel[b], hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&t->ev_copy[b], hipEventDisableTiming);
+        if (e != hipSuccess) return cleanup(e, "creating events");
+    }
+    e = hipEventCreate(&t->ev_t0);
+    if (e == hipSuccess) e = hipEventCreate(&t->ev_t1);
+    if (e != hipSuccess) return cleanup(e, "creating timing events");
+    *tier = t;
+    return SEKV_OK;
+}
+
+sekv_status sekv_tier_destroy(sekv_tier *t) {
+    if (!t) return SEKV_OK;
+    const size_t B = size_t(std::max(t->dims.batch, 0));
+    for (size_t b = 0; b < B; ++b) {
+        if (t->ev_sel && t->ev_sel[b]) (void)hipEventDestroy(t->ev_sel[b]);
+        if (t->ev_copy && t->ev_copy[b]) (void)hipEventDestroy(t->ev_copy[b]);
+    }
+    delete[] t->ev_sel;
+    delete[] t->ev_copy;
+    if (t->ev_t0) (void)hipEventDestroy(t->ev_t0);
+    if (t->ev_t1) (void)hipEventDestroy(t->ev_t1);
+    if (t->d_mem) (void)hipFree(t->d_mem);
+    if (t->h_sel) (void)hipHostFree(t->h_sel);
+    if (t->h_off) (void)hipHostFree(t->h_off);
+    delete t;
+    return SEKV_OK;
+}
+
+size_t sekv_tier_staging_size(const sekv_tier *t) { return t ? t->staging_bytes : 0; }
+
+sekv_status sekv_tier_last_copy(sekv_tier *t, int64_t *bytes, int32_t *copies, float *ms) {
+    if (!t || !bytes || !copies || !ms) return fail(SEKV_ERR_INVALID_ARG, "NULL argument");
+    *bytes = t->last_bytes;
+    *copies = t->last_copies;
+    *ms = 0.0f;
+    if (t->last_copies > 0) {
+        const hipError_t e = hipEventElapsedTime(ms, t->ev_t0, t->ev_t1);
+        if (e != hipSuccess) return hip_fail(e, "copy timing events");
+    }
+    return SEKV_OK;
+}
+
+sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_cache *cache,
+                                    const sekv_host_factors *host, sekv_tier *t, int32_t *sel,
+                                    void *out, void *ws, size_t ws_bytes, hipStream_t main,
+                                    hipStream_t side) {
+    if (!t) return fail(SEKV_ERR_INVALID_ARG, "tier is NULL");
+    sekv_status st = check_dims_impl(dims);
+    if (st != SEKV_OK) return st;
+    if (std::memcmp(dims, &t->dims, sizeof(sekv_dims)) != 0)
+        return fail(SEKV_ERR_INVALID_ARG, "dims differ from the tier's");
+    if (!cache || !host || !host->arena || !host->block_off || !host->span_len)
+        return fail(SEKV_ERR_INVALID_ARG, "cache/host factor tables are NULL");
+    if (host->arena_bytes <= 0) return fail(SEKV_ERR_INVALID_ARG, "arena_bytes <= 0");
+    if (!out || (dims->top_k > 0 && !sel)) return fail(SEKV_ERR_INVALID_ARG, "sel/out is NULL");
+    hipPointerAttribute_t attr{};
+    if (hipPointerGetAttributes(&attr, host->arena) != hipSuccess || attr.type != hipMemoryTypeHost) {
+        (void)hipGetLastError();
+        return fail(SEKV_ERR_INVALID_ARG, "the host factor arena is not pinned (hipHostMalloc) memory");
+    }
+    const int B = dims->batch, Hkv = dims->n_kv_heads, Hq = dims->n_q_heads, k = dims->top_k;
+    const int M = dims->max_spans, d = dims->head_dim;
+    const size_t oe = dims->out_dtype == SEKV_F32 ? 4 : 2;
+    const size_t e = size_t(sekv::elem_bytes(dims->dtype));
+    sekv_dims d1 = *dims;
+    d1.batch = 1;
+    // per-sequence views of the device cache (b is the outermost index of every array)
+    auto seq_cache = [&](int b) {
+        sekv_cache c = *cache;
+        const size_t bb = size_t(b);
+        c.q = static_cast<const unsigned char *>(cache->q) + bb * Hq * d * e;
+        c.anchor_k = cache->anchor_k ? static_cast<const unsigned char *>(cache->anchor_k) +
+                                           bb * Hkv * size_t(dims->max_anchors) * d * e : nullptr;
+        c.anchor_v = cache->anchor_v ? static_cast<const unsigned char *>(cache->anchor_v) +
+                                           bb * Hkv * size_t(dims->max_anchors) * d * e : nullptr;
+        c.n_anchors = cache->n_anchors + bb;
+        c.sum_k = static_cast<const unsigned char *>(cache->sum_k) + bb * Hkv * size_t(M) * d * e;
+        c.sum_v = static_cast<const unsigned char *>(cache->sum_v) + bb * Hkv * size_t(M) * d * e;
+        c.n_spans = cache->n_spans + bb;
+        c.span_len = cache->span_len + bb * M;
+        c.span_logsize = cache->span_logsize + bb * M;
+        c.factors = t->d_staging;
+        c.factors_bytes = int64_t(t->staging_bytes);
+        c.block_off = t->d_off + bb * Hkv * M;
+        return c;
+    };
+    // 1. routing per sequence on the main stream; each selection goes to the pinned mirror
+    for (int b = 0; b < B; ++b) {
+        sekv_cache c = seq_cache(b);
+        st = run(sekv::kModeRoute, &d1, &c, sel ? sel + size_t(b) * Hkv * k : nullptr,
+                 t->d_logits + size_t(b) * Hq * M, nullptr, nullptr, nullptr, ws, ws_bytes, main);
+        if (st != SEKV_OK) return st;
+        if (k > 0) {
+            hipError_t he = hipMemcpyAsync(t->h_sel + size_t(b) * Hkv * k, sel + size_t(b) * Hkv * k,
+                                           size_t(Hkv) * k * sizeof(int32_t), hipMemcpyDeviceToHost, main);
+            if (he == hipSuccess) he = hipEventRecord(t->ev_sel[b], main);
+            if (he != hipSuccess) return hip_fail(he, "selection readback");
+        }
+    }
+    // 2. per sequence: wait for its selection, copy the selected blocks on the side stream
+    //    (runs while later sequences route), then attend on the main stream
+    int64_t bytes = 0;
+    int32_t copies = 0;
+    bool first = true;
+    struct Blk { int64_t src; int64_t len; int64_t slot; int g; int s; };
+    std::vector<Blk> blks;
+    for (int b = 0; b < B; ++b) {
+        hipError_t he = hipSuccess;
+        if (k > 0) {
+            he = hipEventSynchronize(t->ev_sel[b]);
+            if (he != hipSuccess) return hip_fail(he, "waiting for the selection");
+            blks.clear();
+            for (int g = 0; g < Hkv; ++g)
+                for (int j = 0; j < k; ++j) {
+                    const int s = t->h_sel[(size_t(b) * Hkv + g) * k + j];
+                    if (s < 0 || s >= M) continue;
+                    const int L = host->span_len[size_t(b) * M + s];
+                    const int64_t off = host->block_off[(size_t(b) * Hkv + g) * M + s];
+                    const int64_t len = int64_t(tier_block_bytes(*dims, L));
+                    if (L < 1 || L > dims->max_span_len || off < 0 || (off & 15) ||
+                        off + len > host->arena_bytes)
+                        return fail(SEKV_ERR_INVALID_ARG, "host block (%d, %d, %d) outside the arena", b, g, s);
+                    blks.push_back({off, len, 0, g, s});
+                }
+            // staging of sequence b: its blocks packed in arena order (each on a 256-byte
+            // boundary) inside the sequence's region, so blocks that are neighbours in the
+            // arena are neighbours in staging and move with one copy
+            std::sort(blks.begin(), blks.end(), [](const Blk &x, const Blk &y) { return x.src < y.src; });
+            int64_t pos = int64_t(size_t(b) * Hkv * size_t(std::max(k, 1)) * t->slot_bytes);
+            for (auto &x : blks) {
+                x.slot = pos;
+                pos += int64_t(sekv::align256(size_t(x.len)));
+                t->h_off[(size_t(b) * Hkv + x.g) * M + x.s] = x.slot;
+            }
+            for (size_t i = 0; i < blks.size();) {
+                size_t j = i + 1;
+                while (j < blks.size() &&
+                       blks[j].src == blks[j - 1].src + int64_t(sekv::align256(size_t(blks[j - 1].len))))
+                    ++j;
+                const int64_t len = (blks[j - 1].src - blks[i].src) + blks[j - 1].len;
+                if (first) {
+                    he = hipEventRecord(t->ev_t0, side);
+                    if (he != hipSuccess) return hip_fail(he, "copy timing event");
+                    first = false;
+                }
+                he = hipMemcpyAsync(t->d_staging + blks[i].slot,
+                                    static_cast<const unsigned char *>(host->arena) + blks[i].src,
+                                    size_t(len), hipMemcpyHostToDevice, side);
+                if (he != hipSuccess) return hip_fail(he, "factor block copy");
+                bytes += len;
+                ++copies;
+                i = j;
+            }
+            he = hipMemcpyAsync(t->d_off + size_t(b) * Hkv * M, t->h_off + size_t(b) * Hkv * M,
+                                size_t(Hkv) * M * sizeof(int64_t), hipMemcpyHostToDevice, side);
+            if (he == hipSuccess) he = hipEventRecord(t->ev_copy[b], side);
+            if (he == hipSuccess) he = hipStreamWaitEvent(main, t->ev_copy[b], 0);
+            if (he != hipSuccess) return hip_fail(he, "staging offsets");
+        }
+        sekv_cache c = seq_cache(b);
+        st = run(sekv::kModeAttend, &d1, &c, nullptr, nullptr, sel ? sel + size_t(b) * Hkv * k : nullptr,
+                 t->d_logits + size_t(b) * Hq * M, static_cast<unsigned char *>(out) + size_t(b) * Hq * d * oe,
+                 ws, ws_bytes, main);
+        if (st != SEKV_OK) return st;
+    }
+    if (!first) {
+        const hipError_t he = hipEventRecord(t->ev_t1, side);
+        if (he != hipSuccess) return hip_fail(he, "copy timing event");
+    }
+    t->last_bytes = bytes;
+    t->last_copies = copies;
     return SEKV_OK;
 }
 

@@ -24,7 +24,8 @@ DTYPE_CODES = {"f32": SEKV_F32, "bf16": SEKV_BF16}
 EXPORTED = ("sekv_status_string", "sekv_last_error", "sekv_check_dims", "sekv_workspace_size",
             "sekv_workspace_init", "sekv_workspace_status", "sekv_route_topk",
             "sekv_zoom_attend", "sekv_decode_step", "sekv_graph_create", "sekv_graph_launch",
-            "sekv_graph_destroy")
+            "sekv_graph_destroy", "sekv_tier_create", "sekv_tier_destroy",
+            "sekv_tier_staging_size", "sekv_tier_last_copy", "sekv_decode_step_tiered")
 
 
 class SekvError(RuntimeError):
@@ -50,6 +51,11 @@ class CacheStruct(ctypes.Structure):
                 ("n_spans", ctypes.c_void_p), ("span_len", ctypes.c_void_p),
                 ("span_logsize", ctypes.c_void_p), ("factors", ctypes.c_void_p),
                 ("factors_bytes", ctypes.c_int64), ("block_off", ctypes.c_void_p)]
+
+
+class HostFactorsStruct(ctypes.Structure):
+    _fields_ = [("arena", ctypes.c_void_p), ("arena_bytes", ctypes.c_int64),
+                ("block_off", ctypes.c_void_p), ("span_len", ctypes.c_void_p)]
 
 
 def _load():
@@ -82,6 +88,17 @@ def _load():
     lib.sekv_graph_launch.argtypes = [VP, VP]
     lib.sekv_graph_destroy.restype = ctypes.c_int
     lib.sekv_graph_destroy.argtypes = [VP]
+    lib.sekv_tier_create.restype = ctypes.c_int
+    lib.sekv_tier_create.argtypes = [P(Dims), P(VP)]
+    lib.sekv_tier_destroy.restype = ctypes.c_int
+    lib.sekv_tier_destroy.argtypes = [VP]
+    lib.sekv_tier_staging_size.restype = SZ
+    lib.sekv_tier_staging_size.argtypes = [VP]
+    lib.sekv_tier_last_copy.restype = ctypes.c_int
+    lib.sekv_tier_last_copy.argtypes = [VP, P(ctypes.c_int64), I32P, P(ctypes.c_float)]
+    lib.sekv_decode_step_tiered.restype = ctypes.c_int
+    lib.sekv_decode_step_tiered.argtypes = [P(Dims), P(CacheStruct), P(HostFactorsStruct), VP, VP,
+                                            VP, VP, SZ, VP, VP]
     return lib
 
 
@@ -298,3 +315,67 @@ class LayerGraph:
             self.destroy()
         except Exception:
             pass
+
+
+class HostFactors:
+    """The factor arena in pinned host memory plus host copies of block_off and span_len."""
+
+    def __init__(self, factors: np.ndarray, block_off: np.ndarray, span_len: np.ndarray):
+        a = np.ascontiguousarray(factors, dtype=np.uint8)
+        self.arena = torch.empty(a.nbytes, dtype=torch.uint8, pin_memory=True)
+        self.arena.numpy()[:] = a
+        self.block_off = np.ascontiguousarray(block_off, dtype=np.int64)
+        self.span_len = np.ascontiguousarray(span_len, dtype=np.int32)
+
+    def struct(self) -> HostFactorsStruct:
+        return HostFactorsStruct(self.arena.data_ptr(), int(self.arena.numel()),
+                                 self.block_off.ctypes.data, self.span_len.ctypes.data)
+
+
+class Tier:
+    """sekv_tier_*: pinned mirrors, device staging and events for tiered steps."""
+
+    def __init__(self, dims: Dims):
+        h = ctypes.c_void_p(0)
+        _check(LIB.sekv_tier_create(ctypes.byref(dims), ctypes.byref(h)))
+        self._h = h
+        self.dims = dims
+
+    @property
+    def staging_bytes(self) -> int:
+        return int(LIB.sekv_tier_staging_size(self._h))
+
+    def last_copy(self):
+        """(bytes, copies, milliseconds) of the last step's host-to-device copies."""
+        nb, nc, ms = ctypes.c_int64(0), ctypes.c_int32(0), ctypes.c_float(0)
+        _check(LIB.sekv_tier_last_copy(self._h, ctypes.byref(nb), ctypes.byref(nc), ctypes.byref(ms)))
+        return int(nb.value), int(nc.value), float(ms.value)
+
+    def destroy(self):
+        if self._h:
+            h, self._h = self._h, ctypes.c_void_p(0)
+            _check(LIB.sekv_tier_destroy(h))
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def decode_step_tiered(dims: Dims, cache: DeviceCache, host: HostFactors, tier: Tier,
+                       ws: Workspace, sel=None, out=None, stream=None, side=None):
+    """sekv_decode_step_tiered: returns (sel, out).  `side` is the copy stream."""
+    dev = cache.t["q"].device
+    if sel is None:
+        sel = _alloc((dims.batch, dims.n_kv_heads, max(dims.top_k, 0)), torch.int32, dev)
+    if out is None:
+        out = _out_tensor(dims, dev)
+    if side is None:
+        raise ValueError("a side stream is needed for the copies")
+    cs = cache.struct()
+    hs = host.struct()
+    _check(LIB.sekv_decode_step_tiered(ctypes.byref(dims), ctypes.byref(cs), ctypes.byref(hs),
+                                       tier._h, _ptr(sel), _ptr(out), ws.ptr, ws.nbytes,
+                                       _stream(stream), _stream(side)))
+    return sel, out
