@@ -412,7 +412,7 @@ def bench_hosttier(args, dev):
                    "batch": B, "context": spec.context, "rank": spec.rank, "top_k": spec.top_k,
                    "variant": args.variant, "parallelism": "single-gpu"},
         "host_link": {"bytes_per_step": int(np.mean(copy_bytes)),
-                      "copies_per_step": float(np.mean(n_copies)),
+                      "runs_per_step": float(np.mean(n_copies)),
                       "copy_ms_per_step": round(float(np.mean(copy_ms)), 4),
                       "GB_s": round(link, 2)},
         "hbm": {"resident_bytes": resident, "full_bf16_kv_bytes": full,

@@ -194,9 +194,10 @@ SEKV_API sekv_status sekv_graph_destroy(sekv_graph *graph);
  * sekv_decode_step_tiered, per sequence b in order:
  *   1. routing and selection of b on `main` (steps 1-2); the selection is read back to
  *      a pinned mirror;
- *   2. the host waits for that selection only, then enqueues one hipMemcpyAsync per run
- *      of selected blocks that are neighbours in the arena, on `side`, into the tier's
- *      device staging area, plus the staging offset table of b;
+ *   2. the host waits for that selection only, then enqueues on `side` one gather
+ *      kernel that reads the selected blocks (runs of blocks that are neighbours in the
+ *      arena, in chunks of at most 32 KiB) through the arena's device mapping into the
+ *      tier's device staging area, plus a copy of the staging offset table of b;
  *   3. `main` waits for those copies (an event) and runs steps 3-4 of b from staging.
  * Copies of sequence b overlap the routing of later sequences and the attention of
  * earlier ones.  The call returns after enqueuing the last attention; it blocks the
@@ -216,9 +217,9 @@ typedef struct {
 
 typedef struct sekv_tier sekv_tier;
 
-/* Set-up (allocates): pinned mirrors of the selection and of the staging offsets,
- * device staging for batch * Hkv * top_k blocks of max_span_len tokens, a routing-score
- * buffer, and events, on the current device.  dims is copied; every step must pass
+/* Set-up (allocates): pinned mirrors of the selection and of the staging offsets, a
+ * pinned gather table, device staging for batch * Hkv * top_k blocks of max_span_len
+ * tokens, a routing-score buffer, and events, on the current device.  dims is copied; every step must pass
  * identical dims. */
 SEKV_API sekv_status sekv_tier_create(const sekv_dims *dims, sekv_tier **tier);
 
@@ -228,9 +229,9 @@ SEKV_API sekv_status sekv_tier_destroy(sekv_tier *tier);
 /* Device staging bytes the tier holds (0 for NULL). */
 SEKV_API size_t sekv_tier_staging_size(const sekv_tier *tier);
 
-/* Host-link figures of the last tiered step: bytes copied host to device, number of
- * copies, and the time from the first copy's start to the last copy's end on the side
- * stream (valid once that step has completed). */
+/* Host-link figures of the last tiered step: bytes moved host to device, number of
+ * contiguous runs moved, and the time from the start of the first gather to the end of
+ * the last one on the side stream (valid once that step has completed). */
 SEKV_API sekv_status sekv_tier_last_copy(sekv_tier *tier, int64_t *bytes, int32_t *copies,
                                          float *ms);
 
@@ -238,7 +239,7 @@ SEKV_API sekv_status sekv_tier_last_copy(sekv_tier *tier, int64_t *bytes, int32_
  *   cache   device arrays as for sekv_decode_step; cache->factors and cache->block_off
  *           are not read (the host arena replaces them)
  *   host    the pinned arena and host tables; a block outside the arena, or an arena
- *           that is not pinned, is an SEKV_ERR_INVALID_ARG
+ *           that is not pinned, device-mapped memory, is an SEKV_ERR_INVALID_ARG
  *   sel     device int32 [B][Hkv][top_k]; out device [B][Hq][d] in out_dtype
  *   ws      workspace of sekv_workspace_size(dims)
  *   main    stream of the kernels; side: stream of the host-to-device copies (both at the

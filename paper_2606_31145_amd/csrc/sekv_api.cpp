@@ -401,6 +401,9 @@ struct sekv_tier {
     size_t staging_bytes;
     int32_t *h_sel;             // pinned [B][Hkv][k]: selection read back per sequence
     int64_t *h_off;             // pinned [B][Hkv][M_max]: staging offsets of the selected blocks
+    sekv::GatherChunk *h_chunks;        // pinned [B][chunks_per_seq]: gather pieces per sequence
+    sekv::GatherChunk *h_chunks_dev;    // its device mapping
+    size_t chunks_per_seq;
     void *d_mem;                // one device allocation: offsets | logits | staging
     int64_t *d_off;             // [B][Hkv][M_max]
     float *d_logits;            // [B][Hq][M_max]
@@ -436,6 +439,14 @@ sekv_status sekv_tier_create(const sekv_dims *dims, sekv_tier **tier) {
     e = hipHostMalloc(reinterpret_cast<void **>(&t->h_off), B * Hkv * M * sizeof(int64_t), hipHostMallocDefault);
     if (e != hipSuccess) return cleanup(e, "pinned offset table");
     std::memset(t->h_off, 0, B * Hkv * M * sizeof(int64_t));
+    // every block fits a slot, so a sequence moves at most Hkv k slots of bytes in runs
+    // that each add at most one partial chunk
+    t->chunks_per_seq = Hkv * k * ((t->slot_bytes + sekv::kGatherChunk - 1) / sekv::kGatherChunk + 1);
+    e = hipHostMalloc(reinterpret_cast<void **>(&t->h_chunks), B * t->chunks_per_seq * sizeof(sekv::GatherChunk),
+                      hipHostMallocMapped);
+    if (e != hipSuccess) return cleanup(e, "pinned gather table");
+    e = hipHostGetDevicePointer(reinterpret_cast<void **>(&t->h_chunks_dev), t->h_chunks, 0);
+    if (e != hipSuccess) return cleanup(e, "device mapping of the gather table");
     const size_t off_bytes = sekv::align256(B * Hkv * M * sizeof(int64_t));
     const size_t lg_bytes = sekv::align256(B * Hq * M * sizeof(float));
     e = hipMalloc(&t->d_mem, off_bytes + lg_bytes + t->staging_bytes);
@@ -477,6 +488,7 @@ sekv_status sekv_tier_destroy(sekv_tier *t) {
     if (t->d_mem) (void)hipFree(t->d_mem);
     if (t->h_sel) (void)hipHostFree(t->h_sel);
     if (t->h_off) (void)hipHostFree(t->h_off);
+    if (t->h_chunks) (void)hipHostFree(t->h_chunks);
     delete t;
     return SEKV_OK;
 }
@@ -509,10 +521,13 @@ sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_cache *cac
     if (host->arena_bytes <= 0) return fail(SEKV_ERR_INVALID_ARG, "arena_bytes <= 0");
     if (!out || (dims->top_k > 0 && !sel)) return fail(SEKV_ERR_INVALID_ARG, "sel/out is NULL");
     hipPointerAttribute_t attr{};
-    if (hipPointerGetAttributes(&attr, host->arena) != hipSuccess || attr.type != hipMemoryTypeHost) {
+    if (hipPointerGetAttributes(&attr, host->arena) != hipSuccess || attr.type != hipMemoryTypeHost ||
+        !attr.devicePointer) {
         (void)hipGetLastError();
-        return fail(SEKV_ERR_INVALID_ARG, "the host factor arena is not pinned (hipHostMalloc) memory");
+        return fail(SEKV_ERR_INVALID_ARG, "the host factor arena is not pinned, device-mapped memory");
     }
+    // the gather kernel reads the arena through its device mapping
+    const unsigned char *arena_dev = static_cast<const unsigned char *>(attr.devicePointer);
     const int B = dims->batch, Hkv = dims->n_kv_heads, Hq = dims->n_q_heads, k = dims->top_k;
     const int M = dims->max_spans, d = dims->head_dim;
     const size_t oe = dims->out_dtype == SEKV_F32 ? 4 : 2;
@@ -587,25 +602,33 @@ sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_cache *cac
                 pos += int64_t(sekv::align256(size_t(x.len)));
                 t->h_off[(size_t(b) * Hkv + x.g) * M + x.s] = x.slot;
             }
+            // runs of neighbouring blocks, cut into gather chunks
+            sekv::GatherChunk *ch = t->h_chunks + size_t(b) * t->chunks_per_seq;
+            size_t n_ch = 0;
             for (size_t i = 0; i < blks.size();) {
                 size_t j = i + 1;
                 while (j < blks.size() &&
                        blks[j].src == blks[j - 1].src + int64_t(sekv::align256(size_t(blks[j - 1].len))))
                     ++j;
                 const int64_t len = (blks[j - 1].src - blks[i].src) + blks[j - 1].len;
-                if (first) {
-                    he = hipEventRecord(t->ev_t0, side);
-                    if (he != hipSuccess) return hip_fail(he, "copy timing event");
-                    first = false;
+                for (int64_t o = 0; o < len; o += sekv::kGatherChunk) {
+                    if (n_ch == t->chunks_per_seq)
+                        return fail(SEKV_ERR_INVALID_ARG, "gather table overflow (sequence %d)", b);
+                    const int64_t n = std::min<int64_t>(sekv::kGatherChunk, len - o);
+                    ch[n_ch++] = sekv::GatherChunk{blks[i].src + o, blks[i].slot + o, n, 0};
                 }
-                he = hipMemcpyAsync(t->d_staging + blks[i].slot,
-                                    static_cast<const unsigned char *>(host->arena) + blks[i].src,
-                                    size_t(len), hipMemcpyHostToDevice, side);
-                if (he != hipSuccess) return hip_fail(he, "factor block copy");
                 bytes += len;
                 ++copies;
                 i = j;
             }
+            if (first && n_ch > 0) {
+                he = hipEventRecord(t->ev_t0, side);
+                if (he != hipSuccess) return hip_fail(he, "copy timing event");
+                first = false;
+            }
+            he = sekv::launch_gather(arena_dev, t->d_staging, t->h_chunks_dev + size_t(b) * t->chunks_per_seq,
+                                     int(n_ch), side);
+            if (he != hipSuccess) return hip_fail(he, "factor gather launch");
             he = hipMemcpyAsync(t->d_off + size_t(b) * Hkv * M, t->h_off + size_t(b) * Hkv * M,
                                 size_t(Hkv) * M * sizeof(int64_t), hipMemcpyHostToDevice, side);
             if (he == hipSuccess) he = hipEventRecord(t->ev_copy[b], side);

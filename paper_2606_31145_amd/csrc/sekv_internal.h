@@ -131,9 +131,20 @@ struct Params {
     uint64_t *part_ml, *part_o;
 };
 
+// One piece of a host-to-device gather: bytes (a multiple of 16, at most kGatherChunk)
+// from src (offset into the pinned host arena) to dst (offset into device staging), both
+// 16-byte aligned.
+constexpr int kGatherChunk = 32768;
+struct GatherChunk {
+    int64_t src, dst, bytes, pad;
+};
+
 // Launchers (sekv_kernels.hip).  Return the HIP error of the launch.
 hipError_t launch_step(const Params &p, int dtype, int head_dim, int group, hipStream_t stream);
 hipError_t launch_zero(void *ptr, size_t bytes, hipStream_t stream);
+// src: device mapping of pinned host memory; chunks: device-readable (pinned host) table.
+hipError_t launch_gather(const void *src, void *dst, const GatherChunk *chunks, int n_chunks,
+                         hipStream_t stream);
 int resident_workgroups(int dtype, int head_dim, int group);
 
 }  // namespace sekv
