@@ -31,13 +31,15 @@ def build(verbose: bool = False) -> str:
     bdir = os.path.join(PKG, "_build")
     os.makedirs(bdir, exist_ok=True)
     k_obj = os.path.join(bdir, "sekv_kernels.o")
+    t_obj = os.path.join(bdir, "sekv_tier.o")
     a_obj = os.path.join(bdir, "sekv_api.o")
-    _run([HIPCC, *COMMON, f"--offload-arch={ARCH}", *DEVICE_FLAGS, "-c",
-          os.path.join(CSRC, "sekv_kernels.hip"), "-o", k_obj], verbose)
+    for src, obj in (("sekv_kernels.hip", k_obj), ("sekv_tier.hip", t_obj)):
+        _run([HIPCC, *COMMON, f"--offload-arch={ARCH}", *DEVICE_FLAGS, "-c",
+              os.path.join(CSRC, src), "-o", obj], verbose)
     _run([HIPCC, *COMMON, f"--offload-arch={ARCH}", "-c", os.path.join(CSRC, "sekv_api.cpp"), "-o", a_obj],
          verbose)
     tmp = LIB_PATH + ".tmp"
-    _run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", k_obj, a_obj, "-o", tmp], verbose)
+    _run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", k_obj, t_obj, a_obj, "-o", tmp], verbose)
     os.replace(tmp, LIB_PATH)
     return LIB_PATH
 
