@@ -19,6 +19,8 @@ constexpr int kZoomBlock = 512;    // tokens of a zoomed span scored per LDS pas
 constexpr int kMaxTopK = 64;
 constexpr int kMergeBuf = 512;     // candidates ranked in LDS by one workgroup
 constexpr int kMaxSpans = 65536;   // max_spans limit (span indices and record sizes)
+constexpr int kShareTarget = 512;  // share items per launch above which a share item
+                                   // zooms several selection slots
 
 enum Mode : int32_t { kModeRoute = 0, kModeAttend = 1, kModeFused = 2 };
 
@@ -56,7 +58,8 @@ struct Shape {
     int n_rc;     // routing chunks per pair
     int kc;       // candidates kept per routing chunk = min(k, kRouteChunk)
     int n_cand;   // candidates per pair = n_rc * kc
-    int n_zi;     // share items (and partials) per pair = max(k, 1)
+    int n_zi;     // share items (and partials) per pair; share item j zooms the spans
+                  // of ranks j, j + n_zi, ... below k
 };
 
 inline int elem_bytes(int dtype) { return dtype == SEKV_BF16 ? 2 : 4; }
@@ -70,7 +73,13 @@ inline Shape make_shape(const sekv_dims &d) {
     s.n_rc = (s.M_max + kRouteChunk - 1) / kRouteChunk;
     s.kc = s.k < kRouteChunk ? s.k : kRouteChunk;
     s.n_cand = s.n_rc * s.kc;
+    // one share item per selection slot while the pairs leave room for that; with many
+    // pairs, fewer items per pair so the launch runs about one round of share items.
+    // The split depends only on the shapes, so results are the same bits on any device.
+    const int P1 = s.P > 0 ? s.P : 1;
+    const int fit = (kShareTarget + P1 - 1) / P1;
     s.n_zi = s.k > 1 ? s.k : 1;
+    if (s.n_zi > fit) s.n_zi = fit;
     return s;
 }
 

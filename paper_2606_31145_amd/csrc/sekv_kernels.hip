@@ -280,6 +280,7 @@ struct Smem {
         uint4 cand[kMergeBuf];                           // {~span, key lo, key hi, -}
         uint32_t rk[NT];                                 // partial ranks (two scanners)
         int32_t sel[kMaxTopK];                           // the pair's selected spans
+        int4 zi[kMaxTopK];                               // {span, |S|, offset lo, hi} per rank
         float w[G][kMaxTopK];                            // scale*log2e*sigma_K*(Vt_K q)
         float zs[G][kZoomBlock];                         // token scores, then weights
         float yr[4][G][kMaxTopK];                        // per-wave partial sums of p^T U_V
@@ -1110,10 +1111,10 @@ __device__ __forceinline__ void count_ahead(uint32_t &rk, const uint4 &o, uint32
 }
 
 // Rank the pair's candidates (LDS): rank = number of candidates ahead in (key desc,
-// span asc).  Ranks below k fill Z.sel; the owner of rank j leaves {span, |S|, offset}
-// in bcast[4..7].  Up to NT/2 candidates, two threads scan half the list each.
+// span asc).  Ranks below k fill Z.sel and Z.zi ({span, |S|, offset}).  Up to NT/2
+// candidates, two threads scan half the list each.
 template <class T, int D, int G>
-__device__ __forceinline__ void rank_candidates(const Params &p, Smem<T, D, G> &sm, int j, int m_b,
+__device__ __forceinline__ void rank_candidates(const Params &p, Smem<T, D, G> &sm, int m_b,
                                                 const uint64_t (&okey)[kOwn], const uint32_t (&oidx)[kOwn],
                                                 const int32_t (&olen)[kOwn], const int64_t (&ooff)[kOwn],
                                                 int tid) {
@@ -1149,12 +1150,8 @@ __device__ __forceinline__ void rank_candidates(const Params &p, Smem<T, D, G> &
             const int r = int(Z.rk[tid] + Z.rk[tid + NT / 2]);
             if (r < k && r < m_b) {
                 Z.sel[r] = int32_t(oidx[0]);
-                if (r == j) {
-                    sm.bcast[4] = int32_t(oidx[0]);
-                    sm.bcast[5] = olen[0];
-                    sm.bcast[6] = int32_t(ooff[0] & 0xFFFFFFFF);
-                    sm.bcast[7] = int32_t(ooff[0] >> 32);
-                }
+                Z.zi[r] = make_int4(int32_t(oidx[0]), olen[0], int32_t(ooff[0] & 0xFFFFFFFF),
+                                    int32_t(ooff[0] >> 32));
             }
         }
     } else {
@@ -1175,12 +1172,8 @@ __device__ __forceinline__ void rank_candidates(const Params &p, Smem<T, D, G> &
             for (; o < n_cand; ++o) count_ahead(rk, Z.cand[o], m0, m1, m2);
             if (int(rk) < k && int(rk) < m_b) {
                 Z.sel[rk] = int32_t(oidx[u]);
-                if (int(rk) == j) {
-                    sm.bcast[4] = int32_t(oidx[u]);
-                    sm.bcast[5] = olen[u];
-                    sm.bcast[6] = int32_t(ooff[u] & 0xFFFFFFFF);
-                    sm.bcast[7] = int32_t(ooff[u] >> 32);
-                }
+                Z.zi[rk] = make_int4(int32_t(oidx[u]), olen[u], int32_t(ooff[u] & 0xFFFFFFFF),
+                                     int32_t(ooff[u] >> 32));
             }
         }
     }
@@ -1418,9 +1411,8 @@ __device__ __forceinline__ void share_item(const Params &p, Smem<T, D, G> &sm, i
         Z.qf[hl][d] = T::load1(p.q, (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d);
     }
     online_reset(G, sm.m_run, sm.l_run, sm.scale_old, tid);
-    for (int t = tid; t < kMaxTopK; t += NT) Z.sel[t] = -1;
+    for (int t = tid; t < kMaxTopK; t += NT) { Z.sel[t] = -1; Z.zi[t] = make_int4(-1, 0, 0, 0); }
     for (int i = tid; i < 4 * G * D; i += NT) (&sm.red[0][0][0])[i] = 0.0f;
-    if (tid == 0) { sm.bcast[4] = -1; sm.bcast[5] = 0; sm.bcast[6] = 0; sm.bcast[7] = 0; }
     __syncthreads();
     // valid rows of the prefetched blocks
     const int nc0 = max(0, min(min(CB, c_hi - c_lo), m_b - c_lo));
@@ -1458,8 +1450,8 @@ __device__ __forceinline__ void share_item(const Params &p, Smem<T, D, G> &sm, i
             }
             __builtin_amdgcn_s_sleep(2);
         }
-        if (done) rank_candidates<T, D, G>(p, sm, j, m_b, okey, oidx, olen, ooff, tid);
-        if (tid == 0 && j < k && p.sel_out) p.sel_out[size_t(pair) * k + j] = sm.bcast[4];
+        if (done) rank_candidates<T, D, G>(p, sm, m_b, okey, oidx, olen, ooff, tid);
+        if (tid < k && tid % nz == j && p.sel_out) p.sel_out[size_t(pair) * k + tid] = Z.sel[tid];
     } else {
         if (p.mode == kModeFused) {
             // single merger: wait for the pair's selection records
@@ -1477,73 +1469,78 @@ __device__ __forceinline__ void share_item(const Params &p, Smem<T, D, G> &sm, i
                 const int32_t *zr = reinterpret_cast<const int32_t *>(&p.zrec[size_t(pair) * k + tid]);
                 const int s = ld_shared(zr);
                 Z.sel[tid] = s;
-                if (tid == j) {
-                    sm.bcast[4] = s;
-                    sm.bcast[5] = ld_shared(zr + 1);
-                    sm.bcast[6] = ld_shared(zr + 2);
-                    sm.bcast[7] = ld_shared(zr + 3);
-                }
+                if (tid % nz == j) Z.zi[tid] = make_int4(s, ld_shared(zr + 1), ld_shared(zr + 2), ld_shared(zr + 3));
             }
         } else if (tid < k) {
             // the caller's selection
             int s = p.sel_in[size_t(pair) * k + tid];
             if (s >= m_b) { flag_error(p, kErrSelRange); s = -1; }
             Z.sel[tid] = s;
-            if (tid == j && s >= 0) {
+            if (tid % nz == j && s >= 0) {
                 const int64_t off = p.block_off[pr * p.M_max + s];
-                sm.bcast[4] = s;
-                sm.bcast[5] = p.span_len[size_t(b) * p.M_max + s];
-                sm.bcast[6] = int32_t(off & 0xFFFFFFFF);
-                sm.bcast[7] = int32_t(off >> 32);
+                Z.zi[tid] = make_int4(s, p.span_len[size_t(b) * p.M_max + s], int32_t(off & 0xFFFFFFFF),
+                                      int32_t(off >> 32));
             }
         }
         if (nc0 > 0) wait_coarse_logits<T, D, G>(p, sm, pair, c_lo, nc0, tag, tid);
         else __syncthreads();
     }
-    // the zoomed span's block must lie inside the factor arena
-    if (tid == 0) {
-        int S = sm.bcast[4];
-        if (S >= 0) {
-            const int L = sm.bcast[5];
-            const int64_t off = int64_t(uint32_t(sm.bcast[6])) | (int64_t(sm.bcast[7]) << 32);
+    // the zoomed spans' blocks must lie inside the factor arena
+    if (tid < k && tid % nz == j) {
+        const int4 zi = Z.zi[tid];
+        if (zi.x >= 0) {
+            const int L = zi.y;
+            const int64_t off = int64_t(uint32_t(zi.z)) | (int64_t(zi.w) << 32);
             const int64_t bytes = (2 * int64_t(L) * r + 2 * r + 2 * int64_t(r) * D) * T::kBytes;
             if (L < 1 || off < 0 || (off & 15) || off + bytes > p.factors_bytes) {
                 flag_error(p, kErrBlockRange);
-                S = -1;
+                Z.zi[tid].x = -1;
             }
         }
-        sm.bcast[4] = S;
     }
     __syncthreads();
-    const int S = sm.bcast[4];
-    const int L = sm.bcast[5];
-    const int64_t off = int64_t(uint32_t(sm.bcast[6])) | (int64_t(sm.bcast[7]) << 32);
 
-    // 4. zoom the slot's span; its factor loads are in flight while the first summary
-    //    block is folded
+    // 4. zoom the slot's spans (ranks j, j + n_zi, ...).  With one span, the first
+    //    summary block is folded while its factor loads are in flight; with several,
+    //    it is folded first, so its rows are not held in registers across the zooms.
     auto coarse0 = [&]() {
         if (nc0 > 0) coarse_block<T, D, G, NJ>(sm, cv, c_lo, nc0, k, pend, rgrp, tid);
     };
-    if (S >= 0) {
+    auto zoom_one = [&](int L, int64_t off, int tid, auto &&mid) {
         // 16-byte vectors per U row: rank 8..64 gives 1..8 (bf16) or 2..16 (f32)
         const int ru = r * T::kBytes / 16;
         if constexpr (T::kBytes == 2) {
             switch (ru) {
-                case 1: zoom_span<T, D, G, 1>(p, sm, L, off, pend, tid, coarse0); break;
-                case 2: zoom_span<T, D, G, 2>(p, sm, L, off, pend, tid, coarse0); break;
-                case 4: zoom_span<T, D, G, 4>(p, sm, L, off, pend, tid, coarse0); break;
-                default: zoom_span<T, D, G, 8>(p, sm, L, off, pend, tid, coarse0); break;
+                case 1: zoom_span<T, D, G, 1>(p, sm, L, off, pend, tid, mid); break;
+                case 2: zoom_span<T, D, G, 2>(p, sm, L, off, pend, tid, mid); break;
+                case 4: zoom_span<T, D, G, 4>(p, sm, L, off, pend, tid, mid); break;
+                default: zoom_span<T, D, G, 8>(p, sm, L, off, pend, tid, mid); break;
             }
         } else {
             switch (ru) {
-                case 2: zoom_span<T, D, G, 2>(p, sm, L, off, pend, tid, coarse0); break;
-                case 4: zoom_span<T, D, G, 4>(p, sm, L, off, pend, tid, coarse0); break;
-                case 8: zoom_span<T, D, G, 8>(p, sm, L, off, pend, tid, coarse0); break;
-                default: zoom_span<T, D, G, 16>(p, sm, L, off, pend, tid, coarse0); break;
+                case 2: zoom_span<T, D, G, 2>(p, sm, L, off, pend, tid, mid); break;
+                case 4: zoom_span<T, D, G, 4>(p, sm, L, off, pend, tid, mid); break;
+                case 8: zoom_span<T, D, G, 8>(p, sm, L, off, pend, tid, mid); break;
+                default: zoom_span<T, D, G, 16>(p, sm, L, off, pend, tid, mid); break;
             }
         }
+    };
+    if (j + nz >= k) {
+        const int4 zi = Z.zi[j < kMaxTopK ? j : 0];
+        if (j < k && zi.x >= 0)
+            zoom_one(zi.y, int64_t(uint32_t(zi.z)) | (int64_t(zi.w) << 32), tid, coarse0);
+        else
+            coarse0();
     } else {
         coarse0();
+        for (int rk = j; rk < k; rk += nz) {
+            // an opaque copy of the thread index keeps the zoom's per-thread address
+            // arithmetic inside the loop rather than hoisted and alive across it
+            int t;
+            asm volatile("v_mov_b32 %0, %1" : "=v"(t) : "v"(tid));
+            const int4 zi = Z.zi[rk];
+            if (zi.x >= 0) zoom_one(zi.y, int64_t(uint32_t(zi.z)) | (int64_t(zi.w) << 32), t, [] {});
+        }
     }
     // 5. the rest of the summary share (several blocks only when k is small)
     for (int c0 = c_lo + CB; c0 < c_hi && c0 < m_b; c0 += CB) {

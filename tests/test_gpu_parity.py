@@ -73,6 +73,14 @@ def small_cases():
                 span_max=1500, variant="N"),
         _custom("many-spans-merge-rounds", batch=1, n_q_heads=4, n_kv_heads=1, head_dim=64,
                 rank=8, top_k=64, context=70000, dtype="bf16", seed=28, span_min=8, span_max=16),
+        # many (sequence, KV head) pairs: each share item zooms several selection slots
+        # (128 pairs -> 4 items per pair for k = 7; 160 pairs -> 4 items for k = 9)
+        _custom("multi-slot-bf16-k7-ragged", batch=16, n_q_heads=16, n_kv_heads=8, head_dim=64,
+                rank=16, top_k=7, context=2000, n_prefix_anchors=32, window=64, dtype="bf16",
+                seed=29, span_min=16, span_max=160, ragged=True, variant="N"),
+        _custom("multi-slot-f32-k9", batch=40, n_q_heads=8, n_kv_heads=4, head_dim=64, rank=8,
+                top_k=9, context=1200, n_prefix_anchors=16, window=32, dtype="f32", seed=30,
+                span_min=16, span_max=96),
     ]
     return out
 
