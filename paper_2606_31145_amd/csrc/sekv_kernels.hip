@@ -957,13 +957,13 @@ __device__ inline void load_rows(uint4 (&v)[NJ], const unsigned char *base, int 
     }
 }
 
-// One block of na anchor tokens: scores, online softmax, weighted values into sm.red.
+// One block of na anchor tokens, in two halves so that the next block's keys can load
+// while this block's values are used: the scores (into Z.sc), then the online softmax
+// and the weighted values (into sm.red).
 template <class T, int D, int G, int NJ>
-__device__ inline void anchor_block(const Params &p, Smem<T, D, G> &sm, const uint4 (&kr)[NJ],
-                                    const uint4 (&vr)[NJ], int na, float (&pend)[G], int rgrp,
-                                    int col, int tid) {
+__device__ inline void anchor_scores(const Params &p, Smem<T, D, G> &sm, const uint4 (&kr)[NJ], int na,
+                                     int rgrp, int col) {
     using GE = Geo<T, D>;
-    constexpr int AB = Smem<T, D, G>::AB;
     auto &Z = sm.u.share;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
@@ -983,6 +983,14 @@ __device__ inline void anchor_block(const Params &p, Smem<T, D, G> &sm, const ui
             for (int hl = 0; hl < G; ++hl) Z.sc[hl][row] = part[hl] * p.scale_log2;
     }
     __syncthreads();
+}
+
+template <class T, int D, int G, int NJ>
+__device__ inline void anchor_values(Smem<T, D, G> &sm, const uint4 (&vr)[NJ], int na, float (&pend)[G],
+                                     int rgrp, int tid) {
+    using GE = Geo<T, D>;
+    constexpr int AB = Smem<T, D, G>::AB;
+    auto &Z = sm.u.share;
     online_fold(&Z.sc[0][0], AB, na, G, sm.m_run, sm.l_run, sm.scale_old, tid);
     __syncthreads();
     pend_fold<G>(pend, sm.scale_old);
@@ -1422,14 +1430,16 @@ __device__ __forceinline__ void share_item(const Params &p, Smem<T, D, G> &sm, i
 #pragma unroll
     for (int hl = 0; hl < G; ++hl) pend[hl] = 1.0f;
 
-    // 2. the anchor share, while routing runs elsewhere
+    // 2. the anchor share, while routing runs elsewhere; the next block's keys load
+    //    while this block's values are used, its values while the next scores are taken
     for (int a0 = a_lo; a0 < a_hi && a0 < An; a0 += AB) {
         const int na = min(min(AB, a_hi - a0), An - a0);
-        if (a0 != a_lo) {
-            load_rows<T, D, NJ>(kr, ak + size_t(a0) * GE::RB, na, rgrp, col);
-            load_rows<T, D, NJ>(vr, av + size_t(a0) * GE::RB, na, rgrp, col);
-        }
-        anchor_block<T, D, G, NJ>(p, sm, kr, vr, na, pend, rgrp, col, tid);
+        const int a1 = a0 + AB;
+        const int na1 = (a1 < a_hi && a1 < An) ? min(min(AB, a_hi - a1), An - a1) : 0;
+        anchor_scores<T, D, G, NJ>(p, sm, kr, na, rgrp, col);
+        load_rows<T, D, NJ>(kr, ak + size_t(a1) * GE::RB, na1, rgrp, col);
+        anchor_values<T, D, G, NJ>(sm, vr, na, pend, rgrp, tid);
+        load_rows<T, D, NJ>(vr, av + size_t(a1) * GE::RB, na1, rgrp, col);
     }
 
     // 3. the selection (Z.sel, this slot's span in bcast) and the first block's logits
