@@ -53,6 +53,10 @@ constexpr int CR = kRouteChunk;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr double kLog2eD = 1.4426950408889634074;
 constexpr uint32_t kSpinLimit = 1u << 22;
+// A share item that starts with the launch holds its first loads back by this many
+// s_sleep units (64 cycles each, about 1 us) so that the routing items' summary-key
+// loads, which the selection waits for, reach memory first.
+constexpr int kShareHoldBack = 40;
 constexpr uint32_t kInvalidIdx = 0xFFFFFFFFu;
 
 // ---------------------------------------------------------------------------
@@ -1384,7 +1388,7 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
 __device__ __forceinline__ void share_item(const Params &p, Smem<T, D, G> &sm, int pair, int j,
-                                           uint32_t tag, int tid) {
+                                           uint32_t tag, int tid, bool first) {
     using GE = Geo<T, D>;
     using SM = Smem<T, D, G>;
     constexpr int NJ = SM::NJ, AB = SM::AB, CB = SM::CB;
@@ -1404,6 +1408,7 @@ __device__ __forceinline__ void share_item(const Params &p, Smem<T, D, G> &sm, i
     const unsigned char *av = reinterpret_cast<const unsigned char *>(p.anchor_v) + pr * p.A_max * GE::RB;
     const unsigned char *sv = reinterpret_cast<const unsigned char *>(p.sum_v) + pr * p.M_max * GE::RB;
 
+    if (first && p.end_route > 0) __builtin_amdgcn_s_sleep(kShareHoldBack);
     // 1. loads that depend on nothing: the first anchor block, the first summary block
     //    (values only; its logits come from routing), the query
     uint4 kr[NJ], vr[NJ], cv[NJ];
@@ -1585,7 +1590,7 @@ __global__ void __launch_bounds__(NT, 2) sekv_step_kernel(Params p) {
             route_item<T, D, G>(p, sm, item / p.n_rc, item % p.n_rc, tag, t);
         } else {
             const int i = item - p.end_route;
-            share_item<T, D, G>(p, sm, i / p.n_zi, i % p.n_zi, tag, t);
+            share_item<T, D, G>(p, sm, i / p.n_zi, i % p.n_zi, tag, t, item == int(blockIdx.x));
         }
         __syncthreads();
     }
