@@ -183,3 +183,18 @@ def test_config3_full_size(S, variant):
     assert np.array_equal(sel.cpu().numpy(), ref["sel"]), \
         f"selection differs; min boundary gap {min_boundary_gap(ref, case):.3e}"
     assert_out_close(out_to_f64(out), ref["out"], "bf16", where=f"config 3 {variant}")
+    # the launch configuration the bench times: graph replays over cache copies, each
+    # node the same kernel on its own copy; every node must give the stream launch's bits
+    banner("config 3: graph replays over two cache copies")
+    copy = S.DeviceCache({k: v.clone() for k, v in dc.t.items()}, case.dtype)
+    g = S.LayerGraph(dims, [dc, copy], ws)
+    try:
+        for _ in range(3):
+            gsel, gout = g.launch()
+            torch.cuda.synchronize()
+            assert ws.status() == 0
+            for l in range(2):
+                assert torch.equal(gsel[l], sel), f"graph node {l}: selection differs"
+                assert torch.equal(gout[l], out), f"graph node {l}: output differs"
+    finally:
+        g.destroy()
