@@ -5,11 +5,12 @@
 //           coarse mean key as summary).  It publishes every span's score (the coarse
 //           logit) and, when the step selects, the chunk's local top-k as sorted
 //           candidate records.  It waits for nothing.
-//   share   selection slot j of a pair (j < max(k, 1)).  While routing runs it attends
-//           to its share of the anchor tokens; then it ranks the pair's candidates
-//           (Sec. 3.3 budget rule: decreasing routing score, here top-k), takes the j-th
-//           span and attends to its tokens through the factors, K_hat = U diag(sigma) V^T
-//           (eq. key_reconstruction), never forming K_hat in memory; while the factor
+//   share   share slot j of a pair (j < n_zi, n_zi = min(k, about 512 / pairs), at
+//           least 1).  While routing runs it attends to its share of the anchor tokens;
+//           then it ranks the pair's candidates (Sec. 3.3 budget rule: decreasing routing
+//           score, here top-k), takes the spans of ranks j, j + n_zi, ... and attends to
+//           their tokens through the factors, K_hat = U diag(sigma) V^T (eq.
+//           key_reconstruction), never forming K_hat in memory; while the first factor
 //           loads are in flight it folds its share of the summaries, skipping the
 //           selected spans, so every span enters the softmax once: zoomed or coarse.
 // Each share item leaves one partial (max, sum, weighted value sum per head) in a fixed
