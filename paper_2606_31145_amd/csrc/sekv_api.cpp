@@ -169,6 +169,13 @@ sekv_status prepare(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *
     const int n_share = (mode == sekv::kModeRoute) ? 0 : s.P * s.n_zi;
     p.end_route = n_route;
     p.end_share = n_route + n_share;
+    // Share items run slot-major after the routing items.  When the first round of items
+    // ends inside the share items, the slots that start in it take all the anchors, and
+    // the slots that start later (after a routing item) only select, zoom and fold
+    // summaries.
+    p.n_early = s.n_zi;
+    const int first = sekv::kRoundItems - n_route;
+    if (n_share > 0 && first >= s.P && first < n_share) p.n_early = first / s.P;
     p.out_f32 = d->out_dtype == SEKV_F32;
     p.zoom_impl = (d->flags & 3) == SEKV_ZOOM_DEFAULT ? SEKV_ZOOM_FACTORED : (d->flags & 3);
     p.scale = d->softmax_scale;

@@ -21,6 +21,9 @@ constexpr int kMergeBuf = 512;     // candidates ranked in LDS by one workgroup
 constexpr int kMaxSpans = 65536;   // max_spans limit (span indices and record sizes)
 constexpr int kShareTarget = 512;  // share items per launch above which a share item
                                    // zooms several selection slots
+constexpr int kRoundItems = 512;   // items a launch starts at once on a 256-CU device at
+                                   // two workgroups per CU (used only to split the work;
+                                   // a constant, so the split never depends on the device)
 
 enum Mode : int32_t { kModeRoute = 0, kModeAttend = 1, kModeFused = 2 };
 
@@ -108,6 +111,7 @@ struct Params {
     int32_t B, Hq, Hkv, r, k, A_max, M_max;
     int32_t n_rc, kc, n_cand, n_zi;
     int32_t end_route, end_share;                   // item-index ends of each item kind
+    int32_t n_early;                                // share slots j < n_early take the anchors
     int32_t grid;                                   // workgroups in the launch
     int32_t merger;                                 // 1: one workgroup per pair merges the
                                                     // candidates (route mode, or more than

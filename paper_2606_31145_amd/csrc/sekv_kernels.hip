@@ -266,8 +266,9 @@ template <class T, int D, int G>
 struct Smem {
     using GE = Geo<T, D>;
     static constexpr int HPT = (G + 1) / 2;              // routing heads per thread
-    static constexpr int NJ = 4;                          // rows per thread in a block
-    static constexpr int AB = NJ * GE::RPP;               // anchor tokens per block
+    static constexpr int NJ = 4;                          // rows per thread in a summary block
+    static constexpr int NJA = 8;                         // rows per thread in an anchor block
+    static constexpr int AB = NJA * GE::RPP;              // anchor tokens per block
     static constexpr int CB = NJ * GE::RPP;               // summary rows per block
     struct Route {                                       // routing item
         unsigned char kb[CR * GE::RS];                   // summary key rows
@@ -1392,15 +1393,18 @@ __device__ __forceinline__ void share_item(const Params &p, Smem<T, D, G> &sm, i
                                            uint32_t tag, int tid, bool first) {
     using GE = Geo<T, D>;
     using SM = Smem<T, D, G>;
-    constexpr int NJ = SM::NJ, AB = SM::AB, CB = SM::CB;
+    constexpr int NJ = SM::NJ, NJA = SM::NJA, AB = SM::AB, CB = SM::CB;
     auto &Z = sm.u.share;
     const int b = pair / p.Hkv, g = pair % p.Hkv;
     const int k = p.k, r = p.r, nz = p.n_zi;
     // this item's shares: contiguous ranges of the anchor and span index spaces up to
     // the maxima, so the first loads need no table value; the sequence's own counts
     // (n_anchors, n_spans) mask rows where the values are used
-    const int as = (p.A_max + nz - 1) / nz;
-    const int a_lo = min(p.A_max, j * as), a_hi = min(p.A_max, a_lo + as);
+    // anchors go to the slots that start with the launch (j < n_early): they fold them
+    // while routing runs, and later slots reach their selection and zoom sooner
+    const int ne = p.n_early;
+    const int as = (p.A_max + ne - 1) / ne;
+    const int a_lo = j < ne ? min(p.A_max, j * as) : p.A_max, a_hi = min(p.A_max, a_lo + as);
     const int cs = (p.M_max + nz - 1) / nz;
     const int c_lo = min(p.M_max, j * cs), c_hi = min(p.M_max, c_lo + cs);
     const int rgrp = tid / GE::RV, col = tid % GE::RV;
@@ -1412,9 +1416,9 @@ __device__ __forceinline__ void share_item(const Params &p, Smem<T, D, G> &sm, i
     if (first && p.end_route > 0) __builtin_amdgcn_s_sleep(kShareHoldBack);
     // 1. loads that depend on nothing: the first anchor block, the first summary block
     //    (values only; its logits come from routing), the query
-    uint4 kr[NJ], vr[NJ], cv[NJ];
-    load_rows<T, D, NJ>(kr, ak + size_t(a_lo) * GE::RB, min(AB, a_hi - a_lo), rgrp, col);
-    load_rows<T, D, NJ>(vr, av + size_t(a_lo) * GE::RB, min(AB, a_hi - a_lo), rgrp, col);
+    uint4 kr[NJA], vr[NJA], cv[NJ];
+    load_rows<T, D, NJA>(kr, ak + size_t(a_lo) * GE::RB, min(AB, a_hi - a_lo), rgrp, col);
+    load_rows<T, D, NJA>(vr, av + size_t(a_lo) * GE::RB, min(AB, a_hi - a_lo), rgrp, col);
     load_rows<T, D, NJ>(cv, sv + size_t(c_lo) * GE::RB, min(CB, c_hi - c_lo), rgrp, col);
     int m_b = p.n_spans[b];
     m_b = m_b < 0 ? 0 : (m_b > p.M_max ? p.M_max : m_b);
@@ -1442,10 +1446,10 @@ __device__ __forceinline__ void share_item(const Params &p, Smem<T, D, G> &sm, i
         const int na = min(min(AB, a_hi - a0), An - a0);
         const int a1 = a0 + AB;
         const int na1 = (a1 < a_hi && a1 < An) ? min(min(AB, a_hi - a1), An - a1) : 0;
-        anchor_scores<T, D, G, NJ>(p, sm, kr, na, rgrp, col);
-        load_rows<T, D, NJ>(kr, ak + size_t(a1) * GE::RB, na1, rgrp, col);
-        anchor_values<T, D, G, NJ>(sm, vr, na, pend, rgrp, tid);
-        load_rows<T, D, NJ>(vr, av + size_t(a1) * GE::RB, na1, rgrp, col);
+        anchor_scores<T, D, G, NJA>(p, sm, kr, na, rgrp, col);
+        load_rows<T, D, NJA>(kr, ak + size_t(a1) * GE::RB, na1, rgrp, col);
+        anchor_values<T, D, G, NJA>(sm, vr, na, pend, rgrp, tid);
+        load_rows<T, D, NJA>(vr, av + size_t(a1) * GE::RB, na1, rgrp, col);
     }
 
     // 3. the selection (Z.sel, this slot's span in bcast) and the first block's logits
@@ -1590,8 +1594,9 @@ __global__ void __launch_bounds__(NT, 2) sekv_step_kernel(Params p) {
         if (item < p.end_route) {
             route_item<T, D, G>(p, sm, item / p.n_rc, item % p.n_rc, tag, t);
         } else {
-            const int i = item - p.end_route;
-            share_item<T, D, G>(p, sm, i / p.n_zi, i % p.n_zi, tag, t, item == int(blockIdx.x));
+            const int i = item - p.end_route;                // slot-major
+            const int P = p.B * p.Hkv;
+            share_item<T, D, G>(p, sm, i % P, i / P, tag, t, item == int(blockIdx.x));
         }
         __syncthreads();
     }
