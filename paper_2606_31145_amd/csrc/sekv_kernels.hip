@@ -1249,9 +1249,10 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
         const int tok = min((tid + NT * u) / RU, nb0 - 1);
         uv[u] = ld16(UV + size_t(tok) * R * T::kBytes + ucol * 16);
     }
-    __syncthreads();
 
-    // w[h][i] = scale*log2e * sigma_K[i] * (Vt_K[i] . q_h)
+    // w[h][i] = scale*log2e * sigma_K[i] * (Vt_K[i] . q_h).  No barrier first: Z.w was
+    // last read by an earlier zoom, which has passed several barriers since, and the
+    // query rows (Z.qf) were written at the start of the item.
 #pragma unroll
     for (int u = 0; u < NVT; ++u) {
         const int vi = tid + NT * u;
@@ -1340,7 +1341,7 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
                 }
             }
         }
-        __syncthreads();
+        if (t0 + NB < L) __syncthreads();               // Z.zs and scale_old are reused
     }
     // y[h][i]: sum yacc over the lanes sharing ucol, then over the waves
 #pragma unroll

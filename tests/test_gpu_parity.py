@@ -81,6 +81,11 @@ def small_cases():
         _custom("multi-slot-f32-k9", batch=40, n_q_heads=8, n_kv_heads=4, head_dim=64, rank=8,
                 top_k=9, context=1200, n_prefix_anchors=16, window=32, dtype="f32", seed=30,
                 span_min=16, span_max=96),
+        # 256 pairs x 2 routing chunks fill a whole round of routing items, so every share
+        # item starts after one; two share items per pair zoom ranks {0, 2, 4} and {1, 3}
+        _custom("full-route-round-bf16-k5", batch=32, n_q_heads=16, n_kv_heads=8, head_dim=64,
+                rank=16, top_k=5, context=3500, n_prefix_anchors=32, window=64, dtype="bf16",
+                seed=33, span_min=16, span_max=32, variant="N"),
     ]
     return out
 
