@@ -169,6 +169,45 @@ def test_workspace_reuse_across_shapes(S):
     assert ws.status() == 0
 
 
+def test_block_outside_arena_is_skipped_and_flagged(S):
+    """A selected span whose block offset points past the factor arena: the kernels do
+    not read it (no fault), set the block-range bit of the error word, keep the
+    selection, and leave every other (sequence, KV head) pair's output bit for bit."""
+    import torch
+    banner("block outside the arena: fused step and route + attend")
+    dev = torch.device("cuda:0")
+    case = make_case(custom_spec(batch=2, n_q_heads=8, n_kv_heads=2, head_dim=64, rank=16,
+                                 top_k=3, context=2500, dtype="bf16", seed=34, span_min=32,
+                                 span_max=160), variant="N")
+    dims = dims_for(S, case)
+    ws = S.Workspace(dims, dev)
+    dc = S.DeviceCache.from_arrays(case_arrays(case), case.dtype, dev)
+    sel0, out0 = S.decode_step(dims, dc, ws)
+    torch.cuda.synchronize()
+    assert ws.status() == 0
+    sel0 = sel0.cpu().numpy()
+    out0 = out0.cpu()
+    bad = case_arrays(case)
+    bad["block_off"] = case.block_off.copy()
+    s_bad = int(sel0[0, 0, 0])                           # the best span of (b 0, KV head 0)
+    bad["block_off"][0, 0, s_bad] = case.factors.nbytes  # one byte past the end of the arena
+    dcb = S.DeviceCache.from_arrays(bad, case.dtype, dev)
+    G = case.spec.n_q_heads // case.spec.n_kv_heads
+    for how in ("fused", "route+attend"):
+        if how == "fused":
+            sel, out = S.decode_step(dims, dcb, ws)
+        else:
+            sel, logits = S.route_topk(dims, dcb, ws)
+            out = S.zoom_attend(dims, dcb, sel, logits, ws)
+        torch.cuda.synchronize()
+        assert ws.status() & 2, f"{how}: block-range bit not set"
+        assert np.array_equal(sel.cpu().numpy(), sel0), f"{how}: selection changed"
+        o = out.cpu()
+        assert torch.equal(o[0, G:], out0[0, G:]) and torch.equal(o[1], out0[1]), \
+            f"{how}: an unaffected pair's output changed"
+        assert not torch.equal(o[0, :G], out0[0, :G]), f"{how}: the skipped span changed nothing"
+
+
 @pytest.mark.parametrize("variant", ["L", "N"])
 def test_config3_full_size(S, variant):
     """The 128K-context, batch-4 layer at full size: every selection and every output row."""
