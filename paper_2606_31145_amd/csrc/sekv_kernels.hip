@@ -281,6 +281,7 @@ struct Smem {
     };
     struct Share {                                       // share item
         float qf[G][D];
+        uint32_t qb[G][D / 2];                           // the same query, bf16 pairs (bf16 storage)
         float sc[G][AB];                                 // anchor scores, then weights
         float cw[G][CB];                                 // summary logits, then weights
         uint4 cand[kMergeBuf];                           // {~span, key lo, key hi, -}
@@ -312,6 +313,35 @@ struct Smem {
     float m_run[G], l_run[G], scale_old[G];              // online softmax state
     int32_t bcast[8];
 };
+
+// part[h] = sum over the values of 16-byte vector c of a row times query row h: packed
+// bf16 dot products (exact products, fp32 sums) for bf16 storage, fp32 FMAs for fp32.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+template <class T, int D, int G>
+__device__ inline void query_dot(const Smem<T, D, G> &sm, const uint4 &v, int c, float (&part)[G]) {
+    const auto &Z = sm.u.share;
+    if constexpr (T::kBytes == 2) {
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int hl = 0; hl < G; ++hl) {
+            float a = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w[i]),
+                                                    __builtin_bit_cast(bf16x2_t, Z.qb[hl][c * 4 + i]), a, false);
+            part[hl] = a;
+        }
+    } else {
+        float f[T::kVec];
+        T::unpack(v, f);
+#pragma unroll
+        for (int hl = 0; hl < G; ++hl) {
+            part[hl] = 0.0f;
+#pragma unroll
+            for (int e = 0; e < T::kVec; ++e) part[hl] += Z.qf[hl][c * T::kVec + e] * f[e];
+        }
+    }
+}
 
 // ---------------------------------------------------------------------------
 // row-sum helpers: thread (rgrp = tid / RV, col = tid % RV) holds acc[G][VEC]
@@ -974,16 +1004,10 @@ __device__ inline void anchor_scores(const Params &p, Smem<T, D, G> &sm, const u
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
         const int row = rgrp + GE::RPP * j;
-        float f[GE::VEC];
-        T::unpack(kr[j], f);
         float part[G];
+        query_dot<T, D, G>(sm, kr[j], col, part);
 #pragma unroll
-        for (int hl = 0; hl < G; ++hl) {
-            part[hl] = 0.0f;
-#pragma unroll
-            for (int e = 0; e < GE::VEC; ++e) part[hl] += Z.qf[hl][col * GE::VEC + e] * f[e];
-            part[hl] = row_sum<GE::RV>(part[hl]);
-        }
+        for (int hl = 0; hl < G; ++hl) part[hl] = row_sum<GE::RV>(part[hl]);
         if (col == 0 && row < na)
 #pragma unroll
             for (int hl = 0; hl < G; ++hl) Z.sc[hl][row] = part[hl] * p.scale_log2;
@@ -1252,7 +1276,7 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
 
     // w[h][i] = scale*log2e * sigma_K[i] * (Vt_K[i] . q_h).  No barrier first: Z.w was
     // last read by an earlier zoom, which has passed several barriers since, and the
-    // query rows (Z.qf) were written at the start of the item.
+    // query rows (Z.qf / Z.qb) were written at the start of the item.
 #pragma unroll
     for (int u = 0; u < NVT; ++u) {
         const int vi = tid + NT * u;
@@ -1428,6 +1452,10 @@ __device__ __forceinline__ void share_item(const Params &p, Smem<T, D, G> &sm, i
     for (int i = tid; i < G * D; i += NT) {
         const int hl = i / D, d = i % D;
         Z.qf[hl][d] = T::load1(p.q, (size_t(b) * p.Hq + size_t(g) * G + hl) * D + d);
+    }
+    if constexpr (T::kBytes == 2) {
+        const uint32_t *q2 = reinterpret_cast<const uint32_t *>(p.q) + (size_t(b) * p.Hq + size_t(g) * G) * (D / 2);
+        for (int i = tid; i < G * D / 2; i += NT) Z.qb[i / (D / 2)][i % (D / 2)] = q2[i];
     }
     online_reset(G, sm.m_run, sm.l_run, sm.scale_old, tid);
     for (int t = tid; t < kMaxTopK; t += NT) { Z.sel[t] = -1; Z.zi[t] = make_int4(-1, 0, 0, 0); }
