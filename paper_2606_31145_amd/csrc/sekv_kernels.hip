@@ -55,9 +55,9 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr double kLog2eD = 1.4426950408889634074;
 constexpr uint32_t kSpinLimit = 1u << 22;
 // A share item that starts with the launch holds its first loads back by this many
-// s_sleep units (64 cycles each, about 1 us) so that the routing items' summary-key
+// s_sleep units (64 cycles each, about 0.2 us) so that the routing items' summary-key
 // loads, which the selection waits for, reach memory first.
-constexpr int kShareHoldBack = 40;
+constexpr int kShareHoldBack = 8;
 constexpr uint32_t kInvalidIdx = 0xFFFFFFFFu;
 
 // ---------------------------------------------------------------------------
