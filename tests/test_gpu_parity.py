@@ -169,6 +169,36 @@ def test_workspace_reuse_across_shapes(S):
     assert ws.status() == 0
 
 
+# One small case per kernel instantiation (storage type x head_dim x group size), so every
+# compiled variant of the step kernel is checked against the oracle.
+INSTANTIATIONS = [(dt, d, g) for dt in ("bf16", "f32") for d in (64, 128) for g in (1, 2, 4, 8)]
+
+
+@pytest.mark.parametrize("dtype,head_dim,group", INSTANTIATIONS,
+                         ids=[f"{dt}-d{d}-g{g}" for dt, d, g in INSTANTIATIONS])
+def test_every_kernel_instantiation(S, dtype, head_dim, group):
+    import torch
+    banner(f"instantiation {dtype} d{head_dim} G{group}")
+    n_kv = 2
+    case = make_case(custom_spec(batch=2, n_q_heads=n_kv * group, n_kv_heads=n_kv,
+                                 head_dim=head_dim, rank=16, top_k=3, context=1800,
+                                 n_prefix_anchors=24, window=64, dtype=dtype,
+                                 seed=40 + 8 * (dtype == "f32") + 2 * (head_dim == 128) + group,
+                                 span_min=16, span_max=200), variant="N")
+    ref = oracle_result(case)
+    dev = torch.device("cuda:0")
+    dc = S.DeviceCache.from_arrays(case_arrays(case), case.dtype, dev)
+    dims = dims_for(S, case)
+    ws = S.Workspace(dims, dev)
+    sel, out = S.decode_step(dims, dc, ws)
+    torch.cuda.synchronize()
+    assert ws.status() == 0
+    assert np.array_equal(sel.cpu().numpy(), ref["sel"]), \
+        f"selection differs; min boundary gap {min_boundary_gap(ref, case):.3e}"
+    assert_out_close(out_to_f64(out), ref["out"], case.dtype,
+                     where=f"{dtype} d{head_dim} G{group}")
+
+
 def test_block_outside_arena_is_skipped_and_flagged(S):
     """A selected span whose block offset points past the factor arena: the kernels do
     not read it (no fault), set the block-range bit of the error word, keep the
