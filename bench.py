@@ -102,7 +102,7 @@ def main():
 
     from paper_2606_31145_amd import accounting
     from paper_2606_31145_amd import sekv
-    from synth import CONFIGS, make_case
+    from synth import WORKLOADS, make_case
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
@@ -110,7 +110,7 @@ def main():
         return bench_layers32(args, dev)
     if args.workload == "hosttier":
         return bench_hosttier(args, dev)
-    spec = CONFIGS[3]
+    spec = WORKLOADS["llama3-8b-layer-128k-b4"]
     log(f"[bench] generating the 128K x 4 cache (variant {args.variant})")
     t0 = time.time()
     case = make_case(spec, variant=args.variant)
@@ -261,9 +261,9 @@ def bench_layers32(args, dev):
 
     from paper_2606_31145_amd import accounting
     from paper_2606_31145_amd import sekv
-    from synth import CONFIGS, make_case
+    from synth import WORKLOADS, make_case
 
-    spec = CONFIGS[4]
+    spec = WORKLOADS["llama3-8b-32layer-32k-b32"]
     L = spec.n_layers
     D = max(1, min(args.distinct_layers, L))
     t0 = time.time()
@@ -355,9 +355,9 @@ def bench_hosttier(args, dev):
 
     from paper_2606_31145_amd import accounting
     from paper_2606_31145_amd import sekv
-    from synth import CONFIGS, make_case
+    from synth import WORKLOADS, make_case
 
-    spec = CONFIGS[5]
+    spec = WORKLOADS["llama3-8b-layer-128k-b4-hosttier"]
     t0 = time.time()
     case = make_case(spec, variant=args.variant)
     log(f"[bench] generated in {time.time() - t0:.1f}s")

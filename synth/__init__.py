@@ -10,7 +10,7 @@ attention, softmax), and it imports neither the oracle nor the HIP library.
 """
 
 from .cases import (  # noqa: F401
-    CONFIGS,
+    WORKLOADS,
     case_from_factors,
     with_top_k,
     Case,

@@ -207,24 +207,24 @@ class CaseSpec:
         return 1.0 / math.sqrt(self.head_dim)
 
 
-CONFIGS = {
-    1: CaseSpec("tiny-f32", batch=1, n_q_heads=4, n_kv_heads=2, head_dim=64, rank=8,
+WORKLOADS = {
+    "tiny-f32": CaseSpec("tiny-f32", batch=1, n_q_heads=4, n_kv_heads=2, head_dim=64, rank=8,
                 top_k=2, context=2048, n_prefix_anchors=32, window=0,
                 span_dist="uniform", span_min=16, span_max=64, dtype="f32",
                 factor_kind="orthonormal", seed=1),
-    2: CaseSpec("llama3-8b-layer-32k", batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128,
+    "llama3-8b-layer-32k": CaseSpec("llama3-8b-layer-32k", batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128,
                 rank=16, top_k=8, context=32768, n_prefix_anchors=256, window=512,
                 span_dist="uniform", span_min=32, span_max=256, dtype="bf16",
                 factor_kind="gaussian", seed=2),
-    3: CaseSpec("llama3-8b-layer-128k-b4", batch=4, n_q_heads=32, n_kv_heads=8, head_dim=128,
+    "llama3-8b-layer-128k-b4": CaseSpec("llama3-8b-layer-128k-b4", batch=4, n_q_heads=32, n_kv_heads=8, head_dim=128,
                 rank=32, top_k=16, context=131072, n_prefix_anchors=256, window=512,
                 span_dist="loguniform", span_min=32, span_max=512, dtype="bf16",
                 factor_kind="gaussian", seed=3),
-    4: CaseSpec("llama3-8b-32layer-32k-b32", batch=32, n_q_heads=32, n_kv_heads=8,
+    "llama3-8b-32layer-32k-b32": CaseSpec("llama3-8b-32layer-32k-b32", batch=32, n_q_heads=32, n_kv_heads=8,
                 head_dim=128, rank=16, top_k=8, context=32768, n_prefix_anchors=256,
                 window=512, span_dist="uniform", span_min=32, span_max=256, dtype="bf16",
                 factor_kind="gaussian", n_layers=32, seed=4),
-    5: CaseSpec("llama3-8b-layer-128k-b4-hosttier", batch=4, n_q_heads=32, n_kv_heads=8,
+    "llama3-8b-layer-128k-b4-hosttier": CaseSpec("llama3-8b-layer-128k-b4-hosttier", batch=4, n_q_heads=32, n_kv_heads=8,
                 head_dim=128, rank=32, top_k=16, context=131072, n_prefix_anchors=256,
                 window=512, span_dist="loguniform", span_min=32, span_max=512,
                 dtype="bf16", factor_kind="gaussian", seed=3, host_factors=True),

@@ -8,7 +8,7 @@ compared with the eager result."""
 import numpy as np
 import pytest
 
-from synth import CONFIGS, custom_spec, make_case
+from synth import WORKLOADS, custom_spec, make_case
 from tests.gpu_common import (assert_out_close, banner, case_arrays, dims_for, oracle_result,
                               out_to_f64)
 
@@ -81,12 +81,12 @@ def test_graph_small_layers_f32_planted(S):
     _run_graph_case(S, _layers(spec, 3, variant="N"), replays=2)
 
 
-def test_graph_config4_shapes_two_layers(S):
+def test_graph_32layer_b32_shapes_two_layers(S):
     """Two independently seeded layers at the 32-layer workload's per-layer shape
     (batch 32, 32K context, rank 16, top-8)."""
-    banner("graph: config 4 shapes, 2 layers: generating")
-    cases = _layers(CONFIGS[4], 2)
-    banner("graph: config 4 shapes: running")
+    banner("graph: 32-layer batch-32 shapes, 2 layers: generating")
+    cases = _layers(WORKLOADS["llama3-8b-32layer-32k-b32"], 2)
+    banner("graph: 32-layer batch-32 shapes: running")
     _run_graph_case(S, cases, replays=2)
 
 

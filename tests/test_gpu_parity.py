@@ -8,7 +8,7 @@ tiny, near-uniform outputs.  Run on an MI355X with the library built in-tree.
 import numpy as np
 import pytest
 
-from synth import CONFIGS, custom_spec, make_case
+from synth import WORKLOADS, custom_spec, make_case
 from synth.cases import Case
 from tests.gpu_common import (assert_out_close, banner, case_arrays, dims_for, min_boundary_gap,
                               oracle_result, out_to_f64)
@@ -49,10 +49,10 @@ def _custom(name, **kw):
 
 
 def small_cases():
-    out = [("cfg1-L", make_case(CONFIGS[1], variant="L")),
-           ("cfg1-N", make_case(CONFIGS[1], variant="N")),
-           ("cfg2-L", make_case(CONFIGS[2], variant="L")),
-           ("cfg2-N", make_case(CONFIGS[2], variant="N"))]
+    out = [("tiny-f32-L", make_case(WORKLOADS["tiny-f32"], variant="L")),
+           ("tiny-f32-N", make_case(WORKLOADS["tiny-f32"], variant="N")),
+           ("layer-32k-L", make_case(WORKLOADS["llama3-8b-layer-32k"], variant="L")),
+           ("layer-32k-N", make_case(WORKLOADS["llama3-8b-layer-32k"], variant="N"))]
     out += [
         _custom("g1-bf16-d128-r16", n_q_heads=4, n_kv_heads=4, head_dim=128, rank=16, top_k=3,
                 context=3000, dtype="bf16", seed=21, span_min=16, span_max=200),
@@ -239,27 +239,27 @@ def test_block_outside_arena_is_skipped_and_flagged(S):
 
 
 @pytest.mark.parametrize("variant", ["L", "N"])
-def test_config3_full_size(S, variant):
+def test_layer_128k_b4_full_size(S, variant):
     """The 128K-context, batch-4 layer at full size: every selection and every output row."""
     import torch
-    banner(f"config 3 full size, variant {variant}: generating")
-    case = make_case(CONFIGS[3], variant=variant)
-    banner("config 3: oracle")
+    banner(f"128K x 4 full size, variant {variant}: generating")
+    case = make_case(WORKLOADS["llama3-8b-layer-128k-b4"], variant=variant)
+    banner("128K x 4: oracle")
     ref = oracle_result(case)
     dev = torch.device("cuda:0")
     dc = S.DeviceCache.from_arrays(case_arrays(case), case.dtype, dev)
     dims = dims_for(S, case)
     ws = S.Workspace(dims, dev)
-    banner("config 3: decode_step")
+    banner("128K x 4: decode_step")
     sel, out = S.decode_step(dims, dc, ws)
     torch.cuda.synchronize()
     assert ws.status() == 0
     assert np.array_equal(sel.cpu().numpy(), ref["sel"]), \
         f"selection differs; min boundary gap {min_boundary_gap(ref, case):.3e}"
-    assert_out_close(out_to_f64(out), ref["out"], "bf16", where=f"config 3 {variant}")
+    assert_out_close(out_to_f64(out), ref["out"], "bf16", where=f"128K x 4 {variant}")
     # the launch configuration the bench times: graph replays over cache copies, each
     # node the same kernel on its own copy; every node must give the stream launch's bits
-    banner("config 3: graph replays over two cache copies")
+    banner("128K x 4: graph replays over two cache copies")
     copy = S.DeviceCache({k: v.clone() for k, v in dc.t.items()}, case.dtype)
     g = S.LayerGraph(dims, [dc, copy], ws)
     try:

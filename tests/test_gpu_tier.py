@@ -7,7 +7,7 @@ sekv_zoom_attend with the routing scores: bitwise) and against the CPU oracle.""
 import numpy as np
 import pytest
 
-from synth import CONFIGS, custom_spec, make_case
+from synth import WORKLOADS, custom_spec, make_case
 from synth.cases import block_bytes
 from tests.gpu_common import (assert_out_close, banner, case_arrays, dims_for, oracle_result,
                               out_to_f64)
@@ -113,11 +113,11 @@ def test_tier_adjacent_blocks_coalesce(S):
         tier.destroy()
 
 
-def test_tier_config5_full_size(S):
+def test_tier_128k_b4_full_size(S):
     """The 128K x 4 host-tier workload at full size (literal values)."""
-    banner("tier: config 5 full size: generating")
-    case = make_case(CONFIGS[5])
-    banner("tier: config 5: running")
+    banner("tier: 128K x 4 full size: generating")
+    case = make_case(WORKLOADS["llama3-8b-layer-128k-b4-hosttier"])
+    banner("tier: 128K x 4: running")
     _tier_case(S, case, steps=2)
 
 

@@ -6,15 +6,16 @@ import numpy as np
 import pytest
 
 import oracle
-from synth import CONFIGS, custom_spec, make_case
+from synth import WORKLOADS, custom_spec, make_case
 from synth.cases import (bf16_bits_to_f64, f64_to_bf16_bits, from_storage, span_lengths,
                          uniforms)
 from tests.helpers import oracle_kwargs
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3, 4])
-def test_partition_covers_context(cid):
-    spec = CONFIGS[cid]
+@pytest.mark.parametrize("name", ["tiny-f32", "llama3-8b-layer-32k", "llama3-8b-layer-128k-b4",
+                                  "llama3-8b-32layer-32k-b32"])
+def test_partition_covers_context(name):
+    spec = WORKLOADS[name]
     for b in range(min(spec.batch, 4)):
         lens, rem = span_lengths(spec, b)
         assert all(spec.span_min <= L <= spec.span_max for L in lens)
@@ -23,7 +24,7 @@ def test_partition_covers_context(cid):
 
 
 def test_loguniform_partition_statistics():
-    spec = CONFIGS[3]
+    spec = WORKLOADS["llama3-8b-layer-128k-b4"]
     lens = [L for b in range(4) for L in span_lengths(spec, b)[0]]
     assert 165 < np.mean(lens) < 185          # E[min(512, floor(e^U))] ~ 173
     assert 680 < len(lens) / 4 < 800          # about 700 spans per 128K sequence
@@ -65,7 +66,7 @@ def test_counter_stream_is_position_addressable():
 
 
 def test_tiny_config_factors_are_orthonormal():
-    case = make_case(CONFIGS[1])
+    case = make_case(WORKLOADS["tiny-f32"])
     s = case.spec
     for S in range(int(case.n_spans[0])):
         f = oracle.read_span_block(case.factors, int(case.block_off[0, 1, S]),
@@ -77,9 +78,9 @@ def test_tiny_config_factors_are_orthonormal():
             assert np.all(np.diff(f["s" + side]) <= 0)
 
 
-@pytest.mark.parametrize("cid", [1, 2])
-def test_planted_needles_are_selected(cid):
-    case = make_case(CONFIGS[cid], variant="N")
+@pytest.mark.parametrize("name", ["tiny-f32", "llama3-8b-layer-32k"])
+def test_planted_needles_are_selected(name):
+    case = make_case(WORKLOADS[name], variant="N")
     res = oracle.decode_step(**oracle_kwargs(case))
     for b in range(case.spec.batch):
         for g in range(case.spec.n_kv_heads):
@@ -91,7 +92,7 @@ def test_planted_needles_are_selected(cid):
 
 
 def test_literal_layer_is_near_uniform():
-    case = make_case(CONFIGS[2])
+    case = make_case(WORKLOADS["llama3-8b-layer-32k"])
     qd = from_storage(case.q, "bf16")
     kd = from_storage(case.sum_k[0, 0, :5], "bf16")
     assert np.abs(qd[0, 0] @ kd.T * case.spec.softmax_scale).max() < 1e-3
