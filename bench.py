@@ -30,7 +30,8 @@ if ROOT not in sys.path:
 METRIC = "decode-step latency (µs) and achieved HBM GB/s, 128K context, batch 4"
 HBM_PEAK_GBS = 8000.0
 KERNEL_NAME = "sekv_step_kernel"
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_31145_amd", "csrc", "sekv_kernels.hip")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_31145_amd", "csrc", f) for f in
+                  ("sekv_internal.h", "sekv_step.h", "sekv_step_inst.hip", "sekv_kernels.hip")]
 
 
 def log(*a):
@@ -38,11 +39,13 @@ def log(*a):
 
 
 def kernel_source_hash() -> str:
-    """Hash of the kernel source's code: comments and blank space removed, so that an
+    """Hash of the kernel sources' code: comments and blank space removed, so that an
     edit to comments alone does not orphan the committed counter figures."""
     import re
-    with open(KERNEL_SOURCE) as f:
-        src = f.read()
+    src = ""
+    for path in KERNEL_SOURCES:
+        with open(path) as f:
+            src += f.read() + "\n"
     src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
     src = re.sub(r"//[^\n]*", " ", src)
     src = " ".join(src.split())
@@ -75,6 +78,9 @@ def parse():
                     help="L: literal synthetic values; N: planted needle spans")
     ap.add_argument("--rotate", type=int, default=8, help="cache copies cycled through")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-variant", action="store_true",
+                    help="headline workload: skip timing the other value variant (planted "
+                         "needles when --variant L)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time spent timing the oracle")
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
@@ -84,7 +90,12 @@ def parse():
                     help="layer128k: one 128K x 4 layer (the headline); layers32: the 32-layer, "
                          "batch-32, 32K-context step replayed as one HIP graph; hosttier: the "
                          "128K x 4 layer with its factors in pinned host memory")
-    ap.add_argument("--distinct-layers", type=int, default=4,
+    ap.add_argument("--phase-trace", metavar="OUT_MD", default=None,
+                    help="diagnostic: load the phase-trace build (libsekv_trace.so), trace the "
+                         "work items of a few steps of the workload and write a per-phase "
+                         "percentile table to OUT_MD; prints no benchmark line")
+    ap.add_argument("--trace-reps", type=int, default=3)
+    ap.add_argument("--distinct-layers", type=int, default=32,
                     help="layers32: independently seeded layers generated on the host; the "
                          "32 device-resident layers cycle through them, each in its own memory")
     return ap.parse_args()
@@ -97,12 +108,9 @@ def main():
               f"is not sharded across GPUs in this build.", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
+    if args.phase_trace:
+        os.environ["SEKV_LIB"] = "trace"
     import torch
-
-    from paper_2606_31145_amd import accounting
-    from paper_2606_31145_amd import sekv
-    from synth import WORKLOADS, make_case
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
@@ -110,10 +118,76 @@ def main():
         return bench_layers32(args, dev)
     if args.workload == "hosttier":
         return bench_hosttier(args, dev)
+
+    main_run = time_layer128k(args, dev, args.variant)
+    if main_run is None:                     # phase-trace mode
+        return
+    other = None
+    if not args.no_other_variant:
+        other = time_layer128k(args, dev, "N" if args.variant == "L" else "L")
+    ceiling = copy_ceiling(dev)
+    torch.cuda.empty_cache()
+
+    bytes_step = main_run["bytes"]["total"]
+    workload = "sekv-decode-step-128k-b4-r32-k16-bf16-" + args.variant
+    traffic = load_traffic(workload)
+    achieved = main_run["achieved"]
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic, "kernel": KERNEL_NAME,
+                "kernel_us_mean": main_run["kern_us"],
+                "frac_of_measured_ceiling": {k: round(achieved / v, 4) for k, v in ceiling.items()
+                                             if k.endswith("GB_s")},
+                "algorithmic_bytes_per_launch": bytes_step,
+                **{k: main_run[k] for k in ("stream_launch_us_mean", "stream_launch_us_p50",
+                                            "stream_launch_us_p90")}}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(main_run["case"], bytes_step, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC, "value": round(main_run["gbs"], 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(main_run["wall_us"] / 1e3, 5),
+        "us_per_step": round(main_run["wall_us"], 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": workload, "batch": 4, "context": 131072,
+                   "n_q_heads": 32, "n_kv_heads": 8, "head_dim": 128, "rank": 32,
+                   "top_k": 16, "storage_dtype": "bf16", "routing_dtype": "f64",
+                   "arith": "bf16 storage, f32 accumulate, f64 routing keys",
+                   "variant": args.variant, "cache_copies": main_run["copies"],
+                   "parallelism": "single-gpu"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "bytes": main_run["bytes"],
+        "warm_same_cache_kernel_us": main_run["warm_us"],
+        "measured_ceiling": ceiling,
+    }
+    if other is not None:
+        line["other_variant"] = {
+            "variant": other["variant"], "us_per_step": round(other["wall_us"], 3),
+            "kernel_us_mean": other["kern_us"], "achieved_GB_s": round(other["achieved"], 1),
+            "frac": round(other["achieved"] / HBM_PEAK_GBS, 4),
+            "algorithmic_bytes_per_launch": other["bytes"]["total"],
+            "factor_bytes": other["bytes"]["factors"],
+            "mean_selected_len": other["bytes"]["mean_selected_len"]}
+    print(json.dumps(line), flush=True)
+
+
+def time_layer128k(args, dev, variant):
+    """Generate the 128K x 4 cache (one variant), time K graph-replayed steps over rotating
+    device copies, then the same steps launched one by one; returns the figures."""
+    import numpy as np
+    import torch
+
+    from paper_2606_31145_amd import accounting
+    from paper_2606_31145_amd import sekv
+    from synth import WORKLOADS, make_case
+
     spec = WORKLOADS["llama3-8b-layer-128k-b4"]
-    log(f"[bench] generating the 128K x 4 cache (variant {args.variant})")
+    log(f"[bench] generating the 128K x 4 cache (variant {variant})")
     t0 = time.time()
-    case = make_case(spec, variant=args.variant)
+    case = make_case(spec, variant=variant)
     log(f"[bench] generated in {time.time() - t0:.1f}s; factors {case.factors.nbytes / 1e6:.1f} MB")
     arrays = dict(q=case.q, anchor_k=case.anchor_k, anchor_v=case.anchor_v,
                   n_anchors=case.n_anchors, sum_k=case.sum_k, sum_v=case.sum_v,
@@ -148,6 +222,10 @@ def main():
                                  elem=2, out_elem=2, n_anchors=case.n_anchors,
                                  n_spans=case.n_spans, span_len=case.span_len, sel=sel_np)
     bytes_step = acct["total"]
+    if args.phase_trace:
+        phase_trace(args, step, len(caches), dev,
+                    f"128K x 4 layer (batch 4, rank 32, top-16), variant {variant}")
+        return None
 
     # timed region: K steps, replayed from HIP graphs with one kernel node per cache copy
     # (a full graph over every copy, then one over the first K mod copies), one event
@@ -162,7 +240,7 @@ def main():
     torch.cuda.synchronize()
     assert ws.status() == 0, "device error word set during the graph warmup"
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    log(f"[bench] timing {K} steps over {R} cache copies (graph replays)")
+    log(f"[bench] timing {K} steps over {R} cache copies (graph replays), variant {variant}")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record(stream)
@@ -176,10 +254,7 @@ def main():
     assert ws.status() == 0, "device error word set during the timed steps"
     if not torch.equal(graph.sel[0], sels[0]):
         raise RuntimeError("graph replay selected other spans than the stream launch")
-    us_step = wall / K * 1e6
     kern_us = ev0.elapsed_time(ev1) * 1e3 / K
-    gbs = bytes_step * K / wall / 1e9
-    achieved = bytes_step / (kern_us * 1e-6) / 1e9
     graph.destroy()
     if tail is not None:
         tail.destroy()
@@ -220,38 +295,49 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         log(f"[bench] calibration copy of {n} bytes done")
+        del src, dst
 
-    workload = "sekv-decode-step-128k-b4-r32-k16-bf16-" + args.variant
-    traffic = load_traffic(workload)
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": traffic, "kernel": KERNEL_NAME,
-                "kernel_us_mean": round(kern_us, 3),
-                "stream_launch_us_mean": round(float(kern_ms.mean() * 1e3), 3),
-                "stream_launch_us_p50": round(float(np.median(kern_ms) * 1e3), 3),
-                "stream_launch_us_p90": round(float(np.percentile(kern_ms, 90) * 1e3), 3),
-                "algorithmic_bytes_per_launch": bytes_step}
+    res = {"variant": variant, "case": case, "bytes": dict(acct), "copies": R,
+           "wall_us": wall / K * 1e6, "kern_us": round(kern_us, 3),
+           "gbs": bytes_step * K / wall / 1e9, "achieved": bytes_step / (kern_us * 1e-6) / 1e9,
+           "stream_launch_us_mean": round(float(kern_ms.mean() * 1e3), 3),
+           "stream_launch_us_p50": round(float(np.median(kern_ms) * 1e3), 3),
+           "stream_launch_us_p90": round(float(np.percentile(kern_ms, 90) * 1e3), 3),
+           "warm_us": round(warm_us, 3)}
+    del caches, base, graph, tail, ws, sels, outs
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    log(f"[bench] variant {variant}: {res['kern_us']:.2f} us per step (events), "
+        f"{res['achieved']:.0f} GB/s")
+    return res
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(case, bytes_step, args.cpu_seconds)
 
-    line = {
-        "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1,
-        "steps": K, "warmup": args.warmup, "ms_per_step": round(wall / K * 1e3, 5),
-        "us_per_step": round(us_step, 3), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": workload, "batch": B, "context": spec.context,
-                   "n_q_heads": Hq, "n_kv_heads": Hkv, "head_dim": d, "rank": spec.rank,
-                   "top_k": spec.top_k, "storage_dtype": "bf16", "routing_dtype": "f64",
-                   "variant": args.variant, "cache_copies": len(caches),
-                   "parallelism": "single-gpu"},
-        "roofline": roofline,
-        "cpu_baseline": cpu,
-        "bytes": {k: v for k, v in acct.items()},
-        "warm_same_cache_kernel_us": round(warm_us, 3),
-    }
-    print(json.dumps(line), flush=True)
+def copy_ceiling(dev, nbytes=1 << 30, reps=20):
+    """Streaming ceilings on this device, same run: a 1 GiB device-to-device copy (read +
+    write bytes per second) and a 1 GiB read-only reduction (bytes read per second)."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    out = {}
+    for name, fn, mult in (("copy", lambda: dst.copy_(src), 2), ("read", lambda: src.sum(), 1)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        sec = a.elapsed_time(b) * 1e-3 / reps
+        out[f"{name}_GB_s"] = round(mult * nbytes / sec / 1e9, 1)
+    out["bytes"] = nbytes
+    out["how"] = ("torch copy_ of 1 GiB (2 x bytes per second) and torch sum over 1 GiB of "
+                  "float32 (bytes read per second), event-timed, 20 repetitions each")
+    del src, dst
+    torch.cuda.synchronize()
+    log(f"[bench] measured ceilings: {out}")
+    return out
 
 
 def bench_layers32(args, dev):
@@ -349,7 +435,9 @@ def bench_layers32(args, dev):
 
 
 def bench_hosttier(args, dev):
-    """128K x 4 layer; factors in pinned host memory, selected blocks copied per step."""
+    """128K x 4 layer; factors in pinned host memory, selected blocks moved per step, in
+    both copy modes of the tier (device-planned gather kernel; host-planned hipMemcpyAsync
+    per run of neighbouring blocks)."""
     import numpy as np
     import torch
 
@@ -365,7 +453,7 @@ def bench_hosttier(args, dev):
     arrays = dict(q=case.q, anchor_k=case.anchor_k, anchor_v=case.anchor_v,
                   n_anchors=case.n_anchors, sum_k=case.sum_k, sum_v=case.sum_v,
                   n_spans=case.n_spans, span_len=case.span_len, span_logsize=case.span_logsize,
-                  factors=dummy, block_off=np.zeros_like(case.block_off))
+                  factors=dummy, block_off=case.block_off)
     dc = sekv.DeviceCache.from_arrays(arrays, spec.dtype, dev)
     host = sekv.HostFactors(case.factors, case.block_off, case.span_len)
     dims = sekv.make_dims(batch=spec.batch, n_q_heads=spec.n_q_heads, n_kv_heads=spec.n_kv_heads,
@@ -374,64 +462,165 @@ def bench_hosttier(args, dev):
                           max_span_len=case.max_span_len, dtype=spec.dtype,
                           softmax_scale=spec.softmax_scale)
     ws = sekv.Workspace(dims, dev)
-    tier = sekv.Tier(dims)
     side = torch.cuda.Stream()
     stream = torch.cuda.current_stream()
     B, Hq, Hkv, d = spec.batch, spec.n_q_heads, spec.n_kv_heads, spec.head_dim
     sel = torch.empty((B, Hkv, spec.top_k), dtype=torch.int32, device=dev)
     out = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
-    for _ in range(args.warmup):
-        sekv.decode_step_tiered(dims, dc, host, tier, ws, sel=sel, out=out, stream=stream, side=side)
+    # pinned H2D hipMemcpyAsync bandwidth of one large copy, for context
+    probe = torch.empty(256 << 20, dtype=torch.uint8, pin_memory=True)
+    probe_d = torch.empty(probe.numel(), dtype=torch.uint8, device=dev)
+    probe_d.copy_(probe, non_blocking=True)
     torch.cuda.synchronize()
-    assert ws.status() == 0
-    K = args.steps
-    walls, copy_ms, copy_bytes, n_copies = [], [], [], []
-    for _ in range(K):
-        t1 = time.perf_counter()
-        sekv.decode_step_tiered(dims, dc, host, tier, ws, sel=sel, out=out, stream=stream, side=side)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(5):
+        probe_d.copy_(probe, non_blocking=True)
+    b.record()
+    torch.cuda.synchronize()
+    h2d_gbs = 5 * probe.numel() / (a.elapsed_time(b) * 1e-3) / 1e9
+    del probe, probe_d
+    modes = {}
+    for mode in ("gather", "memcpy"):
+        tier = sekv.Tier(dims, mode)
+        for _ in range(args.warmup):
+            sekv.decode_step_tiered(dims, dc, host, tier, ws, sel=sel, out=out, stream=stream, side=side)
         torch.cuda.synchronize()
-        walls.append(time.perf_counter() - t1)
-        nb, nc, ms = tier.last_copy()
-        copy_ms.append(ms)
-        copy_bytes.append(nb)
-        n_copies.append(nc)
-    assert ws.status() == 0
+        assert ws.status() == 0
+        K = args.steps
+        walls, copy_ms, copy_bytes, n_copies = [], [], [], []
+        for _ in range(K):
+            t1 = time.perf_counter()
+            sekv.decode_step_tiered(dims, dc, host, tier, ws, sel=sel, out=out, stream=stream, side=side)
+            torch.cuda.synchronize()
+            walls.append(time.perf_counter() - t1)
+            nb, nc, ms = tier.last_copy()
+            copy_ms.append(ms)
+            copy_bytes.append(nb)
+            n_copies.append(nc)
+        assert ws.status() == 0
+        staging = tier.staging_bytes
+        tier.destroy()
+        step_s = float(np.median(walls))
+        modes[mode] = {"us_per_step": round(step_s * 1e6, 1),
+                       "us_per_step_p90": round(float(np.percentile(walls, 90)) * 1e6, 1),
+                       "bytes_per_step": int(np.mean(copy_bytes)),
+                       "copies_per_step": float(np.mean(n_copies)),
+                       "copy_ms_per_step": round(float(np.mean(copy_ms)), 4),
+                       "host_link_GB_s": round(float(np.mean(copy_bytes)) /
+                                               (float(np.mean(copy_ms)) * 1e-3) / 1e9, 2)}
+        log(f"[bench] hosttier {mode}: {modes[mode]}")
     sel_np = sel.cpu().numpy()
     acct = accounting.step_bytes(n_q_heads=Hq, n_kv_heads=Hkv, head_dim=d, rank=spec.rank,
                                  elem=2, out_elem=2, n_anchors=case.n_anchors,
                                  n_spans=case.n_spans, span_len=case.span_len, sel=sel_np)
-    step_s = float(np.median(walls))
-    link = float(np.mean(copy_bytes)) / (float(np.mean(copy_ms)) * 1e-3) / 1e9
     # HBM held by the tiered step vs a dense bf16 cache of the same tokens
-    resident = int(sum(t.numel() * t.element_size() for k, t in dc.t.items()
-                       if k not in ("factors", "block_off")) + tier.staging_bytes)
+    resident = int(sum(t.numel() * t.element_size() for k, t in dc.t.items() if k != "factors")
+                   + staging)
     full = accounting.full_kv_bytes_same_shapes(n_kv_heads=Hkv, head_dim=d, elem=2,
                                                 n_anchors=case.n_anchors, span_len=case.span_len)
-    tier.destroy()
+    g = modes["gather"]
     line = {
         "metric": "decode-step latency (µs), host-link GB/s and HBM saved, 128K context, batch 4, "
                   "factors in pinned host memory",
-        "value": round(step_s * 1e6, 1), "unit": "us", "n_gpus": 1, "steps": K,
-        "warmup": args.warmup, "ms_per_step": round(step_s * 1e3, 4),
+        "value": g["us_per_step"], "unit": "us", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(g["us_per_step"] / 1e3, 4),
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": f"sekv-decode-step-128k-b4-r32-k16-bf16-hosttier-{args.variant}",
                    "batch": B, "context": spec.context, "rank": spec.rank, "top_k": spec.top_k,
-                   "variant": args.variant, "parallelism": "single-gpu"},
-        "host_link": {"bytes_per_step": int(np.mean(copy_bytes)),
-                      "runs_per_step": float(np.mean(n_copies)),
-                      "copy_ms_per_step": round(float(np.mean(copy_ms)), 4),
-                      "GB_s": round(link, 2)},
+                   "variant": args.variant, "tier_mode": "gather", "parallelism": "single-gpu"},
+        "host_link": g,
+        "modes": modes,
+        "pinned_h2d_memcpy_GB_s": round(h2d_gbs, 2),
         "hbm": {"resident_bytes": resident, "full_bf16_kv_bytes": full,
                 "saved_frac": round(1.0 - resident / full, 4),
                 "algorithmic_bytes_per_step": acct["total"]},
-        "step_us_p90": round(float(np.percentile(walls, 90)) * 1e6, 1),
     }
     print(json.dumps(line), flush=True)
 
 
+TRACE_ROUTE = [("start", 1), ("k rows loaded", 3), ("scored", 4), ("chunk sorted", 5),
+               ("candidates published", 6), ("end", 2)]
+TRACE_SHARE = [("start", 1), ("anchors folded", 3), ("selection known", 4),
+               ("zoom: first factor loads issued", 5), ("zoom: mid fold done", 6),
+               ("zoom: Vt_K q done", 7), ("zoom: token blocks done", 8), ("zoom: done", 9),
+               ("summary share done", 10), ("partial written", 11), ("merged", 12), ("end", 2)]
+
+
+def phase_trace(args, step, n_rot, dev, what):
+    """Trace the work items of single steps (trace build) and write a percentile table."""
+    import numpy as np
+    import torch
+
+    from paper_2606_31145_amd import sekv
+    slots = 16
+    buf = torch.zeros(1 << 20, dtype=torch.int64, device=dev)     # up to 65 536 items
+    sekv.phase_trace(buf)
+    reps = []
+    for r in range(args.trace_reps):
+        for i in range(n_rot):                                     # touch every copy
+            step(i)
+        torch.cuda.synchronize()
+        buf.zero_()
+        torch.cuda.synchronize()
+        step(r)                                                    # the traced step
+        torch.cuda.synchronize()
+        tr = buf.cpu().numpy().reshape(-1, slots)
+        tr = tr[tr[:, 1] != 0]
+        reps.append(tr)
+    sekv.phase_trace(None)
+
+    def pct(x):
+        x = x[np.isfinite(x)]
+        if len(x) == 0:
+            return "| – " * 5
+        return "".join(f"| {v:.2f} " for v in np.percentile(x, [0, 10, 50, 90, 100]))
+
+    lines = [f"# Phase trace: {what}", "",
+             "Per work item, microseconds from the first item's start (the device's 100 MHz "
+             "real-time counter, stamped by thread 0 of the item's workgroup; trace build "
+             "`libsekv_trace.so`, same sources compiled with `SEKV_PHASE_TRACE`).  Columns: "
+             "percentiles 0 / 10 / 50 / 90 / 100 over the items of one step.", "",
+             "Command: `python bench.py --phase-trace OUT.md" +
+             (f" --variant {args.variant}" if args.variant != "L" else "") + "`", ""]
+    for r, tr in enumerate(reps):
+        kind = tr[:, 0] >> 60
+        xcc = (tr[:, 0] >> 48) & 0xF
+        t0 = tr[:, 1].min()
+        rel = (tr[:, 1:].astype(np.float64) - t0) * 0.01
+        rel[tr[:, 1:] == 0] = np.nan
+        span = np.nanmax(rel)
+        lines += [f"## step {r}: {int((kind == 0).sum())} routing items, "
+                  f"{int((kind == 1).sum())} share items, first start to last end "
+                  f"{span:.2f} us, workgroups on {len(set(xcc.tolist()))} XCDs", "",
+                  "| item | phase mark | p0 | p10 | p50 | p90 | p100 |", "|---|---|---|---|---|---|---|"]
+        for nm, table in (("routing", TRACE_ROUTE), ("share", TRACE_SHARE)):
+            sel = kind == (0 if nm == "routing" else 1)
+            for label, slot in table:
+                lines.append(f"| {nm} | {label} " + pct(rel[sel, slot - 1]) + "|")
+        lines.append("")
+    text = "\n".join(lines) + "\n"
+    with open(args.phase_trace, "w") as f:
+        f.write(text)
+    log(text)
+    print(json.dumps({"phase_trace": args.phase_trace, "steps": len(reps)}), flush=True)
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(case, bytes_step, seconds, what="full decode steps of the same 128K x 4 layer"):
-    """The oracle, as it stands, timed on the host on the same workload."""
+    """The oracle, as it stands, timed on the host on the same workload: BLAS limited to all
+    usable cores, then to one thread (about seconds/2 of CPU time each)."""
     import numpy as np
 
     import oracle
@@ -444,26 +633,35 @@ def cpu_baseline(case, bytes_step, seconds, what="full decode steps of the same 
               sum_k=case.sum_k, sum_v=case.sum_v, n_spans=case.n_spans, span_len=case.span_len,
               span_logsize=case.span_logsize, factors=case.factors, block_off=case.block_off,
               rank=s.rank, top_k=s.top_k, softmax_scale=s.softmax_scale, dtype=s.dtype)
-    ctx = threadpool_limits(limits=1) if threadpool_limits else None
-    if ctx:
-        ctx.__enter__()
-    try:
-        times = []
-        t_end = time.perf_counter() + seconds
-        while True:
-            t0 = time.perf_counter()
-            oracle.decode_step(**kw)
-            times.append(time.perf_counter() - t0)
-            if time.perf_counter() > t_end or len(times) >= 100:
-                break
-    finally:
+    cores = len(os.sched_getaffinity(0))
+    runs = {}
+    for label, threads in (("all", cores), ("one", 1)):
+        ctx = threadpool_limits(limits=threads) if threadpool_limits else None
         if ctx:
-            ctx.__exit__(None, None, None)
-    per = float(np.median(times))
-    log(f"[bench] oracle: {len(times)} steps, median {per:.3f}s")
-    return {"value": round(bytes_step / per / 1e9, 4), "unit": "GB/s", "cores": 1,
+            ctx.__enter__()
+        try:
+            times = []
+            t_end = time.perf_counter() + seconds / 2
+            while True:
+                t0 = time.perf_counter()
+                oracle.decode_step(**kw)
+                times.append(time.perf_counter() - t0)
+                if time.perf_counter() > t_end or len(times) >= 100:
+                    break
+        finally:
+            if ctx:
+                ctx.__exit__(None, None, None)
+        runs[label] = (float(np.median(times)), len(times), threads)
+        log(f"[bench] oracle, BLAS threads {threads}: {len(times)} steps, median {runs[label][0]:.3f}s")
+    per, n, threads = runs["all"]
+    per1, n1, _ = runs["one"]
+    return {"value": round(bytes_step / per / 1e9, 4), "unit": "GB/s", "cores": threads,
             "kind": "oracle", "us_per_step": round(per * 1e6, 1),
-            "sample": f"{len(times)} {what}, median, numpy float64, BLAS limited to 1 thread"}
+            "sample": f"{n} {what}, median, numpy float64, BLAS threads limited to the "
+                      f"{threads} usable cores (the oracle's own loops run on one)",
+            "cpu_model": cpu_model(), "usable_cores": cores,
+            "one_thread": {"value": round(bytes_step / per1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+                           "us_per_step": round(per1 * 1e6, 1), "steps": n1}}
 
 
 if __name__ == "__main__":

@@ -35,7 +35,16 @@
  *     The kernels clamp counts and skip out-of-arena blocks (flagging the workspace
  *     error word), so a bad table gives a wrong answer, never an out-of-bounds access.
  *   - Results are bitwise deterministic: fixed reduction order, no floating-point atomics.
- *   - Concurrent calls must use distinct workspaces.
+ *   - Concurrent calls must use distinct workspaces; calls sharing a workspace must be
+ *     ordered on one stream.  The library remembers, per workspace address, the shapes of
+ *     the last call it enqueued there, and enqueues a zeroing kernel before a call whose
+ *     shapes (hence workspace layout) differ.  Calls recorded into a caller's own stream
+ *     capture are tracked at capture time, so such a graph must be replayed in the order
+ *     it was captured relative to eager calls on the same workspace.
+ *   - Forward progress does not depend on how many workgroups are resident: work items
+ *     are claimed in index order from a workspace ticket, and an item only ever waits for
+ *     items of lower index, so a step completes even while other kernels hold most of the
+ *     device.
  */
 #ifndef SEKV_H
 #define SEKV_H
@@ -116,6 +125,16 @@ SEKV_API const char *sekv_status_string(sekv_status status);
 /* Thread-local message describing the last failing call on this thread ("" if none). */
 SEKV_API const char *sekv_last_error(void);
 
+/* Diagnostic phase trace.  In a library built with SEKV_PHASE_TRACE (libsekv_trace.so),
+ * attaches a device buffer to the calling thread: every later step launch on this thread
+ * whose work items fit writes, per item i, 16 int64 words at buf[16 i]: word 0 =
+ * kind (0 routing item, 1 share item) << 60 | XCC id << 48 | workgroup index, words 1..12 =
+ * the device's 100 MHz real-time counter at the item's phase marks (start, end, then
+ * kind-specific marks; see sekv_step.h), 0 where a mark was not reached.  Launches whose
+ * items do not fit in `bytes` are not traced.  buf == NULL detaches.  The product build
+ * (libsekv.so) returns SEKV_ERR_UNSUPPORTED and never traces. */
+SEKV_API sekv_status sekv_phase_trace(void *buf, size_t bytes);
+
 /* Host-only validation of a sekv_dims; SEKV_OK if every library call accepts it. */
 SEKV_API sekv_status sekv_check_dims(const sekv_dims *dims);
 
@@ -192,18 +211,21 @@ SEKV_API sekv_status sekv_graph_destroy(sekv_graph *graph);
  * arena lives in pinned host memory.
  *
  * sekv_decode_step_tiered, per sequence b in order:
- *   1. routing and selection of b on `main` (steps 1-2); the selection is read back to
- *      a pinned mirror;
- *   2. the host waits for that selection only, then enqueues on `side` one gather
- *      kernel that reads the selected blocks (runs of blocks that are neighbours in the
- *      arena, in chunks of at most 32 KiB) through the arena's device mapping into the
- *      tier's device staging area, plus a copy of the staging offset table of b;
+ *   1. routing and selection of b on `main` (steps 1-2);
+ *   2. the selected blocks of b move from the pinned arena to the tier's device staging
+ *      area on `side`, after an event on b's selection:
+ *        SEKV_TIER_GATHER: one kernel reads b's selection and tables on the device and
+ *          copies each selected block, through the arena's device mapping, to the fixed
+ *          staging slot of its selection slot.  Nothing waits on the host: the call only
+ *          enqueues work, and can be captured in a graph.
+ *        SEKV_TIER_MEMCPY: the selection is read back to a pinned mirror; the host waits
+ *          for b's selection, packs its blocks in arena order and issues one
+ *          hipMemcpyAsync per run of blocks that are neighbours in the arena, then the
+ *          staging offset table of b (hipMemcpyAsync).
  *   3. `main` waits for those copies (an event) and runs steps 3-4 of b from staging.
  * Copies of sequence b overlap the routing of later sequences and the attention of
- * earlier ones.  The call returns after enqueuing the last attention; it blocks the
- * host only on the per-sequence selection readbacks.  Results are those of
- * sekv_route_topk followed by sekv_zoom_attend with the routing scores, on a
- * device-resident copy of the arena.
+ * earlier ones.  Results are those of sekv_route_topk followed by sekv_zoom_attend with
+ * the routing scores, on a device-resident copy of the arena, in both modes.
  * -------------------------------------------------------------------------------- */
 
 /* The factor arena in pinned host memory (hipHostMalloc), and host copies of the span
@@ -217,11 +239,14 @@ typedef struct {
 
 typedef struct sekv_tier sekv_tier;
 
-/* Set-up (allocates): pinned mirrors of the selection and of the staging offsets, a
- * pinned gather table, device staging for batch * Hkv * top_k blocks of max_span_len
- * tokens, a routing-score buffer, and events, on the current device.  dims is copied; every step must pass
- * identical dims. */
-SEKV_API sekv_status sekv_tier_create(const sekv_dims *dims, sekv_tier **tier);
+/* How a tier moves the selected blocks (see above). */
+typedef enum { SEKV_TIER_GATHER = 0, SEKV_TIER_MEMCPY = 1 } sekv_tier_copy;
+
+/* Set-up (allocates): pinned mirrors of the selection and of the staging offsets,
+ * device staging for batch * Hkv * top_k blocks of max_span_len tokens, a routing-score
+ * buffer, copy counters and events, on the current device.  copy_mode is a
+ * sekv_tier_copy.  dims is copied; every step must pass identical dims. */
+SEKV_API sekv_status sekv_tier_create(const sekv_dims *dims, int32_t copy_mode, sekv_tier **tier);
 
 /* Free everything the tier holds (NULL is a no-op).  No step may be pending. */
 SEKV_API sekv_status sekv_tier_destroy(sekv_tier *tier);
@@ -230,16 +255,21 @@ SEKV_API sekv_status sekv_tier_destroy(sekv_tier *tier);
 SEKV_API size_t sekv_tier_staging_size(const sekv_tier *tier);
 
 /* Host-link figures of the last tiered step: bytes moved host to device, number of
- * contiguous runs moved, and the time from the start of the first gather to the end of
- * the last one on the side stream (valid once that step has completed). */
+ * copies (runs of neighbouring blocks for SEKV_TIER_MEMCPY, blocks for SEKV_TIER_GATHER),
+ * and the time on the side stream from the first copy's start (gather: from the first
+ * sequence's selection) to the last copy's end.  Valid once that step has completed;
+ * in gather mode the call reads the device's counters (a synchronous copy). */
 SEKV_API sekv_status sekv_tier_last_copy(sekv_tier *tier, int64_t *bytes, int32_t *copies,
                                          float *ms);
 
 /* One decode step with the factors in pinned host memory.
- *   cache   device arrays as for sekv_decode_step; cache->factors and cache->block_off
- *           are not read (the host arena replaces them)
- *   host    the pinned arena and host tables; a block outside the arena, or an arena
- *           that is not pinned, device-mapped memory, is an SEKV_ERR_INVALID_ARG
+ *   cache   device arrays as for sekv_decode_step; cache->factors is not read; in gather
+ *           mode cache->block_off is a device copy of host->block_off (offsets into the
+ *           host arena), in memcpy mode it is not read
+ *   host    the pinned arena and host tables; an arena that is not pinned (gather mode:
+ *           pinned and device-mapped) memory is an SEKV_ERR_INVALID_ARG; a selected block
+ *           outside the arena is an SEKV_ERR_INVALID_ARG in memcpy mode, and in gather
+ *           mode is skipped with the workspace error bit 2 set
  *   sel     device int32 [B][Hkv][top_k]; out device [B][Hq][d] in out_dtype
  *   ws      workspace of sekv_workspace_size(dims)
  *   main    stream of the kernels; side: stream of the host-to-device copies (both at the
@@ -249,6 +279,16 @@ SEKV_API sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_c
                                              const sekv_host_factors *host, sekv_tier *tier,
                                              int32_t *sel, void *out, void *ws, size_t ws_bytes,
                                              hipStream_t main, hipStream_t side);
+
+/* Debug check of the device-side preconditions of the step calls, made on HOST copies of
+ * a cache (every pointer in host_copy is a host pointer; factors_bytes is the arena
+ * size), so it is slow and synchronous.  Checks, for every sequence b:
+ *   0 <= n_anchors[b] <= max_anchors, 0 <= n_spans[b] <= max_spans, n_anchors[b] +
+ *   n_spans[b] >= 1; 1 <= span_len <= max_span_len and span_logsize = ln(span_len) for
+ *   every span; every span's block 16-byte aligned and inside the arena (when top_k > 0);
+ *   every stored value of q, the anchors, the summaries and the factor blocks finite.
+ * Returns SEKV_OK, or SEKV_ERR_INVALID_ARG with the first violation in sekv_last_error(). */
+SEKV_API sekv_status sekv_validate_cache(const sekv_dims *dims, const sekv_cache *host_copy);
 
 #ifdef __cplusplus
 }

@@ -14,90 +14,24 @@
 #include <vector>
 
 #include "sekv.h"
+#include "sekv_host.h"
 #include "sekv_internal.h"
 
 namespace {
 
-thread_local char g_err[512] = "";
+using sekv::fail;
 
-sekv_status fail(sekv_status st, const char *fmt, ...) {
-    va_list ap;
-    va_start(ap, fmt);
-    std::vsnprintf(g_err, sizeof(g_err), fmt, ap);
-    va_end(ap);
-    return st;
-}
+// Diagnostic phase-trace buffer attached by sekv_phase_trace (trace builds only).
+thread_local int64_t *g_trace = nullptr;
+thread_local size_t g_trace_bytes = 0;
 
 sekv_status hip_fail(hipError_t e, const char *what) {
     return fail(SEKV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-
-sekv_status check_dims_impl(const sekv_dims *d) {
-    if (!d) return fail(SEKV_ERR_INVALID_ARG, "dims is NULL");
-    if (d->batch < 0) return fail(SEKV_ERR_INVALID_ARG, "batch < 0");
-    if (d->n_q_heads <= 0 || d->n_kv_heads <= 0)
-        return fail(SEKV_ERR_INVALID_ARG, "head counts must be positive");
-    if (d->n_q_heads % d->n_kv_heads)
-        return fail(SEKV_ERR_INVALID_ARG, "n_q_heads %% n_kv_heads != 0");
-    const int G = d->n_q_heads / d->n_kv_heads;
-    if (G != 1 && G != 2 && G != 4 && G != 8)
-        return fail(SEKV_ERR_UNSUPPORTED, "group size %d not in {1,2,4,8}", G);
-    if (d->head_dim != 64 && d->head_dim != 128)
-        return fail(SEKV_ERR_UNSUPPORTED, "head_dim %d not in {64,128}", d->head_dim);
-    if (d->rank != 8 && d->rank != 16 && d->rank != 32 && d->rank != 64)
-        return fail(SEKV_ERR_UNSUPPORTED, "rank %d: need 8, 16, 32 or 64", d->rank);
-    if (d->top_k < 0 || d->top_k > sekv::kMaxTopK)
-        return fail(SEKV_ERR_UNSUPPORTED, "top_k %d not in [0,%d]", d->top_k, sekv::kMaxTopK);
-    if (d->max_anchors < 0) return fail(SEKV_ERR_INVALID_ARG, "max_anchors < 0");
-    if (d->max_spans < 1) return fail(SEKV_ERR_INVALID_ARG, "max_spans < 1");
-    if (d->max_span_len < 1) return fail(SEKV_ERR_INVALID_ARG, "max_span_len < 1");
-    if (d->dtype != SEKV_F32 && d->dtype != SEKV_BF16)
-        return fail(SEKV_ERR_UNSUPPORTED, "dtype %d", d->dtype);
-    if (d->out_dtype != SEKV_F32 && d->out_dtype != SEKV_BF16)
-        return fail(SEKV_ERR_UNSUPPORTED, "out_dtype %d", d->out_dtype);
-    if (d->dtype == SEKV_F32 && d->out_dtype != SEKV_F32)
-        return fail(SEKV_ERR_UNSUPPORTED, "float32 storage needs float32 output");
-    const int zoom = d->flags & 3;
-    if ((d->flags & ~3) || zoom > SEKV_ZOOM_FACTORED)
-        return fail(SEKV_ERR_UNSUPPORTED, "flags 0x%x", unsigned(d->flags));
-    if (!(d->softmax_scale > 0.0) || !std::isfinite(d->softmax_scale))
-        return fail(SEKV_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
-    if (d->max_spans > sekv::kMaxSpans)
-        return fail(SEKV_ERR_UNSUPPORTED, "max_spans %d > %d", d->max_spans, sekv::kMaxSpans);
-    const long long rows = (long long)d->batch * d->n_kv_heads * std::max(d->max_spans, d->max_anchors);
-    if (rows > (1ll << 31)) return fail(SEKV_ERR_UNSUPPORTED, "tables too large");
-    return SEKV_OK;
-}
-
+sekv_status check_dims_impl(const sekv_dims *d) { return sekv::check_dims(d); }
 sekv_status check_cache(const sekv_dims *d, const sekv_cache *c, bool need_factors) {
-    if (!c) return fail(SEKV_ERR_INVALID_ARG, "cache is NULL");
-    if (d->batch == 0) return SEKV_OK;
-    // data rows are read as 16-byte vectors; tables element by element
-    struct { const void *p; const char *name; uintptr_t align; } ptrs[] = {
-        {c->q, "q", 16}, {c->sum_k, "sum_k", 16}, {c->sum_v, "sum_v", 16},
-        {c->n_spans, "n_spans", 4}, {c->span_len, "span_len", 4},
-        {c->span_logsize, "span_logsize", 8}, {c->n_anchors, "n_anchors", 4}};
-    for (auto &x : ptrs) {
-        if (!x.p) return fail(SEKV_ERR_INVALID_ARG, "cache.%s is NULL", x.name);
-        if (reinterpret_cast<uintptr_t>(x.p) & (x.align - 1))
-            return fail(SEKV_ERR_INVALID_ARG, "cache.%s not %d-byte aligned", x.name, int(x.align));
-    }
-    if (d->max_anchors > 0) {
-        if (!c->anchor_k || !c->anchor_v)
-            return fail(SEKV_ERR_INVALID_ARG, "cache.anchor_k/anchor_v is NULL");
-        if (!aligned16(c->anchor_k) || !aligned16(c->anchor_v))
-            return fail(SEKV_ERR_INVALID_ARG, "anchor arrays not 16-byte aligned");
-    }
-    if (need_factors && d->top_k > 0) {
-        if (!c->factors || !c->block_off)
-            return fail(SEKV_ERR_INVALID_ARG, "cache.factors/block_off is NULL");
-        if (!aligned16(c->factors) || (reinterpret_cast<uintptr_t>(c->block_off) & 7))
-            return fail(SEKV_ERR_INVALID_ARG, "factor arena not 16-byte or offsets not 8-byte aligned");
-        if (c->factors_bytes <= 0) return fail(SEKV_ERR_INVALID_ARG, "factors_bytes <= 0");
-    }
-    return SEKV_OK;
+    return sekv::check_cache(d, c, need_factors);
 }
 
 sekv_status check_ws(const sekv_dims *d, void *ws, size_t ws_bytes) {
@@ -192,6 +126,7 @@ sekv_status prepare(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *
     p.route_cnt = reinterpret_cast<uint32_t *>(w + L.route_cnt);
     p.sel_ready = reinterpret_cast<uint32_t *>(w + L.sel_ready);
     p.part_cnt = reinterpret_cast<uint32_t *>(w + L.part_cnt);
+    p.claim = reinterpret_cast<uint32_t *>(w + L.claim);
     p.zrec = reinterpret_cast<int4 *>(w + L.zrec);
     p.cand = reinterpret_cast<uint64_t *>(w + L.cand);
     p.tlg = reinterpret_cast<uint64_t *>(w + L.tlg);
@@ -204,9 +139,38 @@ sekv_status prepare(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *
     p.merger = (mode == sekv::kModeRoute) || (mode == sekv::kModeFused && !per_item);
     const int cap = resident(d->dtype, d->head_dim, s.G);
     p.grid = std::max(1, std::min(p.end_share, cap));
+    p.trace = nullptr;
+    if (g_trace && g_trace_bytes >= size_t(p.end_share) * sekv::kTraceSlots * sizeof(int64_t))
+        p.trace = g_trace;
     *pp = p;
     *launch = p.end_share > 0;
     return SEKV_OK;
+}
+
+// ------------------------------------------------------------------------------------
+// Workspace state.  A launch leaves its workspace ready for the next launch with the SAME
+// layout (counters zero, epoch advanced).  Sections sit at offsets that depend on the
+// shapes, so a launch with another layout could meet words that an earlier layout left
+// there: stale counters, or untagged data in place of tagged words.  The library
+// therefore remembers, per workspace address, the layout of the last launch it enqueued
+// there (calls sharing a workspace are ordered on one stream, so enqueue order is
+// execution order), and zeroes the whole workspace on the stream before a launch whose
+// layout differs, before the 2^31-th launch since the last zeroing (the 32-bit epoch
+// never wraps), and whenever it has no record (first use, or after eviction).
+// ------------------------------------------------------------------------------------
+std::mutex g_ws_mu;
+sekv::WsTracker g_ws;
+
+void ws_note_zeroed(void *ws, size_t bytes) {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    g_ws.zeroed(reinterpret_cast<uintptr_t>(ws), bytes);
+}
+
+hipError_t ws_prepare(void *ws, size_t ws_bytes, uint64_t key, uint64_t n_launch, hipStream_t stream) {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    if (g_ws.before_launch(reinterpret_cast<uintptr_t>(ws), ws_bytes, key, n_launch))
+        return sekv::launch_zero(ws, ws_bytes & ~size_t(15), stream);
+    return hipSuccess;
 }
 
 sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_out,
@@ -217,20 +181,11 @@ sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_
     const sekv_status st = prepare(mode, d, c, sel_out, logits_out, sel_in, logits_in, out, ws,
                                    ws_bytes, &p, &launch);
     if (st != SEKV_OK || !launch) return st;
-    const hipError_t e = sekv::launch_step(p, d->dtype, d->head_dim, d->n_q_heads / d->n_kv_heads,
-                                           stream);
+    hipError_t e = ws_prepare(ws, ws_bytes, sekv::layout_key(sekv::make_shape(*d)), 1, stream);
+    if (e != hipSuccess) return hip_fail(e, "workspace zero kernel");
+    e = sekv::launch_step(p, d->dtype, d->head_dim, d->n_q_heads / d->n_kv_heads, stream);
     if (e != hipSuccess) return hip_fail(e, "kernel launch");
     return SEKV_OK;
-}
-
-// Bytes of one span block of length L (U|sigma|Vt for keys, then values; every segment
-// starts on a 16-byte boundary, the block on a 256-byte boundary).
-size_t tier_block_bytes(const sekv_dims &d, int L) {
-    const size_t e = size_t(sekv::elem_bytes(d.dtype));
-    auto a16 = [](size_t x) { return (x + 15) & ~size_t(15); };
-    const size_t side = a16(size_t(L) * d.rank * e) + a16(size_t(d.rank) * e) +
-                        a16(size_t(d.rank) * d.head_dim * e);
-    return 2 * side;
 }
 
 }  // namespace
@@ -248,15 +203,29 @@ const char *sekv_status_string(sekv_status status) {
     return "SEKV_ERR_UNKNOWN";
 }
 
-const char *sekv_last_error(void) { return g_err; }
+const char *sekv_last_error(void) { return sekv::last_error(); }
 
 sekv_status sekv_check_dims(const sekv_dims *dims) { return check_dims_impl(dims); }
 
+sekv_status sekv_phase_trace(void *buf, size_t bytes) {
+#ifdef SEKV_PHASE_TRACE
+    if (buf && (reinterpret_cast<uintptr_t>(buf) & 7))
+        return fail(SEKV_ERR_INVALID_ARG, "trace buffer not 8-byte aligned");
+    g_trace = static_cast<int64_t *>(buf);
+    g_trace_bytes = buf ? bytes : 0;
+    return SEKV_OK;
+#else
+    (void)buf;
+    (void)bytes;
+    return fail(SEKV_ERR_UNSUPPORTED, "phase tracing needs the library built with SEKV_PHASE_TRACE");
+#endif
+}
+
 size_t sekv_workspace_size(const sekv_dims *dims) {
-    char saved[sizeof(g_err)];
-    std::memcpy(saved, g_err, sizeof(g_err));
+    char saved[512];
+    std::snprintf(saved, sizeof(saved), "%s", sekv::last_error());
     const sekv_status st = check_dims_impl(dims);
-    std::memcpy(g_err, saved, sizeof(g_err));
+    fail(SEKV_OK, "%s", saved);
     if (st != SEKV_OK) return 0;
     return sekv::make_layout(sekv::make_shape(*dims)).total;
 }
@@ -268,6 +237,7 @@ sekv_status sekv_workspace_init(void *ws, size_t ws_bytes, hipStream_t stream) {
     if (ws_bytes % 16) return fail(SEKV_ERR_WORKSPACE, "workspace size not a multiple of 16");
     const hipError_t e = sekv::launch_zero(ws, ws_bytes, stream);
     if (e != hipSuccess) return hip_fail(e, "workspace zero kernel");
+    ws_note_zeroed(ws, ws_bytes);
     return SEKV_OK;
 }
 
@@ -313,6 +283,9 @@ struct sekv_graph {
     hipGraph_t graph;
     hipGraphExec_t exec;
     int32_t n_layers;
+    void *ws;
+    size_t ws_bytes;
+    uint64_t key;
 };
 
 sekv_status sekv_graph_create(const sekv_dims *dims, const sekv_cache *layers, int32_t n_layers,
@@ -337,8 +310,8 @@ sekv_status sekv_graph_create(const sekv_dims *dims, const sekv_cache *layers, i
         st = prepare(sekv::kModeFused, dims, &layers[l], sel_l, nullptr, nullptr, nullptr, out_l,
                      ws, ws_bytes, &ps[size_t(l)], &launch);
         if (st != SEKV_OK) {
-            char msg[sizeof(g_err)];
-            std::snprintf(msg, sizeof(msg), "%s", g_err);
+            char msg[512];
+            std::snprintf(msg, sizeof(msg), "%s", sekv::last_error());
             return fail(st, "layer %d: %s", int(l), msg);
         }
         go[size_t(l)] = launch;
@@ -370,7 +343,8 @@ sekv_status sekv_graph_create(const sekv_dims *dims, const sekv_cache *layers, i
         (void)hipGraphDestroy(g);
         return hip_fail(e, "instantiating the graph");
     }
-    sekv_graph *h = new (std::nothrow) sekv_graph{g, x, n_layers};
+    sekv_graph *h = new (std::nothrow) sekv_graph{g, x, n_layers, ws, ws_bytes,
+                                                  sekv::layout_key(sekv::make_shape(*dims))};
     if (!h) {
         (void)hipGraphExecDestroy(x);
         (void)hipGraphDestroy(g);
@@ -382,7 +356,9 @@ sekv_status sekv_graph_create(const sekv_dims *dims, const sekv_cache *layers, i
 
 sekv_status sekv_graph_launch(sekv_graph *graph, hipStream_t stream) {
     if (!graph) return fail(SEKV_ERR_INVALID_ARG, "graph is NULL");
-    const hipError_t e = hipGraphLaunch(graph->exec, stream);
+    hipError_t e = ws_prepare(graph->ws, graph->ws_bytes, graph->key, uint64_t(graph->n_layers), stream);
+    if (e != hipSuccess) return hip_fail(e, "workspace zero kernel");
+    e = hipGraphLaunch(graph->exec, stream);
     if (e != hipSuccess) return hip_fail(e, "graph launch");
     return SEKV_OK;
 }
@@ -403,37 +379,41 @@ sekv_status sekv_graph_destroy(sekv_graph *graph) {
 // ------------------------------------------------------------------------------------
 struct sekv_tier {
     sekv_dims dims;
+    int32_t mode;               // SEKV_TIER_*
     int device;
     size_t slot_bytes;          // staging bytes per selection slot (largest block, aligned)
     size_t staging_bytes;
-    int32_t *h_sel;             // pinned [B][Hkv][k]: selection read back per sequence
-    int64_t *h_off;             // pinned [B][Hkv][M_max]: staging offsets of the selected blocks
-    sekv::GatherChunk *h_chunks;        // pinned [B][chunks_per_seq]: gather pieces per sequence
-    sekv::GatherChunk *h_chunks_dev;    // its device mapping
-    size_t chunks_per_seq;
-    void *d_mem;                // one device allocation: offsets | logits | staging
+    int32_t *h_sel;             // pinned [B][Hkv][k]: selection read back per sequence (memcpy mode)
+    int64_t *h_off;             // pinned [B][Hkv][M_max]: staging offsets (memcpy mode)
+    void *d_mem;                // one device allocation: offsets | logits | stats | staging
     int64_t *d_off;             // [B][Hkv][M_max]
     float *d_logits;            // [B][Hq][M_max]
+    unsigned long long *d_stats;  // [2]: bytes and blocks of the last step (gather mode)
     unsigned char *d_staging;   // [B][Hkv][k] slots
-    hipEvent_t *ev_sel;         // [B] selection of sequence b is on the host
-    hipEvent_t *ev_copy;        // [B] factors of sequence b are in staging
+    hipEvent_t *ev_sel;         // [B] selection of sequence b is done (on main)
+    hipEvent_t *ev_copy;        // [B] factors of sequence b are in staging (on side)
     hipEvent_t ev_t0, ev_t1;    // timing of the last step's copies (side stream)
+    sekv::TierPlan plan;        // host plan of one sequence (memcpy mode)
     int64_t last_bytes;
     int32_t last_copies;
+    bool timed;
 };
 
-sekv_status sekv_tier_create(const sekv_dims *dims, sekv_tier **tier) {
+sekv_status sekv_tier_create(const sekv_dims *dims, int32_t copy_mode, sekv_tier **tier) {
     if (!tier) return fail(SEKV_ERR_INVALID_ARG, "tier is NULL");
     *tier = nullptr;
     sekv_status st = check_dims_impl(dims);
     if (st != SEKV_OK) return st;
     if (dims->batch < 1) return fail(SEKV_ERR_INVALID_ARG, "the tier needs batch >= 1");
+    if (copy_mode != SEKV_TIER_GATHER && copy_mode != SEKV_TIER_MEMCPY)
+        return fail(SEKV_ERR_UNSUPPORTED, "tier copy mode %d", int(copy_mode));
     sekv_tier *t = new (std::nothrow) sekv_tier{};
     if (!t) return fail(SEKV_ERR_INVALID_ARG, "out of host memory");
     t->dims = *dims;
+    t->mode = copy_mode;
     const size_t B = size_t(dims->batch), Hkv = size_t(dims->n_kv_heads), Hq = size_t(dims->n_q_heads);
     const size_t M = size_t(dims->max_spans), k = size_t(std::max(dims->top_k, 1));
-    t->slot_bytes = sekv::align256(tier_block_bytes(*dims, dims->max_span_len));
+    t->slot_bytes = sekv::align256(sekv::block_bytes(*dims, dims->max_span_len));
     t->staging_bytes = B * Hkv * k * t->slot_bytes;
     auto cleanup = [&](hipError_t e, const char *what) {
         sekv_tier_destroy(t);
@@ -446,22 +426,16 @@ sekv_status sekv_tier_create(const sekv_dims *dims, sekv_tier **tier) {
     e = hipHostMalloc(reinterpret_cast<void **>(&t->h_off), B * Hkv * M * sizeof(int64_t), hipHostMallocDefault);
     if (e != hipSuccess) return cleanup(e, "pinned offset table");
     std::memset(t->h_off, 0, B * Hkv * M * sizeof(int64_t));
-    // every block fits a slot, so a sequence moves at most Hkv k slots of bytes in runs
-    // that each add at most one partial chunk
-    t->chunks_per_seq = Hkv * k * ((t->slot_bytes + sekv::kGatherChunk - 1) / sekv::kGatherChunk + 1);
-    e = hipHostMalloc(reinterpret_cast<void **>(&t->h_chunks), B * t->chunks_per_seq * sizeof(sekv::GatherChunk),
-                      hipHostMallocMapped);
-    if (e != hipSuccess) return cleanup(e, "pinned gather table");
-    e = hipHostGetDevicePointer(reinterpret_cast<void **>(&t->h_chunks_dev), t->h_chunks, 0);
-    if (e != hipSuccess) return cleanup(e, "device mapping of the gather table");
     const size_t off_bytes = sekv::align256(B * Hkv * M * sizeof(int64_t));
     const size_t lg_bytes = sekv::align256(B * Hq * M * sizeof(float));
-    e = hipMalloc(&t->d_mem, off_bytes + lg_bytes + t->staging_bytes);
+    e = hipMalloc(&t->d_mem, off_bytes + lg_bytes + 256 + t->staging_bytes);
     if (e != hipSuccess) return cleanup(e, "device staging");
-    t->d_off = static_cast<int64_t *>(t->d_mem);
-    t->d_logits = reinterpret_cast<float *>(static_cast<unsigned char *>(t->d_mem) + off_bytes);
-    t->d_staging = static_cast<unsigned char *>(t->d_mem) + off_bytes + lg_bytes;
-    e = hipMemset(t->d_off, 0, off_bytes);
+    unsigned char *m = static_cast<unsigned char *>(t->d_mem);
+    t->d_off = reinterpret_cast<int64_t *>(m);
+    t->d_logits = reinterpret_cast<float *>(m + off_bytes);
+    t->d_stats = reinterpret_cast<unsigned long long *>(m + off_bytes + lg_bytes);
+    t->d_staging = m + off_bytes + lg_bytes + 256;
+    e = hipMemset(t->d_mem, 0, off_bytes + lg_bytes + 256);
     if (e != hipSuccess) return cleanup(e, "clearing the offset table");
     t->ev_sel = new (std::nothrow) hipEvent_t[B]();
     t->ev_copy = new (std::nothrow) hipEvent_t[B]();
@@ -495,7 +469,6 @@ sekv_status sekv_tier_destroy(sekv_tier *t) {
     if (t->d_mem) (void)hipFree(t->d_mem);
     if (t->h_sel) (void)hipHostFree(t->h_sel);
     if (t->h_off) (void)hipHostFree(t->h_off);
-    if (t->h_chunks) (void)hipHostFree(t->h_chunks);
     delete t;
     return SEKV_OK;
 }
@@ -504,10 +477,18 @@ size_t sekv_tier_staging_size(const sekv_tier *t) { return t ? t->staging_bytes 
 
 sekv_status sekv_tier_last_copy(sekv_tier *t, int64_t *bytes, int32_t *copies, float *ms) {
     if (!t || !bytes || !copies || !ms) return fail(SEKV_ERR_INVALID_ARG, "NULL argument");
+    *ms = 0.0f;
+    if (t->mode == SEKV_TIER_GATHER) {
+        // the device counted them; valid once the step has completed
+        unsigned long long st[2] = {0, 0};
+        hipError_t e = hipMemcpy(st, t->d_stats, sizeof(st), hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(e, "reading the copy counters");
+        t->last_bytes = int64_t(st[0]);
+        t->last_copies = int32_t(st[1]);
+    }
     *bytes = t->last_bytes;
     *copies = t->last_copies;
-    *ms = 0.0f;
-    if (t->last_copies > 0) {
+    if (t->timed) {
         const hipError_t e = hipEventElapsedTime(ms, t->ev_t0, t->ev_t1);
         if (e != hipSuccess) return hip_fail(e, "copy timing events");
     }
@@ -527,18 +508,23 @@ sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_cache *cac
         return fail(SEKV_ERR_INVALID_ARG, "cache/host factor tables are NULL");
     if (host->arena_bytes <= 0) return fail(SEKV_ERR_INVALID_ARG, "arena_bytes <= 0");
     if (!out || (dims->top_k > 0 && !sel)) return fail(SEKV_ERR_INVALID_ARG, "sel/out is NULL");
+    const bool gather = t->mode == SEKV_TIER_GATHER;
+    if (gather && dims->top_k > 0 && (!cache->block_off || (reinterpret_cast<uintptr_t>(cache->block_off) & 7)))
+        return fail(SEKV_ERR_INVALID_ARG, "gather mode needs cache.block_off: a device copy of the arena offsets");
     hipPointerAttribute_t attr{};
     if (hipPointerGetAttributes(&attr, host->arena) != hipSuccess || attr.type != hipMemoryTypeHost ||
-        !attr.devicePointer) {
+        (gather && !attr.devicePointer)) {
         (void)hipGetLastError();
-        return fail(SEKV_ERR_INVALID_ARG, "the host factor arena is not pinned, device-mapped memory");
+        return fail(SEKV_ERR_INVALID_ARG, "the host factor arena is not pinned%s memory",
+                    gather ? ", device-mapped" : "");
     }
-    // the gather kernel reads the arena through its device mapping
     const unsigned char *arena_dev = static_cast<const unsigned char *>(attr.devicePointer);
+    const unsigned char *arena_host = static_cast<const unsigned char *>(host->arena);
     const int B = dims->batch, Hkv = dims->n_kv_heads, Hq = dims->n_q_heads, k = dims->top_k;
     const int M = dims->max_spans, d = dims->head_dim;
     const size_t oe = dims->out_dtype == SEKV_F32 ? 4 : 2;
     const size_t e = size_t(sekv::elem_bytes(dims->dtype));
+    const int64_t region = int64_t(size_t(Hkv) * size_t(std::max(k, 1)) * t->slot_bytes);
     sekv_dims d1 = *dims;
     d1.batch = 1;
     // per-sequence views of the device cache (b is the outermost index of every array)
@@ -561,83 +547,80 @@ sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_cache *cac
         c.block_off = t->d_off + bb * Hkv * M;
         return c;
     };
-    // 1. routing per sequence on the main stream; each selection goes to the pinned mirror
+    hipError_t he = hipSuccess;
+    t->timed = false;
+    // 1. routing per sequence on the main stream
     for (int b = 0; b < B; ++b) {
         sekv_cache c = seq_cache(b);
         st = run(sekv::kModeRoute, &d1, &c, sel ? sel + size_t(b) * Hkv * k : nullptr,
                  t->d_logits + size_t(b) * Hq * M, nullptr, nullptr, nullptr, ws, ws_bytes, main);
         if (st != SEKV_OK) return st;
         if (k > 0) {
-            hipError_t he = hipMemcpyAsync(t->h_sel + size_t(b) * Hkv * k, sel + size_t(b) * Hkv * k,
-                                           size_t(Hkv) * k * sizeof(int32_t), hipMemcpyDeviceToHost, main);
+            if (!gather)
+                he = hipMemcpyAsync(t->h_sel + size_t(b) * Hkv * k, sel + size_t(b) * Hkv * k,
+                                    size_t(Hkv) * k * sizeof(int32_t), hipMemcpyDeviceToHost, main);
             if (he == hipSuccess) he = hipEventRecord(t->ev_sel[b], main);
             if (he != hipSuccess) return hip_fail(he, "selection readback");
         }
     }
-    // 2. per sequence: wait for its selection, copy the selected blocks on the side stream
-    //    (runs while later sequences route), then attend on the main stream
+    // 2. per sequence: its selected blocks go to staging on the side stream (overlapping
+    //    the routing of later sequences), then its attention runs on the main stream
     int64_t bytes = 0;
     int32_t copies = 0;
     bool first = true;
-    struct Blk { int64_t src; int64_t len; int64_t slot; int g; int s; };
-    std::vector<Blk> blks;
     for (int b = 0; b < B; ++b) {
-        hipError_t he = hipSuccess;
-        if (k > 0) {
+        if (k > 0 && gather) {
+            he = hipStreamWaitEvent(side, t->ev_sel[b], 0);
+            if (b == 0) {
+                // the copy time runs from the first sequence's selection
+                if (he == hipSuccess) he = hipEventRecord(t->ev_t0, side);
+                if (he == hipSuccess) he = sekv::launch_stats_reset(t->d_stats, side);
+            }
+            sekv::TierGatherArgs a{};
+            a.arena = arena_dev;
+            a.staging = t->d_staging;
+            a.sel = sel + size_t(b) * Hkv * k;
+            a.span_len = cache->span_len + size_t(b) * M;
+            a.block_off = cache->block_off + size_t(b) * Hkv * M;
+            a.stage_off = t->d_off + size_t(b) * Hkv * M;
+            a.stats = t->d_stats;
+            a.error = &static_cast<sekv::WsHeader *>(ws)->error;
+            a.arena_bytes = host->arena_bytes;
+            a.slot0 = int64_t(b) * region;
+            a.slot_bytes = int64_t(t->slot_bytes);
+            a.Hkv = Hkv; a.k = k; a.M = M; a.r = dims->rank; a.d = d; a.elem = int32_t(e);
+            a.max_span_len = dims->max_span_len;
+            a.chunks_per_slot = int32_t((t->slot_bytes + sekv::kGatherChunk - 1) / sekv::kGatherChunk);
+            if (he == hipSuccess) he = sekv::launch_tier_gather(a, side);
+            // the timing event before the last join, so a capture of the step ends joined
+            if (he == hipSuccess && b == B - 1) he = hipEventRecord(t->ev_t1, side);
+            if (he == hipSuccess) he = hipEventRecord(t->ev_copy[b], side);
+            if (he == hipSuccess) he = hipStreamWaitEvent(main, t->ev_copy[b], 0);
+            if (he != hipSuccess) return hip_fail(he, "factor gather");
+        } else if (k > 0) {
             he = hipEventSynchronize(t->ev_sel[b]);
             if (he != hipSuccess) return hip_fail(he, "waiting for the selection");
-            blks.clear();
-            for (int g = 0; g < Hkv; ++g)
-                for (int j = 0; j < k; ++j) {
-                    const int s = t->h_sel[(size_t(b) * Hkv + g) * k + j];
-                    if (s < 0 || s >= M) continue;
-                    const int L = host->span_len[size_t(b) * M + s];
-                    const int64_t off = host->block_off[(size_t(b) * Hkv + g) * M + s];
-                    const int64_t len = int64_t(tier_block_bytes(*dims, L));
-                    if (L < 1 || L > dims->max_span_len || off < 0 || (off & 15) ||
-                        off + len > host->arena_bytes)
-                        return fail(SEKV_ERR_INVALID_ARG, "host block (%d, %d, %d) outside the arena", b, g, s);
-                    blks.push_back({off, len, 0, g, s});
-                }
-            // staging of sequence b: its blocks packed in arena order (each on a 256-byte
-            // boundary) inside the sequence's region, so blocks that are neighbours in the
-            // arena are neighbours in staging and move with one copy
-            std::sort(blks.begin(), blks.end(), [](const Blk &x, const Blk &y) { return x.src < y.src; });
-            int64_t pos = int64_t(size_t(b) * Hkv * size_t(std::max(k, 1)) * t->slot_bytes);
-            for (auto &x : blks) {
-                x.slot = pos;
-                pos += int64_t(sekv::align256(size_t(x.len)));
-                t->h_off[(size_t(b) * Hkv + x.g) * M + x.s] = x.slot;
-            }
-            // runs of neighbouring blocks, cut into gather chunks
-            sekv::GatherChunk *ch = t->h_chunks + size_t(b) * t->chunks_per_seq;
-            size_t n_ch = 0;
-            for (size_t i = 0; i < blks.size();) {
-                size_t j = i + 1;
-                while (j < blks.size() &&
-                       blks[j].src == blks[j - 1].src + int64_t(sekv::align256(size_t(blks[j - 1].len))))
-                    ++j;
-                const int64_t len = (blks[j - 1].src - blks[i].src) + blks[j - 1].len;
-                for (int64_t o = 0; o < len; o += sekv::kGatherChunk) {
-                    if (n_ch == t->chunks_per_seq)
-                        return fail(SEKV_ERR_INVALID_ARG, "gather table overflow (sequence %d)", b);
-                    const int64_t n = std::min<int64_t>(sekv::kGatherChunk, len - o);
-                    ch[n_ch++] = sekv::GatherChunk{blks[i].src + o, blks[i].slot + o, n, 0};
-                }
-                bytes += len;
-                ++copies;
-                i = j;
-            }
-            if (first && n_ch > 0) {
+            sekv::TierPlanIn in{dims, b, t->h_sel + size_t(b) * Hkv * k, host->span_len + size_t(b) * M,
+                                host->block_off + size_t(b) * Hkv * M, host->arena_bytes,
+                                int64_t(b) * region, region};
+            st = sekv::plan_tier_sequence(in, &t->plan);
+            if (st != SEKV_OK) return st;
+            int64_t *hoff = t->h_off + size_t(b) * Hkv * M;
+            for (int32_t i : t->plan.off_set) hoff[i] = t->plan.off[size_t(i)];
+            if (first && !t->plan.runs.empty()) {
                 he = hipEventRecord(t->ev_t0, side);
                 if (he != hipSuccess) return hip_fail(he, "copy timing event");
                 first = false;
             }
-            he = sekv::launch_gather(arena_dev, t->d_staging, t->h_chunks_dev + size_t(b) * t->chunks_per_seq,
-                                     int(n_ch), side);
-            if (he != hipSuccess) return hip_fail(he, "factor gather launch");
-            he = hipMemcpyAsync(t->d_off + size_t(b) * Hkv * M, t->h_off + size_t(b) * Hkv * M,
-                                size_t(Hkv) * M * sizeof(int64_t), hipMemcpyHostToDevice, side);
+            for (const sekv::TierRun &r : t->plan.runs) {
+                he = hipMemcpyAsync(t->d_staging + r.dst, arena_host + r.src, size_t(r.bytes),
+                                    hipMemcpyHostToDevice, side);
+                if (he != hipSuccess) return hip_fail(he, "factor copy");
+            }
+            bytes += t->plan.bytes;
+            copies += int32_t(t->plan.runs.size());
+            he = hipMemcpyAsync(t->d_off + size_t(b) * Hkv * M, hoff, size_t(Hkv) * M * sizeof(int64_t),
+                                hipMemcpyHostToDevice, side);
             if (he == hipSuccess) he = hipEventRecord(t->ev_copy[b], side);
             if (he == hipSuccess) he = hipStreamWaitEvent(main, t->ev_copy[b], 0);
             if (he != hipSuccess) return hip_fail(he, "staging offsets");
@@ -648,13 +631,22 @@ sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_cache *cac
                  ws, ws_bytes, main);
         if (st != SEKV_OK) return st;
     }
-    if (!first) {
-        const hipError_t he = hipEventRecord(t->ev_t1, side);
+    if (gather && k > 0) {
+        t->timed = true;
+    } else if (!first) {
+        he = hipEventRecord(t->ev_t1, side);
         if (he != hipSuccess) return hip_fail(he, "copy timing event");
+        t->timed = true;
     }
-    t->last_bytes = bytes;
-    t->last_copies = copies;
+    if (!gather) {
+        t->last_bytes = bytes;
+        t->last_copies = copies;
+    }
     return SEKV_OK;
+}
+
+sekv_status sekv_validate_cache(const sekv_dims *dims, const sekv_cache *host_copy) {
+    return sekv::validate_cache(dims, host_copy);
 }
 
 }  // extern "C"

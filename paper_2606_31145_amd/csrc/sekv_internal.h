@@ -19,6 +19,7 @@ constexpr int kZoomBlock = 512;    // tokens of a zoomed span scored per LDS pas
 constexpr int kMaxTopK = 64;
 constexpr int kMergeBuf = 512;     // candidates ranked in LDS by one workgroup
 constexpr int kMaxSpans = 65536;   // max_spans limit (span indices and record sizes)
+constexpr int kMaxSpanLen = 1 << 20; // max_span_len limit
 constexpr int kShareTarget = 512;  // share items per launch above which a share item
                                    // zooms several selection slots
 constexpr int kRoundItems = 512;   // items a launch starts at once on a 256-CU device at
@@ -26,6 +27,11 @@ constexpr int kRoundItems = 512;   // items a launch starts at once on a 256-CU 
                                    // a constant, so the split never depends on the device)
 
 enum Mode : int32_t { kModeRoute = 0, kModeAttend = 1, kModeFused = 2 };
+
+// Phase trace (diagnostic builds compiled with SEKV_PHASE_TRACE): per work item,
+// kTraceSlots int64 words; slot 0 holds the item's descriptor, the others the
+// s_memrealtime value (100 MHz) at the phase marks listed with the kernel.
+constexpr int kTraceSlots = 16;
 
 // Device error bits (workspace header word `error`).
 enum : int32_t { kErrSpinTimeout = 1, kErrBlockRange = 2, kErrSelRange = 4 };
@@ -37,7 +43,7 @@ enum : int32_t { kCandKeyHi = 0, kCandKeyLo, kCandIdx, kCandLen, kCandOffLo, kCa
 // it publishes with it, and its last workgroup out advances it (skipping 0, the value
 // of never-written words; initialisation sets 1) and zeroes every counter it used.
 struct WsHeader {
-    uint32_t ticket;
+    uint32_t unused0;
     uint32_t exit_count;
     int32_t error;
     uint32_t epoch;
@@ -47,6 +53,7 @@ struct WsHeader {
 // Byte offsets of the workspace sections for one dims.
 struct WsLayout {
     size_t route_cnt, sel_ready, part_cnt;    // uint32 [P]
+    size_t claim;                             // uint32 [P][n_rc]: tag of the launch that claimed a chunk
     size_t zrec;                              // int32x4 [P][k]: span, |S|, offset lo/hi
     size_t cand;                              // tagged uint64 [kCandFields][P][n_cand]
     size_t tlg;                               // tagged uint64 [P][G][M_max]: base-2 logits
@@ -95,6 +102,7 @@ inline WsLayout make_layout(const Shape &s) {
     L.route_cnt = o; o = align256(o + 4 * P);
     L.sel_ready = o; o = align256(o + 4 * P);
     L.part_cnt = o;  o = align256(o + 4 * P);
+    L.claim = o;     o = align256(o + 4 * P * size_t(s.n_rc));
     L.zrec = o;      o = align256(o + 16 * P * size_t(s.k > 0 ? s.k : 1));
     L.cand = o;      o = align256(o + 8 * size_t(kCandFields) * P * size_t(s.n_cand > 0 ? s.n_cand : 1));
     L.tlg = o;       o = align256(o + 8 * P * size_t(s.G) * size_t(s.M_max));
@@ -138,26 +146,37 @@ struct Params {
     // workspace
     WsHeader *hdr;
     uint32_t *route_cnt, *sel_ready, *part_cnt;
+    uint32_t *claim;
     int4 *zrec;
     uint64_t *cand;
     uint64_t *tlg;
     uint64_t *part_ml, *part_o;
+    int64_t *trace;                                 // [end_share][kTraceSlots] or null
 };
 
-// One piece of a host-to-device gather: bytes (a multiple of 16, at most kGatherChunk)
-// from src (offset into the pinned host arena) to dst (offset into device staging), both
-// 16-byte aligned.
+// Bytes a tier gather workgroup moves at a time.
 constexpr int kGatherChunk = 32768;
-struct GatherChunk {
-    int64_t src, dst, bytes, pad;
+
+// Device-planned tier gather of one sequence (sekv_tier.hip): selection slot (g, j) of
+// the sequence is copied to staging bytes [slot0 + (g k + j) slot_bytes, ...).
+struct TierGatherArgs {
+    const unsigned char *arena;        // device mapping of the pinned host arena
+    unsigned char *staging;
+    const int32_t *sel;                // [Hkv][k] (device)
+    const int32_t *span_len;           // [M] (device)
+    const int64_t *block_off;          // [Hkv][M] arena offsets (device)
+    int64_t *stage_off;                // [Hkv][M] staging offsets, written for selected spans
+    unsigned long long *stats;         // [2]: bytes and blocks moved (accumulated)
+    int32_t *error;                    // workspace error word (out-of-arena blocks)
+    int64_t arena_bytes, slot0, slot_bytes;
+    int32_t Hkv, k, M, r, d, elem, max_span_len, chunks_per_slot;
 };
 
 // Launchers (sekv_kernels.hip).  Return the HIP error of the launch.
 hipError_t launch_step(const Params &p, int dtype, int head_dim, int group, hipStream_t stream);
 hipError_t launch_zero(void *ptr, size_t bytes, hipStream_t stream);
-// src: device mapping of pinned host memory; chunks: device-readable (pinned host) table.
-hipError_t launch_gather(const void *src, void *dst, const GatherChunk *chunks, int n_chunks,
-                         hipStream_t stream);
+hipError_t launch_tier_gather(const TierGatherArgs &a, hipStream_t stream);
+hipError_t launch_stats_reset(unsigned long long *stats, hipStream_t stream);
 int resident_workgroups(int dtype, int head_dim, int group);
 
 }  // namespace sekv

@@ -1,4 +1,10 @@
-// Pinned-host tier: the host-to-device gather of the selected factor blocks.
+// Pinned-host tier: host-to-device moves of the selected factor blocks.
+//
+// tier_gather_kernel plans on the device: it reads the sequence's selection and tables
+// from device memory, gives selection slot (g, j) the fixed staging slot (g, j), and
+// copies the block through the arena's device mapping; nothing waits on the host, so a
+// tiered step in this mode can be captured in a graph.  (The host-planned mode moves the
+// blocks with hipMemcpyAsync instead; see sekv_api.cpp.)
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -7,41 +13,75 @@
 namespace sekv {
 namespace {
 
-// Moves the selected factor blocks from host memory (read through its
-// device mapping) into device staging.  Each workgroup moves whole chunks of at most
-// kGatherChunk bytes, 16-byte aligned at both ends; the chunk table itself sits in
-// pinned host memory.  All of a chunk's loads are issued before its first store.
-__global__ __launch_bounds__(256) void gather_kernel(const unsigned char *src, unsigned char *dst,
-                                                     const GatherChunk *chunks, int n_chunks) {
-    constexpr int kV = kGatherChunk / (16 * 256);
-    for (int c = blockIdx.x; c < n_chunks; c += gridDim.x) {
-        const GatherChunk ch = chunks[c];
-        const int nv = int(ch.bytes >> 4);
-        const uint4 *s = reinterpret_cast<const uint4 *>(src + ch.src);
-        uint4 *d = reinterpret_cast<uint4 *>(dst + ch.dst);
-        uint4 v[kV];
+constexpr int kGT = 256;                                   // threads per workgroup
+constexpr int kGV = kGatherChunk / (16 * kGT);             // 16-byte vectors per thread
+
+// Copy bytes [lo, hi) of a block (lo, hi multiples of 16): every load of the chunk is
+// issued before its first store.
+__device__ inline void copy_chunk(const unsigned char *src, unsigned char *dst, int64_t lo, int64_t hi) {
+    const int nv = int((hi - lo) >> 4);
+    const uint4 *s = reinterpret_cast<const uint4 *>(src + lo);
+    uint4 *d = reinterpret_cast<uint4 *>(dst + lo);
+    uint4 v[kGV];
 #pragma unroll
-        for (int u = 0; u < kV; ++u) {
-            const int i = int(threadIdx.x) + 256 * u;
-            if (i < nv) v[u] = s[i];
-        }
-#pragma unroll
-        for (int u = 0; u < kV; ++u) {
-            const int i = int(threadIdx.x) + 256 * u;
-            if (i < nv) d[i] = v[u];
-        }
+    for (int u = 0; u < kGV; ++u) {
+        const int i = int(threadIdx.x) + kGT * u;
+        if (i < nv) v[u] = s[i];
     }
+#pragma unroll
+    for (int u = 0; u < kGV; ++u) {
+        const int i = int(threadIdx.x) + kGT * u;
+        if (i < nv) d[i] = v[u];
+    }
+}
+
+// Block bytes of a span of length L: U|sigma|Vt for keys and values, 16-byte segments.
+__device__ inline int64_t dev_block_bytes(int64_t L, int r, int d, int e) {
+    auto a16 = [](int64_t x) { return (x + 15) & ~int64_t(15); };
+    return 2 * (a16(L * r * e) + a16(int64_t(r) * e) + a16(int64_t(r) * d * e));
+}
+
+__global__ __launch_bounds__(kGT) void tier_gather_kernel(TierGatherArgs a) {
+    const int slot = int(blockIdx.x) / a.chunks_per_slot, c = int(blockIdx.x) % a.chunks_per_slot;
+    const int g = slot / a.k, j = slot % a.k;
+    const int s = a.sel[size_t(g) * a.k + j];
+    if (s < 0 || s >= a.M) return;
+    const int L = a.span_len[s];
+    const int64_t off = a.block_off[size_t(g) * a.M + s];
+    const int64_t bytes = dev_block_bytes(L, a.r, a.d, a.elem);
+    if (L < 1 || L > a.max_span_len || off < 0 || (off & 15) || off > a.arena_bytes - bytes) {
+        // skipped: the attention reads whatever the slot holds, inside staging
+        if (c == 0 && threadIdx.x == 0)
+            __hip_atomic_fetch_or(a.error, kErrBlockRange, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    const int64_t dst = a.slot0 + int64_t(slot) * a.slot_bytes;
+    if (c == 0 && threadIdx.x == 0) {
+        a.stage_off[size_t(g) * a.M + s] = dst;
+        __hip_atomic_fetch_add(&a.stats[0], (unsigned long long)bytes, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_add(&a.stats[1], 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    const int64_t lo = int64_t(c) * kGatherChunk;
+    if (lo >= bytes) return;
+    const int64_t hi = lo + kGatherChunk < bytes ? lo + kGatherChunk : bytes;
+    copy_chunk(a.arena + off, a.staging + dst, lo, hi);
+}
+
+__global__ void stats_reset_kernel(unsigned long long *stats) {
+    if (threadIdx.x < 2) stats[threadIdx.x] = 0;
 }
 
 }  // namespace
 
-hipError_t launch_gather(const void *src, void *dst, const GatherChunk *chunks, int n_chunks,
-                         hipStream_t stream) {
-    if (n_chunks <= 0) return hipSuccess;
-    const int blocks = n_chunks < 1024 ? n_chunks : 1024;
-    hipLaunchKernelGGL(gather_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream,
-                       static_cast<const unsigned char *>(src), static_cast<unsigned char *>(dst),
-                       chunks, n_chunks);
+hipError_t launch_tier_gather(const TierGatherArgs &a, hipStream_t stream) {
+    const int64_t n = int64_t(a.Hkv) * a.k * a.chunks_per_slot;
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(tier_gather_kernel, dim3(unsigned(n)), dim3(kGT), 0, stream, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_stats_reset(unsigned long long *stats, hipStream_t stream) {
+    hipLaunchKernelGGL(stats_reset_kernel, dim3(1), dim3(64), 0, stream, stats);
     return hipGetLastError();
 }
 

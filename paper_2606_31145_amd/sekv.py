@@ -14,18 +14,24 @@ import numpy as np
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libsekv.so")
+# SEKV_LIB=trace selects the diagnostic phase-trace build of the same sources
+LIB_PATH = os.path.join(_PKG, "libsekv_trace.so" if os.environ.get("SEKV_LIB") == "trace"
+                        else "libsekv.so")
 
 SEKV_OK, SEKV_ERR_INVALID_ARG, SEKV_ERR_UNSUPPORTED, SEKV_ERR_WORKSPACE, SEKV_ERR_HIP = range(5)
 SEKV_F32, SEKV_BF16 = 0, 1
 SEKV_ZOOM_DEFAULT, SEKV_ZOOM_FACTORED = 0, 1
+SEKV_TIER_GATHER, SEKV_TIER_MEMCPY = 0, 1
+TIER_MODES = {"gather": SEKV_TIER_GATHER, "memcpy": SEKV_TIER_MEMCPY}
 DTYPE_CODES = {"f32": SEKV_F32, "bf16": SEKV_BF16}
 
-EXPORTED = ("sekv_status_string", "sekv_last_error", "sekv_check_dims", "sekv_workspace_size",
+EXPORTED = ("sekv_status_string", "sekv_last_error", "sekv_phase_trace", "sekv_check_dims",
+            "sekv_workspace_size",
             "sekv_workspace_init", "sekv_workspace_status", "sekv_route_topk",
             "sekv_zoom_attend", "sekv_decode_step", "sekv_graph_create", "sekv_graph_launch",
             "sekv_graph_destroy", "sekv_tier_create", "sekv_tier_destroy",
-            "sekv_tier_staging_size", "sekv_tier_last_copy", "sekv_decode_step_tiered")
+            "sekv_tier_staging_size", "sekv_tier_last_copy", "sekv_decode_step_tiered",
+            "sekv_validate_cache")
 
 
 class SekvError(RuntimeError):
@@ -67,6 +73,8 @@ def _load():
     lib.sekv_status_string.argtypes = [ctypes.c_int]
     lib.sekv_last_error.restype = ctypes.c_char_p
     lib.sekv_last_error.argtypes = []
+    lib.sekv_phase_trace.restype = ctypes.c_int
+    lib.sekv_phase_trace.argtypes = [VP, SZ]
     lib.sekv_check_dims.restype = ctypes.c_int
     lib.sekv_check_dims.argtypes = [P(Dims)]
     lib.sekv_workspace_size.restype = SZ
@@ -89,7 +97,7 @@ def _load():
     lib.sekv_graph_destroy.restype = ctypes.c_int
     lib.sekv_graph_destroy.argtypes = [VP]
     lib.sekv_tier_create.restype = ctypes.c_int
-    lib.sekv_tier_create.argtypes = [P(Dims), P(VP)]
+    lib.sekv_tier_create.argtypes = [P(Dims), ctypes.c_int32, P(VP)]
     lib.sekv_tier_destroy.restype = ctypes.c_int
     lib.sekv_tier_destroy.argtypes = [VP]
     lib.sekv_tier_staging_size.restype = SZ
@@ -99,6 +107,8 @@ def _load():
     lib.sekv_decode_step_tiered.restype = ctypes.c_int
     lib.sekv_decode_step_tiered.argtypes = [P(Dims), P(CacheStruct), P(HostFactorsStruct), VP, VP,
                                             VP, VP, SZ, VP, VP]
+    lib.sekv_validate_cache.restype = ctypes.c_int
+    lib.sekv_validate_cache.argtypes = [P(Dims), P(CacheStruct)]
     return lib
 
 
@@ -142,6 +152,14 @@ def make_dims(*, batch, n_q_heads, n_kv_heads, head_dim, rank, top_k, max_anchor
         odt = DTYPE_CODES[out_dtype] if isinstance(out_dtype, str) else int(out_dtype)
     return Dims(batch, n_q_heads, n_kv_heads, head_dim, rank, top_k, max_anchors, max_spans,
                 max_span_len, dt, odt, int(zoom), float(softmax_scale))
+
+
+def phase_trace(buf=None):
+    """sekv_phase_trace: attach a device int64 buffer (or detach with None)."""
+    if buf is None:
+        _check(LIB.sekv_phase_trace(None, 0))
+    else:
+        _check(LIB.sekv_phase_trace(_ptr(buf), buf.numel() * buf.element_size()))
 
 
 def check_dims(dims: Dims):
@@ -333,13 +351,17 @@ class HostFactors:
 
 
 class Tier:
-    """sekv_tier_*: pinned mirrors, device staging and events for tiered steps."""
+    """sekv_tier_*: pinned mirrors, device staging and events for tiered steps.
 
-    def __init__(self, dims: Dims):
+    mode "gather" (device-planned gather kernel, no host wait) or "memcpy" (host-planned
+    hipMemcpyAsync per run of neighbouring blocks)."""
+
+    def __init__(self, dims: Dims, mode: str = "gather"):
         h = ctypes.c_void_p(0)
-        _check(LIB.sekv_tier_create(ctypes.byref(dims), ctypes.byref(h)))
+        _check(LIB.sekv_tier_create(ctypes.byref(dims), TIER_MODES[mode], ctypes.byref(h)))
         self._h = h
         self.dims = dims
+        self.mode = mode
 
     @property
     def staging_bytes(self) -> int:
@@ -361,6 +383,25 @@ class Tier:
             self.destroy()
         except Exception:
             pass
+
+
+def validate_cache(dims: Dims, arrays: dict):
+    """sekv_validate_cache on host copies (numpy arrays, storage-typed as for
+    DeviceCache.from_arrays).  Raises SekvError with the first violation."""
+    keep = {}
+    for f in ("q", "anchor_k", "anchor_v", "sum_k", "sum_v"):
+        keep[f] = np.ascontiguousarray(arrays[f])
+    keep["n_anchors"] = np.ascontiguousarray(arrays["n_anchors"], dtype=np.int32)
+    keep["n_spans"] = np.ascontiguousarray(arrays["n_spans"], dtype=np.int32)
+    keep["span_len"] = np.ascontiguousarray(arrays["span_len"], dtype=np.int32)
+    keep["span_logsize"] = np.ascontiguousarray(arrays["span_logsize"], dtype=np.float64)
+    keep["block_off"] = np.ascontiguousarray(arrays["block_off"], dtype=np.int64)
+    keep["factors"] = np.ascontiguousarray(arrays["factors"], dtype=np.uint8)
+    c = lambda f: keep[f].ctypes.data if keep[f].size else None  # noqa: E731
+    cs = CacheStruct(c("q"), c("anchor_k"), c("anchor_v"), c("n_anchors"), c("sum_k"), c("sum_v"),
+                     c("n_spans"), c("span_len"), c("span_logsize"), c("factors"),
+                     int(keep["factors"].nbytes), c("block_off"))
+    _check(LIB.sekv_validate_cache(ctypes.byref(dims), ctypes.byref(cs)))
 
 
 def decode_step_tiered(dims: Dims, cache: DeviceCache, host: HostFactors, tier: Tier,

@@ -101,3 +101,34 @@ def test_empty_batch_is_a_no_op(S):
     fake = ctypes.c_void_p(0x10000)
     ws = S.workspace_size(d)
     assert S.LIB.sekv_decode_step(ctypes.byref(d), ctypes.byref(c), None, None, fake, ws, None) == 0
+
+
+def test_validate_cache_on_host_copies(S):
+    """sekv_validate_cache checks the device-side preconditions on host copies."""
+    import numpy as np
+
+    from synth import custom_spec, make_case
+    case = make_case(custom_spec(batch=2, n_q_heads=4, n_kv_heads=2, head_dim=64, rank=8,
+                                 top_k=2, context=900, dtype="bf16", seed=71))
+    arrays = dict(q=case.q, anchor_k=case.anchor_k, anchor_v=case.anchor_v,
+                  n_anchors=case.n_anchors, sum_k=case.sum_k, sum_v=case.sum_v,
+                  n_spans=case.n_spans, span_len=case.span_len, span_logsize=case.span_logsize,
+                  factors=case.factors, block_off=case.block_off)
+    d = _dims(S, **{k: v for k, v in case.dims().items()})
+    S.validate_cache(d, arrays)
+
+    def bad(field, fn, msg):
+        a = dict(arrays)
+        a[field] = np.array(arrays[field], copy=True)
+        fn(a[field])
+        with pytest.raises(S.SekvError) as ei:
+            S.validate_cache(d, a)
+        assert ei.value.status == S.SEKV_ERR_INVALID_ARG and msg in str(ei.value), str(ei.value)
+
+    bad("n_spans", lambda x: x.__setitem__(0, case.max_spans + 1), "n_spans")
+    bad("n_anchors", lambda x: x.__setitem__(1, -1), "n_anchors")
+    bad("span_len", lambda x: x.__setitem__((0, 0), 0), "span_len")
+    bad("span_logsize", lambda x: x.__setitem__((1, 2), 9.0), "span_logsize")
+    bad("block_off", lambda x: x.__setitem__((1, 1, 0), case.factors.nbytes), "outside")
+    bad("q", lambda x: x.__setitem__((0, 1, 3), 0x7FC0), "not finite")        # bf16 NaN
+    bad("sum_v", lambda x: x.__setitem__((1, 0, 0, 5), 0x7F80), "not finite")  # bf16 +inf

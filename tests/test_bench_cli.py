@@ -23,7 +23,7 @@ def test_more_than_one_gpu_exits_with_a_message():
 def test_kernel_hash_ignores_comments_and_blank_space(tmp_path, monkeypatch):
     src = tmp_path / "k.hip"
     src.write_text("// header\n__global__ void k(int *p) {  /* body */\n  p[0] = 1; // store\n}\n")
-    monkeypatch.setattr(bench, "KERNEL_SOURCE", str(src))
+    monkeypatch.setattr(bench, "KERNEL_SOURCES", [str(src)])
     h0 = bench.kernel_source_hash()
     src.write_text("// another header\n\n__global__   void k(int *p) {\n  p[0] = 1;\n}  /* end */\n")
     assert bench.kernel_source_hash() == h0

@@ -90,6 +90,56 @@ def test_graph_32layer_b32_shapes_two_layers(S):
     _run_graph_case(S, cases, replays=2)
 
 
+def test_graph_32layer_b32_planted_two_layers(S):
+    """The planted-needle variant at the 32-layer workload's per-layer shape, 2 layers."""
+    banner("graph: 32-layer batch-32 shapes, planted, 2 layers: generating")
+    cases = _layers(WORKLOADS["llama3-8b-32layer-32k-b32"], 2, variant="N")
+    banner("graph: 32-layer batch-32 shapes, planted: running")
+    _run_graph_case(S, cases, replays=2)
+
+
+@pytest.mark.slow
+def test_graph_32layer_b32_all_32_seeded_layers(S):
+    """The whole 32-layer step (batch 32, 32K context, rank 16, top-8): 32 independently
+    seeded layers replayed through one 32-node graph; every layer's selection bit for bit
+    and its output against the oracle, and every replay against the first."""
+    import torch
+    spec = WORKLOADS["llama3-8b-32layer-32k-b32"]
+    dev = torch.device("cuda:0")
+    dcs, refs, dims = [], [], None
+    for l in range(spec.n_layers):
+        c = make_case(spec, layer=l)
+        if dims is None:
+            dims = dims_for(S, c)
+        else:
+            assert (c.max_spans, c.max_anchors) == (dims.max_spans, dims.max_anchors)
+            dims.max_span_len = max(dims.max_span_len, c.max_span_len)
+        dcs.append(S.DeviceCache.from_arrays(case_arrays(c), c.dtype, dev))
+        ref = oracle_result(c)
+        refs.append((ref["sel"], ref["out"]))
+        del c
+        banner(f"graph: 32 seeded layers: layer {l} generated and checked by the oracle")
+    ws = S.Workspace(dims, dev)
+    g = S.LayerGraph(dims, dcs, ws)
+    try:
+        first = None
+        for rep in range(2):
+            sel, out = g.launch()
+            torch.cuda.synchronize()
+            assert ws.status() == 0
+            if first is None:
+                first = (sel.clone(), out.clone())
+                for l, (rs, ro) in enumerate(refs):
+                    assert np.array_equal(sel[l].cpu().numpy(), rs), f"layer {l}: selection differs"
+                    assert_out_close(out_to_f64(out[l]), ro, "bf16", where=f"layer {l}")
+            else:
+                assert torch.equal(sel, first[0]) and torch.equal(out.view(torch.uint8),
+                                                                  first[1].view(torch.uint8))
+            banner(f"graph: 32 seeded layers: replay {rep} checked")
+    finally:
+        g.destroy()
+
+
 def test_graph_rejects_bad_layers(S):
     import torch
     dev = torch.device("cuda:0")

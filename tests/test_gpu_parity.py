@@ -169,6 +169,58 @@ def test_workspace_reuse_across_shapes(S):
     assert ws.status() == 0
 
 
+def test_workspace_reuse_few_then_many_pairs(S):
+    """One workspace, calls alternating between 2 and 160 (sequence, KV head) pairs: the
+    second layout's counters and tagged words lie where the first layout kept other data,
+    so the library must re-zero the workspace when the layout changes."""
+    import torch
+    dev = torch.device("cuda:0")
+    few = make_case(custom_spec(batch=1, n_q_heads=8, n_kv_heads=2, head_dim=64, rank=16, top_k=2,
+                                context=1500, dtype="bf16", seed=35, span_min=16, span_max=64))
+    many = make_case(custom_spec(batch=40, n_q_heads=8, n_kv_heads=4, head_dim=64, rank=16,
+                                 top_k=9, context=1200, n_prefix_anchors=16, window=32,
+                                 dtype="bf16", seed=36, span_min=16, span_max=96), variant="N")
+    nbytes = max(S.workspace_size(dims_for(S, few)), S.workspace_size(dims_for(S, many)))
+    ws = S.Workspace(dims_for(S, many), dev, nbytes=nbytes)
+    refs = {id(c): oracle_result(c) for c in (few, many)}
+    dcs = {id(c): S.DeviceCache.from_arrays(case_arrays(c), c.dtype, dev) for c in (few, many)}
+    for i, case in enumerate((few, many, few, many, many, few)):
+        banner(f"workspace reuse: call {i}, {case.spec.batch * case.spec.n_kv_heads} pairs")
+        ref = refs[id(case)]
+        sel, out = S.decode_step(dims_for(S, case), dcs[id(case)], ws)
+        torch.cuda.synchronize()
+        assert ws.status() == 0, f"call {i}"
+        assert np.array_equal(sel.cpu().numpy(), ref["sel"]), f"call {i}: selection differs"
+        assert_out_close(out_to_f64(out), ref["out"], case.dtype, where=f"call {i}")
+
+
+def test_step_completes_while_another_stream_holds_the_device(S):
+    """A decode step launched while matrix products on a second stream (same priority)
+    hold compute units: work items are claimed in order, so the step's waits end and
+    its results are exact, whatever the residency."""
+    import torch
+    banner("concurrent: decode_step beside matmuls on a second stream")
+    dev = torch.device("cuda:0")
+    case = make_case(WORKLOADS["llama3-8b-layer-32k"], variant="N")
+    ref = oracle_result(case)
+    dc = S.DeviceCache.from_arrays(case_arrays(case), case.dtype, dev)
+    dims = dims_for(S, case)
+    ws = S.Workspace(dims, dev)
+    a = torch.randn(4096, 4096, device=dev, dtype=torch.bfloat16)
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        with torch.cuda.stream(side):
+            for _ in range(8):
+                b = a @ a
+        sel, out = S.decode_step(dims, dc, ws)
+        torch.cuda.synchronize()
+        assert ws.status() == 0, f"rep {rep}: a wait timed out"
+        assert np.array_equal(sel.cpu().numpy(), ref["sel"]), f"rep {rep}: selection differs"
+        assert_out_close(out_to_f64(out), ref["out"], case.dtype, where=f"concurrent rep {rep}")
+    del b
+
+
 # One small case per kernel instantiation (storage type x head_dim x group size), so every
 # compiled variant of the step kernel is checked against the oracle.
 INSTANTIATIONS = [(dt, d, g) for dt in ("bf16", "f32") for d in (64, 128) for g in (1, 2, 4, 8)]
