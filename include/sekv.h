@@ -173,6 +173,22 @@ SEKV_API sekv_status sekv_zoom_attend(const sekv_dims *dims, const sekv_cache *c
 SEKV_API sekv_status sekv_decode_step(const sekv_dims *dims, const sekv_cache *cache, int32_t *sel,
                              void *out, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): sekv_decode_step with its workspace
+ * in a static device array the library holds on every device it runs on, until the
+ * process ends (SEKV_NOALLOC_MAX_WORKSPACE bytes per device).  Allocates nothing: the
+ * first call on a device looks up the array's address there; the caller passes inputs
+ * and outputs as for sekv_decode_step.  Shapes whose sekv_workspace_size exceeds the
+ * array are refused with SEKV_ERR_WORKSPACE.  Every call on a device shares that
+ * device's array: calls that may overlap on one device (several streams or threads)
+ * race and give wrong results; order them on one stream.  The array keeps the last
+ * call's contents; the library zeroes it (a kernel on `stream`) on its first use and
+ * whenever the shapes change.  sekv_workspace_status cannot read this array; a
+ * device-side wait timeout or out-of-arena block is not reported. */
+#define SEKV_NOALLOC_MAX_WORKSPACE (16u << 20)
+SEKV_API sekv_status sekv_decode_step_noalloc(const sekv_dims *dims, const sekv_cache *cache,
+                                              int32_t *sel, void *out, hipStream_t stream);
+
 /* ----------------------------------------------------------------------------------
  * Several layers in one HIP graph.  A decode step of an L-layer model runs the step
  * above once per layer (each attention layer keeps its own span cache, Sec. 3.2; the

@@ -190,6 +190,13 @@ sekv_status run(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *sel_
 
 }  // namespace
 
+namespace sekv {
+sekv_status run_fused_step(const sekv_dims *d, const sekv_cache *c, int32_t *sel, void *out, void *ws,
+                           size_t ws_bytes, hipStream_t stream) {
+    return run(kModeFused, d, c, sel, nullptr, nullptr, nullptr, out, ws, ws_bytes, stream);
+}
+}  // namespace sekv
+
 extern "C" {
 
 const char *sekv_status_string(sekv_status status) {

@@ -179,4 +179,8 @@ hipError_t launch_tier_gather(const TierGatherArgs &a, hipStream_t stream);
 hipError_t launch_stats_reset(unsigned long long *stats, hipStream_t stream);
 int resident_workgroups(int dtype, int head_dim, int group);
 
+// The fused step on a given workspace, with every host check (sekv_api.cpp).
+sekv_status run_fused_step(const sekv_dims *d, const sekv_cache *c, int32_t *sel, void *out, void *ws,
+                           size_t ws_bytes, hipStream_t stream);
+
 }  // namespace sekv

@@ -31,7 +31,7 @@ EXPORTED = ("sekv_status_string", "sekv_last_error", "sekv_phase_trace", "sekv_c
             "sekv_zoom_attend", "sekv_decode_step", "sekv_graph_create", "sekv_graph_launch",
             "sekv_graph_destroy", "sekv_tier_create", "sekv_tier_destroy",
             "sekv_tier_staging_size", "sekv_tier_last_copy", "sekv_decode_step_tiered",
-            "sekv_validate_cache")
+            "sekv_validate_cache", "sekv_decode_step_noalloc")
 
 
 class SekvError(RuntimeError):
@@ -107,6 +107,8 @@ def _load():
     lib.sekv_decode_step_tiered.restype = ctypes.c_int
     lib.sekv_decode_step_tiered.argtypes = [P(Dims), P(CacheStruct), P(HostFactorsStruct), VP, VP,
                                             VP, VP, SZ, VP, VP]
+    lib.sekv_decode_step_noalloc.restype = ctypes.c_int
+    lib.sekv_decode_step_noalloc.argtypes = [P(Dims), P(CacheStruct), VP, VP, VP]
     lib.sekv_validate_cache.restype = ctypes.c_int
     lib.sekv_validate_cache.argtypes = [P(Dims), P(CacheStruct)]
     return lib
@@ -288,6 +290,22 @@ def decode_step(dims: Dims, cache: DeviceCache, ws: Workspace, sel=None, out=Non
     cs = cache.struct()
     _check(LIB.sekv_decode_step(ctypes.byref(dims), ctypes.byref(cs), _ptr(sel), _ptr(out),
                                 ws.ptr, ws.nbytes, _stream(stream)))
+    return sel, out
+
+
+NOALLOC_MAX_WORKSPACE = 16 << 20
+
+
+def decode_step_noalloc(dims: Dims, cache: DeviceCache, sel=None, out=None, stream=None):
+    """sekv_decode_step_noalloc (the library's static device workspace): returns (sel, out)."""
+    dev = cache.t["q"].device
+    if sel is None:
+        sel = _alloc((dims.batch, dims.n_kv_heads, max(dims.top_k, 0)), torch.int32, dev)
+    if out is None:
+        out = _out_tensor(dims, dev)
+    cs = cache.struct()
+    _check(LIB.sekv_decode_step_noalloc(ctypes.byref(dims), ctypes.byref(cs), _ptr(sel), _ptr(out),
+                                        _stream(stream)))
     return sel, out
 
 
