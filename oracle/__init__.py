@@ -4,15 +4,23 @@ product path."""
 
 from .sekv_oracle import (  # noqa: F401
     decode_step,
+    decode_step_gated,
+    gate,
+    gate_logits,
+    gated_selection,
     group_keys,
     merge_partials,
     mixed_attention_head,
+    project_queries,
     read_span_block,
     reconstruct,
     routing_logits,
     select_topk,
     softmax_partial,
     softmax_weights,
+    summary_key,
+    surprisal_weights,
+    threshold_logit,
     widen,
     zoom_attend,
     zoom_scores_factored,

@@ -17,6 +17,10 @@ reconstruction of Sec. 3.2):
    one coarse entry per unexpanded span with ln|S| added to its score, and
    the reconstructed tokens of the expanded spans (Sec. 3.3).
 
+The end of the module adds the paper's own selection rule (learned routing
+projection, sigmoid gate, per-head thresholds and the budget cap), which
+replaces steps 1-2 and keeps steps 3-4.
+
 Readings taken where the paper leaves the decode step open (each is listed
 with its reason in the design notes):
 
@@ -260,3 +264,160 @@ def zoom_scores_factored(qh, scale, U, sigma, Vt):
 def zoom_values_factored(p, U, sigma, Vt):
     """sum_t p_t V_hat_t without forming V_hat: ((p^T U) * sigma) Vt."""
     return ((p @ U) * sigma) @ Vt
+
+
+# ---------------------------------------------------------------------------
+# learned routing: the paper's own selection rule
+# (Sec. 3.2 eqs. surprisal_weight, summary_key, query_projection, routing_gate;
+#  Sec. 3.3 eq. zoom_decision and the budget cap)
+# ---------------------------------------------------------------------------
+#
+# Readings (each listed with its reason in the design notes):
+#
+# * Indices.  The projections are per query head (Sec. 3.3, learnable-parameters
+#   paragraph: L x H x d' x d_h with H the 32 query heads): W[h] is d' x d_h, and query
+#   head h routes against summaries built from its KV head's keys with its own
+#   W[h], so the routing summaries are [B][Hq][M][d'].  Thresholds are per
+#   query head.
+# * Union per KV head.  z[h,S] decides per query head; the factors belong to
+#   the KV head, so a span is expanded for a (sequence, KV head) pair when any
+#   of its query heads votes for it, and the expanded tokens serve every query
+#   head of the group (a span whose tokens are on hand is not also kept coarse).
+# * Budget cap.  Candidates (spans with at least one vote) are ordered by the
+#   largest pre-sigmoid gate among the voting heads, descending, ties to the
+#   lower span index (the sigmoid is strictly increasing, so this is the order
+#   of alpha~).  The longest prefix of that order whose token count stays within
+#   the budget and whose length stays within the count cap is expanded.
+# * The threshold is applied in logit space: alpha~ > tau is the same event as
+#   x > ln(tau / (1 - tau)), and the threshold enters as that logit.
+#
+# Floating point (selection must be bit exact, as for the identity routing):
+# q' = W q is summed left to right over d_h in float64 (products of stored
+# values are exact) and rounded once to float32; the gate's dot product
+# q' . Kbar is summed left to right over d' in float64 (float32 x stored
+# products are exact); then x = (s * (1/sqrt(d'))) + ln|S| as two separately
+# rounded float64 operations.  1/sqrt(d') is 1.0 / sqrt(float(d')) in float64.
+
+def surprisal_weights(H) -> np.ndarray:
+    """Span-local token weights w_t = H_t / sum_k H_k (eq. surprisal_weight)."""
+    H = np.asarray(H, dtype=np.float64)
+    return H / H.sum()
+
+
+def summary_key(K_tokens, weights, W) -> np.ndarray:
+    """Normalised, weighted, projected routing summary of one span (eq. summary_key).
+
+    K_tokens [|S|][d_h], weights [|S|], W [d'][d_h]; returns [d'] of unit norm.
+    """
+    K = np.asarray(K_tokens, dtype=np.float64)
+    w = np.asarray(weights, dtype=np.float64)
+    Wm = np.asarray(W, dtype=np.float64)
+    x = np.zeros(Wm.shape[0])
+    for t in range(K.shape[0]):
+        x = x + w[t] * (Wm @ K[t])
+    return x / np.linalg.norm(x)
+
+
+def project_queries(q, W) -> np.ndarray:
+    """q'[b,h] = W[h] q[b,h] for every query head (eq. query_projection).
+
+    q [B][Hq][d_h] and W [Hq][d'][d_h] as float64 values of stored numbers.
+    Summed left to right over d_h in float64, then rounded to float32.
+    Returns the float32 values as float64, [B][Hq][d'].
+    """
+    q = np.asarray(q, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    B, Hq, d = q.shape
+    out = np.zeros((B, Hq, W.shape[1]))
+    for j in range(d):
+        out = out + W[None, :, :, j] * q[:, :, None, j]
+    return out.astype(np.float32).astype(np.float64)
+
+
+def gate_logits(q_proj, sum_route, span_logsize, n_spans) -> np.ndarray:
+    """Pre-sigmoid routing gate x[b,h,S] = q'.Kbar[b,h,S] / sqrt(d') + ln|S| (eq. routing_gate).
+
+    q_proj [B][Hq][d'] (from project_queries), sum_route [B][Hq][M][d'].  The
+    dot product is summed left to right in float64; padding spans get -inf.
+    """
+    qp = np.asarray(q_proj, dtype=np.float64)
+    kr = np.asarray(sum_route, dtype=np.float64)
+    B, Hq, dr = qp.shape
+    M = kr.shape[2]
+    scale = 1.0 / np.sqrt(float(dr))
+    out = np.full((B, Hq, M), -np.inf)
+    for b in range(B):
+        m = int(n_spans[b])
+        for h in range(Hq):
+            s = np.zeros(m)
+            for i in range(dr):
+                s = s + qp[b, h, i] * kr[b, h, :m, i]
+            out[b, h, :m] = s * scale + span_logsize[b, :m]
+    return out
+
+
+def gate(x) -> np.ndarray:
+    """The routing gate alpha~ = sig(x) of eq. routing_gate."""
+    x = np.asarray(x, dtype=np.float64)
+    return 1.0 / (1.0 + np.exp(-x))
+
+
+def threshold_logit(tau) -> np.ndarray:
+    """x-space threshold of eq. zoom_decision: sig(x) > tau exactly when x > ln(tau / (1 - tau))."""
+    tau = np.asarray(tau, dtype=np.float64)
+    return np.log(tau) - np.log1p(-tau)
+
+
+def gated_selection(x, thresholds, span_len, n_spans, n_kv_heads: int, max_zoom: int,
+                    budget_tokens: int) -> np.ndarray:
+    """Spans to expand per (b, KV head): eq. zoom_decision, then the budget cap of Sec. 3.3.
+
+    x [B][Hq][M] pre-sigmoid gates, thresholds [Hq] in x space.  Listed in
+    expansion order; unused slots hold -1.  Returns int32 [B][Hkv][max_zoom].
+    """
+    B, Hq, M = x.shape
+    G = Hq // n_kv_heads
+    sel = np.full((B, n_kv_heads, max_zoom), -1, dtype=np.int32)
+    for b in range(B):
+        m = int(n_spans[b])
+        for g in range(n_kv_heads):
+            heads = range(g * G, (g + 1) * G)
+            cands = []
+            for S in range(m):
+                votes = [x[b, h, S] for h in heads if x[b, h, S] > thresholds[h]]
+                if votes:
+                    cands.append((max(votes), S))
+            cands.sort(key=lambda c: (-c[0], c[1]))
+            used, chosen = 0, []
+            for _, S in cands:
+                if len(chosen) == max_zoom or used + int(span_len[b, S]) > budget_tokens:
+                    break
+                chosen.append(S)
+                used += int(span_len[b, S])
+            sel[b, g, :len(chosen)] = chosen
+    return sel
+
+
+def decode_step_gated(q, anchor_k, anchor_v, n_anchors, sum_k, sum_v, n_spans, span_len,
+                      span_logsize, factors, block_off, proj, sum_route, thresholds, *,
+                      rank: int, max_zoom: int, budget_tokens: int, softmax_scale: float,
+                      dtype: str) -> dict:
+    """One decode step under the learned selection rule.
+
+    The routing (projection, gate, threshold, budget) decides which spans are
+    expanded; the attention is the same mixed-resolution softmax as for the
+    identity routing, with unexpanded spans entering as their coarse mean key
+    and value, score scale * q . k_bar + ln|S| (Sec. 3.3).
+    """
+    qf = widen(q, dtype)
+    qp = project_queries(qf, widen(proj, dtype))
+    x = gate_logits(qp, widen(sum_route, dtype), np.asarray(span_logsize, np.float64), n_spans)
+    Hkv = np.asarray(sum_k).shape[1]
+    sel = gated_selection(x, np.asarray(thresholds, np.float64), span_len, n_spans, Hkv,
+                          max_zoom, budget_tokens)
+    coarse = routing_logits(qf, widen(sum_k, dtype), np.asarray(span_logsize, np.float64),
+                            n_spans, softmax_scale)
+    out = zoom_attend(q, anchor_k, anchor_v, n_anchors, sum_v, n_spans, span_len, factors,
+                      block_off, sel, coarse, rank=rank, softmax_scale=softmax_scale,
+                      dtype=dtype)
+    return {"sel": sel, "out": out, "gate_logits": x, "q_proj": qp}

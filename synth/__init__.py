@@ -4,7 +4,9 @@ This package builds the stored inputs of one decode step (query, anchor K/V,
 span summaries, span factor blocks and the span tables) for the workload
 shapes the decode-step tests and benchmark use.  It plays the part of the
 paper's prefill stage for synthetic data only: it draws values, partitions the
-context into spans, and forms each span's coarse mean key/value.  It holds
+context into spans, and forms each span's coarse mean key/value and, for the
+learned selection rule, random routing projections, the projected normalised
+routing summaries and the zoom thresholds.  It holds
 none of the decode step's arithmetic (routing, selection, reconstruction for
 attention, softmax), and it imports neither the oracle nor the HIP library.
 """
@@ -19,4 +21,7 @@ from .cases import (  # noqa: F401
     custom_spec,
     f64_to_bf16_bits,
     make_case,
+    Gate,
+    NO_BUDGET,
+    make_gate,
 )

@@ -72,6 +72,7 @@ _CHUNK = 1 << 20
 ST_PART, ST_Q, ST_AK, ST_AV = 1, 2, 3, 4
 ST_UK, ST_SK, ST_VK, ST_UV, ST_SV, ST_VV = 5, 6, 7, 8, 9, 10
 ST_NEEDLE = 11
+ST_PROJ, ST_TAU = 12, 13
 
 VARIANTS = {"L": 0, "N": 1}
 PLANT_DELTA = 6.0
@@ -607,3 +608,79 @@ def case_from_factors(q, anchor_k, anchor_v, span_factors, *, dtype: str, top_k:
                 span_len=span_len, span_logsize=span_logsize, factors=arena,
                 block_off=block_off)
     return case
+
+
+# ---------------------------------------------------------------------------
+# inputs of the learned routing rule
+# ---------------------------------------------------------------------------
+
+NO_BUDGET = 1 << 62
+
+
+@dataclass
+class Gate:
+    """Stored inputs of the learned selection rule for one layer.
+
+    proj       [Hq][d'][d]        routing projection W of each query head (storage type)
+    sum_route  [B][Hq][M_max][d'] normalised projected span summaries (storage type)
+    thresholds [Hq] float64       zoom thresholds as pre-sigmoid values, ln(tau / (1 - tau))
+    tau        [Hq] float64       the same thresholds as probabilities
+    budget_tokens                 expanded tokens allowed per (sequence, KV head)
+    """
+    route_dim: int
+    proj: np.ndarray
+    sum_route: np.ndarray
+    thresholds: np.ndarray
+    tau: np.ndarray
+    budget_tokens: int
+
+
+def make_gate(case: Case, route_dim: int = 32, tau="permissive", budget_tokens: int = NO_BUDGET,
+              proj_f64: np.ndarray | None = None) -> Gate:
+    """Random stand-ins for the trained routing parameters of a case.
+
+    The trained projections are not available: W[h] has i.i.d. normal entries of
+    variance 1/d', so that (W q) . (W k) estimates q . k.  The routing summary of
+    span S for head h is W[h] k_bar_S normalised, with k_bar_S the stored mean
+    key of the span (with uniform token weights the weighted projected mean is the
+    projection of the mean).  tau: "permissive" (0.05 for every head, the
+    initialisation the paper trains from), a float or an array of per-head
+    probabilities, or "spread": per-head thresholds ln(L_h) with L_h drawn
+    log-uniformly from the span-length range, so that some spans of every
+    length class fall on either side.  proj_f64 replaces the random W (its
+    values are rounded to storage).
+    """
+    s = case.spec
+    B, Hq, Hkv, d = s.batch, s.n_q_heads, s.n_kv_heads, s.head_dim
+    G = Hq // Hkv
+    dt = s.dtype
+    dr = int(route_dim)
+    vkey = (s.seed, VARIANTS[case.variant], case.layer)
+    if proj_f64 is None:
+        w64 = np.stack([normals(stream_key(*vkey, ST_PROJ, h), dr * d).reshape(dr, d)
+                        for h in range(Hq)]) / math.sqrt(dr)
+    else:
+        w64 = np.asarray(proj_f64, dtype=np.float64).reshape(Hq, dr, d)
+    proj = to_storage(w64, dt)
+    wdec = from_storage(proj, dt)
+    kbar = from_storage(case.sum_k, dt)
+    M = case.sum_k.shape[2]
+    sr = np.zeros((B, Hq, M, dr), dtype=np.float64)
+    for b in range(B):
+        m = int(case.n_spans[b])
+        for h in range(Hq):
+            x = kbar[b, h // G, :m] @ wdec[h].T
+            nrm = np.sqrt((x * x).sum(axis=1))
+            nz = nrm > 0
+            sr[b, h, :m][nz] = x[nz] / nrm[nz, None]
+    if isinstance(tau, str) and tau == "spread":
+        u = uniforms(stream_key(*vkey, ST_TAU), Hq)
+        lo, hi = math.log(max(s.span_min, 1)), math.log(max(s.span_max, 1) + 1)
+        thr = lo + u * (hi - lo)
+        taus = 1.0 / (1.0 + np.exp(-thr))
+    else:
+        taus = np.full(Hq, 0.05) if (isinstance(tau, str) and tau == "permissive") else \
+            np.broadcast_to(np.asarray(tau, dtype=np.float64), (Hq,)).copy()
+        thr = np.array([math.log(t / (1.0 - t)) for t in taus])
+    return Gate(route_dim=dr, proj=proj, sum_route=to_storage(sr, dt), thresholds=thr,
+                tau=taus, budget_tokens=int(budget_tokens))

@@ -97,3 +97,19 @@ def test_literal_layer_is_near_uniform():
     kd = from_storage(case.sum_k[0, 0, :5], "bf16")
     assert np.abs(qd[0, 0] @ kd.T * case.spec.softmax_scale).max() < 1e-3
     assert math.isclose(case.spec.softmax_scale, 1 / math.sqrt(128))
+
+
+def test_gate_inputs_are_deterministic_and_normalised():
+    from synth import make_gate
+    from synth.cases import from_storage
+    case = make_case(custom_spec(dtype="f32", n_q_heads=4, n_kv_heads=2, head_dim=16, context=300, seed=41))
+    a = make_gate(case, route_dim=8, tau="spread")
+    b = make_gate(case, route_dim=8, tau="spread")
+    assert np.array_equal(a.proj, b.proj) and np.array_equal(a.sum_route, b.sum_route)
+    assert np.array_equal(a.thresholds, b.thresholds)
+    kr = from_storage(a.sum_route, "f32")
+    m = int(case.n_spans[0])
+    assert np.allclose(np.linalg.norm(kr[0, :, :m], axis=-1), 1.0, atol=1e-6)
+    assert np.all(kr[0, :, m:] == 0)
+    p = make_gate(case, route_dim=8)
+    assert np.all(p.tau == 0.05) and np.allclose(p.thresholds, np.log(0.05 / 0.95))
