@@ -190,6 +190,50 @@ SEKV_API sekv_status sekv_decode_step_noalloc(const sekv_dims *dims, const sekv_
                                               int32_t *sel, void *out, hipStream_t stream);
 
 /* ----------------------------------------------------------------------------------
+ * The paper's own selection rule (learned routing).  In place of steps 1-2 above:
+ *   q'_h = W_h q_h                                  (Sec. 3.2 eq. query_projection)
+ *   x_h,S = q'_h . Kbar_h,S / sqrt(d') + ln|S|      (eq. routing_gate, before the sigmoid)
+ *   query head h votes for span S when x_h,S > ln(tau_h / (1 - tau_h)), i.e. when the
+ *   gate sig(x_h,S) exceeds its threshold tau_h       (Sec. 3.3 eq. zoom_decision)
+ * A span is expanded for its (sequence, KV head) when a query head of the group votes for
+ * it; voted spans are taken in decreasing order of their largest voting gate (ties to the
+ * lower span index) while the expanded tokens stay within budget_tokens and the count
+ * within top_k (the budget cap of Sec. 3.3); the expanded spans serve every query head of
+ * the group.  The selection is exact: q' is summed over d in float64 in index order and
+ * rounded once to float32, the gate's dot product is summed over d' in float64 in index
+ * order, then x = (s * (1/sqrt(d'))) + ln|S| with two roundings (1/sqrt(d') computed in
+ * float64 as 1.0 / sqrt(d')).
+ * ---------------------------------------------------------------------------------- */
+typedef struct {
+    int32_t route_dim;          /* d': multiple of 8, 8 <= d' <= 64                        */
+    int32_t reserved;           /* must be 0                                               */
+    int64_t budget_tokens;      /* >= 0: expanded tokens allowed per (sequence, KV head)   */
+    const void *proj;           /* device [Hq][d'][d], storage dtype: W of each query head */
+    const void *sum_route;      /* device [B][Hq][M_max][d'], storage dtype: routing
+                                   summaries (normalised, eq. summary_key); rows past
+                                   n_spans[b] are ignored                                  */
+    const double *thresholds;   /* device double [Hq]: ln(tau_h / (1 - tau_h))             */
+} sekv_gate;
+
+/* Selection under the learned rule.  Reads q, n_spans, span_len, span_logsize (not the
+ * factors or the summaries' keys/values) and the gate arrays; proj and sum_route 16-byte
+ * aligned, thresholds and gate_logits 8-byte.
+ *   sel          out, int32 [B][Hkv][top_k]: expanded spans in expansion order, -1 after
+ *   gate_logits  out, double [B][Hq][M_max] or NULL: x_h,S (-inf past n_spans[b]);
+ *                the gate itself is sig(x)
+ * One launch, no wait between workgroups; uses its own section of the workspace. */
+SEKV_API sekv_status sekv_route_gated(const sekv_dims *dims, const sekv_cache *cache,
+                                      const sekv_gate *gate, int32_t *sel, double *gate_logits,
+                                      void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* One decode step under the learned rule: sekv_route_gated, then sekv_zoom_attend with
+ * that selection (coarse entries of unexpanded spans use scale * q.k_bar + ln|S|, as in
+ * the step above).  Two launches on `stream`. */
+SEKV_API sekv_status sekv_decode_step_gated(const sekv_dims *dims, const sekv_cache *cache,
+                                            const sekv_gate *gate, int32_t *sel, void *out,
+                                            void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ----------------------------------------------------------------------------------
  * Several layers in one HIP graph.  A decode step of an L-layer model runs the step
  * above once per layer (each attention layer keeps its own span cache, Sec. 3.2; the
  * per-layer cost analysis of App. D sums over layers).  sekv_graph_create validates

@@ -286,6 +286,99 @@ sekv_status sekv_decode_step(const sekv_dims *dims, const sekv_cache *cache, int
                stream);
 }
 
+}  // extern "C"
+
+namespace {
+
+// Validate a learned-routing call and fill its launch parameters.  *launch is false when
+// there is nothing to compute.
+sekv_status gate_prepare(const sekv_dims *d, const sekv_cache *c, const sekv_gate *gt, int32_t *sel,
+                         double *gate_logits, void *ws, size_t ws_bytes, sekv::GateParams *gp,
+                         bool *launch) {
+    *launch = false;
+    sekv_status st = check_dims_impl(d);
+    if (st != SEKV_OK) return st;
+    st = check_cache(d, c, false);
+    if (st != SEKV_OK) return st;
+    st = check_ws(d, ws, ws_bytes);
+    if (st != SEKV_OK) return st;
+    if (!gt) return fail(SEKV_ERR_INVALID_ARG, "gate is NULL");
+    const int dr = gt->route_dim;
+    if (dr < 8 || dr > sekv::kGateMaxDr || dr % 8)
+        return fail(SEKV_ERR_UNSUPPORTED, "route_dim %d: need a multiple of 8 in [8, %d]", dr,
+                    sekv::kGateMaxDr);
+    if (gt->reserved != 0) return fail(SEKV_ERR_INVALID_ARG, "gate.reserved must be 0");
+    if (gt->budget_tokens < 0) return fail(SEKV_ERR_INVALID_ARG, "budget_tokens < 0");
+    auto mis = [](const void *q, uintptr_t a) { return (reinterpret_cast<uintptr_t>(q) & (a - 1)) != 0; };
+    if (!gt->proj || !gt->sum_route || !gt->thresholds)
+        return fail(SEKV_ERR_INVALID_ARG, "gate proj, sum_route or thresholds is NULL");
+    if (mis(gt->proj, 16) || mis(gt->sum_route, 16) || mis(gt->thresholds, 8) || mis(gate_logits, 8) ||
+        mis(sel, 4))
+        return fail(SEKV_ERR_INVALID_ARG, "gate arrays misaligned");
+    if (d->batch == 0) return SEKV_OK;
+    if (d->top_k > 0 && !sel) return fail(SEKV_ERR_INVALID_ARG, "sel is NULL");
+    const sekv::Shape s = sekv::make_shape(*d);
+    if (s.G > sekv::kGateMaxG || s.d > 128 || s.g_nrc * (s.k > 0 ? s.k : 1) > sekv::kGateMaxCand)
+        return fail(SEKV_ERR_UNSUPPORTED, "shapes outside the learned-routing kernel's limits");
+    const sekv::WsLayout L = sekv::make_layout(s);
+    unsigned char *w = static_cast<unsigned char *>(ws);
+    sekv::GateParams g{};
+    g.B = s.B; g.Hq = s.Hq; g.Hkv = s.Hkv; g.G = s.G; g.d = s.d; g.dr = dr; g.k = s.k;
+    g.M_max = s.M_max; g.cr = s.g_cr; g.n_rc = s.g_nrc;
+    g.budget = gt->budget_tokens;
+    g.scale_r = 1.0 / std::sqrt(double(dr));
+    g.q = c->q; g.proj = gt->proj; g.sum_route = gt->sum_route;
+    g.n_spans = c->n_spans; g.span_len = c->span_len; g.span_logsize = c->span_logsize;
+    g.thr = gt->thresholds;
+    g.sel = sel; g.gate_out = gate_logits;
+    g.cnt = reinterpret_cast<uint32_t *>(w + L.gate_cnt);
+    g.cand = reinterpret_cast<uint64_t *>(w + L.gate_cand);
+    *gp = g;
+    *launch = s.k > 0 || gate_logits != nullptr;
+    return SEKV_OK;
+}
+
+sekv_status run_gate(const sekv_dims *d, const sekv_cache *c, const sekv_gate *gt, int32_t *sel,
+                     double *gate_logits, void *ws, size_t ws_bytes, hipStream_t stream) {
+    sekv::GateParams g{};
+    bool launch = false;
+    const sekv_status st = gate_prepare(d, c, gt, sel, gate_logits, ws, ws_bytes, &g, &launch);
+    if (st != SEKV_OK || !launch) return st;
+    hipError_t e = ws_prepare(ws, ws_bytes, sekv::layout_key(sekv::make_shape(*d)), 1, stream);
+    if (e != hipSuccess) return hip_fail(e, "workspace zero kernel");
+    e = sekv::launch_gate(g, d->dtype, stream);
+    if (e != hipSuccess) return hip_fail(e, "learned-routing kernel launch");
+    return SEKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sekv_status sekv_route_gated(const sekv_dims *dims, const sekv_cache *cache, const sekv_gate *gate,
+                             int32_t *sel, double *gate_logits, void *ws, size_t ws_bytes,
+                             hipStream_t stream) {
+    return run_gate(dims, cache, gate, sel, gate_logits, ws, ws_bytes, stream);
+}
+
+sekv_status sekv_decode_step_gated(const sekv_dims *dims, const sekv_cache *cache,
+                                   const sekv_gate *gate, int32_t *sel, void *out, void *ws,
+                                   size_t ws_bytes, hipStream_t stream) {
+    // validate both halves before enqueuing either
+    sekv::GateParams g{};
+    bool launch = false;
+    sekv_status st = gate_prepare(dims, cache, gate, sel, nullptr, ws, ws_bytes, &g, &launch);
+    if (st != SEKV_OK) return st;
+    sekv::Params p{};
+    bool launch2 = false;
+    st = prepare(sekv::kModeAttend, dims, cache, nullptr, nullptr, sel, nullptr, out, ws, ws_bytes, &p,
+                 &launch2);
+    if (st != SEKV_OK) return st;
+    st = run_gate(dims, cache, gate, sel, nullptr, ws, ws_bytes, stream);
+    if (st != SEKV_OK) return st;
+    return run(sekv::kModeAttend, dims, cache, nullptr, nullptr, sel, nullptr, out, ws, ws_bytes, stream);
+}
+
 struct sekv_graph {
     hipGraph_t graph;
     hipGraphExec_t exec;

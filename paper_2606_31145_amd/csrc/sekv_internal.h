@@ -28,6 +28,13 @@ constexpr int kRoundItems = 512;   // items a launch starts at once on a 256-CU 
 
 enum Mode : int32_t { kModeRoute = 0, kModeAttend = 1, kModeFused = 2 };
 
+// Learned-routing selection (sekv_gate.hip): one workgroup scores a chunk of spans,
+// a power of two >= kGateMinChunk chosen so that a pair's candidates fit one LDS sort.
+constexpr int kGateMinChunk = 256;
+constexpr int kGateMaxCand = 2048;  // candidates (chunks x k) of a pair, and the largest chunk
+constexpr int kGateMaxDr = 64;      // largest routing dimension d'
+constexpr int kGateMaxG = 8;        // largest Hq / Hkv
+
 // Phase trace (diagnostic builds compiled with SEKV_PHASE_TRACE): per work item,
 // kTraceSlots int64 words; slot 0 holds the item's descriptor, the others the
 // s_memrealtime value (100 MHz) at the phase marks listed with the kernel.
@@ -59,6 +66,8 @@ struct WsLayout {
     size_t tlg;                               // tagged uint64 [P][G][M_max]: base-2 logits
     size_t part_ml;                           // float pairs (m, l) [P][n_zi][G]
     size_t part_o;                            // float pairs [P][n_zi][G][d/2]
+    size_t gate_cnt;                          // uint32 [P]: learned-routing chunks done
+    size_t gate_cand;                         // uint64 pairs [P][g_nrc][k]: chunk candidates
     size_t total;
 };
 
@@ -70,6 +79,8 @@ struct Shape {
     int n_cand;   // candidates per pair = n_rc * kc
     int n_zi;     // share items (and partials) per pair; share item j zooms the spans
                   // of ranks j, j + n_zi, ... below k
+    int g_cr;     // learned routing: spans per chunk (power of two)
+    int g_nrc;    // learned routing: chunks per pair
 };
 
 inline int elem_bytes(int dtype) { return dtype == SEKV_BF16 ? 2 : 4; }
@@ -90,6 +101,10 @@ inline Shape make_shape(const sekv_dims &d) {
     const int fit = (kShareTarget + P1 - 1) / P1;
     s.n_zi = s.k > 1 ? s.k : 1;
     if (s.n_zi > fit) s.n_zi = fit;
+    const int kk = s.k > 1 ? s.k : 1;
+    s.g_cr = kGateMinChunk;
+    while (s.g_cr < kGateMaxCand && ((s.M_max + s.g_cr - 1) / s.g_cr) * kk > kGateMaxCand) s.g_cr *= 2;
+    s.g_nrc = (s.M_max + s.g_cr - 1) / s.g_cr;
     return s;
 }
 
@@ -109,6 +124,8 @@ inline WsLayout make_layout(const Shape &s) {
     const size_t ns = P * size_t(s.n_zi) * size_t(s.G);
     L.part_ml = o;   o = align256(o + 8 * ns);
     L.part_o = o;    o = align256(o + 4 * ns * size_t(s.d));
+    L.gate_cnt = o;  o = align256(o + 4 * P);
+    L.gate_cand = o; o = align256(o + 16 * P * size_t(s.g_nrc) * size_t(s.k > 0 ? s.k : 1));
     L.total = o;
     return L;
 }
@@ -154,6 +171,21 @@ struct Params {
     int64_t *trace;                                 // [end_share][kTraceSlots] or null
 };
 
+// Launch parameters of the learned-routing selection kernel (sekv_gate.hip).
+struct GateParams {
+    int32_t B, Hq, Hkv, G, d, dr, k, M_max;
+    int32_t cr, n_rc;                  // spans per chunk (power of two), chunks per pair
+    int64_t budget;                    // expanded tokens allowed per pair
+    double scale_r;                    // 1 / sqrt(d')
+    const void *q, *proj, *sum_route;
+    const int32_t *n_spans, *span_len;
+    const double *span_logsize, *thr;
+    int32_t *sel;                      // [B][Hkv][k]
+    double *gate_out;                  // [B][Hq][M_max] or null
+    uint32_t *cnt;                     // [P]
+    uint64_t *cand;                    // [P][n_rc][k] x 2 words
+};
+
 // Bytes a tier gather workgroup moves at a time.
 constexpr int kGatherChunk = 32768;
 
@@ -177,6 +209,7 @@ hipError_t launch_step(const Params &p, int dtype, int head_dim, int group, hipS
 hipError_t launch_zero(void *ptr, size_t bytes, hipStream_t stream);
 hipError_t launch_tier_gather(const TierGatherArgs &a, hipStream_t stream);
 hipError_t launch_stats_reset(unsigned long long *stats, hipStream_t stream);
+hipError_t launch_gate(const GateParams &g, int dtype, hipStream_t stream);
 int resident_workgroups(int dtype, int head_dim, int group);
 
 // The fused step on a given workspace, with every host check (sekv_api.cpp).

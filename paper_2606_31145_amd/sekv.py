@@ -31,7 +31,8 @@ EXPORTED = ("sekv_status_string", "sekv_last_error", "sekv_phase_trace", "sekv_c
             "sekv_zoom_attend", "sekv_decode_step", "sekv_graph_create", "sekv_graph_launch",
             "sekv_graph_destroy", "sekv_tier_create", "sekv_tier_destroy",
             "sekv_tier_staging_size", "sekv_tier_last_copy", "sekv_decode_step_tiered",
-            "sekv_validate_cache", "sekv_decode_step_noalloc")
+            "sekv_validate_cache", "sekv_decode_step_noalloc", "sekv_route_gated",
+            "sekv_decode_step_gated")
 
 
 class SekvError(RuntimeError):
@@ -62,6 +63,12 @@ class CacheStruct(ctypes.Structure):
 class HostFactorsStruct(ctypes.Structure):
     _fields_ = [("arena", ctypes.c_void_p), ("arena_bytes", ctypes.c_int64),
                 ("block_off", ctypes.c_void_p), ("span_len", ctypes.c_void_p)]
+
+
+class GateStruct(ctypes.Structure):
+    _fields_ = [("route_dim", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("budget_tokens", ctypes.c_int64), ("proj", ctypes.c_void_p),
+                ("sum_route", ctypes.c_void_p), ("thresholds", ctypes.c_void_p)]
 
 
 def _load():
@@ -109,6 +116,10 @@ def _load():
                                             VP, VP, SZ, VP, VP]
     lib.sekv_decode_step_noalloc.restype = ctypes.c_int
     lib.sekv_decode_step_noalloc.argtypes = [P(Dims), P(CacheStruct), VP, VP, VP]
+    lib.sekv_route_gated.restype = ctypes.c_int
+    lib.sekv_route_gated.argtypes = [P(Dims), P(CacheStruct), P(GateStruct), VP, VP, VP, SZ, VP]
+    lib.sekv_decode_step_gated.restype = ctypes.c_int
+    lib.sekv_decode_step_gated.argtypes = [P(Dims), P(CacheStruct), P(GateStruct), VP, VP, VP, SZ, VP]
     lib.sekv_validate_cache.restype = ctypes.c_int
     lib.sekv_validate_cache.argtypes = [P(Dims), P(CacheStruct)]
     return lib
@@ -290,6 +301,56 @@ def decode_step(dims: Dims, cache: DeviceCache, ws: Workspace, sel=None, out=Non
     cs = cache.struct()
     _check(LIB.sekv_decode_step(ctypes.byref(dims), ctypes.byref(cs), _ptr(sel), _ptr(out),
                                 ws.ptr, ws.nbytes, _stream(stream)))
+    return sel, out
+
+
+class DeviceGate:
+    """Device tensors of the learned-routing parameters, laid out as sekv_gate describes."""
+
+    def __init__(self, route_dim: int, proj, sum_route, thresholds, budget_tokens: int):
+        self.route_dim = int(route_dim)
+        self.proj, self.sum_route, self.thresholds = proj, sum_route, thresholds
+        self.budget_tokens = int(budget_tokens)
+
+    @classmethod
+    def from_arrays(cls, route_dim, proj, sum_route, thresholds, budget_tokens, dtype: str,
+                    device="cuda"):
+        """Upload storage-typed numpy arrays (bf16 as uint16 bit patterns)."""
+        thr = torch.from_numpy(np.ascontiguousarray(thresholds, dtype=np.float64)).to(device)
+        return cls(route_dim, _to_device(proj, dtype, device), _to_device(sum_route, dtype, device),
+                   thr, budget_tokens)
+
+    def struct(self, budget_tokens=None) -> GateStruct:
+        bt = self.budget_tokens if budget_tokens is None else int(budget_tokens)
+        return GateStruct(self.route_dim, 0, bt, _ptr(self.proj), _ptr(self.sum_route),
+                          _ptr(self.thresholds))
+
+
+def route_gated(dims: Dims, cache: DeviceCache, gate: DeviceGate, ws: Workspace, sel=None,
+                gate_logits=None, want_logits: bool = False, stream=None):
+    """sekv_route_gated: returns (sel int32 [B][Hkv][k], gate logits float64 [B][Hq][M_max] or None)."""
+    dev = cache.t["q"].device
+    if sel is None:
+        sel = _alloc((dims.batch, dims.n_kv_heads, max(dims.top_k, 0)), torch.int32, dev)
+    if gate_logits is None and want_logits:
+        gate_logits = _alloc((dims.batch, dims.n_q_heads, dims.max_spans), torch.float64, dev)
+    cs, gs = cache.struct(), gate.struct()
+    _check(LIB.sekv_route_gated(ctypes.byref(dims), ctypes.byref(cs), ctypes.byref(gs), _ptr(sel),
+                                _ptr(gate_logits), ws.ptr, ws.nbytes, _stream(stream)))
+    return sel, gate_logits
+
+
+def decode_step_gated(dims: Dims, cache: DeviceCache, gate: DeviceGate, ws: Workspace, sel=None,
+                      out=None, stream=None):
+    """sekv_decode_step_gated: returns (sel, out)."""
+    dev = cache.t["q"].device
+    if sel is None:
+        sel = _alloc((dims.batch, dims.n_kv_heads, max(dims.top_k, 0)), torch.int32, dev)
+    if out is None:
+        out = _out_tensor(dims, dev)
+    cs, gs = cache.struct(), gate.struct()
+    _check(LIB.sekv_decode_step_gated(ctypes.byref(dims), ctypes.byref(cs), ctypes.byref(gs),
+                                      _ptr(sel), _ptr(out), ws.ptr, ws.nbytes, _stream(stream)))
     return sel, out
 
 
