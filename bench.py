@@ -83,6 +83,10 @@ def parse():
                          "needles when --variant L)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time spent timing the oracle")
+    ap.add_argument("--no-gated", action="store_true",
+                    help="skip the learned-routing (gated) step timing")
+    ap.add_argument("--gated-budget", type=int, default=4096,
+                    help="expanded-token budget per (sequence, KV head) of the gated step")
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (counter calibration)")
     ap.add_argument("--workload", choices=["layer128k", "layers32", "hosttier"],
@@ -122,6 +126,9 @@ def main():
     main_run = time_layer128k(args, dev, args.variant)
     if main_run is None:                     # phase-trace mode
         return
+    gated = None
+    if not args.no_gated:
+        gated = time_gated(args, dev, main_run["case"])
     other = None
     if not args.no_other_variant:
         other = time_layer128k(args, dev, "N" if args.variant == "L" else "L")
@@ -171,7 +178,106 @@ def main():
             "algorithmic_bytes_per_launch": other["bytes"]["total"],
             "factor_bytes": other["bytes"]["factors"],
             "mean_selected_len": other["bytes"]["mean_selected_len"]}
+    if gated is not None:
+        line["gated"] = gated
     print(json.dumps(line), flush=True)
+
+
+def time_gated(args, dev, case, route_dim=32):
+    """The same layer under the learned selection rule (random projections, tau = 0.05 for
+    every head, a token budget per pair): the selection kernel alone and the whole gated
+    step (selection, then attention over the chosen spans), K back-to-back calls over
+    rotating cache copies, one event pair around each batch."""
+    import numpy as np
+    import torch
+
+    from paper_2606_31145_amd import accounting
+    from paper_2606_31145_amd import sekv
+    from synth import make_gate
+
+    spec = case.spec
+    budget = args.gated_budget
+    gate = make_gate(case, route_dim=route_dim, tau="permissive", budget_tokens=budget)
+    arrays = dict(q=case.q, anchor_k=case.anchor_k, anchor_v=case.anchor_v,
+                  n_anchors=case.n_anchors, sum_k=case.sum_k, sum_v=case.sum_v,
+                  n_spans=case.n_spans, span_len=case.span_len, span_logsize=case.span_logsize,
+                  factors=case.factors, block_off=case.block_off)
+    base = sekv.DeviceCache.from_arrays(arrays, spec.dtype, dev)
+    gbase = sekv.DeviceGate.from_arrays(route_dim, gate.proj, gate.sum_route, gate.thresholds,
+                                        budget, spec.dtype, dev)
+    R = max(1, args.rotate)
+    caches, gates = [base], [gbase]
+    for _ in range(R - 1):
+        caches.append(sekv.DeviceCache({k: v.clone() for k, v in base.t.items()}, spec.dtype))
+        gates.append(sekv.DeviceGate(route_dim, gbase.proj.clone(), gbase.sum_route.clone(),
+                                     gbase.thresholds.clone(), budget))
+    dims = sekv.make_dims(batch=spec.batch, n_q_heads=spec.n_q_heads, n_kv_heads=spec.n_kv_heads,
+                          head_dim=spec.head_dim, rank=spec.rank, top_k=spec.top_k,
+                          max_anchors=case.max_anchors, max_spans=case.max_spans,
+                          max_span_len=case.max_span_len, dtype=spec.dtype,
+                          softmax_scale=spec.softmax_scale)
+    ws = sekv.Workspace(dims, dev)
+    stream = torch.cuda.current_stream()
+    B, Hq, Hkv, d = spec.batch, spec.n_q_heads, spec.n_kv_heads, spec.head_dim
+    sel = torch.empty((B, Hkv, spec.top_k), dtype=torch.int32, device=dev)
+    out = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
+    K = args.steps
+
+    def timed(fn):
+        """Warm up eagerly, capture one call per cache copy into a HIP graph, and time
+        ceil(K / R) replays with one event pair (host launch cost out of the figure)."""
+        for i in range(args.warmup):
+            fn(i, stream)
+        torch.cuda.synchronize()
+        assert ws.status() == 0, "device error word set in the gated warmup"
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=cap):
+            for j in range(R):
+                fn(j, cap)
+        stream.wait_stream(cap)
+        graph.replay()
+        torch.cuda.synchronize()
+        n = max(1, -(-K // R))
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(n):
+            graph.replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        assert ws.status() == 0, "device error word set in the gated timing"
+        del graph
+        return a.elapsed_time(b) * 1e3 / (n * R)
+
+    log(f"[bench] gated: timing {K} selections and {K} steps over {R} copies (graph replays)")
+    route_us = timed(lambda i, st: sekv.route_gated(dims, caches[i % R], gates[i % R], ws, sel=sel,
+                                                    stream=st))
+    sel_np = sel.cpu().numpy()
+    step_us = timed(lambda i, st: sekv.decode_step_gated(dims, caches[i % R], gates[i % R], ws,
+                                                         sel=sel, out=out, stream=st))
+    if not np.array_equal(sel.cpu().numpy(), sel_np):
+        raise RuntimeError("gated step selected other spans than the selection kernel")
+    gb = accounting.gate_bytes(n_q_heads=Hq, head_dim=d, route_dim=route_dim, elem=2,
+                               n_spans=case.n_spans, top_k=spec.top_k, n_kv_heads=Hkv)
+    sb = accounting.step_bytes(n_q_heads=Hq, n_kv_heads=Hkv, head_dim=d, rank=spec.rank, elem=2,
+                               out_elem=2, n_anchors=case.n_anchors, n_spans=case.n_spans,
+                               span_len=case.span_len, sel=sel_np)
+    total = gb["total"] + sb["total"]
+    res = {"rule": "learned routing: W q, sigmoid gate, per-head threshold, token budget",
+           "route_dim": route_dim, "tau": 0.05, "budget_tokens": budget, "cache_copies": R,
+           "selection_kernel_us": round(route_us, 3),
+           "selection_bytes": gb["total"],
+           "selection_GB_s": round(gb["total"] / (route_us * 1e-6) / 1e9, 1),
+           "selection_frac": round(gb["total"] / (route_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+           "step_us": round(step_us, 3), "step_bytes": total,
+           "step_GB_s": round(total / (step_us * 1e-6) / 1e9, 1),
+           "n_selected": sb["n_selected"], "mean_selected_len": round(sb["mean_selected_len"], 1)}
+    del caches, gates, base, gbase, ws
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    log(f"[bench] gated: selection {route_us:.2f} us, step {step_us:.2f} us")
+    return res
 
 
 def time_layer128k(args, dev, variant):

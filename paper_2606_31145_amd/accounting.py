@@ -80,3 +80,22 @@ def full_kv_bytes_same_shapes(*, n_kv_heads: int, head_dim: int, elem: int, n_an
     tokens = int(np.asarray(n_anchors, dtype=np.int64).sum() +
                  np.asarray(span_len, dtype=np.int64).sum())
     return 2 * n_kv_heads * head_dim * elem * tokens
+
+
+def gate_bytes(*, n_q_heads: int, head_dim: int, route_dim: int, elem: int, n_spans,
+               top_k: int, n_kv_heads: int) -> dict:
+    """Algorithmic HBM bytes of the learned-routing selection of one layer, itemised.
+
+    The query in, each query head's projection W (d' x d), the routing summary of every
+    live span for every query head (d' values), |S| and ln|S| of every span, and the
+    selection out.  The gate values themselves are an optional output and not counted.
+    """
+    n_spans = np.asarray(n_spans, dtype=np.int64)
+    B = n_spans.shape[0]
+    q_in = B * n_q_heads * head_dim * elem
+    proj = n_q_heads * route_dim * head_dim * elem
+    summaries = int(n_q_heads * n_spans.sum() * route_dim * elem)
+    tables = int(4 * B + n_spans.sum() * (4 + 8))
+    sel = B * n_kv_heads * top_k * 4
+    total = q_in + proj + summaries + tables + sel
+    return dict(total=total, q=q_in, proj=proj, summaries=summaries, tables=tables, sel=sel)

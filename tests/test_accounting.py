@@ -46,3 +46,14 @@ def test_step_bytes_by_hand():
     lens = [30, 10, 20, 9, 7, 7]
     assert r["factors"] == sum(2 * 4 * (L + 8 + 1) * 2 for L in lens)
     assert r["total"] == sum(r[k] for k in ("q", "out", "anchors", "mean_k", "mean_v", "factors", "tables"))
+
+
+def test_gate_bytes_by_hand():
+    g = A.gate_bytes(n_q_heads=4, head_dim=8, route_dim=2, elem=2, n_spans=[3, 1], top_k=2,
+                     n_kv_heads=2)
+    assert g["q"] == 2 * 4 * 8 * 2
+    assert g["proj"] == 4 * 2 * 8 * 2
+    assert g["summaries"] == 4 * 4 * 2 * 2
+    assert g["tables"] == 4 * 2 + 4 * 12
+    assert g["sel"] == 2 * 2 * 2 * 4
+    assert g["total"] == sum(g[k] for k in ("q", "proj", "summaries", "tables", "sel"))
