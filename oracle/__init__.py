@@ -3,10 +3,13 @@ the tests, the smoke check and the benchmark's CPU-baseline leg, never by the
 product path."""
 
 from .sekv_oracle import (  # noqa: F401
+    block_ranks,
     decode_step,
+    deploy_factors,
     decode_step_gated,
     gate,
     gate_logits,
+    gated_reconstruct,
     gated_selection,
     group_keys,
     merge_partials,

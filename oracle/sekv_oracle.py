@@ -32,6 +32,8 @@ with its reason in the design notes):
   of its query heads' scores: the union of per-head decisions under one shared
   threshold.  Ties go to the lower span index.
 * The rank gates are folded into sigma (m_i = 1 for the stored components).
+  Per-span retained ranks (the deployment-time drop of Sec. 3.2) come as a
+  table of (r_K, r_V) per block; without one, every block has the common rank.
 * ln is the natural logarithm; an expanded span's coarse entry is replaced by
   its tokens, never kept beside them.
 
@@ -71,23 +73,27 @@ def _elem(dtype: str):
 
 
 def read_span_block(factors: np.ndarray, offset: int, length: int, rank: int,
-                    head_dim: int, dtype: str) -> dict:
-    """Factors of one span: U_K[|S|][r], sigma_K[r], Vt_K[r][d], then the same for V.
+                    head_dim: int, dtype: str, rank_v: int | None = None) -> dict:
+    """Factors of one span: U_K[|S|][r_K], sigma_K[r_K], Vt_K[r_K][d], then the same
+    for V with r_V (rank_v, default rank).
 
     This is the per-span storage of Sec. 3.2 (U of |S| x r_S, Sigma of r_S
-    values, V of d_h x r_S, for keys and for values), one contiguous block.
+    values, V of d_h x r_S, for keys and for values, each with its own retained
+    rank), one contiguous block.
     """
     np_t, e = _elem(dtype)
     if offset % e:
         raise ValueError("misaligned block offset")
-    L, r, d = int(length), int(rank), int(head_dim)
-    n = 2 * (L * r + r + r * d)
+    L, d = int(length), int(head_dim)
+    ranks = {"K": int(rank), "V": int(rank if rank_v is None else rank_v)}
+    n = sum(L * r + r + r * d for r in ranks.values())
     raw = np.frombuffer(np.asarray(factors, dtype=np.uint8).data, dtype=np_t,
                         count=n, offset=int(offset))
     x = widen(raw, dtype)
     out = {}
     pos = 0
     for side in ("K", "V"):
+        r = ranks[side]
         out["U" + side] = x[pos:pos + L * r].reshape(L, r)
         pos += L * r
         out["s" + side] = x[pos:pos + r].copy()
@@ -97,9 +103,32 @@ def read_span_block(factors: np.ndarray, offset: int, length: int, rank: int,
     return out
 
 
+def block_ranks(block_rank, b: int, g: int, S: int, rank: int):
+    """(r_K, r_V) of block (b, g, S): from the packed table (r_K | r_V << 16), or the
+    common rank when there is no table."""
+    if block_rank is None:
+        return int(rank), int(rank)
+    w = int(np.asarray(block_rank)[b, g, S])
+    return w & 0xFFFF, w >> 16
+
+
 # ---------------------------------------------------------------------------
 # the steps
 # ---------------------------------------------------------------------------
+
+def gated_reconstruct(U: np.ndarray, sigma: np.ndarray, Vt: np.ndarray, gates) -> np.ndarray:
+    """sum_i m_i sigma_i u_i v_i^T (eq. key_reconstruction with the gates of eq. rank_gates)."""
+    return U @ np.diag(np.asarray(gates, dtype=np.float64) * sigma) @ Vt
+
+
+def deploy_factors(U: np.ndarray, sigma: np.ndarray, Vt: np.ndarray, gates, keep):
+    """The stored factors at deployment (Sec. 3.2): the components whose gate is kept,
+    with the gate folded into sigma; the others are dropped.  Returns (U, sigma, Vt)
+    of rank r_S = number kept."""
+    idx = np.flatnonzero(np.asarray(keep, dtype=bool))
+    g = np.asarray(gates, dtype=np.float64)
+    return U[:, idx], (g * sigma)[idx], Vt[idx]
+
 
 def reconstruct(U: np.ndarray, sigma: np.ndarray, Vt: np.ndarray) -> np.ndarray:
     """Token-level matrix of a span, sum_i sigma_i u_i v_i^T (eq. key_reconstruction).
@@ -189,11 +218,13 @@ def mixed_attention_head(qh, scale, anchor_k, anchor_v, coarse_logits, coarse_v,
 
 def zoom_attend(q, anchor_k, anchor_v, n_anchors, sum_v, n_spans, span_len, factors,
                 block_off, sel, logits, *, rank: int, softmax_scale: float,
-                dtype: str) -> np.ndarray:
+                dtype: str, block_rank=None) -> np.ndarray:
     """Mixed-resolution decode attention given the selection and routing scores.
 
     q and the cache arrays are stored values (widened here); logits are the
-    float64 routing scores from routing_logits.  Returns float64 [B][Hq][d].
+    float64 routing scores from routing_logits.  block_rank: per-block retained
+    ranks (r_K | r_V << 16, [B][Hkv][M]) or None for the common rank.  Returns
+    float64 [B][Hq][d].
     """
     qf = widen(q, dtype)
     ak, av, sv = widen(anchor_k, dtype), widen(anchor_v, dtype), widen(sum_v, dtype)
@@ -207,8 +238,9 @@ def zoom_attend(q, anchor_k, anchor_v, n_anchors, sum_v, n_spans, span_len, fact
             chosen = [int(S) for S in sel[b, g] if S >= 0]
             zoom = []
             for S in chosen:
+                rk, rv = block_ranks(block_rank, b, g, S, rank)
                 f = read_span_block(factors, int(block_off[b, g, S]), int(span_len[b, S]),
-                                    rank, d, dtype)
+                                    rk, d, dtype, rank_v=rv)
                 zoom.append((reconstruct(f["UK"], f["sK"], f["VtK"]),
                              reconstruct(f["UV"], f["sV"], f["VtV"])))
             coarse = [S for S in range(m) if S not in set(chosen)]
@@ -221,7 +253,7 @@ def zoom_attend(q, anchor_k, anchor_v, n_anchors, sum_v, n_spans, span_len, fact
 
 def decode_step(q, anchor_k, anchor_v, n_anchors, sum_k, sum_v, n_spans, span_len,
                 span_logsize, factors, block_off, *, rank: int, top_k: int,
-                softmax_scale: float, dtype: str) -> dict:
+                softmax_scale: float, dtype: str, block_rank=None) -> dict:
     """Route, select, reconstruct and attend: one SeKV decode step for one layer."""
     qf = widen(q, dtype)
     logits = routing_logits(qf, widen(sum_k, dtype), np.asarray(span_logsize, np.float64),
@@ -230,7 +262,7 @@ def decode_step(q, anchor_k, anchor_v, n_anchors, sum_k, sum_v, n_spans, span_le
     sel = select_topk(keys, n_spans, top_k)
     out = zoom_attend(q, anchor_k, anchor_v, n_anchors, sum_v, n_spans, span_len, factors,
                       block_off, sel, logits, rank=rank, softmax_scale=softmax_scale,
-                      dtype=dtype)
+                      dtype=dtype, block_rank=block_rank)
     return {"sel": sel, "out": out, "logits": logits, "keys": keys}
 
 
@@ -401,7 +433,7 @@ def gated_selection(x, thresholds, span_len, n_spans, n_kv_heads: int, max_zoom:
 def decode_step_gated(q, anchor_k, anchor_v, n_anchors, sum_k, sum_v, n_spans, span_len,
                       span_logsize, factors, block_off, proj, sum_route, thresholds, *,
                       rank: int, max_zoom: int, budget_tokens: int, softmax_scale: float,
-                      dtype: str) -> dict:
+                      dtype: str, block_rank=None) -> dict:
     """One decode step under the learned selection rule.
 
     The routing (projection, gate, threshold, budget) decides which spans are
@@ -419,5 +451,5 @@ def decode_step_gated(q, anchor_k, anchor_v, n_anchors, sum_k, sum_v, n_spans, s
                             n_spans, softmax_scale)
     out = zoom_attend(q, anchor_k, anchor_v, n_anchors, sum_v, n_spans, span_len, factors,
                       block_off, sel, coarse, rank=rank, softmax_scale=softmax_scale,
-                      dtype=dtype)
+                      dtype=dtype, block_rank=block_rank)
     return {"sel": sel, "out": out, "gate_logits": x, "q_proj": qp}

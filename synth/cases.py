@@ -72,7 +72,7 @@ _CHUNK = 1 << 20
 ST_PART, ST_Q, ST_AK, ST_AV = 1, 2, 3, 4
 ST_UK, ST_SK, ST_VK, ST_UV, ST_SV, ST_VV = 5, 6, 7, 8, 9, 10
 ST_NEEDLE = 11
-ST_PROJ, ST_TAU = 12, 13
+ST_PROJ, ST_TAU, ST_RANK = 12, 13, 14
 
 VARIANTS = {"L": 0, "N": 1}
 PLANT_DELTA = 6.0
@@ -198,6 +198,7 @@ class CaseSpec:
     n_layers: int = 1
     seed: int = 0
     host_factors: bool = False   # factors live in pinned host memory (tier case)
+    rank_mode: str = "fixed"     # "fixed": every block has `rank`; "adaptive": per-block ranks
 
     @property
     def group(self) -> int:
@@ -262,6 +263,7 @@ class Case:
     factors: np.ndarray        # uint8 arena
     block_off: np.ndarray      # [B][Hkv][M_max] int64 byte offsets
     needles: np.ndarray = field(default=None)   # [B][Hkv][n_p] planted spans (variant N)
+    block_rank: np.ndarray = field(default=None)  # [B][Hkv][M_max] int32 r_K | r_V << 16, or None
 
     @property
     def dtype(self) -> str:
@@ -319,9 +321,28 @@ def span_lengths(spec: CaseSpec, b: int):
     return lengths, middle - pos
 
 
-def block_bytes(length: int, rank: int, head_dim: int, dtype: str) -> int:
-    raw = (2 * length * rank + 2 * rank + 2 * rank * head_dim) * elem_bytes(dtype)
+def block_bytes(length: int, rank: int, head_dim: int, dtype: str, rank_v: int | None = None) -> int:
+    rv = rank if rank_v is None else rank_v
+    raw = ((length + 1 + head_dim) * (rank + rv)) * elem_bytes(dtype)
     return (raw + 255) // 256 * 256
+
+
+def rank_granule(dtype: str) -> int:
+    """Ranks of adaptive-rank blocks are multiples of this: one 16-byte vector of a U row."""
+    return 16 // elem_bytes(dtype)
+
+
+def draw_ranks(spec: CaseSpec, vkey, b: int, g: int, m: int):
+    """Retained ranks (r_K, r_V) of the m spans of (b, g).
+
+    The trained rank-gate predictor is not available; as its stand-in each side keeps
+    a uniformly drawn number of granules in [1, rank / granule] of its leading
+    components (sigma is sorted descending, so the dropped ones are the smallest)."""
+    gr = rank_granule(spec.dtype)
+    nmax = max(1, spec.rank // gr)
+    u = uniforms(stream_key(*vkey, ST_RANK, b, g), 2 * m).reshape(2, m)
+    n = np.minimum(nmax, 1 + np.floor(u * nmax).astype(np.int64))
+    return (n[0] * gr).astype(np.int64), (n[1] * gr).astype(np.int64)
 
 
 # ---------------------------------------------------------------------------
@@ -392,27 +413,23 @@ def _plant(spec: CaseSpec, fac, lens, needles, qbar):
         s[j] = -np.sort(-s[j])
 
 
-def _write_pair(spec, arena_e, eoff, lens, fac_st):
-    """Copy the stored factors of one (b, g) into the arena (element view)."""
-    r, d = spec.rank, spec.head_dim
-    UK, sK, VK = fac_st["K"]
-    UV, sV, VV = fac_st["V"]
+def _write_pair(spec, arena_e, eoff, lens, fac_st, ranks=None):
+    """Copy the stored factors of one (b, g) into the arena (element view): the leading
+    r_K / r_V components of each span (all `rank` of them without a rank table)."""
+    d = spec.head_dim
     start = 0
     for j, L in enumerate(lens):
         o = int(eoff[j])
-        n_u = L * r
         rows = slice(start, start + L)
-        arena_e[o:o + n_u] = UK[rows].reshape(-1)
-        o += n_u
-        arena_e[o:o + r] = sK[j]
-        o += r
-        arena_e[o:o + r * d] = VK[j].reshape(-1)
-        o += r * d
-        arena_e[o:o + n_u] = UV[rows].reshape(-1)
-        o += n_u
-        arena_e[o:o + r] = sV[j]
-        o += r
-        arena_e[o:o + r * d] = VV[j].reshape(-1)
+        for si, side in enumerate(("K", "V")):
+            U, sg, Vt = fac_st[side]
+            r = spec.rank if ranks is None else int(ranks[si][j])
+            arena_e[o:o + L * r] = U[rows, :r].reshape(-1)
+            o += L * r
+            arena_e[o:o + r] = sg[j, :r]
+            o += r
+            arena_e[o:o + r * d] = Vt[j, :r].reshape(-1)
+            o += r * d
         start += L
 
 
@@ -457,15 +474,28 @@ def make_case(spec: CaseSpec, layer: int = 0, variant: str = "L", threads: int |
     q_st = to_storage(q64, dt)
     q_dec = from_storage(q_st, dt)
 
-    # block offsets
+    # retained ranks and block offsets
+    adaptive = spec.rank_mode == "adaptive"
+    if spec.rank_mode not in ("fixed", "adaptive"):
+        raise ValueError(spec.rank_mode)
+    ranks = {}
+    block_rank = np.zeros((B, Hkv, M_max), dtype=np.int32) if adaptive else None
     block_off = np.zeros((B, Hkv, M_max), dtype=np.int64)
     total = 0
     for b, (lens, _) in enumerate(parts):
-        sizes = np.array([block_bytes(L, r, d, dt) for L in lens], dtype=np.int64)
         for g in range(Hkv):
-            if len(lens):
-                block_off[b, g, :len(lens)] = total + np.concatenate([[0], np.cumsum(sizes)[:-1]])
-                total += int(sizes.sum())
+            if not len(lens):
+                continue
+            if adaptive:
+                rk, rv = draw_ranks(spec, vkey, b, g, len(lens))
+                ranks[(b, g)] = (rk, rv)
+                block_rank[b, g, :len(lens)] = (rk | (rv << 16)).astype(np.int32)
+                sizes = np.array([block_bytes(L, int(a), d, dt, int(c)) for L, a, c in zip(lens, rk, rv)],
+                                 dtype=np.int64)
+            else:
+                sizes = np.array([block_bytes(L, r, d, dt) for L in lens], dtype=np.int64)
+            block_off[b, g, :len(lens)] = total + np.concatenate([[0], np.cumsum(sizes)[:-1]])
+            total += int(sizes.sum())
     total = max(total, 256)
     if arena_out is not None:
         if arena_out.nbytes < total or arena_out.dtype != np.uint8:
@@ -505,9 +535,12 @@ def make_case(spec: CaseSpec, layer: int = 0, variant: str = "L", threads: int |
             needles[b, g, :len(chosen)] = chosen
             _plant(spec, fac, lens, chosen, qbar)
         fac_st = {side: [to_storage(x, dt) for x in fac[side]] for side in fac}
-        _write_pair(spec, arena_e, block_off[b, g, :m] // e, lens, fac_st)
-        for side, dst in (("K", sum_k), ("V", sum_v)):
+        rk_rv = ranks.get((b, g))
+        _write_pair(spec, arena_e, block_off[b, g, :m] // e, lens, fac_st, rk_rv)
+        for si, (side, dst) in enumerate((("K", sum_k), ("V", sum_v))):
             U, s, Vt = (from_storage(x, dt) for x in fac_st[side])
+            if rk_rv is not None:
+                s = s * (np.arange(r)[None, :] < rk_rv[si][:, None])   # dropped components
             dst[b, g, :m] = to_storage(_span_means(U, s, Vt, lens), dt)
 
     pairs = [(b, g) for b in range(B) for g in range(Hkv)]
@@ -522,7 +555,7 @@ def make_case(spec: CaseSpec, layer: int = 0, variant: str = "L", threads: int |
     return Case(spec=spec, layer=layer, variant=variant, q=q_st, anchor_k=anchor_k,
                 anchor_v=anchor_v, n_anchors=n_anch, sum_k=sum_k, sum_v=sum_v,
                 n_spans=n_spans, span_len=span_len, span_logsize=span_logsize,
-                factors=arena, block_off=block_off, needles=needles)
+                factors=arena, block_off=block_off, needles=needles, block_rank=block_rank)
 
 
 def with_top_k(case: Case, k: int) -> Case:

@@ -15,10 +15,13 @@ def banner(msg):
 
 
 def case_arrays(case):
-    return dict(q=case.q, anchor_k=case.anchor_k, anchor_v=case.anchor_v,
-                n_anchors=case.n_anchors, sum_k=case.sum_k, sum_v=case.sum_v,
-                n_spans=case.n_spans, span_len=case.span_len, span_logsize=case.span_logsize,
-                factors=case.factors, block_off=case.block_off)
+    arr = dict(q=case.q, anchor_k=case.anchor_k, anchor_v=case.anchor_v,
+               n_anchors=case.n_anchors, sum_k=case.sum_k, sum_v=case.sum_v,
+               n_spans=case.n_spans, span_len=case.span_len, span_logsize=case.span_logsize,
+               factors=case.factors, block_off=case.block_off)
+    if getattr(case, "block_rank", None) is not None:
+        arr["block_rank"] = case.block_rank
+    return arr
 
 
 def dims_for(S, case, out_dtype=None, top_k=None, zoom=0):

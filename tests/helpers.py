@@ -11,7 +11,8 @@ def oracle_kwargs(case, top_k=None):
                 span_logsize=case.span_logsize, factors=case.factors,
                 block_off=case.block_off, rank=s.rank,
                 top_k=s.top_k if top_k is None else top_k,
-                softmax_scale=s.softmax_scale, dtype=s.dtype)
+                softmax_scale=s.softmax_scale, dtype=s.dtype,
+                block_rank=getattr(case, "block_rank", None))
 
 
 def rng(seed):

@@ -499,7 +499,7 @@ def _mean_group(logits, n_kv_heads):
 
 
 def _keep_coarse(q, anchor_k, anchor_v, n_anchors, sum_v, n_spans, span_len, factors,
-                 block_off, sel, logits, *, rank, softmax_scale, dtype):
+                 block_off, sel, logits, *, rank, softmax_scale, dtype, block_rank=None):
     none = np.full_like(sel, -1)
     # coarse entries of every span stay, and the zoomed tokens are added on top
     qf = orc.widen(q, dtype)
@@ -513,8 +513,9 @@ def _keep_coarse(q, anchor_k, anchor_v, n_anchors, sum_v, n_spans, span_len, fac
         for g in range(Hkv):
             zoom = []
             for S in [int(x) for x in sel[b, g] if x >= 0]:
+                rk, rv = orc.block_ranks(block_rank, b, g, S, rank)
                 f = orc.read_span_block(factors, int(block_off[b, g, S]), int(span_len[b, S]),
-                                        rank, d, dtype)
+                                        rk, d, dtype, rank_v=rv)
                 zoom.append((orc.reconstruct(f["UK"], f["sK"], f["VtK"]),
                              orc.reconstruct(f["UV"], f["sV"], f["VtV"])))
             for h in range(g * G, (g + 1) * G):

@@ -113,3 +113,27 @@ def test_gate_inputs_are_deterministic_and_normalised():
     assert np.all(kr[0, :, m:] == 0)
     p = make_gate(case, route_dim=8)
     assert np.all(p.tau == 0.05) and np.allclose(p.thresholds, np.log(0.05 / 0.95))
+
+
+def test_adaptive_rank_arena_layout():
+    from synth.cases import block_bytes, rank_granule
+    for dt in ("f32", "bf16"):
+        case = make_case(custom_spec(dtype=dt, n_q_heads=4, n_kv_heads=2, head_dim=32, rank=16, context=900,
+                                     span_min=8, span_max=60, seed=44, rank_mode="adaptive"))
+        gr = rank_granule(dt)
+        ends = []
+        for b in range(case.spec.batch):
+            for g in range(case.spec.n_kv_heads):
+                for S in range(int(case.n_spans[b])):
+                    w = int(case.block_rank[b, g, S])
+                    rk, rv = w & 0xFFFF, w >> 16
+                    assert rk % gr == 0 and rv % gr == 0 and gr <= rk <= 16 and gr <= rv <= 16
+                    o = int(case.block_off[b, g, S])
+                    assert o % 256 == 0
+                    ends.append((o, o + block_bytes(int(case.span_len[b, S]), rk, 32, dt, rv)))
+        ends.sort()
+        assert all(a[1] <= b[0] for a, b in zip(ends, ends[1:]))
+        assert ends[-1][1] <= case.factors.nbytes
+        fixed = make_case(custom_spec(dtype=dt, n_q_heads=4, n_kv_heads=2, head_dim=32, rank=16, context=900,
+                                      span_min=8, span_max=60, seed=44))
+        assert fixed.block_rank is None and case.factors.nbytes < fixed.factors.nbytes
