@@ -101,9 +101,16 @@ typedef struct {
  *   span_logsize double [B][M_max]        ln|S|, computed once by the caller
  *   factors      byte arena of span blocks, factors_bytes long
  *   block_off    int64 [B][Hkv][M_max]    byte offset of block (b, g, S); multiple of 16
+ *   block_rank   int32 [B][Hkv][M_max] or NULL: retained ranks r_K | r_V << 16 of block
+ *                (b, g, S); NULL means r_K = r_V = dims.rank for every block
  * A span block holds, in the storage dtype and in this order,
- *   U_K[|S|][r] | sigma_K[r] | Vt_K[r][d] | U_V[|S|][r] | sigma_V[r] | Vt_V[r][d]
- * i.e. the per-span factors of Sec. 3.2 (U, Sigma, V^T for keys, then for values). */
+ *   U_K[|S|][r_K] | sigma_K[r_K] | Vt_K[r_K][d] | U_V[|S|][r_V] | sigma_V[r_V] | Vt_V[r_V][d]
+ * i.e. the per-span factors of Sec. 3.2 (U, Sigma, V^T for keys, then for values), each
+ * side keeping its own number of components after the deployment-time drop of the
+ * components with negligible gates (eqs. rank_gates and key_reconstruction; the kept
+ * gates are folded into sigma).  Ranks are multiples of 16 / element bytes (8 for bf16, 4
+ * for f32) in [that, dims.rank]; a block with another rank is skipped and flagged like a
+ * block outside the arena. */
 typedef struct {
     const void *q;
     const void *anchor_k;
@@ -117,6 +124,7 @@ typedef struct {
     const void *factors;
     int64_t factors_bytes;
     const int64_t *block_off;
+    const int32_t *block_rank;
 } sekv_cache;
 
 /* Human-readable name of a status code (static storage). */
@@ -295,6 +303,8 @@ typedef struct {
     int64_t arena_bytes;
     const int64_t *block_off;       /* host int64 [B][Hkv][M_max]: byte offset of each block */
     const int32_t *span_len;        /* host int32 [B][M_max]: |S|                            */
+    const int32_t *block_rank;      /* host int32 [B][Hkv][M_max] r_K | r_V << 16, or NULL
+                                       (then cache->block_rank must be NULL too)             */
 } sekv_host_factors;
 
 typedef struct sekv_tier sekv_tier;

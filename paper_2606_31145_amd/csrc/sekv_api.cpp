@@ -120,6 +120,7 @@ sekv_status prepare(int mode, const sekv_dims *d, const sekv_cache *c, int32_t *
     p.factors = static_cast<const unsigned char *>(c->factors);
     p.factors_bytes = c->factors_bytes;
     p.block_off = c->block_off;
+    p.block_rank = c->block_rank;
     p.sel_out = sel_out; p.logits_out = logits_out; p.sel_in = sel_in; p.logits_in = logits_in;
     p.out = out;
     p.hdr = reinterpret_cast<sekv::WsHeader *>(w);
@@ -607,6 +608,8 @@ sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_cache *cac
     if (!cache || !host || !host->arena || !host->block_off || !host->span_len)
         return fail(SEKV_ERR_INVALID_ARG, "cache/host factor tables are NULL");
     if (host->arena_bytes <= 0) return fail(SEKV_ERR_INVALID_ARG, "arena_bytes <= 0");
+    if ((host->block_rank == nullptr) != (cache->block_rank == nullptr))
+        return fail(SEKV_ERR_INVALID_ARG, "host and device rank tables: both or neither");
     if (!out || (dims->top_k > 0 && !sel)) return fail(SEKV_ERR_INVALID_ARG, "sel/out is NULL");
     const bool gather = t->mode == SEKV_TIER_GATHER;
     if (gather && dims->top_k > 0 && (!cache->block_off || (reinterpret_cast<uintptr_t>(cache->block_off) & 7)))
@@ -645,6 +648,7 @@ sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_cache *cac
         c.factors = t->d_staging;
         c.factors_bytes = int64_t(t->staging_bytes);
         c.block_off = t->d_off + bb * Hkv * M;
+        c.block_rank = cache->block_rank ? cache->block_rank + bb * Hkv * M : nullptr;
         return c;
     };
     hipError_t he = hipSuccess;
@@ -682,6 +686,7 @@ sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_cache *cac
             a.sel = sel + size_t(b) * Hkv * k;
             a.span_len = cache->span_len + size_t(b) * M;
             a.block_off = cache->block_off + size_t(b) * Hkv * M;
+            a.block_rank = cache->block_rank ? cache->block_rank + size_t(b) * Hkv * M : nullptr;
             a.stage_off = t->d_off + size_t(b) * Hkv * M;
             a.stats = t->d_stats;
             a.error = &static_cast<sekv::WsHeader *>(ws)->error;
@@ -702,7 +707,8 @@ sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_cache *cac
             if (he != hipSuccess) return hip_fail(he, "waiting for the selection");
             sekv::TierPlanIn in{dims, b, t->h_sel + size_t(b) * Hkv * k, host->span_len + size_t(b) * M,
                                 host->block_off + size_t(b) * Hkv * M, host->arena_bytes,
-                                int64_t(b) * region, region};
+                                int64_t(b) * region, region,
+                                host->block_rank ? host->block_rank + size_t(b) * Hkv * M : nullptr};
             st = sekv::plan_tier_sequence(in, &t->plan);
             if (st != SEKV_OK) return st;
             int64_t *hoff = t->h_off + size_t(b) * Hkv * M;

@@ -104,15 +104,32 @@ sekv_status check_cache(const sekv_dims *d, const sekv_cache *c, bool need_facto
             return fail(SEKV_ERR_INVALID_ARG, "factor arena not 16-byte or offsets not 8-byte aligned");
         if (c->factors_bytes <= 0) return fail(SEKV_ERR_INVALID_ARG, "factors_bytes <= 0");
     }
+    if (misaligned(c->block_rank, 4)) return fail(SEKV_ERR_INVALID_ARG, "cache.block_rank not 4-byte aligned");
     return SEKV_OK;
 }
 
-size_t block_bytes(const sekv_dims &d, int L) {
+size_t block_bytes(const sekv_dims &d, int L, int rk, int rv) {
     const size_t e = size_t(elem_bytes(d.dtype));
     auto a16 = [](size_t x) { return (x + 15) & ~size_t(15); };
-    const size_t side = a16(size_t(L) * d.rank * e) + a16(size_t(d.rank) * e) +
-                        a16(size_t(d.rank) * d.head_dim * e);
-    return 2 * side;
+    auto side = [&](int r) {
+        return a16(size_t(L) * r * e) + a16(size_t(r) * e) + a16(size_t(r) * d.head_dim * e);
+    };
+    return side(rk) + side(rv);
+}
+
+size_t block_bytes(const sekv_dims &d, int L) { return block_bytes(d, L, d.rank, d.rank); }
+
+bool block_ranks(const sekv_dims &d, const int32_t *table, size_t i, int *rk, int *rv) {
+    if (!table) {
+        *rk = *rv = d.rank;
+        return true;
+    }
+    const uint32_t w = uint32_t(table[i]);
+    *rk = int(w & 0xFFFFu);
+    *rv = int(w >> 16);
+    const int gran = 16 / elem_bytes(d.dtype);
+    auto ok = [&](int r) { return r >= gran && r <= d.rank && r % gran == 0; };
+    return ok(*rk) && ok(*rv);
 }
 
 sekv_status validate_cache(const sekv_dims *d, const sekv_cache *c) {
@@ -158,13 +175,18 @@ sekv_status validate_cache(const sekv_dims *d, const sekv_cache *c) {
             for (int S = 0; S < m; ++S) {
                 const int L = c->span_len[size_t(b) * M + S];
                 const int64_t off = c->block_off[pr * M + S];
-                const int64_t n = int64_t(block_bytes(*d, L));
+                int rk = r, rv = r;
+                if (!block_ranks(*d, c->block_rank, pr * M + S, &rk, &rv))
+                    return fail(SEKV_ERR_INVALID_ARG,
+                                "block (%d, %d, %d): ranks (%d, %d) not multiples of %d in [%d, %d]", b, g, S, rk,
+                                rv, int(16 / e), int(16 / e), r);
+                const int64_t n = int64_t(block_bytes(*d, L, rk, rv));
                 if (off < 0 || (off & 15) || off + n > c->factors_bytes)
                     return fail(SEKV_ERR_INVALID_ARG,
                                 "block (%d, %d, %d) at %lld (+%lld bytes) outside the %lld-byte arena or misaligned",
                                 b, g, S, (long long)off, (long long)n, (long long)c->factors_bytes);
                 const unsigned char *blk = static_cast<const unsigned char *>(c->factors) + off;
-                const size_t vals = 2 * (size_t(L) * r + r + size_t(r) * D);
+                const size_t vals = (size_t(L) + 1 + size_t(D)) * size_t(rk + rv);
                 if (!all_finite(blk, vals, d->dtype, &bad))
                     return fail(SEKV_ERR_INVALID_ARG, "factor block (%d, %d, %d): value %zu not finite", b, g, S, bad);
             }
@@ -187,7 +209,10 @@ sekv_status plan_tier_sequence(const TierPlanIn &in, TierPlan *out) {
             const int64_t off = in.block_off[size_t(g) * M + s];
             if (L < 1 || L > d.max_span_len)
                 return fail(SEKV_ERR_INVALID_ARG, "span (%d, %d) has length %d", in.b, s, L);
-            const int64_t len = int64_t(block_bytes(d, L));
+            int rk = d.rank, rv = d.rank;
+            if (!block_ranks(d, in.block_rank, size_t(g) * M + s, &rk, &rv))
+                return fail(SEKV_ERR_INVALID_ARG, "host block (%d, %d, %d) has ranks (%d, %d)", in.b, g, s, rk, rv);
+            const int64_t len = int64_t(block_bytes(d, L, rk, rv));
             if (off < 0 || (off & 15) || off > in.arena_bytes - len)
                 return fail(SEKV_ERR_INVALID_ARG, "host block (%d, %d, %d) outside the arena", in.b, g, s);
             blks.push_back({off, len, g, s});

@@ -23,8 +23,14 @@ sekv_status check_dims(const sekv_dims *d);
 sekv_status check_cache(const sekv_dims *d, const sekv_cache *c, bool need_factors);
 
 // Bytes of one span block of length L: U|sigma|Vt for keys, then values, every segment
-// 16-byte aligned (the rank and head_dim in use keep them so).
+// 16-byte aligned (the ranks and head_dim in use keep them so); without ranks, both
+// sides have dims.rank.
 size_t block_bytes(const sekv_dims &d, int L);
+size_t block_bytes(const sekv_dims &d, int L, int rk, int rv);
+// Ranks of a block from its rank-table word (r_K | r_V << 16), or dims.rank for both
+// when there is no table.  False when a rank is not a multiple of 16 / element bytes in
+// [that, dims.rank].
+bool block_ranks(const sekv_dims &d, const int32_t *table, size_t i, int *rk, int *rv);
 
 // Check a cache from HOST copies of its arrays (every pointer in `c` is a host pointer,
 // factors_bytes the arena size): the device-side preconditions of the step calls.
@@ -45,6 +51,7 @@ struct TierPlanIn {
     int64_t arena_bytes;
     int64_t region;               // first staging byte of sequence b
     int64_t region_bytes;         // staging bytes reserved for sequence b
+    const int32_t *block_rank = nullptr;  // [Hkv][M] ranks of sequence b's blocks (host), or null
 };
 struct TierPlan {
     std::vector<TierRun> runs;    // contiguous runs, in arena order

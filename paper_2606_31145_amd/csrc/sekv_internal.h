@@ -154,6 +154,7 @@ struct Params {
     const unsigned char *factors;
     int64_t factors_bytes;
     const int64_t *block_off;
+    const int32_t *block_rank;                      // r_K | r_V << 16 per block, or null
     // caller buffers
     int32_t *sel_out;
     float *logits_out;
@@ -200,6 +201,7 @@ struct TierGatherArgs {
     int64_t *stage_off;                // [Hkv][M] staging offsets, written for selected spans
     unsigned long long *stats;         // [2]: bytes and blocks moved (accumulated)
     int32_t *error;                    // workspace error word (out-of-arena blocks)
+    const int32_t *block_rank;         // [Hkv][M] r_K | r_V << 16 (device), or null: r for both
     int64_t arena_bytes, slot0, slot_bytes;
     int32_t Hkv, k, M, r, d, elem, max_span_len, chunks_per_slot;
 };

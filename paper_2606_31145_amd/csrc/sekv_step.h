@@ -306,6 +306,26 @@ __device__ inline uint64_t pack2(float lo, float hi) {
 __device__ inline float lo_f(uint64_t w) { return __uint_as_float(uint32_t(w)); }
 __device__ inline float hi_f(uint64_t w) { return __uint_as_float(uint32_t(w >> 32)); }
 
+// The span word that travels with a selected span: |S| in bits 0..20, r_K / 4 in bits
+// 21..25 and r_V / 4 in bits 26..30 (the retained ranks of its block).  Ranks read from
+// the caller's table must be multiples of 16 / element bytes in [that, rank]; otherwise
+// both are 0, and the zoom skips the block and flags it like one outside the arena.
+template <class T>
+__device__ inline int32_t span_word(const Params &p, int32_t L, int32_t table_word) {
+    int rk = p.r, rv = p.r;
+    if (p.block_rank) {
+        rk = int(uint32_t(table_word) & 0xFFFFu);
+        rv = int(uint32_t(table_word) >> 16);
+        constexpr int gran = 16 / T::kBytes;
+        const bool ok = rk >= gran && rk <= p.r && rk % gran == 0 && rv >= gran && rv <= p.r && rv % gran == 0;
+        if (!ok) rk = rv = 0;
+    }
+    return int32_t((uint32_t(L) & 0x1FFFFFu) | (uint32_t(rk >> 2) << 21) | (uint32_t(rv >> 2) << 26));
+}
+__device__ inline int word_len(int32_t w) { return int(uint32_t(w) & 0x1FFFFFu); }
+__device__ inline int word_rk(int32_t w) { return int((uint32_t(w) >> 21) & 31u) << 2; }
+__device__ inline int word_rv(int32_t w) { return int((uint32_t(w) >> 26) & 31u) << 2; }
+
 // ---------------------------------------------------------------------------
 // shared memory
 // ---------------------------------------------------------------------------
@@ -667,8 +687,9 @@ __device__ __forceinline__ void merge_selection(const Params &p, Smem<T, D, G> &
             int L = 0;
             int64_t off = 0;
             if (s >= 0) {
-                L = p.span_len[size_t(b) * p.M_max + s];
-                off = p.block_off[(size_t(b) * p.Hkv + g) * p.M_max + s];
+                const size_t bi = (size_t(b) * p.Hkv + g) * p.M_max + s;
+                L = span_word<T>(p, p.span_len[size_t(b) * p.M_max + s], p.block_rank ? p.block_rank[bi] : 0);
+                off = p.block_off[bi];
             }
             int32_t *zr = reinterpret_cast<int32_t *>(&p.zrec[size_t(pair) * k + j]);
             st_shared(zr + 0, s);
@@ -877,11 +898,12 @@ __device__ __forceinline__ void route_item(const Params &p, Smem<T, D, G> &sm, i
             }
         const int ti = min(tid, nr - 1);
         const double lns = p.span_logsize[size_t(b) * p.M_max + s0 + ti];
-        int32_t slen = 0;
+        int32_t slen = 0, srank = 0;
         int64_t boff = 0;
         if (select) {
             slen = p.span_len[size_t(b) * p.M_max + s0 + ti];
             boff = p.block_off[row0 + ti];
+            if (p.block_rank) srank = p.block_rank[row0 + ti];
         }
 #pragma unroll
         for (int m = 0; m < D / 16; ++m)
@@ -889,7 +911,7 @@ __device__ __forceinline__ void route_item(const Params &p, Smem<T, D, G> &sm, i
             for (int u = 0; u < HPT; ++u) qv[m][u] = (hgq * HPT + u < G) ? double(qr[m][u]) : 0.0;
         if (tid < CR) {
             R.lns[tid] = lns;
-            R.slen[tid] = slen;
+            R.slen[tid] = span_word<T>(p, slen, srank);
             R.boff[tid] = boff;
         }
 #pragma unroll
@@ -1308,8 +1330,8 @@ __device__ __forceinline__ void rank_candidates(const Params &p, Smem<T, D, G> &
 // `mid` runs once the first factor loads are issued: work that needs none of them.
 // ---------------------------------------------------------------------------
 template <class T, int D, int G, int RU, class Mid>
-__device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, int L, int64_t off,
-                                          float (&pend)[G], int tid, Mid &&mid) {
+__device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, int L, int rk, int rv,
+                                          int64_t off, float (&pend)[G], int tid, Mid &&mid) {
     using GE = Geo<T, D>;
     auto &Z = sm.u.share;
     constexpr int VEC = GE::VEC;
@@ -1323,13 +1345,20 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
     const int rgrp = tid / GE::RV, col = tid % GE::RV;
     const int ucol = tid % RU;
     const int wave = tid >> 6, lane = tid & 63;
+    // The block keeps r_K <= R key components and r_V <= R value components: rows,
+    // columns and sigmas past them are not loaded and count as zero, so they add nothing
+    // to the scores and values (the dropped components of Sec. 3.2).
+    rk = __builtin_amdgcn_readfirstlane(rk);
+    rv = __builtin_amdgcn_readfirstlane(rv);
+    const int ruk = rk * T::kBytes / 16, ruv = rv * T::kBytes / 16;
     const unsigned char *UK = p.factors + off;
-    const unsigned char *sK = UK + size_t(L) * R * T::kBytes;
-    const unsigned char *VtK = sK + size_t(R) * T::kBytes;
-    const unsigned char *UV = VtK + size_t(R) * D * T::kBytes;
-    const unsigned char *sV = UV + size_t(L) * R * T::kBytes;
-    const unsigned char *VtV = sV + size_t(R) * T::kBytes;
+    const unsigned char *sK = UK + size_t(L) * rk * T::kBytes;
+    const unsigned char *VtK = sK + size_t(rk) * T::kBytes;
+    const unsigned char *UV = VtK + size_t(rk) * D * T::kBytes;
+    const unsigned char *sV = UV + size_t(L) * rv * T::kBytes;
+    const unsigned char *VtV = sV + size_t(rv) * T::kBytes;
     const int nb0 = min(NB, L);
+    const uint4 zero4 = make_uint4(0u, 0u, 0u, 0u);
 
     // issue in the order of use: sigmas, Vt_K, U_K, then (after `mid`) U_V.  Addresses
     // are clamped into the block, validity is applied where values are used.
@@ -1338,19 +1367,22 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
 #pragma unroll
     for (int u = 0; u < NVT; ++u) {
         const int vi = min(tid + NT * u, R * RV - 1);
-        sk_reg[u] = T::load1(sK, vi / RV);
+        sk_reg[u] = vi / RV < rk ? T::load1(sK, vi / RV) : 0.0f;
     }
 #pragma unroll
-    for (int u = 0; u < NSV; ++u) sv_reg[u] = T::load1(sV, (tid + NT * u) % R);
+    for (int u = 0; u < NSV; ++u) {
+        const int i = (tid + NT * u) % R;
+        sv_reg[u] = i < rv ? T::load1(sV, i) : 0.0f;
+    }
 #pragma unroll
     for (int u = 0; u < NVT; ++u) {
         const int vi = min(tid + NT * u, R * RV - 1);
-        vk[u] = ld16(VtK + size_t(vi / RV) * GE::RB + (vi % RV) * 16);
+        vk[u] = vi / RV < rk ? ld16(VtK + size_t(vi / RV) * GE::RB + (vi % RV) * 16) : zero4;
     }
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
         const int tok = min((tid + NT * u) / RU, nb0 - 1);
-        uk[u] = ld16(UK + size_t(tok) * R * T::kBytes + ucol * 16);
+        uk[u] = ucol < ruk ? ld16(UK + size_t(tok) * rk * T::kBytes + ucol * 16) : zero4;
     }
     SEKV_STAMP(p, sm, kTrSZoomIssued);
     mid();
@@ -1358,7 +1390,7 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
         const int tok = min((tid + NT * u) / RU, nb0 - 1);
-        uv[u] = ld16(UV + size_t(tok) * R * T::kBytes + ucol * 16);
+        uv[u] = ucol < ruv ? ld16(UV + size_t(tok) * rv * T::kBytes + ucol * 16) : zero4;
     }
 
     // w[h][i] = scale*log2e * sigma_K[i] * (Vt_K[i] . q_h).  No barrier first: Z.w was
@@ -1386,7 +1418,7 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
 #pragma unroll
     for (int u = 0; u < NVT; ++u) {
         const int vi = min(tid + NT * u, R * RV - 1);
-        vvt[u] = ld16(VtV + size_t(vi / RV) * GE::RB + (vi % RV) * 16);
+        vvt[u] = vi / RV < rv ? ld16(VtV + size_t(vi / RV) * GE::RB + (vi % RV) * 16) : zero4;
     }
 
     __syncthreads();
@@ -1404,12 +1436,12 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
 #pragma unroll
             for (int u = 0; u < NU; ++u) {
                 const int tok = min((tid + NT * u) / RU, nb - 1);
-                uk[u] = ld16(UK + size_t(t0 + tok) * R * T::kBytes + ucol * 16);
+                uk[u] = ucol < ruk ? ld16(UK + size_t(t0 + tok) * rk * T::kBytes + ucol * 16) : zero4;
             }
 #pragma unroll
             for (int u = 0; u < NU; ++u) {
                 const int tok = min((tid + NT * u) / RU, nb - 1);
-                uv[u] = ld16(UV + size_t(t0 + tok) * R * T::kBytes + ucol * 16);
+                uv[u] = ucol < ruv ? ld16(UV + size_t(t0 + tok) * rv * T::kBytes + ucol * 16) : zero4;
             }
         }
 #pragma unroll
@@ -1622,8 +1654,9 @@ __device__ __forceinline__ bool share_item(const Params &p, Smem<T, D, G> &sm, i
             Z.sel[tid] = s;
             if (tid % nz == j && s >= 0) {
                 const int64_t off = p.block_off[pr * p.M_max + s];
-                Z.zi[tid] = make_int4(s, p.span_len[size_t(b) * p.M_max + s], int32_t(off & 0xFFFFFFFF),
-                                      int32_t(off >> 32));
+                const int32_t w = span_word<T>(p, p.span_len[size_t(b) * p.M_max + s],
+                                               p.block_rank ? p.block_rank[pr * p.M_max + s] : 0);
+                Z.zi[tid] = make_int4(s, w, int32_t(off & 0xFFFFFFFF), int32_t(off >> 32));
             }
         }
         if (nc0 > 0) {
@@ -1637,10 +1670,10 @@ __device__ __forceinline__ bool share_item(const Params &p, Smem<T, D, G> &sm, i
     if (tid < k && tid % nz == j) {
         const int4 zi = Z.zi[tid];
         if (zi.x >= 0) {
-            const int L = zi.y;
+            const int L = word_len(zi.y), rk = word_rk(zi.y), rv = word_rv(zi.y);
             const int64_t off = int64_t(uint32_t(zi.z)) | (int64_t(zi.w) << 32);
-            const int64_t bytes = (2 * int64_t(L) * r + 2 * r + 2 * int64_t(r) * D) * T::kBytes;
-            if (L < 1 || off < 0 || (off & 15) || off + bytes > p.factors_bytes) {
+            const int64_t bytes = (int64_t(L) + 1 + D) * (rk + rv) * T::kBytes;
+            if (L < 1 || rk == 0 || rv == 0 || off < 0 || (off & 15) || off + bytes > p.factors_bytes) {
                 flag_error(p, kErrBlockRange);
                 Z.zi[tid].x = -1;
             }
@@ -1654,22 +1687,24 @@ __device__ __forceinline__ bool share_item(const Params &p, Smem<T, D, G> &sm, i
     auto coarse0 = [&]() {
         if (nc0 > 0) coarse_block<T, D, G, NJ>(sm, cv, c_lo, nc0, k, pend, rgrp, tid);
     };
-    auto zoom_one = [&](int L, int64_t off, int tid, auto &&mid) {
-        // 16-byte vectors per U row: rank 8..64 gives 1..8 (bf16) or 2..16 (f32)
+    auto zoom_one = [&](int32_t w, int64_t off, int tid, auto &&mid) {
+        // 16-byte vectors per U row at the largest rank: 8..64 gives 1..8 (bf16) or 2..16
+        // (f32); the block's own ranks r_K, r_V <= r travel in the span word
         const int ru = r * T::kBytes / 16;
+        const int L = word_len(w), rk = word_rk(w), rv = word_rv(w);
         if constexpr (T::kBytes == 2) {
             switch (ru) {
-                case 1: zoom_span<T, D, G, 1>(p, sm, L, off, pend, tid, mid); break;
-                case 2: zoom_span<T, D, G, 2>(p, sm, L, off, pend, tid, mid); break;
-                case 4: zoom_span<T, D, G, 4>(p, sm, L, off, pend, tid, mid); break;
-                default: zoom_span<T, D, G, 8>(p, sm, L, off, pend, tid, mid); break;
+                case 1: zoom_span<T, D, G, 1>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                case 2: zoom_span<T, D, G, 2>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                case 4: zoom_span<T, D, G, 4>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                default: zoom_span<T, D, G, 8>(p, sm, L, rk, rv, off, pend, tid, mid); break;
             }
         } else {
             switch (ru) {
-                case 2: zoom_span<T, D, G, 2>(p, sm, L, off, pend, tid, mid); break;
-                case 4: zoom_span<T, D, G, 4>(p, sm, L, off, pend, tid, mid); break;
-                case 8: zoom_span<T, D, G, 8>(p, sm, L, off, pend, tid, mid); break;
-                default: zoom_span<T, D, G, 16>(p, sm, L, off, pend, tid, mid); break;
+                case 2: zoom_span<T, D, G, 2>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                case 4: zoom_span<T, D, G, 4>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                case 8: zoom_span<T, D, G, 8>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                default: zoom_span<T, D, G, 16>(p, sm, L, rk, rv, off, pend, tid, mid); break;
             }
         }
     };

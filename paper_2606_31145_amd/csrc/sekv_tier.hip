@@ -35,7 +35,8 @@ __device__ inline void copy_chunk(const unsigned char *src, unsigned char *dst, 
     }
 }
 
-// Block bytes of a span of length L: U|sigma|Vt for keys and values, 16-byte segments.
+// Block bytes of a span of length L with rank r on both sides: U|sigma|Vt for keys and
+// values, 16-byte segments (half of it is one side).
 __device__ inline int64_t dev_block_bytes(int64_t L, int r, int d, int e) {
     auto a16 = [](int64_t x) { return (x + 15) & ~int64_t(15); };
     return 2 * (a16(L * r * e) + a16(int64_t(r) * e) + a16(int64_t(r) * d * e));
@@ -48,8 +49,16 @@ __global__ __launch_bounds__(kGT) void tier_gather_kernel(TierGatherArgs a) {
     if (s < 0 || s >= a.M) return;
     const int L = a.span_len[s];
     const int64_t off = a.block_off[size_t(g) * a.M + s];
-    const int64_t bytes = dev_block_bytes(L, a.r, a.d, a.elem);
-    if (L < 1 || L > a.max_span_len || off < 0 || (off & 15) || off > a.arena_bytes - bytes) {
+    int rk = a.r, rv = a.r;
+    if (a.block_rank) {
+        const uint32_t w = uint32_t(a.block_rank[size_t(g) * a.M + s]);
+        rk = int(w & 0xFFFFu);
+        rv = int(w >> 16);
+    }
+    const int gran = 16 / a.elem;
+    const bool ranks_ok = rk >= gran && rk <= a.r && rk % gran == 0 && rv >= gran && rv <= a.r && rv % gran == 0;
+    const int64_t bytes = dev_block_bytes(L, rk, a.d, a.elem) / 2 + dev_block_bytes(L, rv, a.d, a.elem) / 2;
+    if (!ranks_ok || L < 1 || L > a.max_span_len || off < 0 || (off & 15) || off > a.arena_bytes - bytes) {
         // skipped: the attention reads whatever the slot holds, inside staging
         if (c == 0 && threadIdx.x == 0)
             __hip_atomic_fetch_or(a.error, kErrBlockRange, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -57,12 +57,14 @@ class CacheStruct(ctypes.Structure):
                 ("sum_k", ctypes.c_void_p), ("sum_v", ctypes.c_void_p),
                 ("n_spans", ctypes.c_void_p), ("span_len", ctypes.c_void_p),
                 ("span_logsize", ctypes.c_void_p), ("factors", ctypes.c_void_p),
-                ("factors_bytes", ctypes.c_int64), ("block_off", ctypes.c_void_p)]
+                ("factors_bytes", ctypes.c_int64), ("block_off", ctypes.c_void_p),
+                ("block_rank", ctypes.c_void_p)]
 
 
 class HostFactorsStruct(ctypes.Structure):
     _fields_ = [("arena", ctypes.c_void_p), ("arena_bytes", ctypes.c_int64),
-                ("block_off", ctypes.c_void_p), ("span_len", ctypes.c_void_p)]
+                ("block_off", ctypes.c_void_p), ("span_len", ctypes.c_void_p),
+                ("block_rank", ctypes.c_void_p)]
 
 
 class GateStruct(ctypes.Structure):
@@ -248,6 +250,9 @@ class DeviceCache:
         t["factors"] = torch.from_numpy(np.ascontiguousarray(arrays["factors"],
                                                              dtype=np.uint8)).to(
             factors_device or device)
+        if arrays.get("block_rank") is not None:
+            t["block_rank"] = torch.from_numpy(np.ascontiguousarray(arrays["block_rank"],
+                                                                    dtype=np.int32)).to(device)
         return cls(t, dtype)
 
     def struct(self) -> CacheStruct:
@@ -255,7 +260,8 @@ class DeviceCache:
         return CacheStruct(_ptr(t["q"]), _ptr(t["anchor_k"]), _ptr(t["anchor_v"]),
                            _ptr(t["n_anchors"]), _ptr(t["sum_k"]), _ptr(t["sum_v"]),
                            _ptr(t["n_spans"]), _ptr(t["span_len"]), _ptr(t["span_logsize"]),
-                           _ptr(t["factors"]), int(t["factors"].numel()), _ptr(t["block_off"]))
+                           _ptr(t["factors"]), int(t["factors"].numel()), _ptr(t["block_off"]),
+                           _ptr(t.get("block_rank")))
 
 
 def _alloc(shape, dtype, device):
@@ -415,18 +421,22 @@ class LayerGraph:
 
 
 class HostFactors:
-    """The factor arena in pinned host memory plus host copies of block_off and span_len."""
+    """The factor arena in pinned host memory plus host copies of block_off, span_len and
+    (for per-block ranks) block_rank."""
 
-    def __init__(self, factors: np.ndarray, block_off: np.ndarray, span_len: np.ndarray):
+    def __init__(self, factors: np.ndarray, block_off: np.ndarray, span_len: np.ndarray,
+                 block_rank: np.ndarray | None = None):
         a = np.ascontiguousarray(factors, dtype=np.uint8)
         self.arena = torch.empty(a.nbytes, dtype=torch.uint8, pin_memory=True)
         self.arena.numpy()[:] = a
         self.block_off = np.ascontiguousarray(block_off, dtype=np.int64)
         self.span_len = np.ascontiguousarray(span_len, dtype=np.int32)
+        self.block_rank = None if block_rank is None else np.ascontiguousarray(block_rank, dtype=np.int32)
 
     def struct(self) -> HostFactorsStruct:
         return HostFactorsStruct(self.arena.data_ptr(), int(self.arena.numel()),
-                                 self.block_off.ctypes.data, self.span_len.ctypes.data)
+                                 self.block_off.ctypes.data, self.span_len.ctypes.data,
+                                 None if self.block_rank is None else self.block_rank.ctypes.data)
 
 
 class Tier:
@@ -476,10 +486,12 @@ def validate_cache(dims: Dims, arrays: dict):
     keep["span_logsize"] = np.ascontiguousarray(arrays["span_logsize"], dtype=np.float64)
     keep["block_off"] = np.ascontiguousarray(arrays["block_off"], dtype=np.int64)
     keep["factors"] = np.ascontiguousarray(arrays["factors"], dtype=np.uint8)
-    c = lambda f: keep[f].ctypes.data if keep[f].size else None  # noqa: E731
+    if arrays.get("block_rank") is not None:
+        keep["block_rank"] = np.ascontiguousarray(arrays["block_rank"], dtype=np.int32)
+    c = lambda f: keep[f].ctypes.data if f in keep and keep[f].size else None  # noqa: E731
     cs = CacheStruct(c("q"), c("anchor_k"), c("anchor_v"), c("n_anchors"), c("sum_k"), c("sum_v"),
                      c("n_spans"), c("span_len"), c("span_logsize"), c("factors"),
-                     int(keep["factors"].nbytes), c("block_off"))
+                     int(keep["factors"].nbytes), c("block_off"), c("block_rank"))
     _check(LIB.sekv_validate_cache(ctypes.byref(dims), ctypes.byref(cs)))
 
 

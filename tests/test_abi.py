@@ -132,3 +132,36 @@ def test_validate_cache_on_host_copies(S):
     bad("block_off", lambda x: x.__setitem__((1, 1, 0), case.factors.nbytes), "outside")
     bad("q", lambda x: x.__setitem__((0, 1, 3), 0x7FC0), "not finite")        # bf16 NaN
     bad("sum_v", lambda x: x.__setitem__((1, 0, 0, 5), 0x7F80), "not finite")  # bf16 +inf
+
+
+def test_validate_cache_adaptive_ranks(S):
+    """Per-block ranks: a valid ragged-rank cache passes; a rank off the 16-byte granule,
+    above the common rank, or a block that no longer fits the arena fails."""
+    import numpy as np
+
+    from synth import custom_spec, make_case
+    case = make_case(custom_spec(batch=2, n_q_heads=4, n_kv_heads=2, head_dim=64, rank=16, top_k=2,
+                                 context=900, dtype="bf16", seed=72, rank_mode="adaptive"))
+    arrays = dict(q=case.q, anchor_k=case.anchor_k, anchor_v=case.anchor_v,
+                  n_anchors=case.n_anchors, sum_k=case.sum_k, sum_v=case.sum_v,
+                  n_spans=case.n_spans, span_len=case.span_len, span_logsize=case.span_logsize,
+                  factors=case.factors, block_off=case.block_off, block_rank=case.block_rank)
+    d = _dims(S, **{k: v for k, v in case.dims().items()})
+    S.validate_cache(d, arrays)
+    for word, msg in ((4 | (8 << 16), "ranks"), (24 | (8 << 16), "ranks"), (16 | (0 << 16), "ranks")):
+        a = dict(arrays, block_rank=case.block_rank.copy())
+        a["block_rank"][0, 1, 2] = word
+        with pytest.raises(S.SekvError) as ei:
+            S.validate_cache(d, a)
+        assert msg in str(ei.value), str(ei.value)
+    # the last block of the arena grown to the full rank no longer fits
+    last = np.unravel_index(np.argmax(case.block_off), case.block_off.shape)
+    a = dict(arrays, block_rank=case.block_rank.copy())
+    a["block_rank"][last] = 16 | (16 << 16)
+    w = int(case.block_rank[last])
+    if (w & 0xFFFF, w >> 16) != (16, 16):
+        with pytest.raises(S.SekvError) as ei:
+            S.validate_cache(d, dict(a, factors=case.factors[:int(case.block_off[last]) +
+                                                             (int(case.span_len[last[0], last[2]]) + 65) *
+                                                             ((w & 0xFFFF) + (w >> 16)) * 2]))
+        assert "outside" in str(ei.value)
