@@ -83,6 +83,8 @@ def parse():
                          "needles when --variant L)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time spent timing the oracle")
+    ap.add_argument("--no-adaptive", action="store_true",
+                    help="skip the per-span adaptive-rank timing of the same layer")
     ap.add_argument("--no-gated", action="store_true",
                     help="skip the learned-routing (gated) step timing")
     ap.add_argument("--gated-budget", type=int, default=4096,
@@ -114,6 +116,7 @@ def main():
 
     if args.phase_trace:
         os.environ["SEKV_LIB"] = "trace"
+    import numpy as np
     import torch
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
@@ -126,6 +129,9 @@ def main():
     main_run = time_layer128k(args, dev, args.variant)
     if main_run is None:                     # phase-trace mode
         return
+    adaptive = None
+    if not args.no_adaptive:
+        adaptive = time_layer128k(args, dev, args.variant, rank_mode="adaptive")
     gated = None
     if not args.no_gated:
         gated = time_gated(args, dev, main_run["case"])
@@ -178,6 +184,18 @@ def main():
             "algorithmic_bytes_per_launch": other["bytes"]["total"],
             "factor_bytes": other["bytes"]["factors"],
             "mean_selected_len": other["bytes"]["mean_selected_len"]}
+    if adaptive is not None:
+        br = adaptive["case"].block_rank
+        live = br[br != 0]
+        line["adaptive_rank"] = {
+            "rule": "per-span retained ranks r_K, r_V in {8, 16, 24, 32} (uniform draw)",
+            "mean_rank_k": round(float(np.mean(live & 0xFFFF)), 2),
+            "mean_rank_v": round(float(np.mean(live >> 16)), 2),
+            "us_per_step": round(adaptive["wall_us"], 3), "kernel_us_mean": adaptive["kern_us"],
+            "achieved_GB_s": round(adaptive["achieved"], 1),
+            "frac": round(adaptive["achieved"] / HBM_PEAK_GBS, 4),
+            "algorithmic_bytes_per_launch": adaptive["bytes"]["total"],
+            "factor_bytes": adaptive["bytes"]["factors"]}
     if gated is not None:
         line["gated"] = gated
     print(json.dumps(line), flush=True)
@@ -280,9 +298,10 @@ def time_gated(args, dev, case, route_dim=32):
     return res
 
 
-def time_layer128k(args, dev, variant):
+def time_layer128k(args, dev, variant, rank_mode="fixed"):
     """Generate the 128K x 4 cache (one variant), time K graph-replayed steps over rotating
-    device copies, then the same steps launched one by one; returns the figures."""
+    device copies, then the same steps launched one by one; returns the figures.
+    rank_mode "adaptive": every span block keeps its own ranks (r_K, r_V) <= 32."""
     import numpy as np
     import torch
 
@@ -290,15 +309,16 @@ def time_layer128k(args, dev, variant):
     from paper_2606_31145_amd import sekv
     from synth import WORKLOADS, make_case
 
-    spec = WORKLOADS["llama3-8b-layer-128k-b4"]
-    log(f"[bench] generating the 128K x 4 cache (variant {variant})")
+    from dataclasses import replace as _replace
+    spec = _replace(WORKLOADS["llama3-8b-layer-128k-b4"], rank_mode=rank_mode)
+    log(f"[bench] generating the 128K x 4 cache (variant {variant}, {rank_mode} ranks)")
     t0 = time.time()
     case = make_case(spec, variant=variant)
     log(f"[bench] generated in {time.time() - t0:.1f}s; factors {case.factors.nbytes / 1e6:.1f} MB")
     arrays = dict(q=case.q, anchor_k=case.anchor_k, anchor_v=case.anchor_v,
                   n_anchors=case.n_anchors, sum_k=case.sum_k, sum_v=case.sum_v,
                   n_spans=case.n_spans, span_len=case.span_len, span_logsize=case.span_logsize,
-                  factors=case.factors, block_off=case.block_off)
+                  factors=case.factors, block_off=case.block_off, block_rank=case.block_rank)
     base = sekv.DeviceCache.from_arrays(arrays, spec.dtype, dev)
     caches = [base]
     for _ in range(max(1, args.rotate) - 1):
@@ -326,7 +346,8 @@ def time_layer128k(args, dev, variant):
     sel_np = sels[0].cpu().numpy()
     acct = accounting.step_bytes(n_q_heads=Hq, n_kv_heads=Hkv, head_dim=d, rank=spec.rank,
                                  elem=2, out_elem=2, n_anchors=case.n_anchors,
-                                 n_spans=case.n_spans, span_len=case.span_len, sel=sel_np)
+                                 n_spans=case.n_spans, span_len=case.span_len, sel=sel_np,
+                                 block_rank=case.block_rank)
     bytes_step = acct["total"]
     if args.phase_trace:
         phase_trace(args, step, len(caches), dev,

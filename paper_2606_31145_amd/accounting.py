@@ -39,10 +39,11 @@ def transfer_bytes(n_layers: int, n_kv_heads: int, rank: int, spans, head_dim: i
 # -- one device-resident step ------------------------------------------------------------
 
 def step_bytes(*, n_q_heads: int, n_kv_heads: int, head_dim: int, rank: int, elem: int,
-               out_elem: int, n_anchors, n_spans, span_len, sel) -> dict:
+               out_elem: int, n_anchors, n_spans, span_len, sel, block_rank=None) -> dict:
     """Algorithmic HBM bytes of one decode step of one layer, itemised.
 
-    n_anchors [B], n_spans [B], span_len [B][M], sel [B][Hkv][k] (-1 = empty slot).
+    n_anchors [B], n_spans [B], span_len [B][M], sel [B][Hkv][k] (-1 = empty slot);
+    block_rank [B][Hkv][M] (r_K | r_V << 16) or None when every block has `rank`.
     """
     n_anchors = np.asarray(n_anchors, dtype=np.int64)
     n_spans = np.asarray(n_spans, dtype=np.int64)
@@ -64,7 +65,11 @@ def step_bytes(*, n_q_heads: int, n_kv_heads: int, head_dim: int, rank: int, ele
                 if s >= 0:
                     L = int(span_len[b, s])
                     sel_len.append(L)
-                    factors += 2 * r * (L + d + 1) * elem
+                    if block_rank is None:
+                        factors += 2 * r * (L + d + 1) * elem
+                    else:
+                        w = int(block_rank[b, g, s])
+                        factors += ((w & 0xFFFF) + (w >> 16)) * (L + d + 1) * elem
     # span tables: n_spans, n_anchors, |S| (int32) and ln|S| (float64) of every span,
     # block offsets (int64) of the expanded spans
     tables = int(8 * B + n_spans.sum() * (4 + 8) + n_sel * 8)

@@ -1329,7 +1329,7 @@ __device__ __forceinline__ void rank_candidates(const Params &p, Smem<T, D, G> &
 // zoom of one span through its factors, RU = 16-byte vectors per factor row U[t][:].
 // `mid` runs once the first factor loads are issued: work that needs none of them.
 // ---------------------------------------------------------------------------
-template <class T, int D, int G, int RU, class Mid>
+template <class T, int D, int G, int RU, bool RANKED, class Mid>
 __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, int L, int rk, int rv,
                                           int64_t off, float (&pend)[G], int tid, Mid &&mid) {
     using GE = Geo<T, D>;
@@ -1347,9 +1347,15 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
     const int wave = tid >> 6, lane = tid & 63;
     // The block keeps r_K <= R key components and r_V <= R value components: rows,
     // columns and sigmas past them are not loaded and count as zero, so they add nothing
-    // to the scores and values (the dropped components of Sec. 3.2).
-    rk = __builtin_amdgcn_readfirstlane(rk);
-    rv = __builtin_amdgcn_readfirstlane(rv);
+    // to the scores and values (the dropped components of Sec. 3.2).  Without a rank
+    // table every block has R of each (compile-time, so the masks fold away).
+    if constexpr (RANKED) {
+        rk = __builtin_amdgcn_readfirstlane(rk);
+        rv = __builtin_amdgcn_readfirstlane(rv);
+    } else {
+        rk = R;
+        rv = R;
+    }
     const int ruk = rk * T::kBytes / 16, ruv = rv * T::kBytes / 16;
     const unsigned char *UK = p.factors + off;
     const unsigned char *sK = UK + size_t(L) * rk * T::kBytes;
@@ -1687,26 +1693,31 @@ __device__ __forceinline__ bool share_item(const Params &p, Smem<T, D, G> &sm, i
     auto coarse0 = [&]() {
         if (nc0 > 0) coarse_block<T, D, G, NJ>(sm, cv, c_lo, nc0, k, pend, rgrp, tid);
     };
-    auto zoom_one = [&](int32_t w, int64_t off, int tid, auto &&mid) {
+    auto zoom_ranked = [&](auto ranked_c, int32_t w, int64_t off, int tid, auto &&mid) {
+        constexpr bool RANKED = decltype(ranked_c)::value;
         // 16-byte vectors per U row at the largest rank: 8..64 gives 1..8 (bf16) or 2..16
         // (f32); the block's own ranks r_K, r_V <= r travel in the span word
         const int ru = r * T::kBytes / 16;
         const int L = word_len(w), rk = word_rk(w), rv = word_rv(w);
         if constexpr (T::kBytes == 2) {
             switch (ru) {
-                case 1: zoom_span<T, D, G, 1>(p, sm, L, rk, rv, off, pend, tid, mid); break;
-                case 2: zoom_span<T, D, G, 2>(p, sm, L, rk, rv, off, pend, tid, mid); break;
-                case 4: zoom_span<T, D, G, 4>(p, sm, L, rk, rv, off, pend, tid, mid); break;
-                default: zoom_span<T, D, G, 8>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                case 1: zoom_span<T, D, G, 1, RANKED>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                case 2: zoom_span<T, D, G, 2, RANKED>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                case 4: zoom_span<T, D, G, 4, RANKED>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                default: zoom_span<T, D, G, 8, RANKED>(p, sm, L, rk, rv, off, pend, tid, mid); break;
             }
         } else {
             switch (ru) {
-                case 2: zoom_span<T, D, G, 2>(p, sm, L, rk, rv, off, pend, tid, mid); break;
-                case 4: zoom_span<T, D, G, 4>(p, sm, L, rk, rv, off, pend, tid, mid); break;
-                case 8: zoom_span<T, D, G, 8>(p, sm, L, rk, rv, off, pend, tid, mid); break;
-                default: zoom_span<T, D, G, 16>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                case 2: zoom_span<T, D, G, 2, RANKED>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                case 4: zoom_span<T, D, G, 4, RANKED>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                case 8: zoom_span<T, D, G, 8, RANKED>(p, sm, L, rk, rv, off, pend, tid, mid); break;
+                default: zoom_span<T, D, G, 16, RANKED>(p, sm, L, rk, rv, off, pend, tid, mid); break;
             }
         }
+    };
+    auto zoom_one = [&](int32_t w, int64_t off, int tid, auto &&mid) {
+        if (p.block_rank) zoom_ranked(IC<1>{}, w, off, tid, mid);
+        else zoom_ranked(IC<0>{}, w, off, tid, mid);
     };
     if (j + nz >= k) {
         const int4 zi = Z.zi[j < kMaxTopK ? j : 0];

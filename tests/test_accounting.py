@@ -57,3 +57,14 @@ def test_gate_bytes_by_hand():
     assert g["tables"] == 4 * 2 + 4 * 12
     assert g["sel"] == 2 * 2 * 2 * 4
     assert g["total"] == sum(g[k] for k in ("q", "proj", "summaries", "tables", "sel"))
+
+
+def test_step_bytes_with_ranks():
+    import numpy as np
+    base = dict(n_q_heads=2, n_kv_heads=1, head_dim=4, rank=8, elem=2, out_elem=2,
+                n_anchors=[0], n_spans=[2], span_len=np.array([[3, 5]]), sel=np.array([[[1, -1]]]))
+    fixed = A.step_bytes(**base)
+    assert fixed["factors"] == 2 * 8 * (5 + 4 + 1) * 2
+    ragged = A.step_bytes(**base, block_rank=np.array([[[8 | (8 << 16), 4 | (8 << 16)]]]))
+    assert ragged["factors"] == (4 + 8) * (5 + 4 + 1) * 2
+    assert fixed["total"] - ragged["total"] == fixed["factors"] - ragged["factors"]
