@@ -41,10 +41,13 @@
  *     shapes (hence workspace layout) differ.  Calls recorded into a caller's own stream
  *     capture are tracked at capture time, so such a graph must be replayed in the order
  *     it was captured relative to eager calls on the same workspace.
- *   - Forward progress does not depend on how many workgroups are resident: work items
- *     are claimed in index order from a workspace ticket, and an item only ever waits for
- *     items of lower index, so a step completes even while other kernels hold most of the
- *     device.
+ *   - Forward progress does not depend on how many workgroups are resident.  Each routing
+ *     chunk is claimed (an atomic exchange on a per-chunk workspace word) by the first
+ *     workgroup to reach it: its own workgroup, or a workgroup whose share item has waited
+ *     for it for a while and then computes every unclaimed chunk of its pair itself.  A
+ *     share item therefore only ever waits for chunks that a running workgroup holds, and
+ *     such a workgroup never waits, so a step completes even while other kernels hold most
+ *     of the device.  The learned-routing kernel has no waits at all.
  */
 #ifndef SEKV_H
 #define SEKV_H
@@ -154,8 +157,9 @@ SEKV_API size_t sekv_workspace_size(const sekv_dims *dims);
 SEKV_API sekv_status sekv_workspace_init(void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* Read and clear the workspace's device error word (synchronises `stream`).  Bits:
- * 1 = a wait for a selection timed out, 2 = a factor block lay outside the arena,
- * 4 = a selected index was out of range.  0 after every correct call. */
+ * 1 = a wait for a selection timed out, 2 = a factor block lay outside the arena or its
+ * rank-table entry was invalid, 4 = a selected index was out of range.  0 after every
+ * correct call. */
 SEKV_API sekv_status sekv_workspace_status(void *ws, size_t ws_bytes, hipStream_t stream,
                                   int32_t *error_bits);
 
@@ -355,7 +359,8 @@ SEKV_API sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_c
  * size), so it is slow and synchronous.  Checks, for every sequence b:
  *   0 <= n_anchors[b] <= max_anchors, 0 <= n_spans[b] <= max_spans, n_anchors[b] +
  *   n_spans[b] >= 1; 1 <= span_len <= max_span_len and span_logsize = ln(span_len) for
- *   every span; every span's block 16-byte aligned and inside the arena (when top_k > 0);
+ *   every span; every span's block 16-byte aligned and inside the arena (when top_k > 0),
+ *   with valid ranks when the cache has a rank table;
  *   every stored value of q, the anchors, the summaries and the factor blocks finite.
  * Returns SEKV_OK, or SEKV_ERR_INVALID_ARG with the first violation in sekv_last_error(). */
 SEKV_API sekv_status sekv_validate_cache(const sekv_dims *dims, const sekv_cache *host_copy);

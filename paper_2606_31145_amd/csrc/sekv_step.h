@@ -36,11 +36,14 @@
 // observing the counter.  No fence writes back or invalidates whole L2 caches.
 //
 // Scheduling: workgroup w takes items w, w + grid, w + 2 grid, ... with grid no larger
-// than the number of workgroups the device holds at once.  Route items have the lowest
-// indices and never wait, so every route item a share item waits for is reached by its
-// workgroup after finitely many non-waiting items: the waits always end (they are
-// bounded anyway and flag the workspace on timeout).  The last workgroup to leave zeroes
-// the counters, so the workspace is ready for the next launch.
+// than the number of workgroups the device holds at once.  A routing chunk is computed
+// by whichever workgroup first claims it (an atomic exchange of the launch tag into the
+// chunk's claim word): its own routing item, or a share item that has polled for the
+// pair's candidates kHelpAfter times and then runs every unclaimed chunk of the pair
+// itself (help_route) before polling again.  A share item thus only waits for chunks
+// held by running workgroups, which never wait, so every wait ends whatever the
+// residency (waits are bounded anyway and flag the workspace on timeout).  The last
+// workgroup to leave zeroes the counters, so the workspace is ready for the next launch.
 #pragma once
 
 #include <hip/hip_runtime.h>
