@@ -170,17 +170,32 @@ void test_tier_plan(std::mt19937 &rng) {
         d.top_k = 1 + int(rng() % 8);
         d.max_spans = 4 + int(rng() % 40);
         d.max_span_len = 1 + int(rng() % 300);
+        d.rank = 8 << int(rng() % 3);
         d.dtype = (rng() & 1) ? SEKV_BF16 : SEKV_F32;
         d.out_dtype = SEKV_F32;
         const int Hkv = d.n_kv_heads, k = d.top_k, M = d.max_spans;
         std::vector<int32_t> len(M);
         for (auto &L : len) L = 1 + int(rng() % d.max_span_len);
+        // half of the cases carry per-block ranks (multiples of 16 bytes of elements)
+        const bool ranked = (rng() & 1) != 0;
+        const int gran = 16 / sekv::elem_bytes(d.dtype);
+        std::vector<int32_t> rnk(size_t(Hkv) * M, 0);
+        for (auto &w : rnk) {
+            const int nmax = d.rank / gran;
+            const int rk = gran * (1 + int(rng() % nmax)), rv = gran * (1 + int(rng() % nmax));
+            w = rk | (rv << 16);
+        }
+        auto bsz = [&](int g, int s) {
+            if (!ranked) return int64_t(sekv::block_bytes(d, len[s]));
+            const int32_t w = rnk[size_t(g) * M + s];
+            return int64_t(sekv::block_bytes(d, len[s], w & 0xFFFF, w >> 16));
+        };
         std::vector<int64_t> off(size_t(Hkv) * M);
         int64_t pos = 0;
         for (int g = 0; g < Hkv; ++g)
             for (int s = 0; s < M; ++s) {
                 off[size_t(g) * M + s] = pos;
-                pos += int64_t(sekv::align256(sekv::block_bytes(d, len[s])));
+                pos += int64_t(sekv::align256(size_t(bsz(g, s))));
             }
         std::vector<int32_t> sel(size_t(Hkv) * k, -1);
         for (int g = 0; g < Hkv; ++g) {
@@ -192,7 +207,8 @@ void test_tier_plan(std::mt19937 &rng) {
         }
         const int64_t slot = int64_t(sekv::align256(sekv::block_bytes(d, d.max_span_len)));
         const int64_t region0 = 4096, region = int64_t(Hkv) * k * slot;
-        sekv::TierPlanIn in{&d, 0, sel.data(), len.data(), off.data(), pos, region0, region};
+        sekv::TierPlanIn in{&d, 0, sel.data(), len.data(), off.data(), pos, region0, region,
+                            ranked ? rnk.data() : nullptr};
         sekv::TierPlan plan;
         CHECK(sekv::plan_tier_sequence(in, &plan) == SEKV_OK);
         // every selected block: its staging slot lies in the region, 256-aligned, and one run
@@ -204,7 +220,7 @@ void test_tier_plan(std::mt19937 &rng) {
                 const int s = sel[size_t(g) * k + j];
                 if (s < 0) continue;
                 const int64_t st = plan.off[size_t(g) * M + s];
-                const int64_t n = int64_t(sekv::block_bytes(d, len[s]));
+                const int64_t n = bsz(g, s);
                 want_bytes += n;
                 CHECK(st >= region0 && st + n <= region0 + region && st % 256 == 0);
                 slots.push_back({st, st + n});
@@ -233,6 +249,17 @@ void test_tier_plan(std::mt19937 &rng) {
             sekv::TierPlanIn small = in;
             small.region_bytes = 255;
             CHECK(sekv::plan_tier_sequence(small, &plan) == SEKV_ERR_INVALID_ARG);
+            if (ranked) {
+                // a rank off the granule is refused
+                int first = -1;
+                for (int i = 0; i < Hkv * k && first < 0; ++i)
+                    if (sel[size_t(i)] >= 0) first = i;
+                std::vector<int32_t> badr = rnk;
+                badr[size_t(first / k) * M + sel[size_t(first)]] = (gran + 1) | (gran << 16);
+                sekv::TierPlanIn br = in;
+                br.block_rank = badr.data();
+                CHECK(sekv::plan_tier_sequence(br, &plan) == SEKV_ERR_INVALID_ARG);
+            }
         }
     }
 }
