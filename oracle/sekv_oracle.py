@@ -453,3 +453,100 @@ def decode_step_gated(q, anchor_k, anchor_v, n_anchors, sum_k, sum_v, n_spans, s
                       block_off, sel, coarse, rank=rank, softmax_scale=softmax_scale,
                       dtype=dtype, block_rank=block_rank)
     return {"sel": sel, "out": out, "gate_logits": x, "q_proj": qp}
+
+
+# ---------------------------------------------------------------------------
+# prefill-side builder: segmentation, surprisal-weighted summaries, factors
+# (Sec. 3.1; Sec. 3.2 eqs. surprisal_weight, key_svd and the summary paragraph)
+# ---------------------------------------------------------------------------
+#
+# Readings (listed with their reasons in the design notes):
+#
+# * mu and sigma are the mean and the population standard deviation of the
+#   sequence's n surprisal values.  So that the boundary decisions are exact,
+#   both sums have one fixed order: 1024 partial sums, partial j adding tokens
+#   j, j + 1024, j + 2048, ... in increasing order (float64), then the partials
+#   combined by halving (partial j += partial j + h for h = 512, 256, ..., 1).
+#   mu = S1 / n; sigma = sqrt(S2 / n) with S2 over (H_t - mu)^2, each product
+#   and difference rounded on its own (no fused multiply-add); the threshold is
+#   mu + (alpha * sigma) in float64, and H_t (float32) is compared in float64.
+# * Anchors: the boundary tokens, the last `window` tokens (the local window),
+#   and the tokens of any run between neighbouring anchors shorter than
+#   `min_span` (short spans stay at full resolution).  The sequence start and
+#   end act as neighbours for the first and last run.  Spans: the remaining
+#   runs, in token order.
+# * A span whose surprisal sums to zero (or less) gets uniform weights.
+# * The factors of a span are its truncated SVD of rank min(|S|, d, R_max)
+#   (eq. key_svd); stored with the rank rounded up to the 16-byte granule, the
+#   extra components zero.
+
+_SEG_LANES = 1024
+
+
+def _fixed_order_sum(x) -> float:
+    """Sum in the fixed order of the segmentation reading (1024 strided partials, halving)."""
+    x = np.asarray(x, dtype=np.float64)
+    part = np.zeros(_SEG_LANES)
+    for j in range(_SEG_LANES):
+        acc = 0.0
+        for v in x[j::_SEG_LANES]:
+            acc = acc + v
+        part[j] = acc
+    h = _SEG_LANES // 2
+    while h >= 1:
+        part[:h] = part[:h] + part[h:2 * h]
+        h //= 2
+    return float(part[0])
+
+
+def surprisal_threshold(H, n: int, alpha: float):
+    """(mu, sigma, mu + alpha sigma) of the first n surprisal values (Sec. 3.1)."""
+    h = np.asarray(H, dtype=np.float32)[:n].astype(np.float64)
+    mu = _fixed_order_sum(h) / n
+    dev = h - mu
+    sq = dev * dev
+    sigma = float(np.sqrt(_fixed_order_sum(sq) / n))
+    return mu, sigma, mu + alpha * sigma
+
+
+def segment(H, n: int, alpha: float, min_span: int, window: int):
+    """Anchors and spans of one sequence (Sec. 3.1).
+
+    Returns (anchors: sorted token indices, spans: list of (start, length))."""
+    if n <= 0:
+        return [], []
+    _, _, thr = surprisal_threshold(H, n, alpha)
+    h = np.asarray(H, dtype=np.float32)[:n].astype(np.float64)
+    anchor = h > thr
+    anchor[max(0, n - window):n] = True
+    spans = []
+    t = 0
+    while t < n:
+        if anchor[t]:
+            t += 1
+            continue
+        s = t
+        while t < n and not anchor[t]:
+            t += 1
+        if t - s >= min_span:
+            spans.append((s, t - s))
+        else:
+            anchor[s:t] = True
+    return [int(i) for i in np.flatnonzero(anchor)], spans
+
+
+def weighted_summary(X, H):
+    """sum_t w_t X_t with w_t = H_t / sum_k H_k over the span (eq. surprisal_weight)."""
+    X = np.asarray(X, dtype=np.float64)
+    h = np.asarray(H, dtype=np.float32).astype(np.float64)
+    tot = h.sum()
+    w = h / tot if tot > 0 else np.full(h.shape, 1.0 / h.size)
+    return w @ X
+
+
+def truncated_svd(X, r_max: int):
+    """Rank min(|S|, d, R_max) truncated SVD of a span matrix (eq. key_svd): (U, sigma, Vt)."""
+    X = np.asarray(X, dtype=np.float64)
+    U, s, Vt = np.linalg.svd(X, full_matrices=False)
+    r = min(X.shape[0], X.shape[1], int(r_max))
+    return U[:, :r], s[:r], Vt[:r]

@@ -6,7 +6,8 @@ shapes the decode-step tests and benchmark use.  It plays the part of the
 paper's prefill stage for synthetic data only: it draws values, partitions the
 context into spans, and forms each span's coarse mean key/value and, for the
 learned selection rule, random routing projections, the projected normalised
-routing summaries and the zoom thresholds.  It holds
+routing summaries and the zoom thresholds; and, for the prefill-side builder,
+token keys/values and surprisal.  It holds
 none of the decode step's arithmetic (routing, selection, reconstruction for
 attention, softmax), and it imports neither the oracle nor the HIP library.
 """
@@ -24,4 +25,6 @@ from .cases import (  # noqa: F401
     Gate,
     NO_BUDGET,
     make_gate,
+    Prefill,
+    make_prefill,
 )

@@ -717,3 +717,73 @@ def make_gate(case: Case, route_dim: int = 32, tau="permissive", budget_tokens: 
         thr = np.array([math.log(t / (1.0 - t)) for t in taus])
     return Gate(route_dim=dr, proj=proj, sum_route=to_storage(sr, dt), thresholds=thr,
                 tau=taus, budget_tokens=int(budget_tokens))
+
+
+# ---------------------------------------------------------------------------
+# prefill inputs: token keys/values and surprisal (for the cache builder)
+# ---------------------------------------------------------------------------
+
+ST_SURP, ST_KTOK, ST_VTOK, ST_SPIKE, ST_OMEGA = 15, 16, 17, 18, 19
+
+
+@dataclass
+class Prefill:
+    """Token-level inputs of the prefill-side builder for one layer.
+
+    keys/values [B][Hkv][N_max][d] (storage type), surprisal [B][N_max] float32,
+    n_tokens [B] int32, omega [d][l] float32 (the random test matrix of the
+    randomized SVD, drawn here and passed in)."""
+    keys: np.ndarray
+    values: np.ndarray
+    surprisal: np.ndarray
+    n_tokens: np.ndarray
+    omega: np.ndarray
+    dtype: str
+    true_starts: list = field(default_factory=list)
+
+
+def make_prefill(batch: int, n_kv_heads: int, head_dim: int, n_tokens, dtype: str = "bf16",
+                 spike_every: int = 150, true_rank: int = 24, noise: float = 0.02, sketch: int = 40,
+                 seed: int = 0) -> Prefill:
+    """Synthetic prefill of `batch` sequences.
+
+    Surprisal: a background of 1 + 0.05 (sum of four Exp(1) draws - 4) with spikes of +8
+    at roughly one position in `spike_every`, so that the mu + alpha sigma rule finds
+    sparse boundaries.  Keys and values: inside each stretch between spikes,
+    a random rank-`true_rank` matrix plus Gaussian noise of relative size `noise`, scaled
+    by 1/sqrt(d) -- compressible spans, as the paper expects of coherent text."""
+    d = head_dim
+    n_tok = np.broadcast_to(np.asarray(n_tokens, dtype=np.int64), (batch,)).copy()
+    N = max(int(n_tok.max()), 1)
+    st = _np_storage_type(dtype)
+    K = np.zeros((batch, n_kv_heads, N, d), dtype=st)
+    V = np.zeros((batch, n_kv_heads, N, d), dtype=st)
+    H = np.zeros((batch, N), dtype=np.float32)
+    starts_all = []
+    for b in range(batch):
+        n = int(n_tok[b])
+        e = uniforms(stream_key(seed, ST_SURP, b), 4 * n).reshape(4, n)
+        h = 1.0 + 0.05 * ((-np.log1p(-e)).sum(axis=0) - 4.0)
+        u = uniforms(stream_key(seed, ST_SPIKE, b), n)
+        spike = u < 1.0 / spike_every
+        h = h + 8.0 * spike
+        H[b, :n] = h.astype(np.float32)
+        starts = [0] + [int(t) for t in np.flatnonzero(spike)] + [n]
+        starts_all.append(starts)
+        for g in range(n_kv_heads):
+            for side, arr, sk in (("K", K, ST_KTOK), ("V", V, ST_VTOK)):
+                rows = np.zeros((n, d))
+                for j in range(len(starts) - 1):
+                    s0, s1 = starts[j], starts[j + 1]
+                    L = s1 - s0
+                    if L <= 0:
+                        continue
+                    key = stream_key(seed, sk, b, g, j)
+                    z = normals(key, L * true_rank).reshape(L, true_rank)
+                    A = normals(key + 1, true_rank * d).reshape(true_rank, d)
+                    eps = normals(key + 2, L * d).reshape(L, d)
+                    rows[s0:s1] = (z @ A / math.sqrt(true_rank) + noise * eps) / math.sqrt(d)
+                arr[b, g, :n] = to_storage(rows, dtype)
+    omega = normals(stream_key(seed, ST_OMEGA), d * sketch).reshape(d, sketch).astype(np.float32)
+    return Prefill(keys=K, values=V, surprisal=H, n_tokens=n_tok.astype(np.int32), omega=omega, dtype=dtype,
+                   true_starts=starts_all)
