@@ -246,6 +246,82 @@ SEKV_API sekv_status sekv_decode_step_gated(const sekv_dims *dims, const sekv_ca
                                             void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* ----------------------------------------------------------------------------------
+ * Prefill-side builder: the step before the decode path.  From a layer's token keys and
+ * values and the tokens' surprisal H_t (produced by the prefill forward pass, Sec. 3.1),
+ * build the stored cache the calls above read.
+ *   1. sekv_segment: boundaries where H_t > mu + alpha sigma (mu, sigma: mean and
+ *      population standard deviation of the sequence's surprisal, Sec. 3.1), each sum
+ *      formed in one fixed order -- 1024 partial sums, partial j adding tokens j, j + 1024,
+ *      ... in float64, then combined by halving (j += j + h for h = 512, ..., 1) -- and
+ *      threshold mu + (alpha * sigma) without fused multiply-add, so the decisions are
+ *      exact.  Anchors: the boundary tokens, the last `window` tokens, and the tokens of
+ *      any run between neighbouring anchors shorter than `min_span`; spans: the other runs.
+ *   2. sekv_build_layout (host only): block offsets and ranks of the factor arena.
+ *   3. sekv_build_cache: anchor rows, surprisal-weighted mean key/value of each span
+ *      (eq. surprisal_weight), |S|, ln|S|, and each span's factors for keys and values by
+ *      a randomized truncated SVD of rank r = min(|S|, d, R_max) (eq. key_svd), stored with
+ *      the rank rounded up to 16 / element bytes (extra components zero; block_rank).
+ *      The SVD sketches the span with the caller's d x l Gaussian test matrix; each
+ *      subspace iteration (`power`) sketches it again with the right singular vectors of
+ *      the previous pass, which sharpens the captured subspace when the spectrum is flat.
+ * ---------------------------------------------------------------------------------- */
+typedef struct {
+    int32_t batch;          /* B >= 0                                                        */
+    int32_t n_kv_heads;     /* Hkv >= 1                                                      */
+    int32_t head_dim;       /* d in {64, 128}                                                */
+    int32_t max_tokens;     /* N_max >= 1: row stride of the token arrays                    */
+    int32_t rank;           /* R_max: multiple of 16 / element bytes, at most 48 and sketch   */
+    int32_t sketch;         /* l: columns of the random test matrix, even, R_max <= l <= 48   */
+    int32_t min_span;       /* L_min >= 2                                                    */
+    int32_t window;         /* w >= 0                                                        */
+    int32_t sweeps;         /* Jacobi sweeps of the small eigenproblems, 1..32 (8 is ample)   */
+    int32_t dtype;          /* sekv_dtype of keys, values and the built cache                */
+    int32_t power;          /* subspace iterations of the randomized SVD, 0..4 (1 is usual)   */
+    int32_t reserved;       /* 0                                                             */
+    double alpha;           /* boundary sensitivity                                          */
+} sekv_build_dims;
+
+/* Scratch bytes sekv_segment needs (device, 16-byte aligned; no initialisation needed). */
+SEKV_API size_t sekv_segment_workspace_size(const sekv_build_dims *dims);
+
+/* Segmentation.  All device pointers: surprisal float [B][N_max], n_tokens int32 [B] (values
+ * are clamped to [0, N_max]); out: n_anchors [B], anchor_idx [B][N_max] (token indices,
+ * ascending), n_spans [B], span_start [B][N_max], span_len [B][N_max] (token order).  One
+ * workgroup per sequence. */
+SEKV_API sekv_status sekv_segment(const sekv_build_dims *dims, const float *surprisal,
+                                  const int32_t *n_tokens, int32_t *n_anchors, int32_t *anchor_idx,
+                                  int32_t *n_spans, int32_t *span_start, int32_t *span_len, void *ws,
+                                  size_t ws_bytes, hipStream_t stream);
+
+/* Host only: the factor arena of a segmentation read back to the host.  n_spans [B] and
+ * span_len [B][N_max] are the segmentation's; max_spans >= every n_spans[b].  Writes
+ * block_off [B][Hkv][max_spans] (256-byte aligned blocks in (b, g, S) order) and
+ * block_rank [B][Hkv][max_spans] (r_S | r_S << 16, 0 past n_spans[b]); returns the arena
+ * bytes, or -1 with sekv_last_error() set. */
+SEKV_API int64_t sekv_build_layout(const sekv_build_dims *dims, int32_t max_spans, const int32_t *n_spans,
+                                   const int32_t *span_len, int64_t *block_off, int32_t *block_rank);
+
+/* The cache.  Device pointers: keys/values [B][Hkv][N_max][d], surprisal, n_tokens and the
+ * segmentation arrays as above, omega float [d][sketch] (the random test matrix, drawn by
+ * the caller), block_off/block_rank from sekv_build_layout (copied to the device).
+ * Outputs, laid out as sekv_cache: anchor_k/v [B][Hkv][max_anchors][d] (rows past
+ * n_anchors[b] untouched), sum_k/v [B][Hkv][max_spans][d], span_len [B][max_spans],
+ * span_logsize [B][max_spans], the factor arena (factors_bytes).  max_anchors and
+ * max_spans must cover every n_anchors[b] and n_spans[b] (larger counts are clamped).
+ * ws: a step workspace of at least 256 bytes whose error word reports blocks outside the
+ * arena (bit 2). */
+SEKV_API sekv_status sekv_build_cache(const sekv_build_dims *dims, const void *keys, const void *values,
+                                      const float *surprisal, const int32_t *n_tokens,
+                                      const int32_t *n_anchors, const int32_t *anchor_idx,
+                                      const int32_t *n_spans, const int32_t *span_start,
+                                      const int32_t *span_len_seg, const float *omega,
+                                      int32_t max_anchors, int32_t max_spans, void *anchor_k,
+                                      void *anchor_v, void *sum_k, void *sum_v, int32_t *span_len,
+                                      double *span_logsize, void *factors, int64_t factors_bytes,
+                                      const int64_t *block_off, void *ws, size_t ws_bytes,
+                                      hipStream_t stream);
+
+/* ----------------------------------------------------------------------------------
  * Several layers in one HIP graph.  A decode step of an L-layer model runs the step
  * above once per layer (each attention layer keeps its own span cache, Sec. 3.2; the
  * per-layer cost analysis of App. D sums over layers).  sekv_graph_create validates

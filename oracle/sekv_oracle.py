@@ -550,3 +550,70 @@ def truncated_svd(X, r_max: int):
     U, s, Vt = np.linalg.svd(X, full_matrices=False)
     r = min(X.shape[0], X.shape[1], int(r_max))
     return U[:, :r], s[:r], Vt[:r]
+
+
+def narrow(x, dtype: str) -> np.ndarray:
+    """float64 -> stored values: float32 by round-to-nearest-even, then for 'bf16' the
+    upper 16 bits after round-to-nearest-even (returned as uint16 bit patterns)."""
+    f = np.asarray(x, dtype=np.float64).astype(np.float32)
+    if dtype == "f32":
+        return f
+    if dtype != "bf16":
+        raise ValueError(f"unknown storage dtype {dtype!r}")
+    u = f.view(np.uint32).astype(np.uint64)
+    u = u + 0x7FFF + ((u >> 16) & 1)
+    return (u >> 16).astype(np.uint16)
+
+
+def build_layer_cache(keys, values, surprisal, n_tokens, *, alpha: float, min_span: int,
+                      window: int, r_max: int, dtype: str) -> dict:
+    """One layer's stored cache from its token keys/values and surprisal (Sec. 3.1, 3.2).
+
+    keys/values [B][Hkv][N][d] stored values, surprisal [B][N] float32.  Segments each
+    sequence, copies the anchor rows, forms the surprisal-weighted span summaries and
+    each span's truncated SVD, and lays the factors out one block per (b, g, S), both
+    sides of stored rank ceil(r / granule) * granule, blocks 256-byte aligned.  Returns
+    the cache arrays (the decode step's inputs, q excepted) and the segmentation."""
+    B, Hkv, _, d = np.asarray(keys).shape
+    _, e = _elem(dtype)
+    gran = 16 // e
+    segs = [segment(surprisal[b], int(n_tokens[b]), alpha, min_span, window) for b in range(B)]
+    A = max([len(a) for a, _ in segs] + [1])
+    M = max([len(s) for _, s in segs] + [1])
+    st = np.uint16 if dtype == "bf16" else np.float32
+    out = {"anchor_k": np.zeros((B, Hkv, A, d), st), "anchor_v": np.zeros((B, Hkv, A, d), st),
+           "sum_k": np.zeros((B, Hkv, M, d), st), "sum_v": np.zeros((B, Hkv, M, d), st),
+           "n_anchors": np.array([len(a) for a, _ in segs], np.int32),
+           "n_spans": np.array([len(s) for _, s in segs], np.int32),
+           "span_len": np.ones((B, M), np.int32), "span_logsize": np.zeros((B, M)),
+           "block_off": np.zeros((B, Hkv, M), np.int64), "block_rank": np.zeros((B, Hkv, M), np.int32)}
+    chunks, pos = [], 0
+    for b, (anchors, spans) in enumerate(segs):
+        h = np.asarray(surprisal[b], dtype=np.float32)
+        for S, (s0, L) in enumerate(spans):
+            out["span_len"][b, S] = L
+            out["span_logsize"][b, S] = np.log(L)
+        for g in range(Hkv):
+            out["anchor_k"][b, g, :len(anchors)] = np.asarray(keys)[b, g, anchors]
+            out["anchor_v"][b, g, :len(anchors)] = np.asarray(values)[b, g, anchors]
+            for S, (s0, L) in enumerate(spans):
+                block = []
+                r = min(L, d, r_max)
+                rs = -(-r // gran) * gran
+                for src, name in ((keys, "k"), (values, "v")):
+                    X = widen(np.asarray(src)[b, g, s0:s0 + L], dtype)
+                    out["sum_" + name][b, g, S] = narrow(weighted_summary(X, h[s0:s0 + L]), dtype)
+                    U, sig, Vt = truncated_svd(X, r_max)
+                    Up = np.zeros((L, rs)); Up[:, :r] = U
+                    sp = np.zeros(rs); sp[:r] = sig
+                    Vp = np.zeros((rs, d)); Vp[:r] = Vt
+                    block += [Up.ravel(), sp, Vp.ravel()]
+                raw = narrow(np.concatenate(block), dtype).tobytes()
+                raw += b"\0" * (-len(raw) % 256)
+                out["block_off"][b, g, S] = pos
+                out["block_rank"][b, g, S] = rs | (rs << 16)
+                chunks.append(raw)
+                pos += len(raw)
+    out["factors"] = np.frombuffer(b"".join(chunks) or b"\0" * 256, dtype=np.uint8).copy()
+    out["segments"] = segs
+    return out

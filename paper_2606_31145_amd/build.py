@@ -51,13 +51,16 @@ def _jobs(bdir, trace):
         jobs.append(([HIPCC, *COMMON, f"--offload-arch={ARCH}", *DEVICE_FLAGS, *tflag,
                       f"-DSEKV_T={t}", f"-DSEKV_D={d}", "-c",
                       os.path.join(CSRC, "sekv_step_inst.hip"), "-o", obj], obj))
-    for src in ("sekv_kernels.hip", "sekv_tier.hip", "sekv_noalloc.hip", "sekv_gate.hip"):
+    for src in ("sekv_kernels.hip", "sekv_tier.hip", "sekv_noalloc.hip", "sekv_gate.hip", "sekv_build.hip"):
         obj = os.path.join(bdir, src.replace(".hip", ".o"))
         jobs.append(([HIPCC, *COMMON, f"--offload-arch={ARCH}", *DEVICE_FLAGS, "-c",
                       os.path.join(CSRC, src), "-o", obj], obj))
     obj = os.path.join(bdir, f"sekv_api{sfx}.o")
     jobs.append(([HIPCC, *COMMON, f"--offload-arch={ARCH}", *tflag, "-c",
                   os.path.join(CSRC, "sekv_api.cpp"), "-o", obj], obj))
+    obj = os.path.join(bdir, "sekv_build_api.o")
+    jobs.append(([HIPCC, *COMMON, f"--offload-arch={ARCH}", "-c",
+                  os.path.join(CSRC, "sekv_build_api.cpp"), "-o", obj], obj))
     obj = os.path.join(bdir, "sekv_host.o")
     jobs.append(([HIPCC, *COMMON, "-c", os.path.join(CSRC, "sekv_host.cpp"), "-o", obj], obj))
     return jobs

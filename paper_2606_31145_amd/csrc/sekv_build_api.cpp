@@ -1,0 +1,159 @@
+// C ABI of the prefill-side builder: host checks, the arena layout, launches.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstring>
+
+#include "sekv.h"
+#include "sekv_host.h"
+#include "sekv_internal.h"
+
+namespace {
+
+using sekv::fail;
+
+bool misaligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; }
+
+sekv_status check_build_dims(const sekv_build_dims *d) {
+    if (!d) return fail(SEKV_ERR_INVALID_ARG, "build dims is NULL");
+    if (d->batch < 0 || d->n_kv_heads < 1 || d->max_tokens < 1)
+        return fail(SEKV_ERR_INVALID_ARG, "batch/n_kv_heads/max_tokens out of range");
+    if (d->head_dim != 64 && d->head_dim != 128) return fail(SEKV_ERR_UNSUPPORTED, "head_dim %d", d->head_dim);
+    if (d->dtype != SEKV_BF16 && d->dtype != SEKV_F32) return fail(SEKV_ERR_UNSUPPORTED, "dtype %d", d->dtype);
+    const int gran = 16 / sekv::elem_bytes(d->dtype);
+    if (d->rank < gran || d->rank > 48 || d->rank % gran)
+        return fail(SEKV_ERR_UNSUPPORTED, "rank %d: a multiple of %d in [%d, 48]", d->rank, gran, gran);
+    if (d->sketch < d->rank || d->sketch > 48 || (d->sketch & 1))
+        return fail(SEKV_ERR_UNSUPPORTED, "sketch %d: even, in [rank, 48]", d->sketch);
+    if (d->min_span < 2) return fail(SEKV_ERR_INVALID_ARG, "min_span %d < 2", d->min_span);
+    if (d->window < 0) return fail(SEKV_ERR_INVALID_ARG, "window < 0");
+    if (d->sweeps < 1 || d->sweeps > 32) return fail(SEKV_ERR_INVALID_ARG, "sweeps %d outside [1, 32]", d->sweeps);
+    if (d->power < 0 || d->power > 4) return fail(SEKV_ERR_INVALID_ARG, "power %d outside [0, 4]", d->power);
+    if (d->reserved != 0) return fail(SEKV_ERR_INVALID_ARG, "reserved field is not 0");
+    if (!(d->alpha == d->alpha)) return fail(SEKV_ERR_INVALID_ARG, "alpha is NaN");
+    return SEKV_OK;
+}
+
+size_t seg_ws(const sekv_build_dims &d) {
+    const size_t B = size_t(d.batch), N = size_t(d.max_tokens);
+    auto a16 = [](size_t x) { return (x + 15) & ~size_t(15); };
+    return a16(B * N) * 2 + a16(B * (N + 2) * 4);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t sekv_segment_workspace_size(const sekv_build_dims *dims) {
+    if (check_build_dims(dims) != SEKV_OK) return 0;
+    return seg_ws(*dims);
+}
+
+sekv_status sekv_segment(const sekv_build_dims *dims, const float *surprisal, const int32_t *n_tokens,
+                         int32_t *n_anchors, int32_t *anchor_idx, int32_t *n_spans, int32_t *span_start,
+                         int32_t *span_len, void *ws, size_t ws_bytes, hipStream_t stream) {
+    sekv_status st = check_build_dims(dims);
+    if (st != SEKV_OK) return st;
+    if (dims->batch == 0) return SEKV_OK;
+    if (!surprisal || !n_tokens || !n_anchors || !anchor_idx || !n_spans || !span_start || !span_len || !ws)
+        return fail(SEKV_ERR_INVALID_ARG, "NULL argument");
+    if (misaligned(surprisal, 4) || misaligned(n_tokens, 4) || misaligned(anchor_idx, 4) ||
+        misaligned(span_start, 4) || misaligned(span_len, 4) || misaligned(ws, 16))
+        return fail(SEKV_ERR_INVALID_ARG, "misaligned argument");
+    if (ws_bytes < seg_ws(*dims)) return fail(SEKV_ERR_WORKSPACE, "segmentation workspace too small");
+    const size_t B = size_t(dims->batch), N = size_t(dims->max_tokens);
+    auto a16 = [](size_t x) { return (x + 15) & ~size_t(15); };
+    unsigned char *w = static_cast<unsigned char *>(ws);
+    sekv::SegArgs a{};
+    a.surprisal = surprisal; a.n_tokens = n_tokens;
+    a.n_anchors = n_anchors; a.anchor_idx = anchor_idx;
+    a.n_spans = n_spans; a.span_start = span_start; a.span_len = span_len;
+    a.ws_flag = w;
+    a.ws_inspan = w + a16(B * N);
+    a.ws_pos = reinterpret_cast<int32_t *>(w + 2 * a16(B * N));
+    a.alpha = dims->alpha;
+    a.N = dims->max_tokens; a.min_span = dims->min_span; a.window = dims->window;
+    const hipError_t e = sekv::launch_segment(a, dims->batch, stream);
+    if (e != hipSuccess) return fail(SEKV_ERR_HIP, "segmentation launch: %s", hipGetErrorString(e));
+    return SEKV_OK;
+}
+
+int64_t sekv_build_layout(const sekv_build_dims *dims, int32_t max_spans, const int32_t *n_spans,
+                          const int32_t *span_len, int64_t *block_off, int32_t *block_rank) {
+    if (check_build_dims(dims) != SEKV_OK) return -1;
+    if (max_spans < 1 || !n_spans || !span_len || !block_off || !block_rank) {
+        fail(SEKV_ERR_INVALID_ARG, "NULL argument or max_spans < 1");
+        return -1;
+    }
+    const int B = dims->batch, Hkv = dims->n_kv_heads, N = dims->max_tokens, d = dims->head_dim;
+    const int e = sekv::elem_bytes(dims->dtype), gran = 16 / e;
+    int64_t pos = 0;
+    for (int b = 0; b < B; ++b) {
+        const int m = n_spans[b];
+        if (m < 0 || m > max_spans || m > N) {
+            fail(SEKV_ERR_INVALID_ARG, "n_spans[%d] = %d outside [0, %d]", b, m, max_spans);
+            return -1;
+        }
+        for (int g = 0; g < Hkv; ++g)
+            for (int S = 0; S < max_spans; ++S) {
+                const size_t i = (size_t(b) * Hkv + g) * max_spans + S;
+                block_off[i] = 0;
+                block_rank[i] = 0;
+                if (S >= m) continue;
+                const int L = span_len[size_t(b) * N + S];
+                if (L < 1 || L > N) {
+                    fail(SEKV_ERR_INVALID_ARG, "span_len[%d][%d] = %d", b, S, L);
+                    return -1;
+                }
+                int r = L < d ? L : d;
+                if (r > dims->rank) r = dims->rank;
+                const int rs = (r + gran - 1) / gran * gran;
+                block_off[i] = pos;
+                block_rank[i] = rs | (rs << 16);
+                pos += int64_t((2 * int64_t(L + 1 + d) * rs * e + 255) / 256 * 256);
+            }
+    }
+    return pos > 0 ? pos : 256;
+}
+
+sekv_status sekv_build_cache(const sekv_build_dims *dims, const void *keys, const void *values,
+                             const float *surprisal, const int32_t *n_tokens, const int32_t *n_anchors,
+                             const int32_t *anchor_idx, const int32_t *n_spans, const int32_t *span_start,
+                             const int32_t *span_len_seg, const float *omega, int32_t max_anchors,
+                             int32_t max_spans, void *anchor_k, void *anchor_v, void *sum_k, void *sum_v,
+                             int32_t *span_len, double *span_logsize, void *factors, int64_t factors_bytes,
+                             const int64_t *block_off, void *ws, size_t ws_bytes, hipStream_t stream) {
+    sekv_status st = check_build_dims(dims);
+    if (st != SEKV_OK) return st;
+    if (dims->batch == 0) return SEKV_OK;
+    if (max_anchors < 1 || max_spans < 1) return fail(SEKV_ERR_INVALID_ARG, "max_anchors/max_spans < 1");
+    const void *req[] = {keys, values, surprisal, n_tokens, n_anchors, anchor_idx, n_spans, span_start,
+                         span_len_seg, omega, anchor_k, anchor_v, sum_k, sum_v, span_len, span_logsize,
+                         factors, block_off, ws};
+    for (const void *p : req)
+        if (!p) return fail(SEKV_ERR_INVALID_ARG, "NULL argument");
+    if (misaligned(keys, 16) || misaligned(values, 16) || misaligned(anchor_k, 16) || misaligned(anchor_v, 16) ||
+        misaligned(sum_k, 16) || misaligned(sum_v, 16) || misaligned(factors, 16) || misaligned(block_off, 8) ||
+        misaligned(span_logsize, 8) || misaligned(omega, 4) || misaligned(ws, 256))
+        return fail(SEKV_ERR_INVALID_ARG, "misaligned argument");
+    if (factors_bytes <= 0) return fail(SEKV_ERR_INVALID_ARG, "factors_bytes <= 0");
+    if (ws_bytes < sizeof(sekv::WsHeader)) return fail(SEKV_ERR_WORKSPACE, "workspace too small");
+    sekv::BuildArgs a{};
+    a.keys = keys; a.values = values; a.surprisal = surprisal;
+    a.n_anchors = n_anchors; a.anchor_idx = anchor_idx; a.n_spans = n_spans; a.span_start = span_start;
+    a.span_len_seg = span_len_seg; a.omega = omega;
+    a.anchor_k = anchor_k; a.anchor_v = anchor_v; a.sum_k = sum_k; a.sum_v = sum_v;
+    a.span_len_out = span_len; a.span_logsize = span_logsize;
+    a.factors = factors; a.factors_bytes = factors_bytes; a.block_off = block_off;
+    a.error = &static_cast<sekv::WsHeader *>(ws)->error;
+    a.Hkv = dims->n_kv_heads; a.N = dims->max_tokens; a.d = dims->head_dim;
+    a.elem = sekv::elem_bytes(dims->dtype); a.R = dims->rank; a.l = dims->sketch; a.sweeps = dims->sweeps;
+    a.power = dims->power;
+    a.A_max = max_anchors; a.M_max = max_spans;
+    (void)n_tokens;
+    const hipError_t e = sekv::launch_build(a, dims->batch, stream);
+    if (e != hipSuccess) return fail(SEKV_ERR_HIP, "builder launch: %s", hipGetErrorString(e));
+    return SEKV_OK;
+}
+
+}  // extern "C"

@@ -32,7 +32,8 @@ EXPORTED = ("sekv_status_string", "sekv_last_error", "sekv_phase_trace", "sekv_c
             "sekv_graph_destroy", "sekv_tier_create", "sekv_tier_destroy",
             "sekv_tier_staging_size", "sekv_tier_last_copy", "sekv_decode_step_tiered",
             "sekv_validate_cache", "sekv_decode_step_noalloc", "sekv_route_gated",
-            "sekv_decode_step_gated")
+            "sekv_decode_step_gated", "sekv_segment_workspace_size", "sekv_segment",
+            "sekv_build_layout", "sekv_build_cache")
 
 
 class SekvError(RuntimeError):
@@ -71,6 +72,16 @@ class GateStruct(ctypes.Structure):
     _fields_ = [("route_dim", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("budget_tokens", ctypes.c_int64), ("proj", ctypes.c_void_p),
                 ("sum_route", ctypes.c_void_p), ("thresholds", ctypes.c_void_p)]
+
+
+class BuildDims(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("max_tokens", ctypes.c_int32),
+                ("rank", ctypes.c_int32), ("sketch", ctypes.c_int32),
+                ("min_span", ctypes.c_int32), ("window", ctypes.c_int32),
+                ("sweeps", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("power", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("alpha", ctypes.c_double)]
 
 
 def _load():
@@ -124,6 +135,16 @@ def _load():
     lib.sekv_decode_step_gated.argtypes = [P(Dims), P(CacheStruct), P(GateStruct), VP, VP, VP, SZ, VP]
     lib.sekv_validate_cache.restype = ctypes.c_int
     lib.sekv_validate_cache.argtypes = [P(Dims), P(CacheStruct)]
+    lib.sekv_segment_workspace_size.restype = ctypes.c_size_t
+    lib.sekv_segment_workspace_size.argtypes = [P(BuildDims)]
+    lib.sekv_segment.restype = ctypes.c_int
+    lib.sekv_segment.argtypes = [P(BuildDims), VP, VP, VP, VP, VP, VP, VP, VP, SZ, VP]
+    lib.sekv_build_layout.restype = ctypes.c_int64
+    lib.sekv_build_layout.argtypes = [P(BuildDims), ctypes.c_int32, VP, VP, VP, VP]
+    lib.sekv_build_cache.restype = ctypes.c_int
+    lib.sekv_build_cache.argtypes = [P(BuildDims), VP, VP, VP, VP, VP, VP, VP, VP, VP, VP,
+                                     ctypes.c_int32, ctypes.c_int32, VP, VP, VP, VP, VP, VP, VP,
+                                     ctypes.c_int64, VP, VP, SZ, VP]
     return lib
 
 
@@ -511,3 +532,101 @@ def decode_step_tiered(dims: Dims, cache: DeviceCache, host: HostFactors, tier: 
                                        tier._h, _ptr(sel), _ptr(out), ws.ptr, ws.nbytes,
                                        _stream(stream), _stream(side)))
     return sel, out
+
+
+# ---------------------------------------------------------------------------
+# prefill-side builder
+# ---------------------------------------------------------------------------
+
+def make_build_dims(*, batch, n_kv_heads, head_dim, max_tokens, rank, sketch, min_span, window,
+                    dtype, alpha=1.0, sweeps=8, power=1) -> BuildDims:
+    dt = DTYPE_CODES[dtype] if isinstance(dtype, str) else int(dtype)
+    return BuildDims(batch, n_kv_heads, head_dim, max_tokens, rank, sketch, min_span, window,
+                     sweeps, dt, power, 0, float(alpha))
+
+
+def segment(bd: BuildDims, surprisal, n_tokens, stream=None) -> dict:
+    """sekv_segment: surprisal float32 [B][N_max] and n_tokens int32 [B] on the device.
+    Returns device tensors n_anchors, anchor_idx, n_spans, span_start, span_len."""
+    dev = surprisal.device
+    B, N = bd.batch, bd.max_tokens
+    ws_bytes = int(LIB.sekv_segment_workspace_size(ctypes.byref(bd)))
+    if ws_bytes == 0 and B > 0:
+        _check(LIB.sekv_segment(ctypes.byref(bd), None, None, None, None, None, None, None,
+                                None, 0, None))
+    out = {"n_anchors": _alloc((B,), torch.int32, dev), "anchor_idx": _alloc((B, N), torch.int32, dev),
+           "n_spans": _alloc((B,), torch.int32, dev), "span_start": _alloc((B, N), torch.int32, dev),
+           "span_len": _alloc((B, N), torch.int32, dev)}
+    ws = _alloc((max(ws_bytes, 16),), torch.uint8, dev)
+    _check(LIB.sekv_segment(ctypes.byref(bd), _ptr(surprisal), _ptr(n_tokens), _ptr(out["n_anchors"]),
+                            _ptr(out["anchor_idx"]), _ptr(out["n_spans"]), _ptr(out["span_start"]),
+                            _ptr(out["span_len"]), _ptr(ws), ws_bytes, _stream(stream)))
+    out["_ws"] = ws
+    return out
+
+
+def build_layout(bd: BuildDims, max_spans: int, n_spans, span_len):
+    """sekv_build_layout on host arrays: (block_off int64, block_rank int32, arena bytes)."""
+    ns = np.ascontiguousarray(n_spans, dtype=np.int32)
+    sl = np.ascontiguousarray(span_len, dtype=np.int32)
+    shape = (bd.batch, bd.n_kv_heads, max(int(max_spans), 1))
+    off = np.zeros(shape, dtype=np.int64)
+    rank = np.zeros(shape, dtype=np.int32)
+    nbytes = LIB.sekv_build_layout(ctypes.byref(bd), int(max_spans), ns.ctypes.data, sl.ctypes.data,
+                                   off.ctypes.data, rank.ctypes.data)
+    if nbytes < 0:
+        raise SekvError(SEKV_ERR_INVALID_ARG, LIB.sekv_last_error().decode())
+    return off, rank, int(nbytes)
+
+
+def build_cache(bd: BuildDims, keys, values, surprisal, n_tokens, seg: dict, omega, max_anchors: int,
+                max_spans: int, block_off, factors_bytes: int, ws: Workspace, out: dict | None = None,
+                stream=None) -> dict:
+    """sekv_build_cache: returns the device tensors of the stored cache (anchor_k/v, sum_k/v,
+    span_len, span_logsize, factors); `out` may hold them preallocated."""
+    dev = keys.device
+    B, Hkv, d = bd.batch, bd.n_kv_heads, bd.head_dim
+    st = keys.dtype
+    if out is None:
+        out = {"anchor_k": torch.zeros((B, Hkv, max_anchors, d), dtype=st, device=dev),
+               "anchor_v": torch.zeros((B, Hkv, max_anchors, d), dtype=st, device=dev),
+               "sum_k": torch.zeros((B, Hkv, max_spans, d), dtype=st, device=dev),
+               "sum_v": torch.zeros((B, Hkv, max_spans, d), dtype=st, device=dev),
+               "span_len": torch.ones((B, max_spans), dtype=torch.int32, device=dev),
+               "span_logsize": torch.zeros((B, max_spans), dtype=torch.float64, device=dev),
+               "factors": torch.zeros((int(factors_bytes),), dtype=torch.uint8, device=dev)}
+    _check(LIB.sekv_build_cache(
+        ctypes.byref(bd), _ptr(keys), _ptr(values), _ptr(surprisal), _ptr(n_tokens),
+        _ptr(seg["n_anchors"]), _ptr(seg["anchor_idx"]), _ptr(seg["n_spans"]), _ptr(seg["span_start"]),
+        _ptr(seg["span_len"]), _ptr(omega), int(max_anchors), int(max_spans), _ptr(out["anchor_k"]),
+        _ptr(out["anchor_v"]), _ptr(out["sum_k"]), _ptr(out["sum_v"]), _ptr(out["span_len"]),
+        _ptr(out["span_logsize"]), _ptr(out["factors"]), int(out["factors"].numel()), _ptr(block_off),
+        ws.ptr, ws.nbytes, _stream(stream)))
+    return out
+
+
+def build_layer(bd: BuildDims, keys, values, surprisal, n_tokens, omega, ws: Workspace, stream=None):
+    """Segment, lay out and build one layer's cache.  The layout needs the span tables on
+    the host, so the stream is synchronised once between segmentation and the build.
+    Returns (cache tensors, segmentation tensors, host layout dict)."""
+    seg = segment(bd, surprisal, n_tokens, stream)
+    (stream if stream is not None else torch.cuda.current_stream()).synchronize()
+    ns = seg["n_spans"].cpu().numpy()
+    na = seg["n_anchors"].cpu().numpy()
+    span_len = seg["span_len"].cpu().numpy()
+    max_spans = max(int(ns.max(initial=0)), 1)
+    max_anchors = max(int(na.max(initial=0)), 1)
+    off, rank, nbytes = build_layout(bd, max_spans, ns, span_len)
+    dev = keys.device
+    block_off = torch.from_numpy(off).to(dev)
+    cache = build_cache(bd, keys, values, surprisal, n_tokens, seg, omega, max_anchors, max_spans,
+                        block_off, nbytes, ws, stream=stream)
+    cache["block_off"] = block_off
+    cache["block_rank"] = torch.from_numpy(rank).to(dev)
+    cache["n_anchors"] = seg["n_anchors"]
+    cache["n_spans"] = seg["n_spans"]
+    layout = {"n_spans": ns, "n_anchors": na, "max_spans": max_spans, "max_anchors": max_anchors,
+              "block_off": off, "block_rank": rank, "factors_bytes": nbytes,
+              "max_span_len": max([int(span_len[b, :ns[b]].max(initial=1)) for b in range(bd.batch)],
+                                  default=1)}
+    return cache, seg, layout

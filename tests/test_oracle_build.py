@@ -100,8 +100,85 @@ def check_truncated_svd():
         assert np.allclose(U.T @ U, np.eye(r), atol=1e-12) and np.allclose(Vt @ Vt.T, np.eye(r), atol=1e-12)
 
 
+def _dense_attention(q, K, V, n, scale):
+    """Plain softmax attention of every query head over the first n tokens."""
+    Hq, Hkv = q.shape[0], K.shape[0]
+    G = Hq // Hkv
+    out = np.zeros((Hq, K.shape[-1]))
+    for h in range(Hq):
+        s = K[h // G, :n] @ q[h] * scale
+        w = np.exp(s - s.max())
+        out[h] = (w / w.sum()) @ V[h // G, :n]
+    return out
+
+
+def _built(p, alpha, min_span, window, r_max, dtype):
+    return orc.build_layer_cache(p.keys, p.values, p.surprisal, p.n_tokens, alpha=alpha,
+                                 min_span=min_span, window=window, r_max=r_max, dtype=dtype)
+
+
+def _decode(c, q, r_max, top_k, dtype):
+    return orc.decode_step(q, c["anchor_k"], c["anchor_v"], c["n_anchors"], c["sum_k"], c["sum_v"],
+                           c["n_spans"], c["span_len"], c["span_logsize"], c["factors"],
+                           c["block_off"], rank=r_max, top_k=top_k, softmax_scale=0.25,
+                           dtype=dtype, block_rank=c["block_rank"])
+
+
+def check_built_cache_full_zoom_is_dense_attention():
+    """Every span zoomed at full rank (r_max >= d): the built cache reproduces dense attention."""
+    p = make_prefill(2, 2, 16, [90, 61], dtype="f32", spike_every=12, true_rank=6, seed=21)
+    g = rng(22)
+    q = g.standard_normal((2, 4, 16)).astype(np.float32)
+    c = _built(p, 0.5, 3, 5, 16, "f32")
+    assert int(c["n_spans"].min()) >= 2, "the pin needs spans"
+    res = _decode(c, q, 16, int(c["n_spans"].max()), "f32")
+    for b in range(2):
+        n = int(p.n_tokens[b])
+        ref = _dense_attention(q[b].astype(np.float64), p.keys[b].astype(np.float64),
+                               p.values[b].astype(np.float64), n, 0.25)
+        assert np.allclose(res["out"][b], ref, rtol=0, atol=2e-6), np.abs(res["out"][b] - ref).max()
+
+
+def check_built_cache_constant_spans_unzoomed_is_dense_attention():
+    """Tokens constant within each span: the coarse entries (summary logit + ln|S|, summary
+    value) equal attention over the span's tokens, so no zoom at all gives dense attention."""
+    p = make_prefill(1, 2, 16, [120], dtype="f32", spike_every=15, seed=23)
+    anchors, spans = orc.segment(p.surprisal[0], 120, 1.0, 4, 7)
+    assert len(spans) >= 2
+    for s0, L in spans:
+        p.keys[0, :, s0:s0 + L] = p.keys[0, :, s0:s0 + 1]
+        p.values[0, :, s0:s0 + L] = p.values[0, :, s0:s0 + 1]
+    q = rng(24).standard_normal((1, 4, 16)).astype(np.float32)
+    c = _built(p, 1.0, 4, 7, 8, "f32")
+    res = _decode(c, q, 8, 0, "f32")
+    ref = _dense_attention(q[0].astype(np.float64), p.keys[0].astype(np.float64),
+                           p.values[0].astype(np.float64), 120, 0.25)
+    assert np.allclose(res["out"][0], ref, rtol=0, atol=1e-6), np.abs(res["out"][0] - ref).max()
+
+
+def check_built_cache_layout():
+    """Stored ranks round min(|S|, d, R_max) up to the granule; blocks hold the truncated SVD
+    with zero extra components; anchors are the token rows; ln|S| natural."""
+    p = make_prefill(1, 1, 32, [700], dtype="bf16", spike_every=60, seed=25)
+    c = _built(p, 1.0, 2, 16, 24, "bf16")
+    anchors, spans = c["segments"][0]
+    assert np.array_equal(c["anchor_k"][0, 0, :len(anchors)], p.keys[0, 0, anchors])
+    for S, (s0, L) in enumerate(spans):
+        rk, rv = c["block_rank"][0, 0, S] & 0xFFFF, c["block_rank"][0, 0, S] >> 16
+        r = min(L, 32, 24)
+        assert rk == rv == -(-r // 8) * 8 and c["block_off"][0, 0, S] % 256 == 0
+        assert c["span_len"][0, S] == L and c["span_logsize"][0, S] == math.log(L)
+        blk = orc.read_span_block(c["factors"], int(c["block_off"][0, 0, S]), L, rk, 32, "bf16", rv)
+        X = orc.widen(p.keys[0, 0, s0:s0 + L], "bf16")
+        assert np.all(blk["sK"][r:] == 0) and np.all(blk["UK"][:, r:] == 0)
+        full = np.linalg.svd(X, compute_uv=False)
+        err = np.linalg.norm(X - orc.reconstruct(blk["UK"], blk["sK"], blk["VtK"]))
+        assert err <= math.sqrt(np.sum(full[r:] ** 2)) + 2e-2 * np.linalg.norm(X)
+
+
 PINS = [check_worked_example, check_stats_against_library, check_segmentation_invariants,
-        check_weighted_summary, check_truncated_svd]
+        check_weighted_summary, check_truncated_svd, check_built_cache_full_zoom_is_dense_attention,
+        check_built_cache_constant_spans_unzoomed_is_dense_attention, check_built_cache_layout]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda f: f.__name__)
