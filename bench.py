@@ -91,11 +91,14 @@ def parse():
                     help="expanded-token budget per (sequence, KV head) of the gated step")
     ap.add_argument("--calibration-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (counter calibration)")
-    ap.add_argument("--workload", choices=["layer128k", "layers32", "hosttier"],
+    ap.add_argument("--workload", choices=["layer128k", "layers32", "hosttier", "prefill128k"],
                     default="layer128k",
                     help="layer128k: one 128K x 4 layer (the headline); layers32: the 32-layer, "
                          "batch-32, 32K-context step replayed as one HIP graph; hosttier: the "
-                         "128K x 4 layer with its factors in pinned host memory")
+                         "128K x 4 layer with its factors in pinned host memory; prefill128k: "
+                         "the prefill-side builder of one 128K x 4 layer (segmentation, "
+                         "summaries, randomized SVD)")
+    ap.add_argument("--power", type=int, default=1, help="prefill128k: subspace iterations")
     ap.add_argument("--phase-trace", metavar="OUT_MD", default=None,
                     help="diagnostic: load the phase-trace build (libsekv_trace.so), trace the "
                          "work items of a few steps of the workload and write a per-phase "
@@ -125,6 +128,8 @@ def main():
         return bench_layers32(args, dev)
     if args.workload == "hosttier":
         return bench_hosttier(args, dev)
+    if args.workload == "prefill128k":
+        return bench_prefill(args, dev)
 
     main_run = time_layer128k(args, dev, args.variant)
     if main_run is None:                     # phase-trace mode
@@ -663,6 +668,101 @@ def bench_hosttier(args, dev):
         "hbm": {"resident_bytes": resident, "full_bf16_kv_bytes": full,
                 "saved_frac": round(1.0 - resident / full, 4),
                 "algorithmic_bytes_per_step": acct["total"]},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def bench_prefill(args, dev):
+    """The prefill-side builder for one 128K x 4 layer of the headline shape (Hkv 8, d 128,
+    bfloat16, R_max 32, sketch 40): segmentation, then anchors, summaries and the
+    randomized SVD of every span.  Kernel times from HIP events on the launch stream; the
+    whole call (with the span-table read-back and the host layout) by wall clock."""
+    import numpy as np
+    import torch
+
+    from paper_2606_31145_amd import sekv
+    from synth import make_prefill
+
+    B, Hkv, d, N = 4, 8, 128, 131072
+    R, l = 32, 40
+    t0 = time.time()
+    # one generated key/value stream per sequence; KV head g holds it with its feature columns
+    # rotated by 8 g (a permutation: the same spans, ranks and spectra, distinct memory)
+    p = make_prefill(B, 1, d, N, dtype="bf16", spike_every=170, true_rank=24, noise=0.02,
+                     sketch=l, seed=5)
+    log(f"[bench] prefill generated in {time.time() - t0:.1f}s")
+
+    def to_dev(a, bf16=False):
+        a = np.ascontiguousarray(a)
+        t = torch.from_numpy(a.view(np.int16)).view(torch.bfloat16) if bf16 else torch.from_numpy(a)
+        return t.to(dev)
+
+    def heads(a):
+        t = to_dev(a, True)                                          # [B][1][N][d]
+        return torch.cat([torch.roll(t, 8 * g, dims=3) for g in range(Hkv)], dim=1).contiguous()
+
+    keys, values = heads(p.keys), heads(p.values)
+    del p.keys, p.values
+    H, n_tok, omega = to_dev(p.surprisal), to_dev(p.n_tokens), to_dev(p.omega)
+    bd = sekv.make_build_dims(batch=B, n_kv_heads=Hkv, head_dim=d, max_tokens=N, rank=R, sketch=l,
+                              min_span=16, window=512, dtype="bf16", alpha=1.0, sweeps=8,
+                              power=args.power)
+    wdims = sekv.make_dims(batch=1, n_q_heads=1, n_kv_heads=1, head_dim=64, rank=8, top_k=1,
+                           max_anchors=1, max_spans=1, max_span_len=1, dtype="f32",
+                           softmax_scale=1.0)
+    ws = sekv.Workspace(wdims, dev)
+    stream = torch.cuda.current_stream()
+    cache, seg, lay = sekv.build_layer(bd, keys, values, H, n_tok, omega, ws)
+    torch.cuda.synchronize()
+    assert ws.status() == 0
+    block_off = cache["block_off"]
+    walls = []
+    for _ in range(max(1, min(args.warmup, 3))):
+        sekv.build_layer(bd, keys, values, H, n_tok, omega, ws)
+    torch.cuda.synchronize()
+    K = max(1, min(args.steps, 10))
+    for _ in range(K):
+        t1 = time.perf_counter()
+        sekv.build_layer(bd, keys, values, H, n_tok, omega, ws)
+        torch.cuda.synchronize()
+        walls.append(time.perf_counter() - t1)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    seg_ms, build_ms = [], []
+    for _ in range(K):
+        ev[0].record(stream)
+        seg2 = sekv.segment(bd, H, n_tok, stream)
+        ev[1].record(stream)
+        sekv.build_cache(bd, keys, values, H, n_tok, seg2, omega, lay["max_anchors"], lay["max_spans"],
+                         block_off, lay["factors_bytes"], ws, out=cache, stream=stream)
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        seg_ms.append(ev[0].elapsed_time(ev[1]))
+        build_ms.append(ev[1].elapsed_time(ev[2]))
+    assert ws.status() == 0
+    tokens = B * N
+    kern_ms = float(np.mean(seg_ms)) + float(np.mean(build_ms))
+    span_tokens = int(sum(int(cache["span_len"][b, :int(lay["n_spans"][b])].sum().item()) for b in range(B)))
+    kv_bytes = 2 * B * Hkv * N * d * 2
+    out_bytes = int(sum(cache[k].numel() * cache[k].element_size()
+                        for k in ("anchor_k", "anchor_v", "sum_k", "sum_v", "factors")))
+    wall_ms = float(np.median(walls)) * 1e3
+    line = {
+        "metric": "prefill-side build throughput (tokens per second per layer), 128K context, batch 4",
+        "value": round(tokens / (kern_ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(kern_ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "sekv-prefill-build-128k-b4-hkv8-d128-r32-l40-bf16", "batch": B,
+                   "context": N, "n_kv_heads": Hkv, "head_dim": d, "rank": R, "sketch": l,
+                   "power": args.power, "min_span": 16, "window": 512, "alpha": 1.0,
+                   "heads": "one generated stream per sequence, head g with columns rotated by 8 g",
+                   "parallelism": "single-gpu"},
+        "segment_ms": round(float(np.mean(seg_ms)), 4),
+        "build_ms": round(float(np.mean(build_ms)), 4),
+        "call_wall_ms_with_layout": round(wall_ms, 3),
+        "spans": [int(x) for x in lay["n_spans"]], "anchors": [int(x) for x in lay["n_anchors"]],
+        "span_tokens": span_tokens,
+        "hbm": {"kv_read_bytes": kv_bytes, "written_bytes": out_bytes,
+                "GB_s_kv_once": round((kv_bytes + out_bytes) / (kern_ms * 1e-3) / 1e9, 1)},
     }
     print(json.dumps(line), flush=True)
 

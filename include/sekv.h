@@ -262,16 +262,19 @@ SEKV_API sekv_status sekv_decode_step_gated(const sekv_dims *dims, const sekv_ca
  *      a randomized truncated SVD of rank r = min(|S|, d, R_max) (eq. key_svd), stored with
  *      the rank rounded up to 16 / element bytes (extra components zero; block_rank).
  *      The SVD sketches the span with the caller's d x l Gaussian test matrix; each
- *      subspace iteration (`power`) sketches it again with the right singular vectors of
- *      the previous pass, which sharpens the captured subspace when the spectrum is flat.
+ *      subspace iteration (`power`) sketches it again with an orthonormal basis of the
+ *      previous pass's dominant row space, which sharpens the captured subspace when the
+ *      spectrum is flat.  Directions of the sketch below 1e-8 of its largest Gram diagonal
+ *      entry are dropped (rank-deficient spans), as are components below 1e-5 of the
+ *      largest singular value.
  * ---------------------------------------------------------------------------------- */
 typedef struct {
     int32_t batch;          /* B >= 0                                                        */
     int32_t n_kv_heads;     /* Hkv >= 1                                                      */
     int32_t head_dim;       /* d in {64, 128}                                                */
     int32_t max_tokens;     /* N_max >= 1: row stride of the token arrays                    */
-    int32_t rank;           /* R_max: multiple of 16 / element bytes, at most 48 and sketch   */
-    int32_t sketch;         /* l: columns of the random test matrix, even, R_max <= l <= 48   */
+    int32_t rank;           /* R_max: multiple of 16 / element bytes, at most 40 and sketch   */
+    int32_t sketch;         /* l: columns of the random test matrix, even, R_max <= l <= 40   */
     int32_t min_span;       /* L_min >= 2                                                    */
     int32_t window;         /* w >= 0                                                        */
     int32_t sweeps;         /* Jacobi sweeps of the small eigenproblems, 1..32 (8 is ample)   */

@@ -51,10 +51,13 @@ def _jobs(bdir, trace):
         jobs.append(([HIPCC, *COMMON, f"--offload-arch={ARCH}", *DEVICE_FLAGS, *tflag,
                       f"-DSEKV_T={t}", f"-DSEKV_D={d}", "-c",
                       os.path.join(CSRC, "sekv_step_inst.hip"), "-o", obj], obj))
-    for src in ("sekv_kernels.hip", "sekv_tier.hip", "sekv_noalloc.hip", "sekv_gate.hip", "sekv_build.hip"):
+    for src in ("sekv_kernels.hip", "sekv_tier.hip", "sekv_noalloc.hip", "sekv_gate.hip"):
         obj = os.path.join(bdir, src.replace(".hip", ".o"))
         jobs.append(([HIPCC, *COMMON, f"--offload-arch={ARCH}", *DEVICE_FLAGS, "-c",
                       os.path.join(CSRC, src), "-o", obj], obj))
+    obj = os.path.join(bdir, f"sekv_build{sfx}.o")        # the builder's SVD has phase marks too
+    jobs.append(([HIPCC, *COMMON, f"--offload-arch={ARCH}", *DEVICE_FLAGS, *tflag, "-c",
+                  os.path.join(CSRC, "sekv_build.hip"), "-o", obj], obj))
     obj = os.path.join(bdir, f"sekv_api{sfx}.o")
     jobs.append(([HIPCC, *COMMON, f"--offload-arch={ARCH}", *tflag, "-c",
                   os.path.join(CSRC, "sekv_api.cpp"), "-o", obj], obj))

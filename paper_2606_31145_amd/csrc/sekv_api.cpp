@@ -25,6 +25,17 @@ using sekv::fail;
 thread_local int64_t *g_trace = nullptr;
 thread_local size_t g_trace_bytes = 0;
 
+}  // namespace
+
+namespace sekv {
+int64_t *trace_buffer(size_t *bytes) {
+    *bytes = g_trace_bytes;
+    return g_trace;
+}
+}  // namespace sekv
+
+namespace {
+
 sekv_status hip_fail(hipError_t e, const char *what) {
     return fail(SEKV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }

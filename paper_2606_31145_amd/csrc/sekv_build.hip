@@ -12,16 +12,19 @@
 //                    surprisal_weight; float32 accumulation), |S| and ln|S|.
 //   svd_kernel       one (sequence, KV head, span, side) per workgroup: a randomized
 //                    truncated SVD of the span's |S| x d matrix X (eq. key_svd, rank
-//                    r = min(|S|, d, R_max)): sketch Y = X Omega with the caller's random
-//                    d x l test matrix; G = Y^T Y = W diag(lambda) W^T and the orthonormal
-//                    basis Q = Y W diag(lambda^-1/2) of the sketch's range (directions with
-//                    lambda below 1e-6 of the largest dropped, so a rank-deficient sketch
-//                    is handled); B = Q^T X = diag(lambda^-1/2) W^T (Y^T X); B B^T =
-//                    E diag(sigma^2) E^T; V^T = diag(1/sigma) E^T B and U = Q E = Y T with
-//                    T = W diag(lambda^-1/2) E.  Both small eigen-decompositions are cyclic
-//                    Jacobi rotations in LDS.  The factors go into the span's block of the
-//                    factor arena, stored with the rank rounded up to the 16-byte granule
-//                    (the extra components zero).
+//                    r = min(|S|, d, R_max)).  Sketch Y = X Omega with the caller's d x l
+//                    test matrix; G = Y^T Y (float64) = R^T R by Cholesky with diagonal
+//                    pivoting, stopped where the remaining pivots fall below 1e-8 of the
+//                    largest diagonal (a rank-deficient sketch keeps k < l columns), so
+//                    Q = Y_piv R^-1 is an orthonormal basis of the sketch's range;
+//                    B = Q^T X = R^-T (Y_piv^T X).  Each subspace iteration replaces Omega
+//                    by an orthonormal basis of B's row space (pivoted Cholesky of B B^T
+//                    again) and sketches anew.  Last, B B^T = E diag(sigma^2) E^T by
+//                    cyclic Jacobi rotations (stopped once a sweep rotates nothing),
+//                    V^T = diag(1/sigma) E^T B and U = Q E = Y_piv (R^-1 E).  The factors go
+//                    into the span's block of the factor arena, stored with the rank
+//                    rounded up to the 16-byte granule (the extra components zero).
+
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -33,7 +36,7 @@ namespace {
 
 constexpr int kSegThreads = 1024;
 constexpr int BT = 256;                 // builder threads per workgroup
-constexpr int kMaxL = 48;               // largest sketch width
+constexpr int kMaxL = 40;               // largest sketch width
 constexpr int kTile = 16;               // tokens per streamed tile in the SVD
 
 __device__ inline float ld_elem(const void *base, size_t i, int elem) {
@@ -256,90 +259,304 @@ __global__ void __launch_bounds__(BT) gather_kernel(BuildArgs a, int rows) {
 // randomized truncated SVD of one span side
 // ---------------------------------------------------------------------------
 
+// LDS of the SVD.  Region a holds the passes' tiles or, between passes, the two Cholesky
+// factors / Jacobi vectors; bm accumulates Y^T X during a pass and then holds B; am
+// accumulates G during a pass, then B B^T (and the Jacobi matrix, or Rinv), and last T.
+constexpr int KL = kMaxL;
 struct SvdSmem {
     union {
         struct {                              // passes over X
-            float om[kMaxL][128];             // Omega^T (l x d)
+            uint16_t om[KL][128 + 2];         // the test matrix, transposed (l x d), as
+                                              //   bfloat16 (any fixed test matrix serves;
+                                              //   both passes of an iteration use this one);
+                                              //   rows padded: a wave reads one column
             float x[kTile][128 + 1];          // token tile
-            float yt[kTile][kMaxL + 1];       // sketch tile
+            float yt[kTile][KL + 1];          // sketch tile Y = X Omega
         } p;
-        struct {                              // small dense algebra (float64: the Gram
-            float bm[kMaxL][128 + 1];         // matrices square the condition number)
-            double am[kMaxL][kMaxL + 1];      // G, then B B^T (rotated to diagonal)
-        } s;                                  // bm: Y^T X, then B
-    } u;
-    double wm[kMaxL][kMaxL + 1];              // eigenvectors of G, then T = W diag E
-    double em[kMaxL][kMaxL + 1];              // eigenvectors of B B^T
-    double cs[kMaxL / 2][2];                  // a round's rotations (c, s)
-    double scale[kMaxL];                      // lambda^-1/2 of the kept directions, else 0
-    double sig[kMaxL];
-    int order[kMaxL];
-    double lmax;
+        struct {                              // between passes (float64: a Gram matrix
+            double rg[KL][KL + 1];            //   squares the condition number)
+            double em[KL][KL + 1];            // rg: R of G (rows: pivot steps, columns:
+        } s;                                  //   sketch columns); em: R of B B^T
+    } u;                                      //   (subspace iteration) or E (last pass)
+    float bm[KL][128 + 1];                    // Y^T X, then B (rows in pivot order)
+    double am[KL][KL + 1];                    // G; B B^T; Rinv; T = R^-1 E
+    double jd[2][KL];                         // Jacobi: diagonal, and the entries the round
+    double jo[2][KL / 2];                     //   pairs (two alternating copies)
+    double sig[KL];
+    double dg[2][KL];                         // remaining Cholesky diagonal (two copies)
+    int piv[KL], piv2[KL], order[KL];
+    int nconv[2];
 };
+
+// A workgroup's static LDS must stay within 64 KiB: arrays placed past it are not backed.
+static_assert(sizeof(SvdSmem) <= 65536, "SVD LDS over 64 KiB");
 
 // Round-robin pairing of round k among n (even) indices: index n-1 stays, the others
 // rotate; pair i of the round is (p, q) with p < q.  Every pair meets once per sweep.
+// (0 <= k < n - 1, 0 <= i < n / 2: every reduction below is one conditional step.)
 __device__ inline void rr_pair(int n, int k, int i, int *p, int *q) {
+    const int m = n - 1;
     int a0, b0;
-    if (i == 0) { a0 = n - 1; b0 = k % (n - 1); }
-    else { a0 = (k + i) % (n - 1); b0 = (k - i + (n - 1)) % (n - 1); }
+    if (i == 0) { a0 = m; b0 = k; }
+    else {
+        a0 = k + i;
+        if (a0 >= m) a0 -= m;
+        b0 = k - i;
+        if (b0 < 0) b0 += m;
+    }
     *p = min(a0, b0);
     *q = max(a0, b0);
 }
 
+// The partner b of index a in round k of the same pairing, and the number of their pair.
+__device__ inline void rr_partner(int n, int k, int a, int *b, int *i) {
+    const int m = n - 1;
+    if (a == m) { *b = k; *i = 0; return; }
+    int bb = 2 * k - a;                          // in (-m, 2m)
+    if (bb < 0) bb += m;
+    else if (bb >= m) bb -= m;
+    if (bb == a) { *b = m; *i = 0; return; }
+    *b = bb;
+    int d1 = a - k;                              // in (-m, m)
+    if (d1 < 0) d1 += m;
+    *i = d1 <= (m - 1) / 2 ? d1 : m - d1;
+}
+
 // Cyclic Jacobi on the symmetric n x n matrix A (n even): A is rotated towards diagonal,
-// V (set to I here) accumulates the rotations, so that A_in = V diag(A_out) V^T.
-__device__ void jacobi(double (*A)[kMaxL + 1], double (*V)[kMaxL + 1], double (*cs)[2], int n, int sweeps,
-                       int tid) {
+// V (set to I here) accumulates the rotations, so that A_in = V diag(A_out) V^T.  A pair
+// is rotated when its off-diagonal entry exceeds 1e-14 of the geometric mean of its
+// diagonal entries; the sweeps stop after one that rotates no pair.
+//
+// One barrier per round.  Lanes 0 .. n/2 - 1 of every wave compute the round's rotations
+// from the diagonal and the paired entries, which the previous round left in jd / jo (two
+// alternating copies), and pass them on by shuffles.  A is updated as 2 x 2 blocks of
+// pairs (I, J), each block and its transpose by one thread, V as column pairs; the owner
+// of an entry that the next round pairs, or of a diagonal entry, also writes it to jd / jo.
+__device__ void jacobi(double (*A)[KL + 1], double (*V)[KL + 1], SvdSmem &sm, int n, int sweeps, int tid) {
+    const int lane = tid & 63, np = n / 2;
     for (int idx = tid; idx < n * n; idx += BT) V[idx / n][idx % n] = (idx / n == idx % n) ? 1.0 : 0.0;
+    if (tid < n) sm.jd[0][tid] = A[tid][tid];
+    if (tid < np) {
+        int p, q;
+        rr_pair(n, 0, tid, &p, &q);
+        sm.jo[0][tid] = A[p][q];
+    }
+    if (tid < 2) sm.nconv[tid] = 0;
     __syncthreads();
+    constexpr int NB = (KL / 2 * KL / 2 + BT - 1) / BT;          // block slots per thread
+    constexpr int NV = (KL * KL / 2 + BT - 1) / BT;              // V column-pair slots per thread
+    int buf = 0;
     for (int sweep = 0; sweep < sweeps; ++sweep) {
+        const int par = sweep & 1;
         for (int k = 0; k < n - 1; ++k) {
-            if (tid < n / 2) {
+            const int kn = k + 1 == n - 1 ? 0 : k + 1;
+            double c = 1.0, s = 0.0;
+            if (lane < np) {
                 int p, q;
-                rr_pair(n, k, tid, &p, &q);
-                const double app = A[p][p], aqq = A[q][q], apq = A[p][q];
-                double c = 1.0, s = 0.0;
-                if (apq != 0.0 && fabs(apq) > 1e-300 * (fabs(app) + fabs(aqq))) {
+                rr_pair(n, k, lane, &p, &q);
+                const double app = sm.jd[buf][p], aqq = sm.jd[buf][q], apq = sm.jo[buf][lane];
+                if (fabs(apq) > 1e-14 * sqrt(fabs(app) * fabs(aqq)) && apq != 0.0) {
                     const double th = (aqq - app) / (2.0 * apq);
                     const double t = (th >= 0.0 ? 1.0 : -1.0) / (fabs(th) + sqrt(1.0 + th * th));
                     c = 1.0 / sqrt(1.0 + t * t);
                     s = t * c;
+                    sm.nconv[par] = 1;
                 }
-                cs[tid][0] = c;
-                cs[tid][1] = s;
+            }
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                const int idx = tid + BT * u;
+                const bool in = idx < np * np;
+                const int I = in ? idx / np : 0, J = in ? idx % np : 0;
+                const double cI = __shfl(c, I), sI = __shfl(s, I), cJ = __shfl(c, J), sJ = __shfl(s, J);
+                if (in && I <= J) {
+                    int pI, qI, pJ, qJ;
+                    rr_pair(n, k, I, &pI, &qI);
+                    rr_pair(n, k, J, &pJ, &qJ);
+                    const double a = A[pI][pJ], b = A[pI][qJ], cc = A[qI][pJ], dd = A[qI][qJ];
+                    const double t00 = cI * a - sI * cc, t01 = cI * b - sI * dd;
+                    const double t10 = sI * a + cI * cc, t11 = sI * b + cI * dd;
+                    const double n00 = t00 * cJ - t01 * sJ, n01 = t00 * sJ + t01 * cJ;
+                    const double n10 = t10 * cJ - t11 * sJ, n11 = t10 * sJ + t11 * cJ;
+                    A[pI][pJ] = n00; A[pI][qJ] = n01; A[qI][pJ] = n10; A[qI][qJ] = n11;
+                    if (I != J) {
+                        A[pJ][pI] = n00; A[qJ][pI] = n01; A[pJ][qI] = n10; A[qJ][qI] = n11;
+                    } else {
+                        sm.jd[buf ^ 1][pI] = n00;
+                        sm.jd[buf ^ 1][qI] = n11;
+                    }
+                    const int xs[4] = {pI, pI, qI, qI}, ys[4] = {pJ, qJ, pJ, qJ};
+                    const double vs[4] = {n00, n01, n10, n11};
+#pragma unroll
+                    for (int e2 = 0; e2 < 4; ++e2) {
+                        int pb, pi;
+                        rr_partner(n, kn, xs[e2], &pb, &pi);
+                        if (pb == ys[e2]) sm.jo[buf ^ 1][pi] = vs[e2];
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < NV; ++u) {
+                const int idx = tid + BT * u;
+                const bool in = idx < n * np;
+                const int r = in ? idx / np : 0, J = in ? idx % np : 0;
+                const double cJ = __shfl(c, J), sJ = __shfl(s, J);
+                if (in && sJ != 0.0) {
+                    int pJ, qJ;
+                    rr_pair(n, k, J, &pJ, &qJ);
+                    const double vp = V[r][pJ], vq = V[r][qJ];
+                    V[r][pJ] = cJ * vp - sJ * vq;
+                    V[r][qJ] = sJ * vp + cJ * vq;
+                }
             }
             __syncthreads();
-            for (int idx = tid; idx < (n / 2) * n; idx += BT) {        // rows p, q
-                const int i = idx / n, col = idx % n;
-                int p, q;
-                rr_pair(n, k, i, &p, &q);
-                const double c = cs[i][0], s = cs[i][1];
-                const double xp = A[p][col], xq = A[q][col];
-                A[p][col] = c * xp - s * xq;
-                A[q][col] = s * xp + c * xq;
-            }
-            __syncthreads();
-            for (int idx = tid; idx < (n / 2) * n; idx += BT) {        // columns p, q
-                const int i = idx / n, row = idx % n;
-                int p, q;
-                rr_pair(n, k, i, &p, &q);
-                const double c = cs[i][0], s = cs[i][1];
-                const double xp = A[row][p], xq = A[row][q];
-                A[row][p] = c * xp - s * xq;
-                A[row][q] = s * xp + c * xq;
-                const double vp = V[row][p], vq = V[row][q];
-                V[row][p] = c * vp - s * vq;
-                V[row][q] = s * vp + c * vq;
-            }
-            __syncthreads();
+            buf ^= 1;
         }
+        const int rotated = sm.nconv[par];
+        if (tid == 0) sm.nconv[par ^ 1] = 0;     // the next sweep's flag; this one is read
+        __syncthreads();                         // by every thread before it is reset again
+        if (!rotated) break;
     }
 }
 
-__global__ void __launch_bounds__(BT) svd_kernel(BuildArgs a) {
+// Cholesky with diagonal pivoting of the symmetric positive semi-definite n x n matrix A
+// (destroyed): step j takes the largest remaining diagonal entry p = piv[j] and stores
+// row j of the factor over the original indices in Rm (Rm[j][piv[i]] = 0 for i < j), so
+// that A ~ Rm^T Rm.  Stops when the largest remaining entry is not above tau times the
+// largest initial diagonal entry; returns the number of steps k.  Ties go to the lower
+// index.  One barrier per step: every wave finds the pivot itself from the remaining
+// diagonal, kept in two alternating copies (-1 marks a row already taken), and every
+// thread keeps the set of taken rows as a bit mask.
+__device__ int piv_chol(double (*A)[KL + 1], double (*Rm)[KL + 1], int *piv, SvdSmem &sm, int n, double tau,
+                        int tid) {
+    constexpr int NE = (KL * KL + BT - 1) / BT;
+    const int lane = tid & 63;
+    if (tid < KL) {
+        piv[tid] = 0;
+        sm.dg[0][tid] = tid < n ? A[tid][tid] : -1.0;
+    }
+    __syncthreads();
+    double floor_ = 0.0;
+    uint64_t taken = 0;
+    int k = 0;
+    for (int j = 0; j < n; ++j) {
+        const int cur = j & 1;
+        double v = -1.0;
+        int at = KL;
+        if (lane < n && sm.dg[cur][lane] >= 0.0) { v = sm.dg[cur][lane]; at = lane; }
+        for (int off = 32; off >= 1; off >>= 1) {
+            const double ov = __shfl_xor(v, off);
+            const int oa = __shfl_xor(at, off);
+            if (ov > v || (ov == v && oa < at)) { v = ov; at = oa; }
+        }
+        if (j == 0) floor_ = tau * v;
+        if (!(v > 0.0 && v > floor_)) break;                  // the same decision in every wave
+        const int p = at;
+        const double rinv = 1.0 / sqrt(A[p][p]);
+        taken |= uint64_t(1) << p;
+        if (tid < n) {
+            double r = 0.0;
+            if (tid == p) r = 1.0 / rinv;
+            else if (!((taken >> tid) & 1)) r = A[p][tid] * rinv;
+            Rm[j][tid] = r;
+        }
+        if (tid == 0) piv[j] = p;
+#pragma unroll
+        for (int u = 0; u < NE; ++u) {
+            const int idx = tid + BT * u;
+            const int i = idx / KL, m = idx % KL;
+            if (i < n && m < n) {
+                const bool live = !((taken >> i) & 1) && !((taken >> m) & 1);
+                double nv = -1.0;
+                if (live) {
+                    nv = A[i][m] - (A[p][i] * rinv) * (A[p][m] * rinv);
+                    A[i][m] = nv;
+                }
+                if (i == m) sm.dg[cur ^ 1][i] = nv;
+            }
+        }
+        __syncthreads();
+        k = j + 1;
+    }
+    return k;
+}
+
+// Ri = Rt^-1 for Rt[j][m] = Rm[j][piv[m]] (k x k upper triangular; entries past k zero).
+// Rt goes into Rp first; then the rows of Ri from the last up, each row by KL threads in
+// one step (Ri may be the storage of Rm).
+__device__ inline void tri_inverse(const double (*Rm)[KL + 1], const int *piv, double (*Rp)[KL + 1],
+                                   double (*Ri)[KL + 1], int k, int tid) {
+    for (int idx = tid; idx < KL * KL; idx += BT) {
+        const int j = idx / KL, m = idx % KL;
+        Rp[j][m] = (j < k && m < k && m >= j) ? Rm[j][piv[m]] : 0.0;
+    }
+    __syncthreads();
+    for (int idx = tid; idx < KL * KL; idx += BT) {
+        const int j = idx / KL, i = idx % KL;
+        if (j >= k || i >= k) Ri[j][i] = 0.0;
+    }
+    for (int j = k - 1; j >= 0; --j) {                          // row j of Ri: entries i >= j
+        if (tid < k && tid >= j) {
+            const int i = tid;
+            double acc = j == i ? 1.0 : 0.0;
+            for (int m = j + 1; m <= i; ++m) acc -= Rp[j][m] * Ri[m][i];
+            Ri[j][i] = acc / Rp[j][j];
+        } else if (tid < j) {
+            Ri[j][tid] = 0.0;
+        }
+        __syncthreads();
+    }
+}
+
+// Z = Ri^T W[piv] with W and Z in the same LDS rows (rows >= k of Z zero).  Thread tid
+// forms column tid % d of rows tid / d, tid / d + BT / d, ... (a product with one W load
+// per term row), reads every row of W before a barrier, then writes.
+__device__ inline void apply_rinv_t(float (*W)[128 + 1], const double (*Ri)[KL + 1], const int *piv, int k, int d,
+                                    int tid) {
+    constexpr int NR = KL * 128 / BT;                           // output rows per thread (d = 128)
+    const int c = tid % d, h = tid / d, step = BT / d;
+    double acc[NR];
+#pragma unroll
+    for (int u = 0; u < NR; ++u) acc[u] = 0.0;
+    for (int i = 0; i < k; ++i) {
+        const double w = double(W[piv[i]][c]);
+#pragma unroll
+        for (int u = 0; u < NR; ++u) {
+            const int j = h + step * u;
+            if (j < KL && j >= i) acc[u] += Ri[i][j] * w;
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < NR; ++u) {
+        const int j = h + step * u;
+        if (j < KL) W[j][c] = j < k ? float(acc[u]) : 0.0f;
+    }
+}
+
+// Phase marks of the diagnostic trace (builds with SEKV_PHASE_TRACE): slot 0 holds the
+// span length, then one s_memrealtime stamp per mark, for the first trace_items items.
+enum : int {
+    kSvStart = 1, kSvPass = 2, kSvChol = 3, kSvForward = 4, kSvGram = 5, kSvIter = 6,
+    kSvPass2 = 7, kSvChol2 = 8, kSvForward2 = 9, kSvGram2 = 10, kSvJacobi = 11, kSvVrows = 12,
+    kSvT = 13, kSvEnd = 14,
+};
+#ifdef SEKV_PHASE_TRACE
+#define SV_STAMP(SLOT)                                                                         \
+    do {                                                                                       \
+        if (tid == 0 && a.trace && item_ < a.trace_items)                                      \
+            a.trace[item_ * kTraceSlots + (SLOT)] = int64_t(__builtin_amdgcn_s_memrealtime()); \
+    } while (0)
+#else
+#define SV_STAMP(SLOT) do {} while (0)
+#endif
+
+__global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
     __shared__ SvdSmem sm;
     const int tid = threadIdx.x;
+#ifdef SEKV_PHASE_TRACE
+    const int64_t item_ = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
+#endif
     const int side = blockIdx.y;                              // 0 keys, 1 values
     const int pair = blockIdx.x / a.M_max, S = blockIdx.x % a.M_max;
     const int b = pair / a.Hkv;
@@ -366,196 +583,230 @@ __global__ void __launch_bounds__(BT) svd_kernel(BuildArgs a) {
     }
     unsigned char *blk = static_cast<unsigned char *>(a.factors) + boff + (side ? side_elems * e : 0);
     const int64_t s_off = int64_t(L) * rs, v_off = s_off + rs;    // in elements; U at 0
+#ifdef SEKV_PHASE_TRACE
+    if (tid == 0 && a.trace && item_ < a.trace_items) a.trace[item_ * kTraceSlots] = L;
+#endif
+    SV_STAMP(kSvStart);
 
-    constexpr int NP = kMaxL * 128 / BT;                     // entries of an l x d matrix per thread
-    constexpr int NG = (kMaxL * kMaxL + BT - 1) / BT;
-    // the test matrix, transposed (l x d), entries tid + BT u of thread tid: the caller's
-    // Omega, then after each subspace iteration the right singular vectors of that pass
-    float omr[NP];
-#pragma unroll
-    for (int u = 0; u < NP; ++u) {
-        const int idx = tid + BT * u;
+    constexpr int NP = KL * 128 / BT;                        // entries of an l x d matrix per thread
+    auto bf16_bits = [](float f) -> uint32_t {
+        uint32_t q = __float_as_uint(f);
+        q += 0x7FFFu + ((q >> 16) & 1u);                      // round to nearest even
+        return q >> 16;
+    };
+    // the caller's test matrix into om (bfloat16, transposed)
+    for (int idx = tid; idx < l * d; idx += BT) {
         const int j = idx / d, c = idx % d;
-        omr[u] = j < l ? a.omega[size_t(c) * a.l + j] : 0.0f;
+        sm.u.p.om[j][c] = uint16_t(bf16_bits(a.omega[size_t(c) * a.l + j]));
     }
-    auto load_omega = [&]() {
-#pragma unroll
-        for (int u = 0; u < NP; ++u) {
-            const int idx = tid + BT * u;
-            const int j = idx / d, c = idx % d;
-            if (j < l) sm.u.p.om[j][c] = omr[u];
-        }
-    };
-    // one tile of X rows [t0, t0 + nt) and its sketch rows Y = X Omega
+    // one tile of X rows [t0, t0 + nt) and its sketch rows
     auto tile = [&](int t0, int nt) {
-        for (int i = tid; i < kTile * d; i += BT) {
-            const int t = i / d, c = i % d;
-            sm.u.p.x[t][c] = t < nt ? ld_elem(src, (row0 + t0 + t) * d + c, e) : 0.0f;
+        const int per = 16 / e;                              // elements per 16-byte load
+        for (int i = tid; i < kTile * d / per; i += BT) {
+            const int t = i / (d / per), c = (i % (d / per)) * per;
+            float v[8];
+            if (t < nt) {
+                const uint4 q = *reinterpret_cast<const uint4 *>(
+                    static_cast<const unsigned char *>(src) + ((row0 + t0 + t) * d + c) * e);
+                const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+                if (e == 2) {
+#pragma unroll
+                    for (int h = 0; h < 4; ++h) {
+                        v[2 * h] = __uint_as_float(w[h] << 16);
+                        v[2 * h + 1] = __uint_as_float(w[h] & 0xFFFF0000u);
+                    }
+                } else {
+#pragma unroll
+                    for (int h = 0; h < 4; ++h) v[h] = __uint_as_float(w[h]);
+                }
+            } else {
+#pragma unroll
+                for (int h = 0; h < 8; ++h) v[h] = 0.0f;
+            }
+            for (int h = 0; h < per; ++h) sm.u.p.x[t][c + h] = v[h];
         }
         __syncthreads();
-        for (int i = tid; i < kTile * l; i += BT) {
-            const int t = i / l, j = i % l;
-            float acc = 0.0f;
-            for (int c = 0; c < d; ++c) acc += sm.u.p.x[t][c] * sm.u.p.om[j][c];
-            sm.u.p.yt[t][j] = acc;
+        {   // Y rows: thread (t, jb) forms Y[t][jb], Y[t][jb + 16], Y[t][jb + 32]; rows of om
+            // past l are read but their sums dropped
+            const int t = tid >> 4, jb = tid & 15;
+            const float *xr = sm.u.p.x[t];
+            const uint16_t *o0 = sm.u.p.om[jb], *o1 = sm.u.p.om[jb + 16],
+                           *o2 = sm.u.p.om[min(jb + 32, KL - 1)];
+            float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f;
+#pragma unroll 8
+            for (int c = 0; c < d; ++c) {
+                const float xv = xr[c];
+                a0 += xv * __uint_as_float(uint32_t(o0[c]) << 16);
+                a1 += xv * __uint_as_float(uint32_t(o1[c]) << 16);
+                a2 += xv * __uint_as_float(uint32_t(o2[c]) << 16);
+            }
+            if (jb < l) sm.u.p.yt[t][jb] = a0;
+            if (jb + 16 < l) sm.u.p.yt[t][jb + 16] = a1;
+            if (jb + 32 < l) sm.u.p.yt[t][jb + 32] = a2;
         }
         __syncthreads();
     };
-
-    for (int it = 0;; ++it) {
-        const bool last = it >= a.power;
-        // 1. pass over X: G = Y^T Y (float64 sums) and P = Y^T X (float32), in registers
+    // a pass over X with the test matrix in om: G = Y^T Y (float64 sums) into am and
+    // P = Y^T X (float32 sums) into bm, accumulated in registers token by token; thread tid
+    // owns column tid % d of rows tid / d, tid / d + BT / d, ... of P and entries tid,
+    // tid + BT, ... of G
+    auto sketch_pass = [&]() {
+        constexpr int NG = (KL * KL + BT - 1) / BT;
         float pacc[NP];
         double gacc[NG];
 #pragma unroll
         for (int u = 0; u < NP; ++u) pacc[u] = 0.0f;
 #pragma unroll
         for (int u = 0; u < NG; ++u) gacc[u] = 0.0;
-        load_omega();
+        const int pc = tid % d, pj = tid / d, pstep = BT / d;
         __syncthreads();
         for (int t0 = 0; t0 < L; t0 += kTile) {
             const int nt = min(kTile, L - t0);
             tile(t0, nt);
+            for (int t = 0; t < nt; ++t) {
+                const float xv = sm.u.p.x[t][pc];
 #pragma unroll
-            for (int u = 0; u < NP; ++u) {
-                const int idx = tid + BT * u;
-                const int j = idx / d, c = idx % d;
-                if (j < l) {
-                    float acc = pacc[u];
-                    for (int t = 0; t < nt; ++t) acc += sm.u.p.yt[t][j] * sm.u.p.x[t][c];
-                    pacc[u] = acc;
+                for (int u = 0; u < NP; ++u) {
+                    const int j = pj + pstep * u;
+                    if (j < l) pacc[u] += sm.u.p.yt[t][j] * xv;
                 }
-            }
 #pragma unroll
-            for (int u = 0; u < NG; ++u) {
-                const int idx = tid + BT * u;
-                const int i = idx / kMaxL, j = idx % kMaxL;
-                if (i < l && j < l) {
-                    double acc = gacc[u];
-                    for (int t = 0; t < nt; ++t) acc += double(sm.u.p.yt[t][i]) * double(sm.u.p.yt[t][j]);
-                    gacc[u] = acc;
+                for (int u = 0; u < NG; ++u) {
+                    const int idx = tid + BT * u;
+                    const int i = idx / KL, j = idx % KL;
+                    if (i < l && j < l) gacc[u] += double(sm.u.p.yt[t][i]) * double(sm.u.p.yt[t][j]);
                 }
             }
             __syncthreads();
         }
 #pragma unroll
         for (int u = 0; u < NP; ++u) {
-            const int idx = tid + BT * u;
-            const int j = idx / d, c = idx % d;
-            if (j < l) sm.u.s.bm[j][c] = pacc[u];
+            const int j = pj + pstep * u;
+            if (j < l) sm.bm[j][pc] = pacc[u];
         }
 #pragma unroll
         for (int u = 0; u < NG; ++u) {
             const int idx = tid + BT * u;
-            const int i = idx / kMaxL, j = idx % kMaxL;
-            if (i < l && j < l) sm.u.s.am[i][j] = gacc[u];
+            const int i = idx / KL, j = idx % KL;
+            if (i < l && j < l) sm.am[i][j] = gacc[u];
         }
         __syncthreads();
-        // 2. G = W diag(lambda) W^T; keep directions above 1e-6 of the largest eigenvalue
-        jacobi(sm.u.s.am, sm.wm, sm.cs, l, a.sweeps, tid);
-        if (tid == 0) {
-            double mx = 0.0;
-            for (int i = 0; i < l; ++i) mx = fmax(mx, sm.u.s.am[i][i]);
-            sm.lmax = mx;
-        }
+    };
+    // after a pass: G = R^T R (pivoted) into rg, B = R^-T P[piv] over P, B B^T into am;
+    // rg then holds R^-1 (pivot order)
+    auto factor_b = [&](int it) -> int {
+        const int kk = piv_chol(sm.am, sm.u.s.rg, sm.piv, sm, l, 1e-8, tid);
+        SV_STAMP(it == 0 ? kSvChol : kSvChol2);
+        tri_inverse(sm.u.s.rg, sm.piv, sm.am, sm.u.s.rg, kk, tid);
+        apply_rinv_t(sm.bm, sm.u.s.rg, sm.piv, kk, d, tid);
         __syncthreads();
-        if (tid < l) {
-            const double lam = sm.u.s.am[tid][tid];
-            sm.scale[tid] = (lam > 1e-6 * sm.lmax && lam > 0.0) ? 1.0 / sqrt(lam) : 0.0;
-        }
-        __syncthreads();
-        // 3. B = diag(scale) W^T P, in place of P: each column c from its own column
-        for (int c = tid; c < d; c += BT) {
-            float col[kMaxL];
-#pragma unroll
-            for (int k = 0; k < kMaxL; ++k) col[k] = k < l ? sm.u.s.bm[k][c] : 0.0f;
-            for (int i = 0; i < l; ++i) {
-                double v = 0.0;
-#pragma unroll
-                for (int k = 0; k < kMaxL; ++k)
-                    if (k < l) v += sm.wm[k][i] * double(col[k]);     // rows >= l of W unset
-                sm.u.s.bm[i][c] = float(sm.scale[i] * v);
-            }
-        }
-        __syncthreads();
-        // 4. B B^T = E diag(sigma^2) E^T
-        for (int idx = tid; idx < l * l; idx += BT) {
+        SV_STAMP(it == 0 ? kSvForward : kSvForward2);
+        for (int idx = tid; idx < l * l; idx += BT) {       // rows >= kk of B are zero
             const int i = idx / l, j = idx % l;
             double acc = 0.0;
-            for (int c = 0; c < d; ++c) acc += double(sm.u.s.bm[i][c]) * double(sm.u.s.bm[j][c]);
-            sm.u.s.am[i][j] = acc;
+            if (i < kk && j < kk)
+                for (int c = 0; c < d; ++c) acc += double(sm.bm[i][c]) * double(sm.bm[j][c]);
+            sm.am[i][j] = acc;
         }
         __syncthreads();
-        jacobi(sm.u.s.am, sm.em, sm.cs, l, a.sweeps, tid);
-        // 5. order (descending, ties to the lower index), sigma; components below 1e-10 of
-        //    the largest eigenvalue are numerically undetermined: zero
-        if (tid < l) {
-            const double me = sm.u.s.am[tid][tid];
-            int rank = 0;
-            for (int j = 0; j < l; ++j) {
-                const double o = sm.u.s.am[j][j];
-                rank += (o > me || (o == me && j < tid)) ? 1 : 0;
-            }
-            sm.order[rank] = tid;
-        }
+        SV_STAMP(it == 0 ? kSvGram : kSvGram2);
+        return kk;
+    };
+
+    // subspace iterations: the next test matrix is an orthonormal basis of B's row space,
+    // R2^-T B[piv2] from the pivoted Cholesky B B^T = R2^T R2, written into om
+    for (int it = 0; it < a.power; ++it) {
+        sketch_pass();
+        SV_STAMP(kSvPass);
+        factor_b(0);
+        const int k2 = piv_chol(sm.am, sm.u.s.em, sm.piv2, sm, l, 1e-8, tid);
+        tri_inverse(sm.u.s.em, sm.piv2, sm.am, sm.u.s.em, k2, tid);
+        apply_rinv_t(sm.bm, sm.u.s.em, sm.piv2, k2, d, tid);
         __syncthreads();
-        if (tid < kMaxL) {
-            double sg = 0.0;
-            if (tid < l) {
-                const double lam = sm.u.s.am[sm.order[tid]][sm.order[tid]];
-                const double top = sm.u.s.am[sm.order[0]][sm.order[0]];
-                sg = (lam > 0.0 && lam > 1e-10 * top) ? sqrt(lam) : 0.0;
-            }
-            sm.sig[tid] = sg;
+        for (int idx = tid; idx < l * d; idx += BT) {
+            const int j = idx / d, c = idx % d;
+            sm.u.p.om[j][c] = uint16_t(bf16_bits(sm.bm[j][c]));
         }
-        __syncthreads();
-        if (last) break;
-        // subspace iteration: the next test matrix is V (all l right singular vectors of
-        // B = Q^T X), which spans the row space of X^T Q with orthonormal columns
-#pragma unroll
-        for (int u = 0; u < NP; ++u) {
-            const int idx = tid + BT * u;
-            const int i = idx / d, c = idx % d;
-            double v = 0.0;
-            if (i < l && sm.sig[i] > 0.0) {
-                const int ci = sm.order[i];
-                for (int k = 0; k < l; ++k) v += sm.em[k][ci] * double(sm.u.s.bm[k][c]);
-                v /= sm.sig[i];
-            }
-            omr[u] = float(v);
-        }
-        __syncthreads();
+        SV_STAMP(kSvIter);
     }
+    // the last pass; its test matrix is kept in registers (bfloat16 pairs) for the U pass
+    constexpr int NO = (KL * 128 / BT + 1) / 2;
+    uint32_t omk[NO];
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < NO; ++u) {
+        uint32_t w = 0;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int idx = tid + BT * (2 * u + h);
+            const int j = idx / d, c = idx % d;
+            if (j < l) w |= uint32_t(sm.u.p.om[j][c]) << (16 * h);
+        }
+        omk[u] = w;
+    }
+    sketch_pass();
+    SV_STAMP(kSvPass2);
+    const int k = factor_b(1);
+    // B B^T = E diag(sigma^2) E^T; order (descending, ties to the lower index); components
+    // below 1e-10 of the largest eigenvalue are numerically undetermined: zero
+    jacobi(sm.am, sm.u.s.em, sm, l, a.sweeps, tid);
+    SV_STAMP(kSvJacobi);
+    if (tid < l) {
+        const double me = sm.am[tid][tid];
+        int rank = 0;
+        for (int j = 0; j < l; ++j) {
+            const double o = sm.am[j][j];
+            rank += (o > me || (o == me && j < tid)) ? 1 : 0;
+        }
+        sm.order[rank] = tid;
+    }
+    __syncthreads();
+    if (tid < KL) {
+        double sg = 0.0;
+        if (tid < l && tid < k) {
+            const double lam = sm.am[sm.order[tid]][sm.order[tid]];
+            const double top = sm.am[sm.order[0]][sm.order[0]];
+            sg = (lam > 0.0 && lam > 1e-10 * top) ? sqrt(lam) : 0.0;
+        }
+        sm.sig[tid] = sg;
+    }
+    __syncthreads();
     if (tid < rs) st_elem(blk, size_t(s_off) + tid, tid < r ? float(sm.sig[tid]) : 0.0f, e);
-    // 6. V^T rows (E_i^T B) / sigma_i for the kept components, zero rows after
+    // V^T rows (E_i^T B) / sigma_i for the kept components, zero rows after
     for (int idx = tid; idx < rs * d; idx += BT) {
         const int i = idx / d, c = idx % d;
         double v = 0.0;
-        if (i < r && i < l && sm.sig[i] > 0.0) {
+        if (i < r && sm.sig[i] > 0.0) {
             const int ci = sm.order[i];
-            for (int k = 0; k < l; ++k) v += sm.em[k][ci] * double(sm.u.s.bm[k][c]);
+            for (int j = 0; j < k; ++j) v += sm.u.s.em[j][ci] * double(sm.bm[j][c]);
             v /= sm.sig[i];
         }
         st_elem(blk, size_t(v_off) + size_t(i) * d + c, float(v), e);
     }
-    // 7. T = W diag(scale) E_r, row j by thread j, written over row j of W
-    if (tid < l) {
-        double trow[kMaxL];
-#pragma unroll
-        for (int i = 0; i < kMaxL; ++i) {
-            double v = 0.0;
-            if (i < r && i < l && sm.sig[i] > 0.0) {
-                const int ci = sm.order[i];
-                for (int k = 0; k < l; ++k) v += sm.wm[tid][k] * sm.scale[k] * sm.em[k][ci];
-            }
-            trow[i] = v;
+    __syncthreads();
+    SV_STAMP(kSvVrows);
+    // T = R^-1 E_r = Ri E_r (Ri upper triangular, in rg), over the Jacobi matrix
+    for (int idx = tid; idx < KL * KL; idx += BT) {
+        const int j = idx / KL, i = idx % KL;
+        double v = 0.0;
+        if (j < k && i < r && sm.sig[i] > 0.0) {
+            const int ci = sm.order[i];
+            for (int m = j; m < k; ++m) v += sm.u.s.rg[j][m] * sm.u.s.em[m][ci];
         }
-#pragma unroll
-        for (int i = 0; i < kMaxL; ++i) sm.wm[tid][i] = trow[i];
+        sm.am[j][i] = v;
     }
     __syncthreads();
-    // 8. second pass over X: U rows = (X Omega) T
-    load_omega();
+    SV_STAMP(kSvT);
+    // last pass over X: U rows = Y[:, piv] T with the kept test matrix
+#pragma unroll
+    for (int u = 0; u < NO; ++u) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int idx = tid + BT * (2 * u + h);
+            const int j = idx / d, c = idx % d;
+            if (j < l) sm.u.p.om[j][c] = uint16_t(omk[u] >> (16 * h));
+        }
+    }
     __syncthreads();
     for (int t0 = 0; t0 < L; t0 += kTile) {
         const int nt = min(kTile, L - t0);
@@ -563,12 +814,13 @@ __global__ void __launch_bounds__(BT) svd_kernel(BuildArgs a) {
         for (int idx = tid; idx < nt * rs; idx += BT) {
             const int t = idx / rs, i = idx % rs;
             double v = 0.0;
-            if (i < r && i < l)
-                for (int j = 0; j < l; ++j) v += double(sm.u.p.yt[t][j]) * sm.wm[j][i];
+            if (i < r)
+                for (int j = 0; j < k; ++j) v += double(sm.u.p.yt[t][sm.piv[j]]) * sm.am[j][i];
             st_elem(blk, size_t(t0 + t) * rs + i, float(v), e);
         }
         __syncthreads();
     }
+    SV_STAMP(kSvEnd);
 }
 
 }  // namespace

@@ -21,10 +21,10 @@ sekv_status check_build_dims(const sekv_build_dims *d) {
     if (d->head_dim != 64 && d->head_dim != 128) return fail(SEKV_ERR_UNSUPPORTED, "head_dim %d", d->head_dim);
     if (d->dtype != SEKV_BF16 && d->dtype != SEKV_F32) return fail(SEKV_ERR_UNSUPPORTED, "dtype %d", d->dtype);
     const int gran = 16 / sekv::elem_bytes(d->dtype);
-    if (d->rank < gran || d->rank > 48 || d->rank % gran)
-        return fail(SEKV_ERR_UNSUPPORTED, "rank %d: a multiple of %d in [%d, 48]", d->rank, gran, gran);
-    if (d->sketch < d->rank || d->sketch > 48 || (d->sketch & 1))
-        return fail(SEKV_ERR_UNSUPPORTED, "sketch %d: even, in [rank, 48]", d->sketch);
+    if (d->rank < gran || d->rank > 40 || d->rank % gran)
+        return fail(SEKV_ERR_UNSUPPORTED, "rank %d: a multiple of %d in [%d, 40]", d->rank, gran, gran);
+    if (d->sketch < d->rank || d->sketch > 40 || (d->sketch & 1))
+        return fail(SEKV_ERR_UNSUPPORTED, "sketch %d: even, in [rank, 40]", d->sketch);
     if (d->min_span < 2) return fail(SEKV_ERR_INVALID_ARG, "min_span %d < 2", d->min_span);
     if (d->window < 0) return fail(SEKV_ERR_INVALID_ARG, "window < 0");
     if (d->sweeps < 1 || d->sweeps > 32) return fail(SEKV_ERR_INVALID_ARG, "sweeps %d outside [1, 32]", d->sweeps);
@@ -149,6 +149,9 @@ sekv_status sekv_build_cache(const sekv_build_dims *dims, const void *keys, cons
     a.Hkv = dims->n_kv_heads; a.N = dims->max_tokens; a.d = dims->head_dim;
     a.elem = sekv::elem_bytes(dims->dtype); a.R = dims->rank; a.l = dims->sketch; a.sweeps = dims->sweeps;
     a.power = dims->power;
+    size_t tb = 0;
+    a.trace = sekv::trace_buffer(&tb);
+    a.trace_items = a.trace ? int64_t(tb / (sizeof(int64_t) * sekv::kTraceSlots)) : 0;
     a.A_max = max_anchors; a.M_max = max_spans;
     (void)n_tokens;
     const hipError_t e = sekv::launch_build(a, dims->batch, stream);

@@ -212,7 +212,12 @@ struct BuildArgs {
     const int64_t *block_off;          // [B][Hkv][M_max]
     int32_t *error;                    // device error word (out-of-arena blocks)
     int32_t Hkv, N, d, elem, R, l, sweeps, power, A_max, M_max;
+    int64_t *trace;                    // diagnostic builds: [trace_items][kTraceSlots] or null
+    int64_t trace_items;
 };
+
+// The phase-trace buffer attached by sekv_phase_trace (null unless a trace build has one).
+int64_t *trace_buffer(size_t *bytes);
 
 // Bytes a tier gather workgroup moves at a time.
 constexpr int kGatherChunk = 32768;

@@ -37,8 +37,8 @@ def test_workspace_size(S):
 
 
 @pytest.mark.parametrize("kw", [
-    dict(head_dim=96), dict(rank=12), dict(rank=56), dict(rank=0), dict(sketch=30), dict(sketch=41),
-    dict(sketch=50), dict(min_span=1), dict(window=-1), dict(sweeps=0), dict(sweeps=33), dict(power=5),
+    dict(head_dim=96), dict(rank=12), dict(rank=48), dict(rank=0), dict(sketch=30), dict(sketch=41),
+    dict(sketch=42), dict(min_span=1), dict(window=-1), dict(sweeps=0), dict(sweeps=33), dict(power=5),
     dict(power=-1), dict(batch=-1), dict(n_kv_heads=0), dict(max_tokens=0), dict(alpha=float("nan")),
     dict(dtype="f32", rank=6),
 ])
@@ -77,7 +77,7 @@ def _layout_rule(n_spans, span_len, Hkv, d, R, e, M):
     return off, rank, max(pos, 256)
 
 
-@pytest.mark.parametrize("dtype,d,R", [("bf16", 128, 32), ("f32", 64, 8), ("bf16", 64, 48)])
+@pytest.mark.parametrize("dtype,d,R", [("bf16", 128, 32), ("f32", 64, 8), ("bf16", 64, 40)])
 def test_layout_matches_rule(S, dtype, d, R):
     p = make_prefill(3, 1, 16, [1200, 3, 700], dtype="f32", spike_every=50, seed=81)
     N = p.surprisal.shape[1]
@@ -87,7 +87,7 @@ def test_layout_matches_rule(S, dtype, d, R):
     for b, (_, spans) in enumerate(segs):
         sl[b, :len(spans)] = [L for _, L in spans]
     M = int(ns.max())
-    bd = _bd(S, batch=3, n_kv_heads=3, head_dim=d, max_tokens=N, rank=R, sketch=48, dtype=dtype)
+    bd = _bd(S, batch=3, n_kv_heads=3, head_dim=d, max_tokens=N, rank=R, sketch=40, dtype=dtype)
     off, rank, nbytes = S.build_layout(bd, M, ns, sl)
     e = 2 if dtype == "bf16" else 4
     ro, rr, rn = _layout_rule(ns, sl, 3, d, R, e, M)

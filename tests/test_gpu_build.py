@@ -7,9 +7,10 @@ surprisal_weight summaries and eq. key_svd factors) against the CPU oracle.
 * Anchor rows and span lengths bit for bit; ln|S| within 2 ulp; summaries within one
   storage ulp plus the float32 accumulation bound 1e-4 max|X|.
 * Factors: the GPU's randomized SVD against the optimal truncated SVD (numpy): Frobenius
-  reconstruction error at most 1.25 x the optimal plus the storage rounding term (2^-7
-  ||X|| for bfloat16, 1e-5 ||X|| for float32); orthonormal columns of U and rows of Vt;
-  stored ranks and zero extra components.
+  reconstruction error at most 1.25 x the optimal with one or more subspace iterations
+  (2 x with none) plus the storage rounding term (2^-7 ||X|| for bfloat16, 1e-5 ||X|| for
+  float32); orthonormal columns of U and rows of Vt; stored ranks and zero extra
+  components.
 * End to end: the decode step on the GPU-built cache against the oracle's decode step on
   the oracle-built cache (exact SVD) for exactly low-rank spans, where both
   factorisations reproduce the span: selection equal wherever the oracle's k-th and
@@ -45,11 +46,11 @@ def _dev(a, dtype=None):
     return torch.from_numpy(a).cuda()
 
 
-def _bdims(S, p, Hkv, d, rank=32, sketch=40, alpha=1.0, min_span=16, window=64, sweeps=8):
+def _bdims(S, p, Hkv, d, rank=32, sketch=40, alpha=1.0, min_span=16, window=64, sweeps=8, power=1):
     return S.make_build_dims(batch=p.surprisal.shape[0], n_kv_heads=Hkv, head_dim=d,
                              max_tokens=p.surprisal.shape[1], rank=rank, sketch=sketch,
                              min_span=min_span, window=window, dtype=p.dtype, alpha=alpha,
-                             sweeps=sweeps)
+                             sweeps=sweeps, power=power)
 
 
 def _segment(S, bd, p):
@@ -107,16 +108,20 @@ def test_segment_full_size_128k_x4(S):
 BUILD_CASES = [
     ("bf16-d128", dict(dtype="bf16", d=128, Hkv=2, n=[1500, 900], rank=32, sketch=40, min_span=4, window=64)),
     ("f32-d64", dict(dtype="f32", d=64, Hkv=2, n=[1200, 1], rank=32, sketch=40, min_span=2, window=16)),
-    ("bf16-d64-r48", dict(dtype="bf16", d=64, Hkv=1, n=[2000], rank=48, sketch=48, min_span=8, window=0)),
+    ("bf16-d64-r40-p2", dict(dtype="bf16", d=64, Hkv=1, n=[2000], rank=40, sketch=40, min_span=8, window=0,
+                             power=2)),
     ("f32-d128-r8", dict(dtype="f32", d=128, Hkv=3, n=[800, 1100, 0], rank=8, sketch=12, min_span=3,
                          window=32)),
+    # no subspace iteration: a plain Gaussian sketch, whose error bound is looser
+    ("bf16-d128-p0", dict(dtype="bf16", d=128, Hkv=1, n=[1800], rank=16, sketch=24, min_span=4, window=16,
+                          power=0, bound=2.0)),
 ]
 
 
 def _build(S, p, c, ws_dims=None):
     import torch
     bd = _bdims(S, p, c["Hkv"], c["d"], rank=c["rank"], sketch=c["sketch"], min_span=c["min_span"],
-                window=c["window"])
+                window=c["window"], power=c.get("power", 1))
     # the builder uses only the workspace's error word: any valid dims will do
     dims = S.make_dims(batch=1, n_q_heads=1, n_kv_heads=1, head_dim=64, rank=8, top_k=1, max_anchors=1,
                        max_spans=1, max_span_len=1, dtype="f32", softmax_scale=1.0)
@@ -189,7 +194,8 @@ def test_build_matches_oracle(S, name, c):
                     opt = math.sqrt(np.sum(full[r:] ** 2))
                     err = np.linalg.norm(X - oracle.reconstruct(U, sg, Vt))
                     nx = np.linalg.norm(X)
-                    assert err <= 1.25 * opt + rec_rel * nx + 1e-30, (name, b, g, S_, side, err, opt, nx)
+                    assert err <= c.get("bound", 1.25) * opt + rec_rel * nx + 1e-30, (name, b, g, S_, side, err,
+                                                                                     opt, nx)
                     worst = max(worst, (err - opt) / max(nx, 1e-30))
                     live = sg > 1e-3 * max(sg.max(initial=0), 1e-30)
                     if live.any():
