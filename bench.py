@@ -29,6 +29,7 @@ if ROOT not in sys.path:
 
 METRIC = "decode-step latency (µs) and achieved HBM GB/s, 128K context, batch 4"
 HBM_PEAK_GBS = 8000.0
+FP32_PEAK_TFLOPS = 157.3          # MI355X dense fp32 vector
 KERNEL_NAME = "sekv_step_kernel"
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_31145_amd", "csrc", f) for f in
                   ("sekv_internal.h", "sekv_step.h", "sekv_step_inst.hip", "sekv_kernels.hip")]
@@ -746,6 +747,17 @@ def bench_prefill(args, dev):
     out_bytes = int(sum(cache[k].numel() * cache[k].element_size()
                         for k in ("anchor_k", "anchor_v", "sum_k", "sum_v", "factors")))
     wall_ms = float(np.median(walls)) * 1e3
+    # algorithmic work of the SVD (the dominant kernel): per span side of |S| tokens, each of
+    # the power + 1 sketch passes forms Y = X Omega (2 |S| d l), Y^T X (2 l |S| d) and Y^T Y
+    # (2 l^2 |S|); the last pass forms Y again and U = Y T (2 |S| l r).  The small dense
+    # algebra (Cholesky, Jacobi) is not counted.
+    flops = 0.0
+    for b in range(B):
+        for Ls in cache["span_len"][b, :int(lay["n_spans"][b])].cpu().numpy().astype(np.float64):
+            r_ = min(Ls, d, R)
+            per = (args.power + 1) * (2 * Ls * d * l * 2 + 2 * l * l * Ls) + 2 * Ls * d * l + 2 * Ls * l * r_
+            flops += 2 * Hkv * per                                   # both sides, every KV head
+    build_s = float(np.mean(build_ms)) * 1e-3
     line = {
         "metric": "prefill-side build throughput (tokens per second per layer), 128K context, batch 4",
         "value": round(tokens / (kern_ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
@@ -756,6 +768,13 @@ def bench_prefill(args, dev):
                    "power": args.power, "min_span": 16, "window": 512, "alpha": 1.0,
                    "heads": "one generated stream per sequence, head g with columns rotated by 8 g",
                    "parallelism": "single-gpu"},
+        "roofline": {"bound": "alu", "achieved": round(flops / build_s / 1e12, 3),
+                     "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(flops / build_s / 1e12 / FP32_PEAK_TFLOPS, 5), "traffic": None,
+                     "kernel": "svd_kernel (+ gather_kernel in the timed launch pair)",
+                     "algorithmic_flops_per_launch": flops,
+                     "note": "latency-bound: per span side, 40-step Cholesky factorisations and "
+                             "Jacobi rounds with a workgroup barrier each"},
         "segment_ms": round(float(np.mean(seg_ms)), 4),
         "build_ms": round(float(np.mean(build_ms)), 4),
         "call_wall_ms_with_layout": round(wall_ms, 3),
