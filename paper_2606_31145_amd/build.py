@@ -22,7 +22,10 @@ ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Device code: no packed-fp32 instructions (their use is disabled on this target).
-DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Device code must not use scratch memory (a build whose kernel spilled registers to scratch
+# gave wrong results): any kernel with a stack frame fails to compile.
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-Xarch_device", "-Wframe-larger-than=0", "-Xarch_device", "-Werror=frame-larger-than"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", f"-I{INCLUDE}", f"-I{CSRC}"]
 INSTANCES = [("BF16", 128), ("BF16", 64), ("F32", 128), ("F32", 64)]
 

@@ -1760,7 +1760,7 @@ __device__ __forceinline__ bool share_item(const Params &p, Smem<T, D, G> &sm, i
 // the persistent kernel
 // ---------------------------------------------------------------------------
 template <class T, int D, int G>
-__global__ void __launch_bounds__(NT, 2) sekv_step_kernel(Params p) {
+__global__ void __launch_bounds__(NT, G == 8 ? 1 : 2) sekv_step_kernel(Params p) {
     __shared__ Smem<T, D, G> sm;
     const int tid = threadIdx.x;
     // the tag of this launch's published words, used as loaded: its first use is when

@@ -26,7 +26,7 @@ __device__ inline void copy_chunk(const unsigned char *src, unsigned char *dst, 
 #pragma unroll
     for (int u = 0; u < kGV; ++u) {
         const int i = int(threadIdx.x) + kGT * u;
-        if (i < nv) v[u] = s[i];
+        v[u] = i < nv ? s[i] : make_uint4(0u, 0u, 0u, 0u);
     }
 #pragma unroll
     for (int u = 0; u < kGV; ++u) {
