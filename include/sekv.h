@@ -433,6 +433,43 @@ SEKV_API sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_c
                                              int32_t *sel, void *out, void *ws, size_t ws_bytes,
                                              hipStream_t main, hipStream_t side);
 
+/* Several layers of one decode step with the factors in pinned host memory, and the
+ * cross-layer prefetch of the paper's pipelined transfer (Sec. 3.2, last paragraph: the
+ * GPU computation overlaps the CPU-GPU transfer of the selected bases).  Span boundaries
+ * come from the sequence's surprisal (Sec. 3.1), so every layer has the same spans; a
+ * span zoomed by layer l is a likely zoom of layer l + 1.  Per layer l, in order:
+ *   1. routing and selection of every sequence on `main`, after layer l - 1's attention
+ *      (in a model, layer l's queries need layer l - 1's output);
+ *   2. on `side`, after an event on that selection: every selected block of layer l that
+ *      is not already in the layer's staging is copied there through the arena's device
+ *      mapping (the "miss" copies, on the critical path);
+ *   3. with prefetch = 1, still on `side`: layer l + 1's blocks of the spans layer l
+ *      selected are copied into layer l + 1's staging, overlapping layer l's attention
+ *      and layer l + 1's routing (the speculative copies, off the critical path);
+ *   4. `main` waits for step 2 and runs layer l's attention from staging.
+ * Layers alternate between two staging buffers, each a prefetch region and a miss region
+ * of batch * Hkv * top_k slots; the tier allocates them on the first call (2 x 2 x the
+ * staging of sekv_tier_staging_size, plus offset tables).  Results are bit for bit those
+ * of sekv_decode_step_tiered layer by layer, with or without prefetch.
+ *   dims      as for sekv_decode_step_tiered (identical to the tier's; every layer has them)
+ *   caches    n_layers device caches (cache.factors not read; cache.block_off is the
+ *             device copy of the host offsets, as in gather mode)
+ *   hosts     n_layers pinned, device-mapped host arenas and tables
+ *   sel       device int32 [n_layers][B][Hkv][top_k]; out device [n_layers][B][Hq][d]
+ * The tier must be a SEKV_TIER_GATHER tier.  A selected block outside its arena is skipped
+ * with the workspace error bit 2 set. */
+SEKV_API sekv_status sekv_decode_layers_tiered(const sekv_dims *dims, const sekv_cache *caches,
+                                               const sekv_host_factors *hosts, int32_t n_layers,
+                                               int32_t prefetch, sekv_tier *tier, int32_t *sel,
+                                               void *out, void *ws, size_t ws_bytes, hipStream_t main,
+                                               hipStream_t side);
+
+/* Copy counters of the last sekv_decode_layers_tiered call, over all its layers:
+ * stats[0] bytes and stats[1] blocks copied after a selection (the critical path),
+ * stats[2] bytes and stats[3] blocks prefetched.  Valid once that call has completed
+ * (a synchronous read of the device counters). */
+SEKV_API sekv_status sekv_tier_layer_stats(sekv_tier *tier, int64_t stats[4]);
+
 /* Debug check of the device-side preconditions of the step calls, made on HOST copies of
  * a cache (every pointer in host_copy is a host pointer; factors_bytes is the arena
  * size), so it is slow and synchronous.  Checks, for every sequence b:

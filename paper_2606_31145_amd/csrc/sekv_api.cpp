@@ -509,6 +509,14 @@ struct sekv_tier {
     int64_t last_bytes;
     int32_t last_copies;
     bool timed;
+    // layered steps (sekv_decode_layers_tiered), allocated on first use: two layer buffers,
+    // each staging (prefetch region | miss region), staging offsets and prefetch records
+    void *d_layer;
+    unsigned char *d_lstage[2];
+    int64_t *d_loff[2];
+    int32_t *d_lpf[2];
+    unsigned long long *d_lstats;  // [4]
+    hipEvent_t ev_lsel, ev_lcopy;
 };
 
 sekv_status sekv_tier_create(const sekv_dims *dims, int32_t copy_mode, sekv_tier **tier) {
@@ -579,6 +587,9 @@ sekv_status sekv_tier_destroy(sekv_tier *t) {
     if (t->ev_t0) (void)hipEventDestroy(t->ev_t0);
     if (t->ev_t1) (void)hipEventDestroy(t->ev_t1);
     if (t->d_mem) (void)hipFree(t->d_mem);
+    if (t->d_layer) (void)hipFree(t->d_layer);
+    if (t->ev_lsel) (void)hipEventDestroy(t->ev_lsel);
+    if (t->ev_lcopy) (void)hipEventDestroy(t->ev_lcopy);
     if (t->h_sel) (void)hipHostFree(t->h_sel);
     if (t->h_off) (void)hipHostFree(t->h_off);
     delete t;
@@ -759,6 +770,138 @@ sekv_status sekv_decode_step_tiered(const sekv_dims *dims, const sekv_cache *cac
         t->last_bytes = bytes;
         t->last_copies = copies;
     }
+    return SEKV_OK;
+}
+
+sekv_status sekv_decode_layers_tiered(const sekv_dims *dims, const sekv_cache *caches,
+                                      const sekv_host_factors *hosts, int32_t n_layers, int32_t prefetch,
+                                      sekv_tier *t, int32_t *sel, void *out, void *ws, size_t ws_bytes,
+                                      hipStream_t main, hipStream_t side) {
+    if (!t) return fail(SEKV_ERR_INVALID_ARG, "tier is NULL");
+    sekv_status st = check_dims_impl(dims);
+    if (st != SEKV_OK) return st;
+    if (std::memcmp(dims, &t->dims, sizeof(sekv_dims)) != 0)
+        return fail(SEKV_ERR_INVALID_ARG, "dims differ from the tier's");
+    if (t->mode != SEKV_TIER_GATHER) return fail(SEKV_ERR_UNSUPPORTED, "layered steps need a gather-mode tier");
+    if (n_layers < 1 || !caches || !hosts) return fail(SEKV_ERR_INVALID_ARG, "n_layers < 1 or NULL layer arrays");
+    if (prefetch != 0 && prefetch != 1) return fail(SEKV_ERR_INVALID_ARG, "prefetch must be 0 or 1");
+    const int B = dims->batch, Hkv = dims->n_kv_heads, Hq = dims->n_q_heads, k = dims->top_k;
+    const int M = dims->max_spans, d = dims->head_dim;
+    if (!out || (k > 0 && !sel)) return fail(SEKV_ERR_INVALID_ARG, "sel/out is NULL");
+    const size_t oe = dims->out_dtype == SEKV_F32 ? 4 : 2;
+    const size_t e = size_t(sekv::elem_bytes(dims->dtype));
+    std::vector<const unsigned char *> arena_dev(size_t(n_layers), nullptr);
+    for (int l = 0; l < n_layers; ++l) {
+        const sekv_cache &c = caches[l];
+        const sekv_host_factors &h = hosts[l];
+        if (!h.arena || !h.block_off || !h.span_len || h.arena_bytes <= 0)
+            return fail(SEKV_ERR_INVALID_ARG, "layer %d: host factor tables are NULL or empty", l);
+        if ((h.block_rank == nullptr) != (c.block_rank == nullptr))
+            return fail(SEKV_ERR_INVALID_ARG, "layer %d: host and device rank tables: both or neither", l);
+        if (k > 0 && (!c.block_off || (reinterpret_cast<uintptr_t>(c.block_off) & 7)))
+            return fail(SEKV_ERR_INVALID_ARG, "layer %d: cache.block_off must be a device copy of the arena offsets", l);
+        hipPointerAttribute_t attr{};
+        if (hipPointerGetAttributes(&attr, h.arena) != hipSuccess || attr.type != hipMemoryTypeHost ||
+            !attr.devicePointer) {
+            (void)hipGetLastError();
+            return fail(SEKV_ERR_INVALID_ARG, "layer %d: the host factor arena is not pinned, device-mapped memory", l);
+        }
+        arena_dev[size_t(l)] = static_cast<const unsigned char *>(attr.devicePointer);
+    }
+    const size_t slots = size_t(B) * Hkv * size_t(std::max(k, 1));
+    const size_t region = slots * t->slot_bytes;
+    hipError_t he = hipSuccess;
+    if (!t->d_layer) {
+        // two layer buffers: staging (prefetch | miss), offsets, prefetch records; counters
+        const size_t off_b = sekv::align256(size_t(B) * Hkv * M * sizeof(int64_t));
+        const size_t pf_b = sekv::align256(slots * sizeof(int32_t));
+        const size_t per = 2 * region + off_b + pf_b;
+        he = hipMalloc(&t->d_layer, 2 * per + 256);
+        if (he != hipSuccess) return hip_fail(he, "layered staging");
+        unsigned char *m = static_cast<unsigned char *>(t->d_layer);
+        for (int i = 0; i < 2; ++i) {
+            unsigned char *base = m + size_t(i) * per;
+            t->d_lstage[i] = base;
+            t->d_loff[i] = reinterpret_cast<int64_t *>(base + 2 * region);
+            t->d_lpf[i] = reinterpret_cast<int32_t *>(base + 2 * region + off_b);
+        }
+        t->d_lstats = reinterpret_cast<unsigned long long *>(m + 2 * per);
+        he = hipMemset(t->d_layer, 0, 2 * per + 256);
+        if (he == hipSuccess) he = hipEventCreateWithFlags(&t->ev_lsel, hipEventDisableTiming);
+        if (he == hipSuccess) he = hipEventCreateWithFlags(&t->ev_lcopy, hipEventDisableTiming);
+        if (he != hipSuccess) {
+            if (t->ev_lsel) (void)hipEventDestroy(t->ev_lsel);
+            (void)hipFree(t->d_layer);
+            t->d_layer = nullptr;
+            t->ev_lsel = nullptr;
+            return hip_fail(he, "layered staging set-up");
+        }
+    }
+    const int chunks = int32_t((t->slot_bytes + sekv::kGatherChunk - 1) / sekv::kGatherChunk);
+    auto copy_args = [&](int l, int buf, const int32_t *which, int pf, int use_pf) {
+        sekv::LayerCopyArgs a{};
+        a.arena = arena_dev[size_t(l)];
+        a.staging = t->d_lstage[buf];
+        a.sel = which;
+        a.span_len = caches[l].span_len;
+        a.block_off = caches[l].block_off;
+        a.block_rank = caches[l].block_rank;
+        a.stage_off = t->d_loff[buf];
+        a.pf_span = t->d_lpf[buf];
+        a.stats = t->d_lstats;
+        a.error = &static_cast<sekv::WsHeader *>(ws)->error;
+        a.arena_bytes = hosts[l].arena_bytes;
+        a.slot_bytes = int64_t(t->slot_bytes);
+        a.miss0 = int64_t(region);
+        a.B = B; a.Hkv = Hkv; a.k = k; a.M = M; a.r = dims->rank; a.d = d; a.elem = int32_t(e);
+        a.max_span_len = dims->max_span_len; a.chunks_per_slot = chunks;
+        a.prefetch = pf; a.use_pf = use_pf;
+        return a;
+    };
+    he = sekv::launch_stats_reset4(t->d_lstats, side);
+    if (he != hipSuccess) return hip_fail(he, "layer counters");
+    for (int l = 0; l < n_layers; ++l) {
+        const int buf = l & 1;
+        int32_t *sel_l = k > 0 ? sel + size_t(l) * B * Hkv * k : nullptr;
+        sekv_cache c = caches[l];
+        c.factors = t->d_lstage[buf];
+        c.factors_bytes = int64_t(2 * region);
+        c.block_off = t->d_loff[buf];
+        // 1. routing and selection of layer l (after layer l - 1's attention on main)
+        st = run(sekv::kModeRoute, dims, &c, sel_l, t->d_logits, nullptr, nullptr, nullptr, ws, ws_bytes, main);
+        if (st != SEKV_OK) return st;
+        if (k > 0) {
+            // 2. the blocks layer l selected that are not in its staging yet
+            he = hipEventRecord(t->ev_lsel, main);
+            if (he == hipSuccess) he = hipStreamWaitEvent(side, t->ev_lsel, 0);
+            if (he == hipSuccess) he = sekv::launch_layer_copy(copy_args(l, buf, sel_l, 0, prefetch && l > 0), side);
+            if (he == hipSuccess) he = hipEventRecord(t->ev_lcopy, side);
+            // 3. layer l + 1's blocks of the spans layer l selected, behind layer l's attention
+            if (he == hipSuccess && prefetch && l + 1 < n_layers)
+                he = sekv::launch_layer_copy(copy_args(l + 1, buf ^ 1, sel_l, 1, 0), side);
+            if (he == hipSuccess) he = hipStreamWaitEvent(main, t->ev_lcopy, 0);
+            if (he != hipSuccess) return hip_fail(he, "layered copies");
+        }
+        // 4. layer l's attention from staging
+        st = run(sekv::kModeAttend, dims, &c, nullptr, nullptr, sel_l, t->d_logits,
+                 static_cast<unsigned char *>(out) + size_t(l) * B * Hq * d * oe, ws, ws_bytes, main);
+        if (st != SEKV_OK) return st;
+    }
+    // the side stream's last work (a prefetch nobody uses is not enqueued) joins main
+    he = hipEventRecord(t->ev_lcopy, side);
+    if (he == hipSuccess) he = hipStreamWaitEvent(main, t->ev_lcopy, 0);
+    if (he != hipSuccess) return hip_fail(he, "joining the copy stream");
+    return SEKV_OK;
+}
+
+sekv_status sekv_tier_layer_stats(sekv_tier *t, int64_t stats[4]) {
+    if (!t || !stats) return fail(SEKV_ERR_INVALID_ARG, "NULL argument");
+    for (int i = 0; i < 4; ++i) stats[i] = 0;
+    if (!t->d_layer) return SEKV_OK;
+    unsigned long long st[4] = {0, 0, 0, 0};
+    const hipError_t e = hipMemcpy(st, t->d_lstats, sizeof(st), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "reading the layer copy counters");
+    for (int i = 0; i < 4; ++i) stats[i] = int64_t(st[i]);
     return SEKV_OK;
 }
 

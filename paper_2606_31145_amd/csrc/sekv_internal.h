@@ -238,11 +238,33 @@ struct TierGatherArgs {
     int32_t Hkv, k, M, r, d, elem, max_span_len, chunks_per_slot;
 };
 
+// One pass of the layered tier over every sequence (sekv_tier.hip).  prefetch = 1: copy
+// the blocks of `sel` (the previous layer's selection) into the prefetch slots and record
+// which span each slot holds in pf_span.  prefetch = 0: for every selected span, point
+// stage_off at its prefetch slot when pf_span holds it (use_pf), else copy it into its
+// miss slot.
+struct LayerCopyArgs {
+    const unsigned char *arena;        // device mapping of the layer's pinned arena
+    unsigned char *staging;            // the layer buffer: prefetch region, then miss region
+    const int32_t *sel;                // [B][Hkv][k]
+    const int32_t *span_len;           // [B][M]
+    const int64_t *block_off;          // [B][Hkv][M] arena offsets (device)
+    const int32_t *block_rank;         // [B][Hkv][M] or null
+    int64_t *stage_off;                // [B][Hkv][M]
+    int32_t *pf_span;                  // [B][Hkv][k]
+    unsigned long long *stats;         // [4]: miss bytes, miss blocks, prefetch bytes, blocks
+    int32_t *error;
+    int64_t arena_bytes, slot_bytes, miss0;   // miss0: byte offset of the miss region
+    int32_t B, Hkv, k, M, r, d, elem, max_span_len, chunks_per_slot, prefetch, use_pf;
+};
+
 // Launchers (sekv_kernels.hip).  Return the HIP error of the launch.
 hipError_t launch_step(const Params &p, int dtype, int head_dim, int group, hipStream_t stream);
 hipError_t launch_zero(void *ptr, size_t bytes, hipStream_t stream);
 hipError_t launch_tier_gather(const TierGatherArgs &a, hipStream_t stream);
 hipError_t launch_stats_reset(unsigned long long *stats, hipStream_t stream);
+hipError_t launch_layer_copy(const LayerCopyArgs &a, hipStream_t stream);
+hipError_t launch_stats_reset4(unsigned long long *stats, hipStream_t stream);
 hipError_t launch_gate(const GateParams &g, int dtype, hipStream_t stream);
 hipError_t launch_segment(const SegArgs &a, int batch, hipStream_t stream);
 hipError_t launch_build(const BuildArgs &a, int batch, hipStream_t stream);

@@ -76,8 +76,54 @@ __global__ __launch_bounds__(kGT) void tier_gather_kernel(TierGatherArgs a) {
     copy_chunk(a.arena + off, a.staging + dst, lo, hi);
 }
 
-__global__ void stats_reset_kernel(unsigned long long *stats) {
-    if (threadIdx.x < 2) stats[threadIdx.x] = 0;
+__global__ void stats_reset_kernel(unsigned long long *stats, int n) {
+    if (int(threadIdx.x) < n) stats[threadIdx.x] = 0;
+}
+
+// Layered tier: slot (b, g, j) of the launch, chunk c of its block.
+__global__ __launch_bounds__(kGT) void layer_copy_kernel(LayerCopyArgs a) {
+    const int slot = int(blockIdx.x) / a.chunks_per_slot, c = int(blockIdx.x) % a.chunks_per_slot;
+    const int pg = slot / a.k;                                // b * Hkv + g
+    const int b = pg / a.Hkv;
+    const int s = a.sel[slot];
+    const bool first = c == 0 && threadIdx.x == 0;
+    if (a.prefetch && first) a.pf_span[slot] = -1;            // set again below once copied
+    if (s < 0 || s >= a.M) return;
+    const size_t at = size_t(pg) * a.M + s;
+    if (!a.prefetch && a.use_pf) {
+        for (int jj = 0; jj < a.k; ++jj)
+            if (a.pf_span[size_t(pg) * a.k + jj] == s) {
+                if (first) a.stage_off[at] = int64_t(size_t(pg) * a.k + jj) * a.slot_bytes;
+                return;
+            }
+    }
+    const int L = a.span_len[size_t(b) * a.M + s];
+    const int64_t off = a.block_off[at];
+    int rk = a.r, rv = a.r;
+    if (a.block_rank) {
+        const uint32_t w = uint32_t(a.block_rank[at]);
+        rk = int(w & 0xFFFFu);
+        rv = int(w >> 16);
+    }
+    const int gran = 16 / a.elem;
+    const bool ranks_ok = rk >= gran && rk <= a.r && rk % gran == 0 && rv >= gran && rv <= a.r && rv % gran == 0;
+    const int64_t bytes = dev_block_bytes(L, rk, a.d, a.elem) / 2 + dev_block_bytes(L, rv, a.d, a.elem) / 2;
+    if (!ranks_ok || L < 1 || L > a.max_span_len || off < 0 || (off & 15) || off > a.arena_bytes - bytes) {
+        if (first) __hip_atomic_fetch_or(a.error, kErrBlockRange, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    const int64_t dst = (a.prefetch ? 0 : a.miss0) + int64_t(slot) * a.slot_bytes;
+    if (first) {
+        if (a.prefetch) a.pf_span[slot] = s;
+        else a.stage_off[at] = dst;
+        unsigned long long *st = a.stats + (a.prefetch ? 2 : 0);
+        __hip_atomic_fetch_add(&st[0], (unsigned long long)bytes, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_add(&st[1], 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    const int64_t lo = int64_t(c) * kGatherChunk;
+    if (lo >= bytes) return;
+    const int64_t hi = lo + kGatherChunk < bytes ? lo + kGatherChunk : bytes;
+    copy_chunk(a.arena + off, a.staging + dst, lo, hi);
 }
 
 }  // namespace
@@ -90,7 +136,19 @@ hipError_t launch_tier_gather(const TierGatherArgs &a, hipStream_t stream) {
 }
 
 hipError_t launch_stats_reset(unsigned long long *stats, hipStream_t stream) {
-    hipLaunchKernelGGL(stats_reset_kernel, dim3(1), dim3(64), 0, stream, stats);
+    hipLaunchKernelGGL(stats_reset_kernel, dim3(1), dim3(64), 0, stream, stats, 2);
+    return hipGetLastError();
+}
+
+hipError_t launch_stats_reset4(unsigned long long *stats, hipStream_t stream) {
+    hipLaunchKernelGGL(stats_reset_kernel, dim3(1), dim3(64), 0, stream, stats, 4);
+    return hipGetLastError();
+}
+
+hipError_t launch_layer_copy(const LayerCopyArgs &a, hipStream_t stream) {
+    const int64_t n = int64_t(a.B) * a.Hkv * a.k * a.chunks_per_slot;
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(layer_copy_kernel, dim3(unsigned(n)), dim3(kGT), 0, stream, a);
     return hipGetLastError();
 }
 

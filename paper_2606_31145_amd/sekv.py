@@ -33,7 +33,8 @@ EXPORTED = ("sekv_status_string", "sekv_last_error", "sekv_phase_trace", "sekv_c
             "sekv_tier_staging_size", "sekv_tier_last_copy", "sekv_decode_step_tiered",
             "sekv_validate_cache", "sekv_decode_step_noalloc", "sekv_route_gated",
             "sekv_decode_step_gated", "sekv_segment_workspace_size", "sekv_segment",
-            "sekv_build_layout", "sekv_build_cache")
+            "sekv_build_layout", "sekv_build_cache", "sekv_decode_layers_tiered",
+            "sekv_tier_layer_stats")
 
 
 class SekvError(RuntimeError):
@@ -135,6 +136,11 @@ def _load():
     lib.sekv_decode_step_gated.argtypes = [P(Dims), P(CacheStruct), P(GateStruct), VP, VP, VP, SZ, VP]
     lib.sekv_validate_cache.restype = ctypes.c_int
     lib.sekv_validate_cache.argtypes = [P(Dims), P(CacheStruct)]
+    lib.sekv_decode_layers_tiered.restype = ctypes.c_int
+    lib.sekv_decode_layers_tiered.argtypes = [P(Dims), P(CacheStruct), P(HostFactorsStruct), ctypes.c_int32,
+                                              ctypes.c_int32, VP, VP, VP, VP, SZ, VP, VP]
+    lib.sekv_tier_layer_stats.restype = ctypes.c_int
+    lib.sekv_tier_layer_stats.argtypes = [VP, P(ctypes.c_int64)]
     lib.sekv_segment_workspace_size.restype = ctypes.c_size_t
     lib.sekv_segment_workspace_size.argtypes = [P(BuildDims)]
     lib.sekv_segment.restype = ctypes.c_int
@@ -477,6 +483,13 @@ class Tier:
     def staging_bytes(self) -> int:
         return int(LIB.sekv_tier_staging_size(self._h))
 
+    def layer_stats(self):
+        """Counters of the last layered call: (critical bytes, critical blocks, prefetched
+        bytes, prefetched blocks)."""
+        st = (ctypes.c_int64 * 4)()
+        _check(LIB.sekv_tier_layer_stats(self._h, st))
+        return tuple(int(x) for x in st)
+
     def last_copy(self):
         """(bytes, copies, milliseconds) of the last step's host-to-device copies."""
         nb, nc, ms = ctypes.c_int64(0), ctypes.c_int32(0), ctypes.c_float(0)
@@ -493,6 +506,29 @@ class Tier:
             self.destroy()
         except Exception:
             pass
+
+
+def decode_layers_tiered(dims: Dims, caches, hosts, tier: Tier, ws: Workspace, prefetch: bool = True,
+                         sel=None, out=None, stream=None, side=None):
+    """sekv_decode_layers_tiered over len(caches) layers: returns (sel [L][B][Hkv][k],
+    out [L][B][Hq][d]).  `side` is the copy stream."""
+    if side is None:
+        raise ValueError("a side stream is needed for the copies")
+    L = len(caches)
+    if len(hosts) != L:
+        raise ValueError("one host arena per layer")
+    dev = caches[0].t["q"].device
+    if sel is None:
+        sel = _alloc((L, dims.batch, dims.n_kv_heads, max(dims.top_k, 0)), torch.int32, dev)
+    if out is None:
+        o = _out_tensor(dims, dev)
+        out = _alloc((L,) + tuple(o.shape), o.dtype, dev)
+    cs = (CacheStruct * L)(*[c.struct() for c in caches])
+    hs = (HostFactorsStruct * L)(*[h.struct() for h in hosts])
+    _check(LIB.sekv_decode_layers_tiered(ctypes.byref(dims), cs, hs, L, int(bool(prefetch)), tier._h,
+                                         _ptr(sel), _ptr(out), ws.ptr, ws.nbytes, _stream(stream),
+                                         _stream(side)))
+    return sel, out
 
 
 def validate_cache(dims: Dims, arrays: dict):

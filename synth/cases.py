@@ -443,8 +443,12 @@ def _span_means(U, s, Vt, lens):
 
 
 def make_case(spec: CaseSpec, layer: int = 0, variant: str = "L", threads: int | None = None,
-              arena_out: np.ndarray | None = None) -> Case:
-    """Build the stored inputs of one layer of a decode step."""
+              arena_out: np.ndarray | None = None, needle_layer: int | None = None) -> Case:
+    """Build the stored inputs of one layer of a decode step.
+
+    needle_layer (variant N): draw the planted spans' positions as for that layer, so that
+    layers built with the same needle_layer plant the same spans (their keys and values
+    are still this layer's own): a stand-in for spans that many layers attend to."""
     if variant not in VARIANTS:
         raise ValueError(variant)
     planted = variant == "N"
@@ -530,7 +534,8 @@ def make_case(spec: CaseSpec, layer: int = 0, variant: str = "L", threads: int |
         qbar = q_dec[b, g * G:(g + 1) * G].mean(axis=0)
         fac = _pair_factors(spec, vkey, b, g, lens, planted, qbar)
         if planted:
-            h = uniforms(stream_key(*vkey, ST_NEEDLE, b, g), m)
+            nkey = vkey if needle_layer is None else (spec.seed, VARIANTS[variant], needle_layer)
+            h = uniforms(stream_key(*nkey, ST_NEEDLE, b, g), m)
             chosen = np.sort(np.argsort(h, kind="stable")[:min(n_p, m)])
             needles[b, g, :len(chosen)] = chosen
             _plant(spec, fac, lens, chosen, qbar)
