@@ -280,3 +280,54 @@ def test_decode_on_built_cache(S, name, c):
             assert_out_close(got_out[b, g * G:(g + 1) * G], ref_out[b, g * G:(g + 1) * G], dt, f"{name} b{b} g{g}")
             checked += 1
     assert checked > 0
+
+
+def test_build_full_size_128k_x4_sampled(S):
+    """The builder in the launch configuration of the prefill bench (B 4, Hkv 8, d 128, 131072
+    tokens, bf16, R_max 32, sketch 40, one subspace iteration; head g holds the sequence's
+    generated stream with its feature columns rotated by 8 g): segmentation bit for bit,
+    anchors and span tables, and 24 sampled span sides against the optimal truncated SVD."""
+    import torch
+    banner("build 131072 x 4 x 8 heads, sampled spans")
+    B, Hkv, d, N, R, l = 4, 8, 128, 131072, 32, 40
+    p = make_prefill(B, 1, d, N, dtype="bf16", spike_every=170, true_rank=24, noise=0.02, sketch=l, seed=5)
+    keys1, vals1 = p.keys, p.values                                  # [B][1][N][d]
+    rot = lambda a: np.concatenate([np.roll(a, 8 * g, axis=3) for g in range(Hkv)], axis=1)
+    keys, values = rot(keys1), rot(vals1)
+    bd = S.make_build_dims(batch=B, n_kv_heads=Hkv, head_dim=d, max_tokens=N, rank=R, sketch=l, min_span=16,
+                           window=512, dtype="bf16", power=1)
+    wd = S.make_dims(batch=1, n_q_heads=1, n_kv_heads=1, head_dim=64, rank=8, top_k=1, max_anchors=1,
+                     max_spans=1, max_span_len=1, dtype="f32", softmax_scale=1.0)
+    ws = S.Workspace(wd)
+    cache, seg, lay = S.build_layer(bd, _dev(keys, "bf16"), _dev(values, "bf16"), _dev(p.surprisal),
+                                    _dev(p.n_tokens), _dev(p.omega), ws)
+    torch.cuda.synchronize()
+    assert ws.status() == 0
+    segh = {k: v.cpu().numpy() for k, v in seg.items() if not k.startswith("_")}
+    _check_segments(segh, p, 1.0, 16, 512, "full size")
+    factors = cache["factors"].cpu().numpy()
+    span_len = cache["span_len"].cpu().numpy()
+    ak = cache["anchor_k"].view(torch.int16).cpu().numpy().view(np.uint16)
+    g_ = np.random.default_rng(99)
+    worst = 0.0
+    for _ in range(24):
+        b = int(g_.integers(B))
+        anchors, spans = oracle.segment(p.surprisal[b], N, 1.0, 16, 512)
+        g = int(g_.integers(Hkv))
+        assert np.array_equal(ak[b, g, :len(anchors)], keys[b, g, anchors])
+        S_ = int(g_.integers(len(spans)))
+        s0, L = spans[S_]
+        assert span_len[b, S_] == L
+        side, src = (("K", keys), ("V", values))[int(g_.integers(2))]
+        w = int(lay["block_rank"][b, g, S_])
+        rk, rv = w & 0xFFFF, w >> 16
+        blk = oracle.read_span_block(factors, int(lay["block_off"][b, g, S_]), L, rk, d, "bf16", rv)
+        X = oracle.widen(src[b, g, s0:s0 + L], "bf16")
+        r = min(L, d, R)
+        full = np.linalg.svd(X, compute_uv=False)
+        opt = math.sqrt(np.sum(full[r:] ** 2))
+        err = np.linalg.norm(X - oracle.reconstruct(blk["U" + side], blk["s" + side], blk["Vt" + side]))
+        nx = np.linalg.norm(X)
+        assert err <= 1.25 * opt + 2.0 ** -7 * nx, (b, g, S_, side, err, opt, nx)
+        worst = max(worst, (err - opt) / nx)
+    banner(f"full size: worst excess reconstruction error {worst:.2e} of ||X||")
