@@ -165,3 +165,14 @@ def test_validate_cache_adaptive_ranks(S):
                                                              (int(case.span_len[last[0], last[2]]) + 65) *
                                                              ((w & 0xFFFF) + (w >> 16)) * 2]))
         assert "outside" in str(ei.value)
+
+
+def test_layered_tier_rejects_null_arguments(S):
+    """sekv_decode_layers_tiered and sekv_tier_layer_stats fail on the host, before any device
+    call, without a tier or counters."""
+    dims = _dims(S)
+    with pytest.raises(S.SekvError):
+        S._check(S.LIB.sekv_decode_layers_tiered(ctypes.byref(dims), None, None, 2, 1, None, None, None,
+                                                 None, 0, None, None))
+    with pytest.raises(S.SekvError):
+        S._check(S.LIB.sekv_tier_layer_stats(None, None))
