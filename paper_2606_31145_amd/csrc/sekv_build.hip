@@ -30,6 +30,7 @@
 #include <stdint.h>
 
 #include "sekv_internal.h"
+#include "sekv_build_internal.h"
 
 namespace sekv {
 namespace {

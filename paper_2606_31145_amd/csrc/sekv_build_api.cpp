@@ -7,6 +7,7 @@
 #include "sekv.h"
 #include "sekv_host.h"
 #include "sekv_internal.h"
+#include "sekv_build_internal.h"
 
 namespace {
 
