@@ -325,7 +325,7 @@ __device__ inline void rr_partner(int n, int k, int a, int *b, int *i) {
 
 // Cyclic Jacobi on the symmetric n x n matrix A (n even): A is rotated towards diagonal,
 // V (set to I here) accumulates the rotations, so that A_in = V diag(A_out) V^T.  A pair
-// is rotated when its off-diagonal entry exceeds 1e-14 of the geometric mean of its
+// is rotated when its off-diagonal entry exceeds 1e-10 of the geometric mean of its
 // diagonal entries; the sweeps stop after one that rotates no pair.
 //
 // One barrier per round.  Lanes 0 .. n/2 - 1 of every wave compute the round's rotations
@@ -356,7 +356,7 @@ __device__ void jacobi(double (*A)[KL + 1], double (*V)[KL + 1], SvdSmem &sm, in
                 int p, q;
                 rr_pair(n, k, lane, &p, &q);
                 const double app = sm.jd[buf][p], aqq = sm.jd[buf][q], apq = sm.jo[buf][lane];
-                if (fabs(apq) > 1e-14 * sqrt(fabs(app) * fabs(aqq)) && apq != 0.0) {
+                if (fabs(apq) > 1e-10 * sqrt(fabs(app) * fabs(aqq)) && apq != 0.0) {
                     const double th = (aqq - app) / (2.0 * apq);
                     const double t = (th >= 0.0 ? 1.0 : -1.0) / (fabs(th) + sqrt(1.0 + th * th));
                     c = 1.0 / sqrt(1.0 + t * t);
