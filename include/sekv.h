@@ -264,9 +264,9 @@ SEKV_API sekv_status sekv_decode_step_gated(const sekv_dims *dims, const sekv_ca
  *      The SVD sketches the span with the caller's d x l Gaussian test matrix; each
  *      subspace iteration (`power`) sketches it again with an orthonormal basis of the
  *      previous pass's dominant row space, which sharpens the captured subspace when the
- *      spectrum is flat.  Directions of the sketch below 1e-8 of its largest Gram diagonal
- *      entry are dropped (rank-deficient spans), as are components below 1e-5 of the
- *      largest singular value.
+ *      spectrum is flat (a span of at most `sketch` tokens needs none and gets none).
+ *      Directions of the sketch below 1e-8 of its largest Gram diagonal entry are dropped
+ *      (rank-deficient spans), as are components below 1e-5 of the largest singular value.
  * ---------------------------------------------------------------------------------- */
 typedef struct {
     int32_t batch;          /* B >= 0                                                        */

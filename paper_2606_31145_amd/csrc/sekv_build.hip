@@ -716,7 +716,10 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
 
     // subspace iterations: the next test matrix is an orthonormal basis of B's row space,
     // R2^-T B[piv2] from the pivoted Cholesky B B^T = R2^T R2, written into om
-    for (int it = 0; it < a.power; ++it) {
+    // a span of at most l tokens is spanned by its sketch already (X Omega has the rank of X
+    // for a generic Omega): an iteration would change nothing but the rounding
+    const int power = L <= l ? 0 : a.power;
+    for (int it = 0; it < power; ++it) {
         sketch_pass();
         SV_STAMP(kSvPass);
         factor_b(0);
