@@ -158,8 +158,8 @@ SEKV_API sekv_status sekv_workspace_init(void *ws, size_t ws_bytes, hipStream_t 
 
 /* Read and clear the workspace's device error word (synchronises `stream`).  Bits:
  * 1 = a wait for a selection timed out, 2 = a factor block lay outside the arena or its
- * rank-table entry was invalid, 4 = a selected index was out of range.  0 after every
- * correct call. */
+ * rank-table entry was invalid, 4 = a selected index was out of range (sekv_build_cache:
+ * an anchor index or span outside the sequence's tokens).  0 after every correct call. */
 SEKV_API sekv_status sekv_workspace_status(void *ws, size_t ws_bytes, hipStream_t stream,
                                   int32_t *error_bits);
 
@@ -311,8 +311,10 @@ SEKV_API int64_t sekv_build_layout(const sekv_build_dims *dims, int32_t max_span
  * n_anchors[b] untouched), sum_k/v [B][Hkv][max_spans][d], span_len [B][max_spans],
  * span_logsize [B][max_spans], the factor arena (factors_bytes).  max_anchors and
  * max_spans must cover every n_anchors[b] and n_spans[b] (larger counts are clamped).
+ * Anchor indices and spans must lie in [0, n_tokens[b]) (n_tokens clamped to [0, N_max]);
+ * an anchor row or span outside it is skipped.
  * ws: a step workspace of at least 256 bytes whose error word reports blocks outside the
- * arena (bit 2). */
+ * arena (bit 2) and skipped anchor rows or spans (bit 4). */
 SEKV_API sekv_status sekv_build_cache(const sekv_build_dims *dims, const void *keys, const void *values,
                                       const float *surprisal, const int32_t *n_tokens,
                                       const int32_t *n_anchors, const int32_t *anchor_idx,

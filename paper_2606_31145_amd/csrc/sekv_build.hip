@@ -187,6 +187,17 @@ __global__ void __launch_bounds__(kSegThreads) segment_kernel(SegArgs a) {
 // anchors and summaries
 // ---------------------------------------------------------------------------
 
+// Tokens of sequence b, clamped to [0, N] as the segmentation clamps them.
+__device__ inline int seq_tokens(const BuildArgs &a, int b) {
+    const int n = a.n_tokens[b];
+    return n < 0 ? 0 : min(n, a.N);
+}
+
+// An anchor index or span outside the sequence's tokens: the row or span is skipped.
+__device__ inline void flag_table(const BuildArgs &a) {
+    __hip_atomic_fetch_or(a.error, kErrSelRange, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // grid = B * Hkv * rows workgroups; workgroup (pair, y) copies anchor rows
 // [64 y, 64 y + 64) and summarises span y.
 __global__ void __launch_bounds__(BT) gather_kernel(BuildArgs a, int rows) {
@@ -194,6 +205,7 @@ __global__ void __launch_bounds__(BT) gather_kernel(BuildArgs a, int rows) {
     const int y = blockIdx.x % rows, tid = threadIdx.x;
     const int d = a.d, e = a.elem;
     const size_t tok0 = size_t(pair) * a.N;                 // row of token 0 of (b, g)
+    const int nt = seq_tokens(a, b);
     int na = a.n_anchors[b];
     na = na < 0 ? 0 : min(na, min(a.A_max, a.N));
     int ns = a.n_spans[b];
@@ -203,10 +215,12 @@ __global__ void __launch_bounds__(BT) gather_kernel(BuildArgs a, int rows) {
         const int r = y * 64 + i / d, col = i % d;
         if (r < na) {
             const int t = a.anchor_idx[size_t(b) * a.N + r];
-            if (t >= 0 && t < a.N) {
+            if (t >= 0 && t < nt) {
                 const size_t dst = (size_t(pair) * a.A_max + r) * d + col;
                 st_elem(a.anchor_k, dst, ld_elem(a.keys, (tok0 + t) * d + col, e), e);
                 st_elem(a.anchor_v, dst, ld_elem(a.values, (tok0 + t) * d + col, e), e);
+            } else if (col == 0) {
+                flag_table(a);
             }
         }
     }
@@ -214,7 +228,10 @@ __global__ void __launch_bounds__(BT) gather_kernel(BuildArgs a, int rows) {
     if (y >= ns) return;
     const int s0 = a.span_start[size_t(b) * a.N + y];
     int L = a.span_len_seg[size_t(b) * a.N + y];
-    if (s0 < 0 || L < 1 || s0 + L > a.N) return;
+    if (s0 < 0 || L < 1 || s0 + L > nt) {
+        if (tid == 0 && g == 0) flag_table(a);
+        return;
+    }
     __shared__ float red[2][BT];
     __shared__ float hs;
     // weight normaliser sum_t H_t over the span (float64 then float32)
@@ -567,7 +584,7 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
     if (S >= ns) return;
     const int s0 = a.span_start[size_t(b) * a.N + S];
     const int L = a.span_len_seg[size_t(b) * a.N + S];
-    if (s0 < 0 || L < 1 || s0 + L > a.N) return;
+    if (s0 < 0 || L < 1 || s0 + L > seq_tokens(a, b)) return;   // flagged by the gather kernel
     const int gran = 16 / e;
     const int r = min(min(L, d), R);                        // rank kept (eq. key_svd)
     const int rs = (r + gran - 1) / gran * gran;            // stored rank

@@ -140,7 +140,7 @@ sekv_status sekv_build_cache(const sekv_build_dims *dims, const void *keys, cons
     if (factors_bytes <= 0) return fail(SEKV_ERR_INVALID_ARG, "factors_bytes <= 0");
     if (ws_bytes < sizeof(sekv::WsHeader)) return fail(SEKV_ERR_WORKSPACE, "workspace too small");
     sekv::BuildArgs a{};
-    a.keys = keys; a.values = values; a.surprisal = surprisal;
+    a.keys = keys; a.values = values; a.surprisal = surprisal; a.n_tokens = n_tokens;
     a.n_anchors = n_anchors; a.anchor_idx = anchor_idx; a.n_spans = n_spans; a.span_start = span_start;
     a.span_len_seg = span_len_seg; a.omega = omega;
     a.anchor_k = anchor_k; a.anchor_v = anchor_v; a.sum_k = sum_k; a.sum_v = sum_v;
@@ -154,7 +154,6 @@ sekv_status sekv_build_cache(const sekv_build_dims *dims, const void *keys, cons
     a.trace = sekv::trace_buffer(&tb);
     a.trace_items = a.trace ? int64_t(tb / (sizeof(int64_t) * sekv::kTraceSlots)) : 0;
     a.A_max = max_anchors; a.M_max = max_spans;
-    (void)n_tokens;
     const hipError_t e = sekv::launch_build(a, dims->batch, stream);
     if (e != hipSuccess) return fail(SEKV_ERR_HIP, "builder launch: %s", hipGetErrorString(e));
     return SEKV_OK;

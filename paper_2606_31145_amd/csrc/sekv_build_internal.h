@@ -23,6 +23,7 @@ struct SegArgs {
 struct BuildArgs {
     const void *keys, *values;         // [B][Hkv][N][d]
     const float *surprisal;            // [B][N]
+    const int32_t *n_tokens;           // [B]
     const int32_t *n_anchors, *anchor_idx, *n_spans, *span_start, *span_len_seg;
     const float *omega;                // [d][l]
     void *anchor_k, *anchor_v;         // [B][Hkv][A_max][d]
@@ -32,7 +33,7 @@ struct BuildArgs {
     void *factors;
     int64_t factors_bytes;
     const int64_t *block_off;          // [B][Hkv][M_max]
-    int32_t *error;                    // device error word (out-of-arena blocks)
+    int32_t *error;                    // device error word (out-of-arena blocks, bad tables)
     int32_t Hkv, N, d, elem, R, l, sweeps, power, A_max, M_max;
     int64_t *trace;                    // diagnostic builds: [trace_items][kTraceSlots] or null
     int64_t trace_items;

@@ -204,6 +204,39 @@ def test_build_matches_oracle(S, name, c):
     banner(f"build {name}: worst excess reconstruction error {worst:.2e} of ||X||")
 
 
+def test_build_rejects_tables_past_n_tokens(S):
+    """Anchor indices and spans past a sequence's own token count are skipped and flagged
+    (error bit 4); everything inside is built as usual."""
+    import torch
+    banner("build: tables past n_tokens")
+    c = dict(dtype="f32", d=64, Hkv=1, n=[900, 600], rank=8, sketch=12, min_span=4, window=16)
+    p = make_prefill(2, 1, 64, c["n"], dtype="f32", spike_every=60, seed=77)
+    bd = _bdims(S, p, 1, 64, rank=8, sketch=12, min_span=4, window=16)
+    dims = S.make_dims(batch=1, n_q_heads=1, n_kv_heads=1, head_dim=64, rank=8, top_k=1, max_anchors=1,
+                       max_spans=1, max_span_len=1, dtype="f32", softmax_scale=1.0)
+    ws = S.Workspace(dims)
+    keys, values, surp = _dev(p.keys), _dev(p.values), _dev(p.surprisal)
+    seg = S.segment(bd, surp, _dev(p.n_tokens))
+    torch.cuda.synchronize()
+    ns, na = seg["n_spans"].cpu().numpy(), seg["n_anchors"].cpu().numpy()
+    span_len = seg["span_len"].cpu().numpy()
+    off, _, nbytes = S.build_layout(bd, int(ns.max()), ns, span_len)
+    # sequence 0 claims 50 tokens fewer than were segmented: its tail anchors fall outside
+    short = p.n_tokens.copy()
+    short[0] -= 50
+    cache = S.build_cache(bd, keys, values, surp, _dev(short), seg, _dev(p.omega[:, :12].copy()), int(na.max()),
+                          int(ns.max()), torch.from_numpy(off).cuda(), nbytes, ws)
+    torch.cuda.synchronize()
+    assert ws.status() == 4
+    assert ws.status() == 0                                   # read and cleared
+    anchors, _ = oracle.segment(p.surprisal[1], int(p.n_tokens[1]), 1.0, 4, 16)
+    got = cache["anchor_k"].cpu().numpy()
+    assert np.array_equal(got[1, 0, :len(anchors)], p.keys[1, 0, anchors])
+    anchors0, _ = oracle.segment(p.surprisal[0], int(p.n_tokens[0]), 1.0, 4, 16)
+    inside = [i for i, t in enumerate(anchors0) if t < short[0]]
+    assert np.array_equal(got[0, 0, inside], p.keys[0, 0, [anchors0[i] for i in inside]])
+
+
 def test_build_layout_and_validate(S):
     """The built cache passes the library's own cache validation with its block ranks."""
     banner("build layout + validate")
