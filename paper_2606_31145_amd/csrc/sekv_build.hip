@@ -298,8 +298,9 @@ struct SvdSmem {
     } u;                                      //   (subspace iteration) or E (last pass)
     float bm[KL][128 + 1];                    // Y^T X, then B (rows in pivot order)
     double am[KL][KL + 1];                    // G; B B^T; Rinv; T = R^-1 E
-    double jd[2][KL];                         // Jacobi: diagonal, and the entries the round
-    double jo[2][KL / 2];                     //   pairs (two alternating copies)
+    double a2[KL][KL + 1];                    // Jacobi: the second copy of the rotated matrix
+    double2 jcs[BT / 64][KL / 2];             // Jacobi: each wave's (c, s) of the round
+    uint16_t jpq[KL - 1][KL / 2];             // Jacobi: pair i of round k is (p, q) = (lo, hi byte)
     double sig[KL];
     double dg[2][KL];                         // remaining Cholesky diagonal (two copies)
     int piv[KL], piv2[KL], order[KL];
@@ -326,53 +327,51 @@ __device__ inline void rr_pair(int n, int k, int i, int *p, int *q) {
     *q = max(a0, b0);
 }
 
-// The partner b of index a in round k of the same pairing, and the number of their pair.
-__device__ inline void rr_partner(int n, int k, int a, int *b, int *i) {
-    const int m = n - 1;
-    if (a == m) { *b = k; *i = 0; return; }
-    int bb = 2 * k - a;                          // in (-m, 2m)
-    if (bb < 0) bb += m;
-    else if (bb >= m) bb -= m;
-    if (bb == a) { *b = m; *i = 0; return; }
-    *b = bb;
-    int d1 = a - k;                              // in (-m, m)
-    if (d1 < 0) d1 += m;
-    *i = d1 <= (m - 1) / 2 ? d1 : m - d1;
-}
-
 // Cyclic Jacobi on the symmetric n x n matrix A (n even): A is rotated towards diagonal,
-// V (set to I here) accumulates the rotations, so that A_in = V diag(A_out) V^T.  A pair
-// is rotated when its off-diagonal entry exceeds 1e-10 of the geometric mean of its
+// V (set to I here) accumulates the rotations, so that A_in = V diag(A_out) V^T; on
+// return the diagonal of A holds A_out's (the rest of A is left undefined).  A pair is
+// rotated when its off-diagonal entry exceeds 1e-10 of the geometric mean of its
 // diagonal entries; the sweeps stop after one that rotates no pair.
 //
-// One barrier per round.  Lanes 0 .. n/2 - 1 of every wave compute the round's rotations
-// from the diagonal and the paired entries, which the previous round left in jd / jo (two
-// alternating copies), and pass them on by shuffles.  A is updated as 2 x 2 blocks of
-// pairs (I, J), each block and its transpose by one thread, V as column pairs; the owner
-// of an entry that the next round pairs, or of a diagonal entry, also writes it to jd / jo.
+// One barrier per round.  A is kept in two copies (A and sm.a2): a round reads one and
+// writes the other in full, so lanes 0 .. n/2 - 1 of every wave can take the round's
+// rotations from the copy being read while other waves already write theirs.  Each wave
+// keeps its rotations in its own row of sm.jcs (written and read by that wave only: its
+// LDS accesses complete in order).  A is updated as 2 x 2 blocks of pairs (I <= J), each
+// block and its transpose by one thread; V as column pairs, one pair J and several rows
+// per thread.
 __device__ void jacobi(double (*A)[KL + 1], double (*V)[KL + 1], SvdSmem &sm, int n, int sweeps, int tid) {
-    const int lane = tid & 63, np = n / 2;
+    const int lane = tid & 63, wave = tid >> 6, np = n / 2;
     for (int idx = tid; idx < n * n; idx += BT) V[idx / n][idx % n] = (idx / n == idx % n) ? 1.0 : 0.0;
-    if (tid < n) sm.jd[0][tid] = A[tid][tid];
-    if (tid < np) {
+    for (int idx = tid; idx < (n - 1) * np; idx += BT) {
         int p, q;
-        rr_pair(n, 0, tid, &p, &q);
-        sm.jo[0][tid] = A[p][q];
+        rr_pair(n, idx / np, idx % np, &p, &q);
+        sm.jpq[idx / np][idx % np] = uint16_t(p | (q << 8));
     }
     if (tid < 2) sm.nconv[tid] = 0;
+    // this thread's block (bI, bJ), bI <= bJ, of the np (np + 1) / 2 blocks
+    const int nblk = np * (np + 1) / 2;
+    int bI = 0, bJ = 0;
+    if (tid < nblk) {
+        int t = tid;
+        while (t >= np - bI) { t -= np - bI; ++bI; }
+        bJ = bI + t;
+    }
+    // this thread's V column pair vJ and rows vr0, vr0 + vstep, ... (threads past
+    // vstep * np have none)
+    const int vstep = BT / np, vJ = tid % np, vr0 = tid / np;
+    constexpr int NVR = (KL + (BT / (KL / 2)) - 1) / (BT / (KL / 2)) + 1;   // rows per thread, bound
     __syncthreads();
-    constexpr int NB = (KL / 2 * KL / 2 + BT - 1) / BT;          // block slots per thread
-    constexpr int NV = (KL * KL / 2 + BT - 1) / BT;              // V column-pair slots per thread
-    int buf = 0;
+    double(*cur)[KL + 1] = A;
+    double(*nxt)[KL + 1] = sm.a2;
     for (int sweep = 0; sweep < sweeps; ++sweep) {
         const int par = sweep & 1;
         for (int k = 0; k < n - 1; ++k) {
-            const int kn = k + 1 == n - 1 ? 0 : k + 1;
-            double c = 1.0, s = 0.0;
             if (lane < np) {
-                int p, q;
-                rr_pair(n, k, lane, &p, &q);
-                const double app = sm.jd[buf][p], aqq = sm.jd[buf][q], apq = sm.jo[buf][lane];
+                const uint32_t pq = sm.jpq[k][lane];
+                const int p = pq & 255, q = pq >> 8;
+                const double app = cur[p][p], aqq = cur[q][q], apq = cur[p][q];
+                double c = 1.0, s = 0.0;
                 if (fabs(apq) > 1e-10 * sqrt(fabs(app) * fabs(aqq)) && apq != 0.0) {
                     const double th = (aqq - app) / (2.0 * apq);
                     const double t = (th >= 0.0 ? 1.0 : -1.0) / (fabs(th) + sqrt(1.0 + th * th));
@@ -380,61 +379,50 @@ __device__ void jacobi(double (*A)[KL + 1], double (*V)[KL + 1], SvdSmem &sm, in
                     s = t * c;
                     sm.nconv[par] = 1;
                 }
+                sm.jcs[wave][lane] = make_double2(c, s);
             }
-#pragma unroll
-            for (int u = 0; u < NB; ++u) {
-                const int idx = tid + BT * u;
-                const bool in = idx < np * np;
-                const int I = in ? idx / np : 0, J = in ? idx % np : 0;
-                const double cI = __shfl(c, I), sI = __shfl(s, I), cJ = __shfl(c, J), sJ = __shfl(s, J);
-                if (in && I <= J) {
-                    int pI, qI, pJ, qJ;
-                    rr_pair(n, k, I, &pI, &qI);
-                    rr_pair(n, k, J, &pJ, &qJ);
-                    const double a = A[pI][pJ], b = A[pI][qJ], cc = A[qI][pJ], dd = A[qI][qJ];
-                    const double t00 = cI * a - sI * cc, t01 = cI * b - sI * dd;
-                    const double t10 = sI * a + cI * cc, t11 = sI * b + cI * dd;
-                    const double n00 = t00 * cJ - t01 * sJ, n01 = t00 * sJ + t01 * cJ;
-                    const double n10 = t10 * cJ - t11 * sJ, n11 = t10 * sJ + t11 * cJ;
-                    A[pI][pJ] = n00; A[pI][qJ] = n01; A[qI][pJ] = n10; A[qI][qJ] = n11;
-                    if (I != J) {
-                        A[pJ][pI] = n00; A[qJ][pI] = n01; A[pJ][qI] = n10; A[qJ][qI] = n11;
-                    } else {
-                        sm.jd[buf ^ 1][pI] = n00;
-                        sm.jd[buf ^ 1][qI] = n11;
-                    }
-                    const int xs[4] = {pI, pI, qI, qI}, ys[4] = {pJ, qJ, pJ, qJ};
-                    const double vs[4] = {n00, n01, n10, n11};
-#pragma unroll
-                    for (int e2 = 0; e2 < 4; ++e2) {
-                        int pb, pi;
-                        rr_partner(n, kn, xs[e2], &pb, &pi);
-                        if (pb == ys[e2]) sm.jo[buf ^ 1][pi] = vs[e2];
-                    }
-                }
+            __builtin_amdgcn_wave_barrier();
+            if (tid < nblk) {
+                const uint32_t pqI = sm.jpq[k][bI], pqJ = sm.jpq[k][bJ];
+                const int pI = pqI & 255, qI = pqI >> 8, pJ = pqJ & 255, qJ = pqJ >> 8;
+                const double2 csI = sm.jcs[wave][bI], csJ = sm.jcs[wave][bJ];
+                const double cI = csI.x, sI = csI.y, cJ = csJ.x, sJ = csJ.y;
+                const double a = cur[pI][pJ], b = cur[pI][qJ], cc = cur[qI][pJ], dd = cur[qI][qJ];
+                const double t00 = cI * a - sI * cc, t01 = cI * b - sI * dd;
+                const double t10 = sI * a + cI * cc, t11 = sI * b + cI * dd;
+                const double n00 = t00 * cJ - t01 * sJ, n01 = t00 * sJ + t01 * cJ;
+                const double n10 = t10 * cJ - t11 * sJ, n11 = t10 * sJ + t11 * cJ;
+                nxt[pI][pJ] = n00; nxt[pI][qJ] = n01; nxt[qI][pJ] = n10; nxt[qI][qJ] = n11;
+                if (bI != bJ) { nxt[pJ][pI] = n00; nxt[qJ][pI] = n01; nxt[pJ][qI] = n10; nxt[qJ][qI] = n11; }
             }
+            if (vr0 < vstep) {
+                const uint32_t pqJ = sm.jpq[k][vJ];
+                const int pJ = pqJ & 255, qJ = pqJ >> 8;
+                const double2 csJ = sm.jcs[wave][vJ];
+                if (csJ.y != 0.0) {
 #pragma unroll
-            for (int u = 0; u < NV; ++u) {
-                const int idx = tid + BT * u;
-                const bool in = idx < n * np;
-                const int r = in ? idx / np : 0, J = in ? idx % np : 0;
-                const double cJ = __shfl(c, J), sJ = __shfl(s, J);
-                if (in && sJ != 0.0) {
-                    int pJ, qJ;
-                    rr_pair(n, k, J, &pJ, &qJ);
-                    const double vp = V[r][pJ], vq = V[r][qJ];
-                    V[r][pJ] = cJ * vp - sJ * vq;
-                    V[r][qJ] = sJ * vp + cJ * vq;
+                    for (int u = 0; u < NVR; ++u) {
+                        const int r = vr0 + vstep * u;
+                        if (r < n) {
+                            const double vp = V[r][pJ], vq = V[r][qJ];
+                            V[r][pJ] = csJ.x * vp - csJ.y * vq;
+                            V[r][qJ] = csJ.y * vp + csJ.x * vq;
+                        }
+                    }
                 }
             }
             __syncthreads();
-            buf ^= 1;
+            double(*sw)[KL + 1] = cur;
+            cur = nxt;
+            nxt = sw;
         }
         const int rotated = sm.nconv[par];
         if (tid == 0) sm.nconv[par ^ 1] = 0;     // the next sweep's flag; this one is read
         __syncthreads();                         // by every thread before it is reset again
         if (!rotated) break;
     }
+    if (cur != A && tid < n) A[tid][tid] = cur[tid][tid];
+    __syncthreads();
 }
 
 // Cholesky with diagonal pivoting of the symmetric positive semi-definite n x n matrix A
