@@ -39,6 +39,7 @@ constexpr int kSegThreads = 1024;
 constexpr int BT = 256;                 // builder threads per workgroup
 constexpr int kMaxL = 40;               // largest sketch width
 constexpr int kTile = 16;               // tokens per streamed tile in the SVD
+template <int N> struct Cint { static constexpr int value = N; };
 
 __device__ inline float ld_elem(const void *base, size_t i, int elem) {
     if (elem == 2) {
@@ -284,12 +285,13 @@ constexpr int KL = kMaxL;
 struct SvdSmem {
     union {
         struct {                              // passes over X
-            uint16_t om[KL][128 + 2];         // the test matrix, transposed (l x d), as
+            uint16_t om[KL][128 + 4];         // the test matrix, transposed (l x d), as
                                               //   bfloat16 (any fixed test matrix serves;
                                               //   both passes of an iteration use this one);
-                                              //   rows padded: a wave reads one column
-            float x[kTile][128 + 1];          // token tile
-            float yt[kTile][KL + 1];          // sketch tile Y = X Omega
+                                              //   rows padded to 8-byte vectors off the
+                                              //   same banks
+            float x[kTile][128 + 4];          // token tile (rows: 16-byte vectors)
+            float yt[kTile][KL + 4];          // sketch tile Y = X Omega (rows: 16-byte vectors)
         } p;
         struct {                              // between passes (float64: a Gram matrix
             double rg[KL][KL + 1];            //   squares the condition number)
@@ -594,7 +596,6 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
 #endif
     SV_STAMP(kSvStart);
 
-    constexpr int NP = KL * 128 / BT;                        // entries of an l x d matrix per thread
     auto bf16_bits = [](float f) -> uint32_t {
         uint32_t q = __float_as_uint(f);
         q += 0x7FFFu + ((q >> 16) & 1u);                      // round to nearest even
@@ -632,19 +633,25 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
             for (int h = 0; h < per; ++h) sm.u.p.x[t][c + h] = v[h];
         }
         __syncthreads();
-        {   // Y rows: thread (t, jb) forms Y[t][jb], Y[t][jb + 16], Y[t][jb + 32]; rows of om
-            // past l are read but their sums dropped
+        {   // Y rows: thread (t, jb) forms Y[t][jb], Y[t][jb + 16], Y[t][jb + 32], summing
+            // over c in order, four columns per LDS read; rows of om past l are read but
+            // their sums dropped
             const int t = tid >> 4, jb = tid & 15;
-            const float *xr = sm.u.p.x[t];
-            const uint16_t *o0 = sm.u.p.om[jb], *o1 = sm.u.p.om[jb + 16],
-                           *o2 = sm.u.p.om[min(jb + 32, KL - 1)];
+            const float4 *xr = reinterpret_cast<const float4 *>(sm.u.p.x[t]);
+            const uint2 *o0 = reinterpret_cast<const uint2 *>(sm.u.p.om[jb]);
+            const uint2 *o1 = reinterpret_cast<const uint2 *>(sm.u.p.om[jb + 16]);
+            const uint2 *o2 = reinterpret_cast<const uint2 *>(sm.u.p.om[min(jb + 32, KL - 1)]);
+            auto lo = [](uint32_t w) { return __uint_as_float(w << 16); };
+            auto hi = [](uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); };
             float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f;
-#pragma unroll 8
-            for (int c = 0; c < d; ++c) {
-                const float xv = xr[c];
-                a0 += xv * __uint_as_float(uint32_t(o0[c]) << 16);
-                a1 += xv * __uint_as_float(uint32_t(o1[c]) << 16);
-                a2 += xv * __uint_as_float(uint32_t(o2[c]) << 16);
+#pragma unroll 4
+            for (int c4 = 0; c4 < d / 4; ++c4) {
+                const float4 xv = xr[c4];
+                const uint2 w0 = o0[c4], w1 = o1[c4], w2 = o2[c4];
+                a0 += xv.x * lo(w0.x); a1 += xv.x * lo(w1.x); a2 += xv.x * lo(w2.x);
+                a0 += xv.y * hi(w0.x); a1 += xv.y * hi(w1.x); a2 += xv.y * hi(w2.x);
+                a0 += xv.z * lo(w0.y); a1 += xv.z * lo(w1.y); a2 += xv.z * lo(w2.y);
+                a0 += xv.w * hi(w0.y); a1 += xv.w * hi(w1.y); a2 += xv.w * hi(w2.y);
             }
             if (jb < l) sm.u.p.yt[t][jb] = a0;
             if (jb + 16 < l) sm.u.p.yt[t][jb + 16] = a1;
@@ -653,50 +660,75 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
         __syncthreads();
     };
     // a pass over X with the test matrix in om: G = Y^T Y (float64 sums) into am and
-    // P = Y^T X (float32 sums) into bm, accumulated in registers token by token; thread tid
-    // owns column tid % d of rows tid / d, tid / d + BT / d, ... of P and entries tid,
-    // tid + BT, ... of G
-    auto sketch_pass = [&]() {
-        constexpr int NG = (KL * KL + BT - 1) / BT;
-        float pacc[NP];
-        double gacc[NG];
+    // P = Y^T X (float32 sums) into bm, accumulated in registers token by token.  Thread
+    // tid owns the 5 x CW block of P at rows 5 (tid / 32), columns CW (tid % 32) (CW = d / 32)
+    // and, for tid < 200, the 2 x 4 block of G at rows 2 (tid / 10), columns 4 (tid % 10);
+    // sums over blocks past l are dropped.
+    auto sketch_pass = [&](auto cw_c) {
+        constexpr int CW = decltype(cw_c)::value;
+        constexpr int GI = KL / 2, GJ = KL / 4;               // G blocks: GI x GJ of 2 x 4
+        const int j0 = 5 * (tid >> 5), c0 = CW * (tid & 31);
+        const bool gown = tid < GI * GJ;
+        const int i0 = 2 * (tid / GJ), jj0 = 4 * (tid % GJ);
+        float pacc[5][CW];
+        double gacc[2][4];
 #pragma unroll
-        for (int u = 0; u < NP; ++u) pacc[u] = 0.0f;
+        for (int jj = 0; jj < 5; ++jj)
 #pragma unroll
-        for (int u = 0; u < NG; ++u) gacc[u] = 0.0;
-        const int pc = tid % d, pj = tid / d, pstep = BT / d;
+            for (int cc = 0; cc < CW; ++cc) pacc[jj][cc] = 0.0f;
+#pragma unroll
+        for (int a2 = 0; a2 < 2; ++a2)
+#pragma unroll
+            for (int b4 = 0; b4 < 4; ++b4) gacc[a2][b4] = 0.0;
         __syncthreads();
         for (int t0 = 0; t0 < L; t0 += kTile) {
             const int nt = min(kTile, L - t0);
             tile(t0, nt);
             for (int t = 0; t < nt; ++t) {
-                const float xv = sm.u.p.x[t][pc];
-#pragma unroll
-                for (int u = 0; u < NP; ++u) {
-                    const int j = pj + pstep * u;
-                    if (j < l) pacc[u] += sm.u.p.yt[t][j] * xv;
+                float xv[CW];
+                if constexpr (CW == 4) {
+                    const float4 v = *reinterpret_cast<const float4 *>(&sm.u.p.x[t][c0]);
+                    xv[0] = v.x; xv[1] = v.y; xv[2] = v.z; xv[3] = v.w;
+                } else {
+                    const float2 v = *reinterpret_cast<const float2 *>(&sm.u.p.x[t][c0]);
+                    xv[0] = v.x; xv[1] = v.y;
                 }
+                float yv[5];
 #pragma unroll
-                for (int u = 0; u < NG; ++u) {
-                    const int idx = tid + BT * u;
-                    const int i = idx / KL, j = idx % KL;
-                    if (i < l && j < l) gacc[u] += double(sm.u.p.yt[t][i]) * double(sm.u.p.yt[t][j]);
+                for (int jj = 0; jj < 5; ++jj) yv[jj] = sm.u.p.yt[t][j0 + jj];
+#pragma unroll
+                for (int jj = 0; jj < 5; ++jj)
+#pragma unroll
+                    for (int cc = 0; cc < CW; ++cc) pacc[jj][cc] += yv[jj] * xv[cc];
+                if (gown) {
+                    const float2 yi = *reinterpret_cast<const float2 *>(&sm.u.p.yt[t][i0]);
+                    const float4 yj = *reinterpret_cast<const float4 *>(&sm.u.p.yt[t][jj0]);
+                    const double di[2] = {double(yi.x), double(yi.y)};
+                    const double dj[4] = {double(yj.x), double(yj.y), double(yj.z), double(yj.w)};
+#pragma unroll
+                    for (int a2 = 0; a2 < 2; ++a2)
+#pragma unroll
+                        for (int b4 = 0; b4 < 4; ++b4) gacc[a2][b4] += di[a2] * dj[b4];
                 }
             }
             __syncthreads();
         }
 #pragma unroll
-        for (int u = 0; u < NP; ++u) {
-            const int j = pj + pstep * u;
-            if (j < l) sm.bm[j][pc] = pacc[u];
-        }
+        for (int jj = 0; jj < 5; ++jj)
 #pragma unroll
-        for (int u = 0; u < NG; ++u) {
-            const int idx = tid + BT * u;
-            const int i = idx / KL, j = idx % KL;
-            if (i < l && j < l) sm.am[i][j] = gacc[u];
-        }
+            for (int cc = 0; cc < CW; ++cc)
+                if (j0 + jj < l) sm.bm[j0 + jj][c0 + cc] = pacc[jj][cc];
+        if (gown)
+#pragma unroll
+            for (int a2 = 0; a2 < 2; ++a2)
+#pragma unroll
+                for (int b4 = 0; b4 < 4; ++b4)
+                    if (i0 + a2 < l && jj0 + b4 < l) sm.am[i0 + a2][jj0 + b4] = gacc[a2][b4];
         __syncthreads();
+    };
+    auto sketch = [&]() {
+        if (d == 128) sketch_pass(Cint<4>{});
+        else sketch_pass(Cint<2>{});
     };
     // after a pass: G = R^T R (pivoted) into rg, B = R^-T P[piv] over P, B B^T into am;
     // rg then holds R^-1 (pivot order)
@@ -725,7 +757,7 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
     // for a generic Omega): an iteration would change nothing but the rounding
     const int power = L <= l ? 0 : a.power;
     for (int it = 0; it < power; ++it) {
-        sketch_pass();
+        sketch();
         SV_STAMP(kSvPass);
         factor_b(0);
         const int k2 = piv_chol(sm.am, sm.u.s.em, sm.piv2, sm, l, 1e-8, tid);
@@ -753,7 +785,7 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
         }
         omk[u] = w;
     }
-    sketch_pass();
+    sketch();
     SV_STAMP(kSvPass2);
     const int k = factor_b(1);
     // B B^T = E diag(sigma^2) E^T; order (descending, ties to the lower index); components
