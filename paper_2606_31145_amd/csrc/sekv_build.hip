@@ -298,7 +298,7 @@ struct SvdSmem {
             double em[KL][KL + 1];            // rg: R of G (rows: pivot steps, columns:
         } s;                                  //   sketch columns); em: R of B B^T
     } u;                                      //   (subspace iteration) or E (last pass)
-    float bm[KL][128 + 1];                    // Y^T X, then B (rows in pivot order)
+    float bm[KL][128 + 4];                    // Y^T X, then B (rows in pivot order; 16-byte vectors)
     double am[KL][KL + 1];                    // G; B B^T; Rinv; T = R^-1 E
     double a2[KL][KL + 1];                    // Jacobi: the second copy of the rotated matrix
     double2 jcs[BT / 64][KL / 2];             // Jacobi: each wave's (c, s) of the round
@@ -490,8 +490,9 @@ __device__ int piv_chol(double (*A)[KL + 1], double (*Rm)[KL + 1], int *piv, Svd
 }
 
 // Ri = Rt^-1 for Rt[j][m] = Rm[j][piv[m]] (k x k upper triangular; entries past k zero).
-// Rt goes into Rp first; then the rows of Ri from the last up, each row by KL threads in
-// one step (Ri may be the storage of Rm).
+// Rt goes into Rp first; then thread i < k forms column i of Ri by back substitution,
+// rows from the last up: a column needs only its own earlier entries, so no thread waits
+// for another (Ri may be the storage of Rm).
 __device__ inline void tri_inverse(const double (*Rm)[KL + 1], const int *piv, double (*Rp)[KL + 1],
                                    double (*Ri)[KL + 1], int k, int tid) {
     for (int idx = tid; idx < KL * KL; idx += BT) {
@@ -503,43 +504,64 @@ __device__ inline void tri_inverse(const double (*Rm)[KL + 1], const int *piv, d
         const int j = idx / KL, i = idx % KL;
         if (j >= k || i >= k) Ri[j][i] = 0.0;
     }
-    for (int j = k - 1; j >= 0; --j) {                          // row j of Ri: entries i >= j
-        if (tid < k && tid >= j) {
-            const int i = tid;
-            double acc = j == i ? 1.0 : 0.0;
-            for (int m = j + 1; m <= i; ++m) acc -= Rp[j][m] * Ri[m][i];
-            Ri[j][i] = acc / Rp[j][j];
-        } else if (tid < j) {
-            Ri[j][tid] = 0.0;
+    if (tid < k) {
+        const int i = tid;
+        for (int j = k - 1; j >= 0; --j) {
+            if (j <= i) {
+                double acc = j == i ? 1.0 : 0.0;
+                for (int m = j + 1; m <= i; ++m) acc -= Rp[j][m] * Ri[m][i];
+                Ri[j][i] = acc / Rp[j][j];
+            } else {
+                Ri[j][i] = 0.0;
+            }
         }
-        __syncthreads();
     }
+    __syncthreads();
 }
 
 // Z = Ri^T W[piv] with W and Z in the same LDS rows (rows >= k of Z zero).  Thread tid
-// forms column tid % d of rows tid / d, tid / d + BT / d, ... (a product with one W load
-// per term row), reads every row of W before a barrier, then writes.
-__device__ inline void apply_rinv_t(float (*W)[128 + 1], const double (*Ri)[KL + 1], const int *piv, int k, int d,
-                                    int tid) {
-    constexpr int NR = KL * 128 / BT;                           // output rows per thread (d = 128)
-    const int c = tid % d, h = tid / d, step = BT / d;
-    double acc[NR];
+// forms the 5 x CW block of Z at rows 5 (tid / 32), columns CW (tid % 32) (CW = d / 32),
+// each entry summed over i in order, reads every row of W before a barrier, then writes.
+template <int CW>
+__device__ inline void apply_rinv_t_cw(float (*W)[128 + 4], const double (*Ri)[KL + 1], const int *piv, int k,
+                                       int tid) {
+    const int j0 = 5 * (tid >> 5), c0 = CW * (tid & 31);
+    double acc[5][CW];
 #pragma unroll
-    for (int u = 0; u < NR; ++u) acc[u] = 0.0;
+    for (int jj = 0; jj < 5; ++jj)
+#pragma unroll
+        for (int cc = 0; cc < CW; ++cc) acc[jj][cc] = 0.0;
     for (int i = 0; i < k; ++i) {
-        const double w = double(W[piv[i]][c]);
+        double w[CW];
+        if constexpr (CW == 4) {
+            const float4 v = *reinterpret_cast<const float4 *>(&W[piv[i]][c0]);
+            w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+        } else {
+            const float2 v = *reinterpret_cast<const float2 *>(&W[piv[i]][c0]);
+            w[0] = v.x; w[1] = v.y;
+        }
 #pragma unroll
-        for (int u = 0; u < NR; ++u) {
-            const int j = h + step * u;
-            if (j < KL && j >= i) acc[u] += Ri[i][j] * w;
+        for (int jj = 0; jj < 5; ++jj) {
+            const int j = j0 + jj;
+            if (j >= i) {
+                const double r = Ri[i][j];
+#pragma unroll
+                for (int cc = 0; cc < CW; ++cc) acc[jj][cc] += r * w[cc];
+            }
         }
     }
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < NR; ++u) {
-        const int j = h + step * u;
-        if (j < KL) W[j][c] = j < k ? float(acc[u]) : 0.0f;
+    for (int jj = 0; jj < 5; ++jj) {
+        const int j = j0 + jj;
+#pragma unroll
+        for (int cc = 0; cc < CW; ++cc) W[j][c0 + cc] = j < k ? float(acc[jj][cc]) : 0.0f;
     }
+}
+__device__ inline void apply_rinv_t(float (*W)[128 + 4], const double (*Ri)[KL + 1], const int *piv, int k, int d,
+                                    int tid) {
+    if (d == 128) apply_rinv_t_cw<4>(W, Ri, piv, k, tid);
+    else apply_rinv_t_cw<2>(W, Ri, piv, k, tid);
 }
 
 // Phase marks of the diagnostic trace (builds with SEKV_PHASE_TRACE): slot 0 holds the
@@ -739,12 +761,45 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
         apply_rinv_t(sm.bm, sm.u.s.rg, sm.piv, kk, d, tid);
         __syncthreads();
         SV_STAMP(it == 0 ? kSvForward : kSvForward2);
-        for (int idx = tid; idx < l * l; idx += BT) {       // rows >= kk of B are zero
-            const int i = idx / l, j = idx % l;
-            double acc = 0.0;
-            if (i < kk && j < kk)
-                for (int c = 0; c < d; ++c) acc += double(sm.bm[i][c]) * double(sm.bm[j][c]);
-            sm.am[i][j] = acc;
+        {   // B B^T (rows >= kk of B are zero): thread tid < 200 forms the 2 x 4 block at
+            // rows 2 (tid / 10), columns 4 (tid % 10), each entry summed over c in order
+            constexpr int GJ = KL / 4;
+            if (tid < (KL / 2) * GJ) {
+                const int i0 = 2 * (tid / GJ), jj0 = 4 * (tid % GJ);
+                double acc[2][4];
+#pragma unroll
+                for (int a2 = 0; a2 < 2; ++a2)
+#pragma unroll
+                    for (int b4 = 0; b4 < 4; ++b4) acc[a2][b4] = 0.0;
+                const int ilim = min(2, max(0, kk - i0)), jlim = min(4, max(0, kk - jj0));
+                if (ilim > 0 && jlim > 0) {
+                    for (int c = 0; c < d; c += 4) {
+                        float4 vi[2], vj[4];
+#pragma unroll
+                        for (int a2 = 0; a2 < 2; ++a2)
+                            vi[a2] = *reinterpret_cast<const float4 *>(&sm.bm[i0 + a2][c]);
+#pragma unroll
+                        for (int b4 = 0; b4 < 4; ++b4)
+                            vj[b4] = *reinterpret_cast<const float4 *>(&sm.bm[jj0 + b4][c]);
+#pragma unroll
+                        for (int a2 = 0; a2 < 2; ++a2)
+#pragma unroll
+                            for (int b4 = 0; b4 < 4; ++b4) {
+                                acc[a2][b4] += double(vi[a2].x) * double(vj[b4].x);
+                                acc[a2][b4] += double(vi[a2].y) * double(vj[b4].y);
+                                acc[a2][b4] += double(vi[a2].z) * double(vj[b4].z);
+                                acc[a2][b4] += double(vi[a2].w) * double(vj[b4].w);
+                            }
+                    }
+                }
+#pragma unroll
+                for (int a2 = 0; a2 < 2; ++a2)
+#pragma unroll
+                    for (int b4 = 0; b4 < 4; ++b4) {
+                        const int i = i0 + a2, j = jj0 + b4;
+                        if (i < l && j < l) sm.am[i][j] = (a2 < ilim && b4 < jlim) ? acc[a2][b4] : 0.0;
+                    }
+            }
         }
         __syncthreads();
         SV_STAMP(it == 0 ? kSvGram : kSvGram2);
