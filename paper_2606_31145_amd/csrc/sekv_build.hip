@@ -369,20 +369,25 @@ __device__ void jacobi(double (*A)[KL + 1], double (*V)[KL + 1], SvdSmem &sm, in
     for (int sweep = 0; sweep < sweeps; ++sweep) {
         const int par = sweep & 1;
         for (int k = 0; k < n - 1; ++k) {
+            double c = 1.0, s = 0.0;
             if (lane < np) {
                 const uint32_t pq = sm.jpq[k][lane];
                 const int p = pq & 255, q = pq >> 8;
                 const double app = cur[p][p], aqq = cur[q][q], apq = cur[p][q];
-                double c = 1.0, s = 0.0;
-                if (fabs(apq) > 1e-10 * sqrt(fabs(app) * fabs(aqq)) && apq != 0.0) {
-                    const double th = (aqq - app) / (2.0 * apq);
-                    const double t = (th >= 0.0 ? 1.0 : -1.0) / (fabs(th) + sqrt(1.0 + th * th));
-                    c = 1.0 / sqrt(1.0 + t * t);
-                    s = t * c;
-                    sm.nconv[par] = 1;
-                }
-                sm.jcs[wave][lane] = make_double2(c, s);
+                // the test and the rotation side by side (no branch between them): when
+                // the test fails, the rotation (possibly of a zero apq) is dropped
+                const bool rot = fabs(apq) > 1e-10 * sqrt(fabs(app) * fabs(aqq)) && apq != 0.0;
+                const double th = (aqq - app) / (2.0 * apq);
+                const double t = (th >= 0.0 ? 1.0 : -1.0) / (fabs(th) + sqrt(1.0 + th * th));
+                const double cr = 1.0 / sqrt(1.0 + t * t);
+                if (rot) { c = cr; s = t * cr; }
             }
+            // a round that rotates no pair leaves A and V as they are (its update would
+            // copy them exactly): every wave sees the same rotations, so all skip it
+            // together, with no barrier and no change of copy
+            if (__ballot(s != 0.0) == 0) continue;
+            if (lane == 0) sm.nconv[par] = 1;
+            if (lane < np) sm.jcs[wave][lane] = make_double2(c, s);
             __builtin_amdgcn_wave_barrier();
             if (tid < nblk) {
                 const uint32_t pqI = sm.jpq[k][bI], pqJ = sm.jpq[k][bJ];
