@@ -106,8 +106,9 @@ def parse():
     ap.add_argument("--power", type=int, default=1, help="prefill128k: subspace iterations")
     ap.add_argument("--phase-trace", metavar="OUT_MD", default=None,
                     help="diagnostic: load the phase-trace build (libsekv_trace.so), trace the "
-                         "work items of a few steps of the workload and write a per-phase "
-                         "percentile table to OUT_MD; prints no benchmark line")
+                         "work items of a few steps of the workload (of one build for "
+                         "prefill128k) and write a per-phase percentile table to OUT_MD; prints "
+                         "no benchmark line")
     ap.add_argument("--trace-reps", type=int, default=3)
     ap.add_argument("--distinct-layers", type=int, default=32,
                     help="layers32: independently seeded layers generated on the host; the "
@@ -746,6 +747,9 @@ def bench_prefill(args, dev):
         seg_ms.append(ev[0].elapsed_time(ev[1]))
         build_ms.append(ev[1].elapsed_time(ev[2]))
     assert ws.status() == 0
+    if args.phase_trace:
+        builder_phase_trace(args, bd, keys, values, H, n_tok, seg2, omega, lay, cache, block_off, ws, dev)
+        return
     tokens = B * N
     kern_ms = float(np.mean(seg_ms)) + float(np.mean(build_ms))
     span_tokens = int(sum(int(cache["span_len"][b, :int(lay["n_spans"][b])].sum().item()) for b in range(B)))
@@ -790,6 +794,60 @@ def bench_prefill(args, dev):
                 "GB_s_kv_once": round((kv_bytes + out_bytes) / (kern_ms * 1e-3) / 1e9, 1)},
     }
     print(json.dumps(line), flush=True)
+
+
+BUILD_PHASES = [("sketch pass", 2), ("Cholesky", 3), ("R^-1, B", 4), ("B B^T", 5),
+                ("iteration (Cholesky + R2^-1 + basis)", 6), ("last pass", 7), ("Cholesky", 8),
+                ("R^-1, B", 9), ("B B^T", 10), ("Jacobi", 11), ("V rows", 12), ("T", 13), ("U pass", 14)]
+
+
+def builder_phase_trace(args, bd, keys, values, H, n_tok, seg, omega, lay, cache, block_off, ws, dev):
+    """One build_cache of the trace build with a phase-trace buffer: per span side, the time
+    of each phase of the randomized SVD (percentiles over the span sides of the layer)."""
+    import numpy as np
+    import torch
+
+    from paper_2606_31145_amd import sekv
+    slots = 16
+    items = 2 * bd.batch * bd.n_kv_heads * int(lay["max_spans"])
+    buf = torch.zeros(items * slots, dtype=torch.int64, device=dev)
+    sekv.phase_trace(buf)
+    sekv.build_cache(bd, keys, values, H, n_tok, seg, omega, lay["max_anchors"], lay["max_spans"], block_off,
+                     lay["factors_bytes"], ws, out=cache)
+    torch.cuda.synchronize()
+    sekv.phase_trace(None)
+    assert ws.status() == 0
+    t = buf.cpu().numpy().reshape(items, slots)
+    t = t[t[:, 1] > 0]
+    L = t[:, 0].astype(np.float64)
+
+    def pct(x):
+        return "".join(f"| {v:.1f} " for v in np.percentile(x, [10, 50, 90]))
+
+    lines = ["# Phase trace of the SVD kernel (trace build), one 128K x 4 layer", "",
+             "Per span side, microseconds between the phase marks (the device's 100 MHz real-time "
+             "counter, stamped by thread 0 of the span side's workgroup; trace build "
+             "`libsekv_trace.so`, same sources compiled with `SEKV_PHASE_TRACE`).  Columns: "
+             "percentiles 10 / 50 / 90 over the span sides.", "",
+             f"Command: `python bench.py --workload prefill128k --phase-trace OUT.md`"
+             + (f" `--power {args.power}`" if args.power != 1 else ""), "",
+             f"{len(t)} span sides; |S| p10 / p50 / p90: {np.percentile(L, 10):.0f} / "
+             f"{np.percentile(L, 50):.0f} / {np.percentile(L, 90):.0f} tokens.", "",
+             "| phase | p10 | p50 | p90 |", "|---|---|---|---|"]
+    prev = t[:, 1]
+    for label, slot in BUILD_PHASES:
+        cur = t[:, slot]
+        ok = cur > 0
+        lines.append(f"| {label} " + pct((cur[ok] - prev[ok]) * 0.01) + "|")
+        prev = np.where(ok, cur, prev)
+    lines.append("| whole span side " + pct((t[:, 14] - t[:, 1]) * 0.01) + "|")
+    lines.append("")
+    lines.append(f"First start to last end: {(t[:, 14].max() - t[:, 1].min()) * 0.01:.0f} us.")
+    text = "\n".join(lines) + "\n"
+    with open(args.phase_trace, "w") as f:
+        f.write(text)
+    log(text)
+    print(json.dumps({"phase_trace": args.phase_trace, "span_sides": int(len(t))}), flush=True)
 
 
 def bench_hosttier_layers(args, dev):
@@ -878,7 +936,8 @@ def bench_hosttier_layers(args, dev):
 
 TRACE_ROUTE = [("start", 1), ("k rows loaded", 3), ("scored", 4), ("chunk sorted", 5),
                ("candidates published", 6), ("end", 2)]
-TRACE_SHARE = [("start", 1), ("anchors folded", 3), ("selection known", 4),
+TRACE_SHARE = [("start", 1), ("anchors folded", 3), ("first candidate poll answered", 13),
+               ("selection known", 4),
                ("zoom: first factor loads issued", 5), ("zoom: mid fold done", 6),
                ("zoom: Vt_K q done", 7), ("zoom: token blocks done", 8), ("zoom: done", 9),
                ("summary share done", 10), ("partial written", 11), ("merged", 12), ("end", 2)]
@@ -935,6 +994,10 @@ def phase_trace(args, step, n_rot, dev, what):
             sel = kind == (0 if nm == "routing" else 1)
             for label, slot in table:
                 lines.append(f"| {nm} | {label} " + pct(rel[sel, slot - 1]) + "|")
+        polls = tr[kind == 1, 14].astype(np.float64)
+        polls = polls[polls > 0]
+        if len(polls):
+            lines.append("| share | candidate polls (count, not us) " + pct(polls) + "|")
         lines.append("")
     text = "\n".join(lines) + "\n"
     with open(args.phase_trace, "w") as f:

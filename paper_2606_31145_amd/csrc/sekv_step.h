@@ -270,6 +270,8 @@ enum : int {
     // share item
     kTrSAnchors = 3, kTrSSelected = 4, kTrSZoomIssued = 5, kTrSZoomMid = 6, kTrSZoomW = 7,
     kTrSZoomTokens = 8, kTrSZoomDone = 9, kTrSCoarse = 10, kTrSPartial = 11, kTrSMerged = 12,
+    kTrSPolled = 13,    // the first poll of the candidate records answered
+    kTrSPolls = 14,     // a count, not a time: polls until every record was current
 };
 #ifdef SEKV_PHASE_TRACE
 __device__ inline uint32_t xcc_id() {
@@ -295,9 +297,15 @@ __device__ inline uint32_t xcc_id() {
             (P).trace[size_t((SM).trace_item) * kTraceSlots + (SLOT)] =                       \
                 int64_t(__builtin_amdgcn_s_memrealtime());                                    \
     } while (0)
+#define SEKV_NOTE(P, SM, SLOT, V)                                                             \
+    do {                                                                                      \
+        if (threadIdx.x == 0 && (P).trace)                                                    \
+            (P).trace[size_t((SM).trace_item) * kTraceSlots + (SLOT)] = int64_t(V);           \
+    } while (0)
 #else
 #define SEKV_TRACE_BEGIN(P, SM, ITEM) do {} while (0)
 #define SEKV_STAMP(P, SM, SLOT) do {} while (0)
+#define SEKV_NOTE(P, SM, SLOT, V) do {} while (0)
 #endif
 
 // Tagged words: payload in the low half, the launch tag in the high half.
@@ -1626,7 +1634,13 @@ __device__ __forceinline__ bool share_item(const Params &p, Smem<T, D, G> &sm, i
         for (uint32_t it = 0;; ++it) {
             bool ok = load_candidates(p, pair, tag, okey, oidx, olen, ooff, tid);
             ok &= coarse_logits<T, D, G>(p, sm, pair, c_lo, nc0, tag, tid);
-            if (__syncthreads_and(ok)) { done = true; break; }
+            const bool all = __syncthreads_and(ok);
+            if (it == 0) SEKV_STAMP(p, sm, kTrSPolled);
+            if (all) {
+                SEKV_NOTE(p, sm, kTrSPolls, it + 1);
+                done = true;
+                break;
+            }
             if (it >= kSpinLimit) {
                 if (tid == 0) flag_error(p, kErrSpinTimeout);
                 break;
