@@ -620,16 +620,43 @@ __device__ __forceinline__ void final_merge(const Params &p, Smem<T, D, G> &sm, 
     }
 }
 
+// Shutdown of a launch, by the last workgroup out: zero the counters and advance the epoch
+// (0 marks unwritten words).
+__device__ inline void shutdown(const Params &p, uint32_t tag, int tid) {
+    const int P = p.B * p.Hkv;
+    for (int i = tid; i < P; i += NT) {
+        p.route_cnt[i] = 0u;
+        p.sel_ready[i] = 0u;
+        p.part_cnt[i] = 0u;
+    }
+    if (tid == 0) {
+        p.hdr->exit_count = 0u;
+        st_shared(&p.hdr->epoch, tag + 1u == 0u ? 1u : tag + 1u);
+    }
+}
+
 // Count one finished partial of `pair` (written, stores completed by every wave); the
-// item completing the pair merges.
+// item completing the pair merges.  In the workgroup's last item (`leave`) the workgroup
+// also counts itself out here, once the partial's count has returned (so every counter it
+// touches is final), and the round trip of that count overlaps the merge; the last
+// workgroup out shuts the launch down.  After this point the workgroup reads only untagged
+// partials, so the shutdown may overlap another workgroup's merge.
 template <class T, int D, int G>
-__device__ inline void count_partial(const Params &p, Smem<T, D, G> &sm, int pair, int tid) {
+__device__ inline void count_partial(const Params &p, Smem<T, D, G> &sm, int pair, int tid, bool leave,
+                                     uint32_t tag) {
     if (tid == 0) {
         const uint32_t prev = counter_add(&p.part_cnt[pair], 1u);
         sm.bcast[0] = (prev + 1u == uint32_t(p.n_zi));
     }
     __syncthreads();
+    uint32_t out = 0u;
+    if (leave && tid == 0) out = counter_add(&p.hdr->exit_count, 1u);
     if (sm.bcast[0]) final_merge<T, D, G>(p, sm, pair, tid);
+    if (leave) {
+        if (tid == 0) sm.bcast[3] = (out == uint32_t(p.grid - 1));
+        __syncthreads();
+        if (sm.bcast[3]) shutdown(p, tag, tid);
+    }
     __syncthreads();
 }
 
@@ -1556,7 +1583,7 @@ __device__ __forceinline__ void zoom_span(const Params &p, Smem<T, D, G> &sm, in
 // (help_route) and runs the item again from the start.
 template <class T, int D, int G>
 __device__ __forceinline__ bool share_item(const Params &p, Smem<T, D, G> &sm, int pair, int j,
-                                           uint32_t tag, int tid, bool first, bool may_give_up) {
+                                           uint32_t tag, int tid, bool first, bool may_give_up, bool leave) {
     using GE = Geo<T, D>;
     using SM = Smem<T, D, G>;
     constexpr int NJ = SM::NJ, NJA = SM::NJA, AB = SM::AB, CB = SM::CB;
@@ -1765,7 +1792,7 @@ __device__ __forceinline__ bool share_item(const Params &p, Smem<T, D, G> &sm, i
     write_partial<T, D, G>(p, sm, pair, j, tid);
     stores_done_barrier();
     SEKV_STAMP(p, sm, kTrSPartial);
-    count_partial<T, D, G>(p, sm, pair, tid);
+    count_partial<T, D, G>(p, sm, pair, tid, leave, tag);
     SEKV_STAMP(p, sm, kTrSMerged);
     return false;
 }
@@ -1785,6 +1812,7 @@ __global__ void __launch_bounds__(NT, G == 8 ? 1 : 2) sekv_step_kernel(Params p)
     // then share items, which wait only for routing chunks and take over any chunk whose
     // owner has not started (help_route), so no wait depends on residency.
     int helps = 0;                                      // help rounds of the current item
+    bool left = false;                                  // counted out in its last share item
     for (int item = blockIdx.x; item < n_items;) {
         // an opaque copy of the thread index keeps per-thread address arithmetic inside
         // each item instead of alive across the whole loop (register pressure)
@@ -1796,35 +1824,29 @@ __global__ void __launch_bounds__(NT, G == 8 ? 1 : 2) sekv_step_kernel(Params p)
         } else {
             const int i = item - p.end_route;                // slot-major
             const int P = p.B * p.Hkv;
+            const bool leave = item + p.grid >= n_items;
             if (share_item<T, D, G>(p, sm, i % P, i / P, tag, t, item == int(blockIdx.x) && helps == 0,
-                                    helps < kMaxHelps)) {
+                                    helps < kMaxHelps, leave)) {
                 help_route<T, D, G>(p, sm, i % P, tag, t);
                 ++helps;
                 continue;                                    // the same item again
             }
+            left = leave;
         }
         SEKV_STAMP(p, sm, kTrEnd);
         __syncthreads();
         helps = 0;
         item += p.grid;
     }
-    // shutdown: the last workgroup out zeroes the counters and advances the epoch
-    if (tid == 0) {
-        const uint32_t prev = counter_add(&p.hdr->exit_count, 1u);
-        sm.bcast[3] = (prev == uint32_t(p.grid - 1));
-    }
-    __syncthreads();
-    if (sm.bcast[3]) {
-        const int P = p.B * p.Hkv;
-        for (int i = tid; i < P; i += NT) {
-            p.route_cnt[i] = 0u;
-            p.sel_ready[i] = 0u;
-            p.part_cnt[i] = 0u;
-        }
+    // a workgroup whose last item was a routing item (or that had none) counts itself out
+    // here; the last workgroup out zeroes the counters and advances the epoch
+    if (!left) {
         if (tid == 0) {
-            p.hdr->exit_count = 0u;
-            st_shared(&p.hdr->epoch, tag + 1u == 0u ? 1u : tag + 1u);   // 0 marks unwritten words
+            const uint32_t prev = counter_add(&p.hdr->exit_count, 1u);
+            sm.bcast[3] = (prev == uint32_t(p.grid - 1));
         }
+        __syncthreads();
+        if (sm.bcast[3]) shutdown(p, tag, tid);
     }
 }
 
