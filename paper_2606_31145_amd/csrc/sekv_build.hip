@@ -633,31 +633,42 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
         const int j = idx / d, c = idx % d;
         sm.u.p.om[j][c] = uint16_t(bf16_bits(a.omega[size_t(c) * a.l + j]));
     }
-    // one tile of X rows [t0, t0 + nt) and its sketch rows
-    auto tile = [&](int t0, int nt) {
+    // the X rows of tile [t0, t0 + nt) as this thread's 16-byte pieces (rows past nt zero);
+    // fetched one tile ahead, so that a tile's loads are in flight while the one before is used
+    constexpr int NQ = 2;                                    // pieces per thread (f32, d = 128)
+    auto tile_fetch = [&](int t0, int nt, uint4 (&q)[NQ]) __attribute__((always_inline)) {
         const int per = 16 / e;                              // elements per 16-byte load
-        for (int i = tid; i < kTile * d / per; i += BT) {
+#pragma unroll
+        for (int u = 0; u < NQ; ++u) {
+            const int i = tid + BT * u;
             const int t = i / (d / per), c = (i % (d / per)) * per;
-            float v[8];
-            if (t < nt) {
-                const uint4 q = *reinterpret_cast<const uint4 *>(
+            q[u] = make_uint4(0u, 0u, 0u, 0u);
+            if (i < kTile * d / per && t < nt)
+                q[u] = *reinterpret_cast<const uint4 *>(
                     static_cast<const unsigned char *>(src) + ((row0 + t0 + t) * d + c) * e);
-                const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+        }
+    };
+    // one fetched tile of X rows into LDS (float32), and its sketch rows
+    auto tile = [&](const uint4 (&q)[NQ]) __attribute__((always_inline)) {
+        const int per = 16 / e;
+#pragma unroll
+        for (int u = 0; u < NQ; ++u) {
+            const int i = tid + BT * u;
+            if (i < kTile * d / per) {
+                const int t = i / (d / per), c = (i % (d / per)) * per;
+                const uint32_t w[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
+                float *xr = &sm.u.p.x[t][c];
                 if (e == 2) {
 #pragma unroll
                     for (int h = 0; h < 4; ++h) {
-                        v[2 * h] = __uint_as_float(w[h] << 16);
-                        v[2 * h + 1] = __uint_as_float(w[h] & 0xFFFF0000u);
+                        xr[2 * h] = __uint_as_float(w[h] << 16);
+                        xr[2 * h + 1] = __uint_as_float(w[h] & 0xFFFF0000u);
                     }
                 } else {
 #pragma unroll
-                    for (int h = 0; h < 4; ++h) v[h] = __uint_as_float(w[h]);
+                    for (int h = 0; h < 4; ++h) xr[h] = __uint_as_float(w[h]);
                 }
-            } else {
-#pragma unroll
-                for (int h = 0; h < 8; ++h) v[h] = 0.0f;
             }
-            for (int h = 0; h < per; ++h) sm.u.p.x[t][c + h] = v[h];
         }
         __syncthreads();
         {   // Y rows: thread (t, jb) forms Y[t][jb], Y[t][jb + 16], Y[t][jb + 32], summing
@@ -691,7 +702,7 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
     // tid owns the 5 x CW block of P at rows 5 (tid / 32), columns CW (tid % 32) (CW = d / 32)
     // and, for tid < 200, the 2 x 4 block of G at rows 2 (tid / 10), columns 4 (tid % 10);
     // sums over blocks past l are dropped.
-    auto sketch_pass = [&](auto cw_c) {
+    auto sketch_pass = [&](auto cw_c) __attribute__((always_inline)) {
         constexpr int CW = decltype(cw_c)::value;
         constexpr int GI = KL / 2, GJ = KL / 4;               // G blocks: GI x GJ of 2 x 4
         const int j0 = 5 * (tid >> 5), c0 = CW * (tid & 31);
@@ -708,9 +719,15 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
 #pragma unroll
             for (int b4 = 0; b4 < 4; ++b4) gacc[a2][b4] = 0.0;
         __syncthreads();
+        uint4 qn[NQ];
+        tile_fetch(0, min(kTile, L), qn);
         for (int t0 = 0; t0 < L; t0 += kTile) {
             const int nt = min(kTile, L - t0);
-            tile(t0, nt);
+            uint4 q[NQ];
+#pragma unroll
+            for (int u = 0; u < NQ; ++u) q[u] = qn[u];
+            if (t0 + kTile < L) tile_fetch(t0 + kTile, min(kTile, L - t0 - kTile), qn);
+            tile(q);
             for (int t = 0; t < nt; ++t) {
                 float xv[CW];
                 if constexpr (CW == 4) {
@@ -753,13 +770,13 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
                     if (i0 + a2 < l && jj0 + b4 < l) sm.am[i0 + a2][jj0 + b4] = gacc[a2][b4];
         __syncthreads();
     };
-    auto sketch = [&]() {
+    auto sketch = [&]() __attribute__((always_inline)) {
         if (d == 128) sketch_pass(Cint<4>{});
         else sketch_pass(Cint<2>{});
     };
     // after a pass: G = R^T R (pivoted) into rg, B = R^-T P[piv] over P, B B^T into am;
     // rg then holds R^-1 (pivot order)
-    auto factor_b = [&](int it) -> int {
+    auto factor_b = [&](int it) __attribute__((always_inline)) -> int {
         const int kk = piv_chol(sm.am, sm.u.s.rg, sm.piv, sm, l, 1e-8, tid);
         SV_STAMP(it == 0 ? kSvChol : kSvChol2);
         tri_inverse(sm.u.s.rg, sm.piv, sm.am, sm.u.s.rg, kk, tid);
@@ -909,9 +926,15 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
         }
     }
     __syncthreads();
+    uint4 qn[NQ];
+    tile_fetch(0, min(kTile, L), qn);
     for (int t0 = 0; t0 < L; t0 += kTile) {
         const int nt = min(kTile, L - t0);
-        tile(t0, nt);
+        uint4 q[NQ];
+#pragma unroll
+        for (int u = 0; u < NQ; ++u) q[u] = qn[u];
+        if (t0 + kTile < L) tile_fetch(t0 + kTile, min(kTile, L - t0 - kTile), qn);
+        tile(q);
         for (int idx = tid; idx < nt * rs; idx += BT) {
             const int t = idx / rs, i = idx % rs;
             double v = 0.0;
