@@ -306,6 +306,7 @@ struct SvdSmem {
     double sig[KL];
     double dg[2][KL];                         // remaining Cholesky diagonal (two copies)
     int piv[KL], piv2[KL], order[KL];
+    int pos[KL];                              // U pass: column of sketch column m (pivot order)
     int nconv[2];
 };
 
@@ -649,7 +650,7 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
         }
     };
     // one fetched tile of X rows into LDS (float32), and its sketch rows
-    auto tile = [&](const uint4 (&q)[NQ]) __attribute__((always_inline)) {
+    auto tile = [&](const uint4 (&q)[NQ], const int *cmap) __attribute__((always_inline)) {
         const int per = 16 / e;
 #pragma unroll
         for (int u = 0; u < NQ; ++u) {
@@ -691,9 +692,10 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
                 a0 += xv.z * lo(w0.y); a1 += xv.z * lo(w1.y); a2 += xv.z * lo(w2.y);
                 a0 += xv.w * hi(w0.y); a1 += xv.w * hi(w1.y); a2 += xv.w * hi(w2.y);
             }
-            if (jb < l) sm.u.p.yt[t][jb] = a0;
-            if (jb + 16 < l) sm.u.p.yt[t][jb + 16] = a1;
-            if (jb + 32 < l) sm.u.p.yt[t][jb + 32] = a2;
+            // column j of Y goes to column cmap[j] of yt (the identity without a map)
+            if (jb < l) sm.u.p.yt[t][cmap ? cmap[jb] : jb] = a0;
+            if (jb + 16 < l) sm.u.p.yt[t][cmap ? cmap[jb + 16] : jb + 16] = a1;
+            if (jb + 32 < l) sm.u.p.yt[t][cmap ? cmap[jb + 32] : jb + 32] = a2;
         }
         __syncthreads();
     };
@@ -727,7 +729,7 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
 #pragma unroll
             for (int u = 0; u < NQ; ++u) q[u] = qn[u];
             if (t0 + kTile < L) tile_fetch(t0 + kTile, min(kTile, L - t0 - kTile), qn);
-            tile(q);
+            tile(q, nullptr);
             for (int t = 0; t < nt; ++t) {
                 float xv[CW];
                 if constexpr (CW == 4) {
@@ -915,6 +917,15 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
     }
     __syncthreads();
     SV_STAMP(kSvT);
+    // the U pass writes Y's columns in pivot order: column piv[j] to j (j < k), the other
+    // columns after them
+    if (tid == 0) {
+        int nxt = k;
+        for (int m = 0; m < l; ++m) sm.pos[m] = -1;
+        for (int j = 0; j < k; ++j) sm.pos[sm.piv[j]] = j;
+        for (int m = 0; m < l; ++m)
+            if (sm.pos[m] < 0) sm.pos[m] = nxt++;
+    }
     // last pass over X: U rows = Y[:, piv] T with the kept test matrix
 #pragma unroll
     for (int u = 0; u < NO; ++u) {
@@ -934,13 +945,35 @@ __global__ void __launch_bounds__(BT, 2) svd_kernel(BuildArgs a) {
 #pragma unroll
         for (int u = 0; u < NQ; ++u) q[u] = qn[u];
         if (t0 + kTile < L) tile_fetch(t0 + kTile, min(kTile, L - t0 - kTile), qn);
-        tile(q);
-        for (int idx = tid; idx < nt * rs; idx += BT) {
-            const int t = idx / rs, i = idx % rs;
-            double v = 0.0;
-            if (i < r)
-                for (int j = 0; j < k; ++j) v += double(sm.u.p.yt[t][sm.piv[j]]) * sm.am[j][i];
-            st_elem(blk, size_t(t0 + t) * rs + i, float(v), e);
+        tile(q, sm.pos);
+        {   // thread (t, ig) forms U[t][ig + 16 o], o < 3, summing over j in order; yt holds
+            // Y's columns in pivot order, four per LDS read
+            const int t = tid >> 4, ig = tid & 15;
+            if (t < nt) {
+                double v[3] = {0.0, 0.0, 0.0};
+                const float *yr = sm.u.p.yt[t];
+                int j = 0;
+                for (; j + 4 <= k; j += 4) {
+                    const float4 y4 = *reinterpret_cast<const float4 *>(yr + j);
+                    const float yy[4] = {y4.x, y4.y, y4.z, y4.w};
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                        for (int o = 0; o < 3; ++o)
+                            if (ig + 16 * o < r) v[o] += double(yy[jj]) * sm.am[j + jj][ig + 16 * o];
+                }
+                for (; j < k; ++j) {
+                    const float y = yr[j];
+#pragma unroll
+                    for (int o = 0; o < 3; ++o)
+                        if (ig + 16 * o < r) v[o] += double(y) * sm.am[j][ig + 16 * o];
+                }
+#pragma unroll
+                for (int o = 0; o < 3; ++o) {
+                    const int i = ig + 16 * o;
+                    if (i < rs) st_elem(blk, size_t(t0 + t) * rs + i, i < r ? float(v[o]) : 0.0f, e);
+                }
+            }
         }
         __syncthreads();
     }
