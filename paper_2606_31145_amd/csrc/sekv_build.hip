@@ -513,13 +513,15 @@ __device__ inline void tri_inverse(const double (*Rm)[KL + 1], const int *piv, d
     if (tid < k) {
         const int i = tid;
         for (int j = k - 1; j >= 0; --j) {
-            if (j <= i) {
-                double acc = j == i ? 1.0 : 0.0;
-                for (int m = j + 1; m <= i; ++m) acc -= Rp[j][m] * Ri[m][i];
-                Ri[j][i] = acc / Rp[j][j];
-            } else {
-                Ri[j][i] = 0.0;
+            // the same trip count in every lane (terms past the lane's diagonal are not
+            // added), so the loop's LDS reads can be issued ahead of the sums
+            double acc = j == i ? 1.0 : 0.0;
+#pragma unroll 4
+            for (int m = j + 1; m < k; ++m) {
+                const double t = acc - Rp[j][m] * Ri[m][i];
+                acc = m <= i ? t : acc;
             }
+            Ri[j][i] = j <= i ? acc / Rp[j][j] : 0.0;
         }
     }
     __syncthreads();
