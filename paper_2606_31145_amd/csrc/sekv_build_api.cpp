@@ -11,29 +11,10 @@
 
 namespace {
 
+using sekv::check_build_dims;
 using sekv::fail;
 
 bool misaligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) != 0; }
-
-sekv_status check_build_dims(const sekv_build_dims *d) {
-    if (!d) return fail(SEKV_ERR_INVALID_ARG, "build dims is NULL");
-    if (d->batch < 0 || d->n_kv_heads < 1 || d->max_tokens < 1)
-        return fail(SEKV_ERR_INVALID_ARG, "batch/n_kv_heads/max_tokens out of range");
-    if (d->head_dim != 64 && d->head_dim != 128) return fail(SEKV_ERR_UNSUPPORTED, "head_dim %d", d->head_dim);
-    if (d->dtype != SEKV_BF16 && d->dtype != SEKV_F32) return fail(SEKV_ERR_UNSUPPORTED, "dtype %d", d->dtype);
-    const int gran = 16 / sekv::elem_bytes(d->dtype);
-    if (d->rank < gran || d->rank > 40 || d->rank % gran)
-        return fail(SEKV_ERR_UNSUPPORTED, "rank %d: a multiple of %d in [%d, 40]", d->rank, gran, gran);
-    if (d->sketch < d->rank || d->sketch > 40 || (d->sketch & 1))
-        return fail(SEKV_ERR_UNSUPPORTED, "sketch %d: even, in [rank, 40]", d->sketch);
-    if (d->min_span < 2) return fail(SEKV_ERR_INVALID_ARG, "min_span %d < 2", d->min_span);
-    if (d->window < 0) return fail(SEKV_ERR_INVALID_ARG, "window < 0");
-    if (d->sweeps < 1 || d->sweeps > 32) return fail(SEKV_ERR_INVALID_ARG, "sweeps %d outside [1, 32]", d->sweeps);
-    if (d->power < 0 || d->power > 4) return fail(SEKV_ERR_INVALID_ARG, "power %d outside [0, 4]", d->power);
-    if (d->reserved != 0) return fail(SEKV_ERR_INVALID_ARG, "reserved field is not 0");
-    if (!(d->alpha == d->alpha)) return fail(SEKV_ERR_INVALID_ARG, "alpha is NaN");
-    return SEKV_OK;
-}
 
 size_t seg_ws(const sekv_build_dims &d) {
     const size_t B = size_t(d.batch), N = size_t(d.max_tokens);
@@ -81,40 +62,7 @@ sekv_status sekv_segment(const sekv_build_dims *dims, const float *surprisal, co
 
 int64_t sekv_build_layout(const sekv_build_dims *dims, int32_t max_spans, const int32_t *n_spans,
                           const int32_t *span_len, int64_t *block_off, int32_t *block_rank) {
-    if (check_build_dims(dims) != SEKV_OK) return -1;
-    if (max_spans < 1 || !n_spans || !span_len || !block_off || !block_rank) {
-        fail(SEKV_ERR_INVALID_ARG, "NULL argument or max_spans < 1");
-        return -1;
-    }
-    const int B = dims->batch, Hkv = dims->n_kv_heads, N = dims->max_tokens, d = dims->head_dim;
-    const int e = sekv::elem_bytes(dims->dtype), gran = 16 / e;
-    int64_t pos = 0;
-    for (int b = 0; b < B; ++b) {
-        const int m = n_spans[b];
-        if (m < 0 || m > max_spans || m > N) {
-            fail(SEKV_ERR_INVALID_ARG, "n_spans[%d] = %d outside [0, %d]", b, m, max_spans);
-            return -1;
-        }
-        for (int g = 0; g < Hkv; ++g)
-            for (int S = 0; S < max_spans; ++S) {
-                const size_t i = (size_t(b) * Hkv + g) * max_spans + S;
-                block_off[i] = 0;
-                block_rank[i] = 0;
-                if (S >= m) continue;
-                const int L = span_len[size_t(b) * N + S];
-                if (L < 1 || L > N) {
-                    fail(SEKV_ERR_INVALID_ARG, "span_len[%d][%d] = %d", b, S, L);
-                    return -1;
-                }
-                int r = L < d ? L : d;
-                if (r > dims->rank) r = dims->rank;
-                const int rs = (r + gran - 1) / gran * gran;
-                block_off[i] = pos;
-                block_rank[i] = rs | (rs << 16);
-                pos += int64_t((2 * int64_t(L + 1 + d) * rs * e + 255) / 256 * 256);
-            }
-    }
-    return pos > 0 ? pos : 256;
+    return sekv::build_layout(dims, max_spans, n_spans, span_len, block_off, block_rank);
 }
 
 sekv_status sekv_build_cache(const sekv_build_dims *dims, const void *keys, const void *values,

@@ -86,4 +86,12 @@ class WsTracker {
     uint64_t clock_ = 0;
 };
 
+// ---- prefill-side builder ------------------------------------------------------------
+sekv_status check_build_dims(const sekv_build_dims *d);
+// The factor arena of a segmentation from host copies of n_spans [B] and span_len
+// [B][max_tokens] (sekv_build_layout): block_off and block_rank [B][Hkv][max_spans];
+// returns the arena bytes, or -1 with the error message set.
+int64_t build_layout(const sekv_build_dims *dims, int32_t max_spans, const int32_t *n_spans,
+                     const int32_t *span_len, int64_t *block_off, int32_t *block_rank);
+
 }  // namespace sekv

@@ -1,5 +1,6 @@
 // Host-only checks of the library's host layer (argument validation, the host-side cache
-// check, the pinned-host tier's copy plan and the workspace bookkeeping), built with g++
+// check, the pinned-host tier's copy plan, the workspace bookkeeping and the builder's
+// dims check and factor-arena layout), built with g++
 // under the address and undefined-behaviour sanitizers by tests/test_host_sanitized.py.
 // No GPU and no HIP runtime are involved.  Prints "all host checks passed" on success.
 #include <algorithm>
@@ -288,6 +289,107 @@ void test_ws_tracker() {
     CHECK(t.before_launch(ws, 8192, k2, 1));
 }
 
+
+sekv_build_dims base_build_dims() {
+    sekv_build_dims d{};
+    d.batch = 3; d.n_kv_heads = 2; d.head_dim = 128; d.max_tokens = 700; d.rank = 32; d.sketch = 40;
+    d.min_span = 4; d.window = 16; d.sweeps = 8; d.dtype = SEKV_BF16; d.power = 1; d.reserved = 0;
+    d.alpha = 1.0;
+    return d;
+}
+
+// The builder's dims check and the arena layout from random span tables: blocks in (b, g, S)
+// order, 256-byte aligned, back to back without overlap, each of the size its span and
+// stored rank give, ranks min(|S|, d, R_max) rounded up to the granule, zero entries past
+// n_spans[b]; bad tables and arguments rejected.
+void test_build_layout(std::mt19937 &rng) {
+    sekv_build_dims d = base_build_dims();
+    CHECK(sekv::check_build_dims(&d) == SEKV_OK);
+    CHECK(sekv::check_build_dims(nullptr) == SEKV_ERR_INVALID_ARG);
+    struct Case { int field; int32_t value; sekv_status want; };
+    const Case cases[] = {
+        {0, -1, SEKV_ERR_INVALID_ARG}, {1, 0, SEKV_ERR_INVALID_ARG}, {2, 96, SEKV_ERR_UNSUPPORTED},
+        {3, 0, SEKV_ERR_INVALID_ARG}, {4, 36, SEKV_ERR_UNSUPPORTED}, {4, 48, SEKV_ERR_UNSUPPORTED},
+        {5, 30, SEKV_ERR_UNSUPPORTED}, {5, 39, SEKV_ERR_UNSUPPORTED}, {5, 42, SEKV_ERR_UNSUPPORTED},
+        {6, 1, SEKV_ERR_INVALID_ARG}, {7, -1, SEKV_ERR_INVALID_ARG}, {8, 0, SEKV_ERR_INVALID_ARG},
+        {8, 33, SEKV_ERR_INVALID_ARG}, {9, 7, SEKV_ERR_UNSUPPORTED}, {10, 5, SEKV_ERR_INVALID_ARG},
+        {11, 1, SEKV_ERR_INVALID_ARG},
+    };
+    for (const Case &c : cases) {
+        sekv_build_dims x = d;
+        int32_t *f[] = {&x.batch, &x.n_kv_heads, &x.head_dim, &x.max_tokens, &x.rank, &x.sketch,
+                        &x.min_span, &x.window, &x.sweeps, &x.dtype, &x.power, &x.reserved};
+        *f[c.field] = c.value;
+        CHECK(sekv::check_build_dims(&x) == c.want);
+    }
+    {
+        sekv_build_dims x = d;
+        x.alpha = std::nan("");
+        CHECK(sekv::check_build_dims(&x) == SEKV_ERR_INVALID_ARG);
+    }
+    for (int round = 0; round < 200; ++round) {
+        sekv_build_dims x = d;
+        x.head_dim = (round & 1) ? 64 : 128;
+        x.dtype = (round & 2) ? SEKV_F32 : SEKV_BF16;
+        const int e = x.dtype == SEKV_BF16 ? 2 : 4, gran = 16 / e;
+        x.rank = gran * (1 + int(rng() % unsigned(40 / gran)));
+        x.sketch = std::max(x.rank + (x.rank & 1), 2 * int((x.rank + 1 + rng() % 8) / 2));
+        if (x.sketch > 40) x.sketch = 40;
+        x.batch = 1 + int(rng() % 3);
+        const int B = x.batch, Hkv = x.n_kv_heads, N = x.max_tokens, dd = x.head_dim;
+        const int max_spans = 1 + int(rng() % 12);
+        std::vector<int32_t> ns(B), len(size_t(B) * N, 0);
+        for (int b = 0; b < B; ++b) {
+            ns[b] = int(rng() % unsigned(max_spans + 1));
+            for (int S = 0; S < ns[b]; ++S) len[size_t(b) * N + S] = 1 + int(rng() % unsigned(N));
+        }
+        const size_t nb = size_t(B) * Hkv * max_spans;
+        std::vector<int64_t> off(nb, -7);
+        std::vector<int32_t> rk(nb, -7);
+        const int64_t bytes = sekv::build_layout(&x, max_spans, ns.data(), len.data(), off.data(), rk.data());
+        CHECK(bytes > 0 && bytes % 256 == 0);
+        int64_t pos = 0;
+        for (int b = 0; b < B; ++b)
+            for (int g = 0; g < Hkv; ++g)
+                for (int S = 0; S < max_spans; ++S) {
+                    const size_t i = (size_t(b) * Hkv + g) * max_spans + S;
+                    if (S >= ns[b]) {
+                        CHECK(off[i] == 0 && rk[i] == 0);
+                        continue;
+                    }
+                    const int L = len[size_t(b) * N + S];
+                    const int r = std::min(std::min(L, dd), x.rank);
+                    const int rs = (r + gran - 1) / gran * gran;
+                    CHECK(rk[i] == (rs | (rs << 16)));
+                    CHECK(off[i] == pos && off[i] % 256 == 0);
+                    const int64_t need = 2 * int64_t(L + 1 + dd) * rs * e;
+                    pos += (need + 255) / 256 * 256;
+                    CHECK(off[i] + need <= bytes);
+                }
+        CHECK(bytes == (pos > 0 ? pos : 256));
+        // a span longer than the row stride, an empty span, more spans than max_spans
+        if (ns[0] > 0) {
+            std::vector<int32_t> bad = len;
+            bad[0] = N + 1;
+            CHECK(sekv::build_layout(&x, max_spans, ns.data(), bad.data(), off.data(), rk.data()) == -1);
+            bad[0] = 0;
+            CHECK(sekv::build_layout(&x, max_spans, ns.data(), bad.data(), off.data(), rk.data()) == -1);
+        }
+        std::vector<int32_t> many = ns;
+        many[0] = max_spans + 1;
+        CHECK(sekv::build_layout(&x, max_spans, many.data(), len.data(), off.data(), rk.data()) == -1);
+        many[0] = -1;
+        CHECK(sekv::build_layout(&x, max_spans, many.data(), len.data(), off.data(), rk.data()) == -1);
+    }
+    std::vector<int32_t> ns(3, 0), len(size_t(3) * d.max_tokens, 0);
+    std::vector<int64_t> off(6);
+    std::vector<int32_t> rk(6);
+    CHECK(sekv::build_layout(&d, 1, ns.data(), len.data(), off.data(), rk.data()) == 256);
+    CHECK(sekv::build_layout(&d, 0, ns.data(), len.data(), off.data(), rk.data()) == -1);
+    CHECK(sekv::build_layout(&d, 1, nullptr, len.data(), off.data(), rk.data()) == -1);
+    CHECK(sekv::build_layout(&d, 1, ns.data(), len.data(), nullptr, rk.data()) == -1);
+}
+
 }  // namespace
 
 int main() {
@@ -296,6 +398,7 @@ int main() {
     test_validate_cache(rng);
     test_tier_plan(rng);
     test_ws_tracker();
+    test_build_layout(rng);
     if (g_fail) {
         std::printf("%d host checks failed\n", g_fail);
         return 1;
