@@ -433,14 +433,43 @@ __device__ void jacobi(double (*A)[KL + 1], double (*V)[KL + 1], SvdSmem &sm, in
     __syncthreads();
 }
 
+// Largest 64-bit key over the wave, in every lane: quad and row steps by DPP, then the
+// row and half swaps (permlane16 / permlane32), all without LDS round trips.
+template <int CTRL>
+__device__ inline uint64_t dpp64(uint64_t x) {
+    const uint32_t lo = uint32_t(__builtin_amdgcn_update_dpp(0, int(uint32_t(x)), CTRL, 0xF, 0xF, false));
+    const uint32_t hi = uint32_t(__builtin_amdgcn_update_dpp(0, int(uint32_t(x >> 32)), CTRL, 0xF, 0xF, false));
+    return (uint64_t(hi) << 32) | lo;
+}
+__device__ inline uint64_t max64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+__device__ inline uint64_t wave_max_key(uint64_t x) {
+    x = max64(x, dpp64<0xB1>(x));                               // quad_perm [1,0,3,2]
+    x = max64(x, dpp64<0x4E>(x));                               // quad_perm [2,3,0,1]
+    x = max64(x, dpp64<0x124>(x));                              // row_ror:4
+    x = max64(x, dpp64<0x128>(x));                              // row_ror:8
+    {
+        const auto lo = __builtin_amdgcn_permlane16_swap(uint32_t(x), uint32_t(x), false, false);
+        const auto hi = __builtin_amdgcn_permlane16_swap(uint32_t(x >> 32), uint32_t(x >> 32), false, false);
+        x = max64((uint64_t(hi[0]) << 32) | lo[0], (uint64_t(hi[1]) << 32) | lo[1]);
+    }
+    {
+        const auto lo = __builtin_amdgcn_permlane32_swap(uint32_t(x), uint32_t(x), false, false);
+        const auto hi = __builtin_amdgcn_permlane32_swap(uint32_t(x >> 32), uint32_t(x >> 32), false, false);
+        x = max64((uint64_t(hi[0]) << 32) | lo[0], (uint64_t(hi[1]) << 32) | lo[1]);
+    }
+    return x;
+}
+
 // Cholesky with diagonal pivoting of the symmetric positive semi-definite n x n matrix A
 // (destroyed): step j takes the largest remaining diagonal entry p = piv[j] and stores
 // row j of the factor over the original indices in Rm (Rm[j][piv[i]] = 0 for i < j), so
 // that A ~ Rm^T Rm.  Stops when the largest remaining entry is not above tau times the
 // largest initial diagonal entry; returns the number of steps k.  Ties go to the lower
 // index.  One barrier per step: every wave finds the pivot itself from the remaining
-// diagonal, kept in two alternating copies (-1 marks a row already taken), and every
-// thread keeps the set of taken rows as a bit mask.
+// diagonal, kept in two alternating copies (-1 marks a row already taken): the largest
+// positive entry by a wave maximum of the entries' bits (a positive double's bits order as
+// its value), its lowest row by a ballot; every thread keeps the set of taken rows as a
+// bit mask.
 __device__ int piv_chol(double (*A)[KL + 1], double (*Rm)[KL + 1], int *piv, SvdSmem &sm, int n, double tau,
                         int tid) {
     constexpr int NE = (KL * KL + BT - 1) / BT;
@@ -455,17 +484,14 @@ __device__ int piv_chol(double (*A)[KL + 1], double (*Rm)[KL + 1], int *piv, Svd
     int k = 0;
     for (int j = 0; j < n; ++j) {
         const int cur = j & 1;
-        double v = -1.0;
-        int at = KL;
-        if (lane < n && sm.dg[cur][lane] >= 0.0) { v = sm.dg[cur][lane]; at = lane; }
-        for (int off = 32; off >= 1; off >>= 1) {
-            const double ov = __shfl_xor(v, off);
-            const int oa = __shfl_xor(at, off);
-            if (ov > v || (ov == v && oa < at)) { v = ov; at = oa; }
-        }
+        const double dl = lane < n ? sm.dg[cur][lane] : -1.0;
+        const uint64_t key = dl > 0.0 ? uint64_t(__double_as_longlong(dl)) : 0ull;
+        const uint64_t kmax = wave_max_key(key);
+        if (kmax == 0ull) break;                              // nothing positive remains
+        const double v = __longlong_as_double(static_cast<long long>(kmax));
         if (j == 0) floor_ = tau * v;
-        if (!(v > 0.0 && v > floor_)) break;                  // the same decision in every wave
-        const int p = at;
+        if (!(v > floor_)) break;                             // the same decision in every wave
+        const int p = __ffsll(static_cast<long long>(__ballot(key == kmax))) - 1;
         const double rinv = 1.0 / sqrt(A[p][p]);
         taken |= uint64_t(1) << p;
         if (tid < n) {
