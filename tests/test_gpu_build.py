@@ -204,6 +204,24 @@ def test_build_matches_oracle(S, name, c):
     banner(f"build {name}: worst excess reconstruction error {worst:.2e} of ||X||")
 
 
+@pytest.mark.parametrize("power", [0, 1])
+def test_build_is_deterministic(S, power):
+    """The builder sums in fixed orders only (no atomics in the arithmetic): two builds of
+    the same layer give the same bytes in every output, factors included."""
+    banner(f"build determinism, power {power}")
+    c = dict(dtype="bf16", d=128, Hkv=2, n=[2600, 1900], rank=32, sketch=40, min_span=4, window=64,
+             power=power)
+    p = make_prefill(2, 2, 128, c["n"], dtype="bf16", spike_every=120, true_rank=24, noise=0.05,
+                     sketch=40, seed=78)
+    first, seg1, lay1 = _build(S, p, c)
+    second, seg2, lay2 = _build(S, p, c)
+    assert lay1["factors_bytes"] == lay2["factors_bytes"]
+    for key in seg1:
+        assert np.array_equal(seg1[key], seg2[key]), key
+    for key in first:
+        assert np.array_equal(first[key], second[key]), f"{key} differs between two builds"
+
+
 def test_build_rejects_tables_past_n_tokens(S):
     """Anchor indices and spans past a sequence's own token count are skipped and flagged
     (error bit 4); everything inside is built as usual."""
