@@ -514,8 +514,24 @@ def bench_layers32(args, dev):
                           max_span_len=max(c.max_span_len for c in cases), dtype=spec.dtype,
                           softmax_scale=spec.softmax_scale)
     ws = sekv.Workspace(dims, dev)
-    graph = sekv.LayerGraph(dims, caches, ws)
     stream = torch.cuda.current_stream()
+    if args.phase_trace:
+        B, Hq, Hkv, d = spec.batch, spec.n_q_heads, spec.n_kv_heads, spec.head_dim
+        sel = torch.empty((B, Hkv, spec.top_k), dtype=torch.int32, device=dev)
+        out = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
+
+        def step(i):
+            sekv.decode_step(dims, caches[i % L], ws, sel=sel, out=out, stream=stream)
+
+        for i in range(args.warmup):
+            step(i)
+        torch.cuda.synchronize()
+        assert ws.status() == 0, "device error word set during warmup"
+        phase_trace(args, step, L, dev, "one layer of the 32-layer step (batch 32, 32K context, "
+                    f"rank 16, top-8), variant {args.variant}, launched alone",
+                    extra=f" --workload layers32 --distinct-layers {D} --warmup {args.warmup}")
+        return None
+    graph = sekv.LayerGraph(dims, caches, ws)
     log(f"[bench] 32-layer graph built; warmup {args.warmup}")
     for _ in range(args.warmup):
         graph.launch(stream)
@@ -943,7 +959,7 @@ TRACE_SHARE = [("start", 1), ("anchors folded", 3), ("first candidate poll answe
                ("summary share done", 10), ("partial written", 11), ("merged", 12), ("end", 2)]
 
 
-def phase_trace(args, step, n_rot, dev, what):
+def phase_trace(args, step, n_rot, dev, what, extra=""):
     """Trace the work items of single steps (trace build) and write a percentile table."""
     import numpy as np
     import torch
@@ -977,7 +993,7 @@ def phase_trace(args, step, n_rot, dev, what):
              "real-time counter, stamped by thread 0 of the item's workgroup; trace build "
              "`libsekv_trace.so`, same sources compiled with `SEKV_PHASE_TRACE`).  Columns: "
              "percentiles 0 / 10 / 50 / 90 / 100 over the items of one step.", "",
-             "Command: `python bench.py --phase-trace OUT.md" +
+             "Command: `python bench.py --phase-trace OUT.md" + extra +
              (f" --variant {args.variant}" if args.variant != "L" else "") + "`", ""]
     for r, tr in enumerate(reps):
         kind = tr[:, 0] >> 60

@@ -25,7 +25,8 @@ def S():
 
 
 def _ragged(case: Case) -> Case:
-    """Shrink some sequences: fewer spans, no spans, no anchors (tables only)."""
+    """Shrink some sequences: fewer spans, no spans, no anchors, a third of the anchors
+    (tables only)."""
     B = case.spec.batch
     if B >= 2:
         case.n_spans = case.n_spans.copy()
@@ -36,6 +37,8 @@ def _ragged(case: Case) -> Case:
             case.n_spans[2] = max(1, int(case.n_spans[2]) // 3)
         if B >= 4:
             case.n_spans[3] = min(int(case.n_spans[3]), max(1, case.spec.top_k // 2))
+        if B >= 5:
+            case.n_anchors[4] = int(case.n_anchors[4]) // 3
     return case
 
 
@@ -86,6 +89,22 @@ def small_cases():
         _custom("full-route-round-bf16-k5", batch=32, n_q_heads=16, n_kv_heads=8, head_dim=64,
                 rank=16, top_k=5, context=3500, n_prefix_anchors=32, window=64, dtype="bf16",
                 seed=33, span_min=16, span_max=32, variant="N"),
+        # the 32-layer workload's shape of work: 256 pairs x 2 routing chunks, two share
+        # items per pair with four spans each at rank 16 and up to 392 anchors each (three
+        # full anchor blocks and a partial one); ragged: a sequence without spans, one
+        # without anchors, one with few spans, one with a third of its anchors
+        _custom("many-anchors-multi-span-bf16-k8-ragged", batch=32, n_q_heads=32, n_kv_heads=8,
+                head_dim=128, rank=16, top_k=8, context=4000, n_prefix_anchors=256, window=512,
+                dtype="bf16", seed=34, span_min=16, span_max=32, ragged=True, variant="N"),
+        # float32, three share items per pair (three spans, then two); the first round ends
+        # inside the share items, so the first slot folds all 768+ anchors (seven blocks)
+        _custom("many-anchors-multi-span-f32-k7", batch=24, n_q_heads=8, n_kv_heads=8,
+                head_dim=64, rank=16, top_k=7, context=2000, n_prefix_anchors=256, window=512,
+                dtype="f32", seed=35, span_min=24, span_max=120),
+        # rank 32 with four spans per share item and many anchors
+        _custom("many-anchors-multi-span-bf16-r32-k8", batch=32, n_q_heads=16, n_kv_heads=8,
+                head_dim=64, rank=32, top_k=8, context=2500, n_prefix_anchors=256, window=512,
+                dtype="bf16", seed=36, span_min=32, span_max=200),
     ]
     return out
 
