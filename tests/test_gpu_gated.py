@@ -199,6 +199,52 @@ def test_gated_workspace_shared_with_topk_step(S):
             assert torch.equal(gout, first[0]) and torch.equal(tout, first[1])
 
 
+def test_gated_step_in_a_graph(S):
+    """The gated step (selection kernel, then the step in attend mode) captured into a HIP
+    graph: several replays over two cache copies, with eager calls on the same workspace in
+    between, each bit for bit equal to the eager call, whose selection is the oracle's."""
+    import torch
+    case = make_case(custom_spec(dtype="bf16", n_q_heads=8, n_kv_heads=2, head_dim=128, rank=16, top_k=6,
+                                 context=6000, span_min=16, span_max=90, seed=61))
+    gate = make_gate(case, route_dim=32, tau="spread", budget_tokens=400)
+    dev = torch.device("cuda:0")
+    dc, dg = _upload(S, case, gate, 400, dev)
+    dc2 = S.DeviceCache({k: v.clone() for k, v in dc.t.items()}, case.dtype)
+    dims = dims_for(S, case)
+    ws = S.Workspace(dims, dev)
+    ref = _oracle(case, gate, 6, 400)
+    stream = torch.cuda.current_stream()
+    sel_e, out_e = S.decode_step_gated(dims, dc, dg, ws, stream=stream)   # eager first
+    torch.cuda.synchronize()
+    assert ws.status() == 0
+    assert np.array_equal(sel_e.cpu().numpy(), ref["sel"])
+    assert_out_close(out_to_f64(out_e), ref["out"], "bf16", where="gated, eager")
+    sels = [torch.empty_like(sel_e) for _ in range(2)]
+    outs = [torch.empty_like(out_e) for _ in range(2)]
+    cap = torch.cuda.Stream()
+    cap.wait_stream(stream)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=cap):
+        for j, c in enumerate((dc, dc2)):
+            S.decode_step_gated(dims, c, dg, ws, sel=sels[j], out=outs[j], stream=cap)
+    stream.wait_stream(cap)
+    for rep in range(4):
+        for j in range(2):
+            sels[j].fill_(-7)
+            outs[j].zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert ws.status() == 0, f"replay {rep}"
+        for j in range(2):
+            assert torch.equal(sels[j], sel_e), f"replay {rep}, copy {j}: selection"
+            assert torch.equal(outs[j], out_e), f"replay {rep}, copy {j}: output"
+        e_sel, e_out = S.decode_step_gated(dims, dc2, dg, ws, stream=stream)
+        t_sel, t_out = S.decode_step(dims, dc, ws, stream=stream)
+        torch.cuda.synchronize()
+        assert torch.equal(e_out, out_e) and torch.equal(e_sel, sel_e), f"eager call after replay {rep}"
+    del graph
+
+
 @pytest.mark.parametrize("budget", [4096, NO_BUDGET])
 def test_gated_layer_128k_b4_full_size(S, budget):
     """The 128K-context, batch-4 layer at full size under the learned rule (tau = 0.05 for
