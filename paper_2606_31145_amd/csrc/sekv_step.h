@@ -66,9 +66,9 @@ constexpr uint32_t kHelpAfter = 256;
 // kSpinLimit, which flags the workspace): every wait of a launch ends.
 constexpr int kMaxHelps = 64;
 // A share item that starts with the launch holds its first loads back by this many
-// s_sleep units (64 cycles each, about 0.2 us) so that the routing items' summary-key
+// s_sleep units (64 cycles each, about 0.4 us) so that the routing items' summary-key
 // loads, which the selection waits for, reach memory first.
-constexpr int kShareHoldBack = 8;
+constexpr int kShareHoldBack = 16;
 constexpr uint32_t kInvalidIdx = 0xFFFFFFFFu;
 
 // ---------------------------------------------------------------------------
